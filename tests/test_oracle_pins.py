@@ -1,0 +1,383 @@
+"""Pins for the CPU oracle: each test checks the oracle against something other
+than itself -- hand-derived values, closed forms, exact arithmetic, brute force,
+or an independent library routine -- so that a dropped term, a wrong sign or a
+transposed operand in the oracle fails here.  CPU only."""
+import itertools
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import rift_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ----------------------------------------------------------------------------- cdot / csum
+def test_cdot_exact_on_small_integers():
+    """Small-integer inputs times a power of two: every partial sum is exact,
+    so the result must equal the exact integer dot product."""
+    rng = np.random.default_rng(11)
+    for d in (32, 256, 4096):
+        a = rng.integers(-2, 3, size=(5, d)).astype(np.float64) * 2.0 ** -7
+        b = rng.integers(-2, 3, size=d).astype(np.float64) * 2.0 ** 3
+        exact = [sum(Fraction(float(x)) * Fraction(float(y)) for x, y in zip(row, b)) for row in a]
+        got = O.cdot(a, b)
+        assert [Fraction(float(g)) for g in got] == exact
+
+
+def test_cdot_within_error_bound_of_fsum():
+    """Against math.fsum (correctly rounded sum of the exact products): the
+    4-accumulator order has error <= (d/4 + 2) eps sum|a_i b_i|.  A missing or
+    doubled product (magnitude ~1) would exceed that by orders of magnitude."""
+    rng = np.random.default_rng(12)
+    d = 4096
+    a = synth.bf16_to_f32(synth.round_bf16(rng.standard_normal((8, d)).astype(np.float32))).astype(np.float64)
+    b = rng.standard_normal(d).astype(np.float32).astype(np.float64)
+    got = O.cdot(a, b)
+    for i in range(a.shape[0]):
+        ref = math.fsum(a[i] * b)
+        bound = (d / 4 + 2) * 2.0 ** -53 * float(np.abs(a[i] * b).sum())
+        assert abs(got[i] - ref) <= bound
+        assert bound < 1e-9
+
+
+def test_cdot_order_hand_case():
+    """The fixed order, checked on a case where orders disagree (worked by hand):
+    granule 0 holds 2^53 and 1, granule 1 holds 1, granule 2 holds -2^53.
+    acc0 = 2^53 + 1 -> 2^53 (ties to even), acc1 = 1, acc2 = -2^53, acc3 = 0;
+    (acc0 + acc2) + (acc1 + acc3) = 1.  Left-to-right would give 0, exact is 2."""
+    a = np.zeros(32)
+    a[0], a[1], a[8], a[16] = 2.0 ** 53, 1.0, 1.0, -(2.0 ** 53)
+    assert O.cdot(a[None, :], np.ones(32))[0] == 1.0
+    # accumulators are fed by granule index mod 4: granule 4 (index 32) joins acc0
+    a = np.zeros(64)
+    a[0], a[32], a[8] = 2.0 ** 53, 1.0, -(2.0 ** 53)
+    # acc0 = 2^53 + 1 -> 2^53; acc1 = -2^53; (acc0 + acc2) + (acc1 + acc3) = 0
+    assert O.cdot(a[None, :], np.ones(64))[0] == 0.0
+
+
+def test_csum64_order_and_value():
+    rng = np.random.default_rng(13)
+    v = rng.standard_normal(576)
+    assert abs(O.csum64(v) - math.fsum(v)) <= 20 * 2.0 ** -53 * np.abs(v).sum()
+    # order: lane 0 gets v[0] and v[64]; hand case where it matters
+    v = np.zeros(128)
+    v[0], v[64], v[1] = 2.0 ** 53, 1.0, 1.0
+    # p0 = 2^53 + 1 -> 2^53, p1 = 1; tree: ... p0 += p1 last -> 2^53 + 1 -> 2^53
+    assert O.csum64(v) == 2.0 ** 53
+    v = np.zeros(128)
+    v[0], v[64], v[1], v[65] = 2.0 ** 53, -(2.0 ** 53), 1.0, 1.0
+    assert O.csum64(v) == 2.0
+
+
+# ----------------------------------------------------------------------------- keys
+def _unit(v):
+    return v / np.sqrt((v * v).sum())
+
+
+def test_query_direction_matches_eq1_terms():
+    """w must make x.w equal Eq. 1's margin x.t - mean_j x.B_j (up to w's
+    rounding to float32)."""
+    rng = np.random.default_rng(14)
+    d, m = 256, 5
+    qb = np.stack([_unit(rng.standard_normal(d)) for _ in range(1 + m)]).astype(np.float32).astype(np.float64)
+    w = O.query_direction(qb)
+    x = rng.standard_normal(d)
+    margin = math.fsum(x * qb[0]) - math.fsum(math.fsum(x * qb[j]) for j in range(1, m + 1)) / m
+    assert abs(math.fsum(x * w) - margin) <= 2.0 ** -23 * np.abs(x).sum()
+    # M = 0 means no background term: w = t
+    assert np.array_equal(O.query_direction(qb[:1]), qb[0])
+
+
+def test_token_key_is_eq1_margin_of_unit_token():
+    rng = np.random.default_rng(15)
+    d, m = 256, 3
+    qb = np.stack([_unit(rng.standard_normal(d)) for _ in range(1 + m)]).astype(np.float32).astype(np.float64)
+    w = O.query_direction(qb)
+    x = rng.standard_normal((6, d)).astype(np.float32).astype(np.float64)
+    r = O.token_keys(x, w)
+    for i in range(x.shape[0]):
+        xh = x[i] / math.sqrt(math.fsum(x[i] * x[i]))
+        cos = [math.fsum(xh * qb[j]) for j in range(1 + m)]
+        eq1 = cos[0] - sum(cos[1:]) / m
+        assert abs(r[i] - eq1) < 1e-7
+
+
+def test_token_key_textbook_cosine_without_background():
+    rng = np.random.default_rng(16)
+    d = 128
+    t = _unit(rng.standard_normal(d)).astype(np.float32).astype(np.float64)
+    x = rng.standard_normal((4, d))
+    r = O.token_keys(x, O.query_direction(t[None, :]))
+    for i in range(4):
+        ref = math.fsum(x[i] * t) / math.sqrt(math.fsum(x[i] * x[i]))
+        assert abs(r[i] - ref) <= 1e-14
+
+
+def test_token_key_scale_invariance_and_zero():
+    rng = np.random.default_rng(17)
+    d = 256
+    w = rng.standard_normal(d).astype(np.float32).astype(np.float64)
+    x = synth.bf16_to_f32(synth.round_bf16(rng.standard_normal((16, d)).astype(np.float32))).astype(np.float64)
+    r = O.token_keys(x, w)
+    for k in (-3, 1, 5):
+        assert np.array_equal(O.token_keys(x * 2.0 ** k, w), r)
+    z = O.token_keys(np.zeros((2, d)), w)
+    assert np.all(z == 0.0) and not np.any(np.signbit(z))
+
+
+# ----------------------------------------------------------------------------- tile scores, u, rank
+def test_tile_score_is_eq1_with_mean_unit_embedding():
+    """s_i = V_i.t - mean_j V_i.B_j with V_i the mean of unit tokens (reading R1),
+    against Eq. 1 evaluated directly with fsum."""
+    rng = np.random.default_rng(18)
+    d, m, n_tiles, n_v = 64, 4, 3, 70
+    qb = np.stack([_unit(rng.standard_normal(d)) for _ in range(1 + m)]).astype(np.float32).astype(np.float64)
+    x = rng.standard_normal((n_tiles, n_v, d))
+    s = O.tile_scores(np.stack([O.token_keys(x[i], O.query_direction(qb)) for i in range(n_tiles)]))
+    for i in range(n_tiles):
+        xh = x[i] / np.sqrt((x[i] ** 2).sum(axis=1, keepdims=True))
+        V = np.array([math.fsum(xh[:, k]) / n_v for k in range(d)])
+        eq1 = math.fsum(V * qb[0]) - sum(math.fsum(V * qb[j]) for j in range(1, m + 1)) / m
+        assert abs(s[i] - eq1) < 1e-7
+
+
+def test_normalise_extremes_and_degenerate():
+    rng = np.random.default_rng(19)
+    s = rng.standard_normal(400)
+    u = O.normalise(s)
+    assert u.max() == 1.0 and u.min() == 0.0
+    assert u[np.argmax(s)] == 1.0  # App. B Step 3: the top tile has u = 1
+    assert np.all(O.normalise(np.full(7, 0.25)) == 1.0)
+
+
+def test_rank_matches_python_sort_and_permutes():
+    rng = np.random.default_rng(20)
+    s = rng.integers(0, 5, size=50).astype(np.float64) / 7.0  # many ties
+    order, n_keep = O.rank_and_keep(s, O.normalise(s), 10, 0.0)
+    ref = sorted(range(50), key=lambda i: (-s[i], i))
+    assert list(order) == ref and n_keep == 10
+    # threshold mode keeps exactly the u >= tau tiles, as a prefix of the order
+    u = O.normalise(s)
+    order, n_keep = O.rank_and_keep(s, u, 0, 0.37)
+    assert set(order[:n_keep]) == {i for i in range(50) if u[i] >= 0.37}
+    # tile scores are independent per tile: permuting tiles permutes s bitwise
+    x = rng.standard_normal((6, 64, 32))
+    w = rng.standard_normal(32)
+    r = np.stack([O.token_keys(x[i], w) for i in range(6)])
+    perm = rng.permutation(6)
+    assert np.array_equal(O.tile_scores(r[perm]), O.tile_scores(r)[perm])
+
+
+def test_keep_count_edges():
+    s = np.array([0.3, 0.1, 0.2])
+    assert O.rank_and_keep(s, O.normalise(s), 10, 0.5)[1] == 3
+    assert O.rank_and_keep(s, O.normalise(s), 0, 1.5)[1] == 0   # tau above 1: nothing kept
+    assert O.rank_and_keep(s, O.normalise(s), 0, 1.0)[1] == 1   # the top tile always has u = 1
+
+
+# ----------------------------------------------------------------------------- budgets
+def test_budget_tiers_closed_form():
+    lv, num, den = (576, 288, 144, 64), (1, 3, 4), 16
+    b16 = O.assign_budgets(16, lv, num, den)
+    assert [int((b16 == v).sum()) for v in lv] == [1, 3, 4, 8] and int(b16.sum()) == 2528
+    b100 = O.assign_budgets(100, lv, num, den)
+    assert [int((b100 == v).sum()) for v in lv] == [6, 18, 25, 51] and int(b100.sum()) == 15504
+    assert int(b100.sum()) <= int(0.3 * 100 * 576)     # <= 30% of the retained tiles' tokens
+    assert list(b100) == sorted(b100, reverse=True)     # higher rank, larger budget
+    assert list(O.assign_budgets(1, lv, num, den)) == [64]
+    assert len(O.assign_budgets(0, lv, num, den)) == 0
+    assert list(O.assign_budgets(2, (64,), (), 16)) == [64, 64]
+
+
+# ----------------------------------------------------------------------------- selection
+def _brute_select(r, k):
+    """The unique k-subset S with: for i in S, j not in S, r_i > r_j or
+    (r_i == r_j and i < j).  Found by enumerating every subset."""
+    n = len(r)
+    found = []
+    for S in itertools.combinations(range(n), k):
+        inside = set(S)
+        ok = all((r[i] > r[j]) or (r[i] == r[j] and i < j)
+                 for i in inside for j in range(n) if j not in inside)
+        if ok:
+            found.append(list(S))
+    assert len(found) == 1
+    return found[0]
+
+
+def test_select_matches_brute_force_with_ties():
+    rng = np.random.default_rng(21)
+    for trial in range(40):
+        n = int(rng.integers(1, 13))
+        r = rng.integers(-2, 3, size=(1, n)).astype(np.float64) if trial % 2 else rng.standard_normal((1, n))
+        k = int(rng.integers(0, n + 1))
+        offs, sel = O.select_tokens(r, [0], [k])
+        assert list(sel) == _brute_select(list(r[0]), k)
+        assert list(offs) == [0, k]
+
+
+def test_select_invariants_full_budget_identity():
+    rng = np.random.default_rng(22)
+    r = rng.standard_normal((5, 40))
+    kept, budgets = [3, 0, 4], [7, 40, 1]
+    offs, sel = O.select_tokens(r, kept, budgets)
+    for rho, b in enumerate(budgets):
+        part = sel[offs[rho]:offs[rho + 1]]
+        assert len(part) == b and np.all(np.diff(part) > 0)  # count = budget, sorted, unique
+    assert list(sel[offs[1]:offs[2]]) == list(range(40))      # full budget keeps every token in order
+
+
+# ----------------------------------------------------------------------------- compact
+def test_compact_layout_and_full_budget_identity():
+    rng = np.random.default_rng(23)
+    x = rng.standard_normal((3, 10, 32))
+    sysr, qry = rng.standard_normal((2, 32)), rng.standard_normal((3, 32))
+    r = rng.standard_normal((3, 10))
+    kept = [2, 0]
+    offs, sel = O.select_tokens(r, kept, [4, 10])
+    packed, cu, pos = O.compact(x, kept, offs, sel, sysr, qry)
+    assert list(cu) == [0, 9, 24] and packed.shape == (24, 32)
+    assert np.array_equal(pos, np.r_[np.arange(9), np.arange(15)])
+    assert np.array_equal(packed[9:11], sysr) and np.array_equal(packed[21:24], qry)
+    assert np.array_equal(packed[11:21], x[0])                # full budget: the tile verbatim
+    assert np.array_equal(packed[2:6], x[2][sel[:4]])
+
+
+# ----------------------------------------------------------------------------- golden hand example
+def _vec(terms, d):
+    v = np.zeros(d)
+    for t in terms:
+        if t.startswith("3*"):
+            v[int(t[3:])] += 3.0
+        else:
+            v[int(t[1:])] += 1.0
+    return v
+
+
+def test_stage1_hand_example():
+    with open(os.path.join(GOLDEN, "stage1_hand_example.json")) as f:
+        g = json.load(f)
+    d = g["d"]
+    x = np.stack([np.stack([_vec(tok, d) for tok in tile]) for tile in g["tiles"]])
+    qb = np.stack([_vec([e], d) for e in g["qbank"]])
+    st = O.scene_query_stage1(x, qb, 0, g["tau"])
+    r2 = math.sqrt(2.0)
+    env = {"sqrt": math.sqrt}
+    exp_s = [eval(e, env) for e in g["expected"]["s"]]
+    exp_u = [eval(e, env) for e in g["expected"]["u"]]
+    assert np.allclose(st["s"], exp_s, rtol=0, atol=1e-15), (st["s"], exp_s, r2)
+    assert np.allclose(st["u"], exp_u, rtol=0, atol=1e-15)
+    assert list(st["order"]) == g["expected"]["order"] and st["n_keep"] == g["expected"]["n_keep"]
+    kept = list(st["order"][: st["n_keep"]])
+    b = O.assign_budgets(st["n_keep"], g["levels"], g["tier_num"], g["tier_den"])
+    assert list(b) == g["expected"]["budgets"]
+    offs, sel = O.select_tokens(st["r"], kept, b)
+    assert list(offs) == g["expected"]["sel_offsets"] and list(sel) == g["expected"]["sel_idx"]
+
+
+# ----------------------------------------------------------------------------- prefill pieces
+def _naive_attention(q, k, v):
+    """Explicit loops: for each query i, softmax over keys 0..i."""
+    L, H, hd = q.shape
+    out = np.zeros_like(q)
+    for h in range(H):
+        for i in range(L):
+            sc = [sum(q[i, h, c] * k[j, h, c] for c in range(hd)) / math.sqrt(hd) for j in range(i + 1)]
+            mx = max(sc)
+            e = [math.exp(s - mx) for s in sc]
+            z = sum(e)
+            for c in range(hd):
+                out[i, h, c] = sum(e[j] / z * v[j, h, c] for j in range(i + 1))
+    return out
+
+
+def test_attention_vs_naive_loops():
+    rng = np.random.default_rng(24)
+    q, k, v = (rng.standard_normal((9, 2, 8)) for _ in range(3))
+    assert np.allclose(O.causal_attention(q, k, v), _naive_attention(q, k, v), rtol=0, atol=1e-13)
+
+
+def test_attention_special_cases():
+    rng = np.random.default_rng(25)
+    v = rng.standard_normal((6, 2, 8))
+    q = rng.standard_normal((6, 2, 8))
+    k = rng.standard_normal((6, 2, 8))
+    # length 1: softmax of one score is 1, the output is v
+    assert np.allclose(O.causal_attention(q[:1], k[:1], v[:1]), v[:1], atol=1e-15)
+    # all-equal scores (zero queries): output i is the mean of v[0..i]
+    out = O.causal_attention(np.zeros_like(q), k, v)
+    pref = np.cumsum(v, axis=0) / np.arange(1, 7)[:, None, None]
+    assert np.allclose(out, pref, atol=1e-14)
+
+
+def test_rope_identity_norm_and_complex_form():
+    rng = np.random.default_rng(26)
+    x = rng.standard_normal((5, 3, 16))
+    pos = np.array([0, 1, 2, 7, 100])
+    y = O.rope(x, pos, 10000.0)
+    assert np.allclose(y[0], x[0], atol=0)  # position 0 is the identity
+    half = 8
+    assert np.allclose(np.sqrt((y ** 2).sum(-1)), np.sqrt((x ** 2).sum(-1)), atol=1e-12)
+    # complex form: (x_j + i x_{j+half}) * exp(i pos theta_j)
+    for p_i, p in enumerate(pos):
+        for j in range(half):
+            th = 10000.0 ** (-2 * j / 16)
+            z = complex(x[p_i, 0, j], x[p_i, 0, j + half]) * complex(math.cos(p * th), math.sin(p * th))
+            assert abs(y[p_i, 0, j] - z.real) < 1e-12 and abs(y[p_i, 0, j + half] - z.imag) < 1e-12
+
+
+def test_rmsnorm_and_silu_closed_forms():
+    x = np.array([[3.0, 4.0]])
+    # mean square 12.5 -> x / sqrt(12.5 + eps)
+    assert np.allclose(O.rmsnorm(x, np.ones(2), 0.0), x / math.sqrt(12.5), atol=1e-15)
+    assert O.silu(np.array([0.0]))[0] == 0.0
+    assert abs(O.silu(np.array([1.0]))[0] - 1.0 / (1.0 + math.exp(-1.0))) < 1e-16
+
+
+@pytest.mark.slow
+def test_decoder_layer_vs_transformers_llama():
+    """One layer against transformers' LlamaDecoderLayer in float64 on CPU
+    (a library routine, used as is).  The library builds its rotary inverse
+    frequencies in float32, so the positions are kept short and the tolerance
+    covers that rounding; the angle formula itself is pinned by the complex
+    form test above."""
+    torch = pytest.importorskip("torch")
+    tr = pytest.importorskip("transformers")
+    from transformers.models.llama.modeling_llama import LlamaDecoderLayer, LlamaRotaryEmbedding
+    w = synth.get("tiny")
+    m = w.model
+    W = {k: synth.to_f64(v, w.dtype) for k, v in synth.make_layer(w, 0).items()}
+    rng = np.random.default_rng(27)
+    W["g_attn"] = 1.0 + 0.1 * rng.standard_normal(m.d)   # non-trivial gains exercise the norm weights
+    W["g_ffn"] = 1.0 + 0.1 * rng.standard_normal(m.d)
+    L = 12
+    x = rng.standard_normal((L, m.d))
+    cfg = tr.LlamaConfig(hidden_size=m.d, intermediate_size=m.ffn, num_attention_heads=m.n_heads,
+                         num_key_value_heads=m.n_heads, head_dim=m.head_dim, rms_norm_eps=m.rms_eps,
+                         attention_bias=False, mlp_bias=False, max_position_embeddings=4096,
+                         rope_parameters={"rope_type": "default", "rope_theta": m.rope_base})
+    cfg._attn_implementation = "eager"
+    layer = LlamaDecoderLayer(cfg, 0).double()
+    rot = LlamaRotaryEmbedding(cfg).double()
+    names = {"self_attn.q_proj.weight": "wq", "self_attn.k_proj.weight": "wk",
+             "self_attn.v_proj.weight": "wv", "self_attn.o_proj.weight": "wo",
+             "mlp.gate_proj.weight": "w_gate", "mlp.up_proj.weight": "w_up",
+             "mlp.down_proj.weight": "w_down", "input_layernorm.weight": "g_attn",
+             "post_attention_layernorm.weight": "g_ffn"}
+    with torch.no_grad():
+        for pn, p in layer.named_parameters():
+            p.copy_(torch.from_numpy(W[names[pn]]))
+        xt = torch.from_numpy(x)[None]
+        pos = torch.arange(L)[None]
+        mask = torch.full((L, L), float("-inf"), dtype=torch.float64).triu(1)[None, None]
+        ref = layer(xt, attention_mask=mask, position_ids=pos,
+                    position_embeddings=rot(xt, pos))[0].numpy()
+    got = O.decoder_layer(x, W, m.n_heads, m.head_dim, m.rms_eps, m.rope_base, np.arange(L))
+    err = np.abs(got - ref).max(axis=1) / np.abs(ref).max(axis=1)
+    assert err.max() < 1e-6, err.max()
