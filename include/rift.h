@@ -1,0 +1,236 @@
+/*
+ * rift.h -- C ABI of the Rift hot path on AMD Instinct MI355X (gfx950).
+ *
+ * The four stages of one scene-query, in the order the paper applies them:
+ *   1. rift_score_tiles    query-conditioned tile relevance and pruning
+ *                          (Sec. 2.3 Stage 1, Eq. 1, Listing 1, App. B Step 3)
+ *   2. rift_select_tokens  per-tile dominant-token selection under elastic
+ *                          budgets (Sec. 2.3 Stage 2)
+ *   3. rift_compact        packing of each retained tile's prompt into one
+ *                          varlen batch (each tile is its own VLM call,
+ *                          Sec. 2.3 Stage 2 and App. B Step 5)
+ *   4. rift_prefill        LLaMA-7B-shaped decoder prefill of the packed
+ *                          prompts (Sec. 2.1; LLaVA-1.5-7B, Sec. 3)
+ * plus the host-side budget assignment rift_assign_budgets.
+ *
+ * Conventions shared by every call
+ *   - Pointers are DEVICE pointers unless the comment says [host].
+ *   - The caller owns every buffer (inputs, outputs, workspace).  The library
+ *     allocates no device memory and keeps no per-call state.
+ *   - Calls are asynchronous and ordered on `stream` (a hipStream_t; NULL is
+ *     the null stream).  The library never synchronises the device.
+ *   - Arguments are validated on the host first; on failure a call returns a
+ *     non-OK status and enqueues nothing.  Errors that only the device can see
+ *     (a budget out of range, an index out of bounds) are reported through a
+ *     device status word, and the kernels then write nothing out of bounds.
+ *   - Storage types: RIFT_BF16 (bfloat16) or RIFT_F32.  One dtype is shared by
+ *     tokens, query bank, system/query embeddings and weights of a call chain.
+ */
+#ifndef RIFT_H
+#define RIFT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RIFT_ABI_VERSION 1
+
+#if defined(__GNUC__) || defined(__clang__)
+#define RIFT_API __attribute__((visibility("default")))
+#else
+#define RIFT_API
+#endif
+
+typedef enum {
+    RIFT_OK = 0,
+    RIFT_ERR_NULL = 1,        /* a required pointer is NULL                       */
+    RIFT_ERR_SHAPE = 2,       /* a size breaks the shape rules of the call        */
+    RIFT_ERR_DTYPE = 3,       /* unknown or mismatched storage type               */
+    RIFT_ERR_BUDGET = 4,      /* budget, level or tier out of range               */
+    RIFT_ERR_WORKSPACE = 5,   /* workspace too small or not 256-byte aligned      */
+    RIFT_ERR_HIP = 6,         /* a HIP runtime call or a kernel launch failed     */
+    RIFT_ERR_UNSUPPORTED = 7  /* valid request outside what this build implements */
+} rift_status;
+
+typedef enum { RIFT_F32 = 0, RIFT_BF16 = 1 } rift_dtype;
+
+typedef void* rift_stream; /* hipStream_t */
+
+/* ABI version of the loaded library (RIFT_ABI_VERSION it was built with). */
+RIFT_API int32_t rift_abi_version(void);
+
+/* Static text for a status code. */
+RIFT_API const char* rift_status_string(rift_status s);
+
+/* ------------------------------------------------------------------ Stage 1 */
+
+/* Workspace bytes rift_score_tiles needs for a scene of this shape. */
+RIFT_API size_t rift_score_workspace_size(int32_t n_tiles, int32_t n_v, int32_t d);
+
+/*
+ * rift_score_tiles -- Stage 1 of Sec. 2.3: Eq. 1 background-margin relevance,
+ * per-scene min-max normalisation and retention (Listing 1; App. B Step 3).
+ *
+ * tokens      [n_tiles][n_v][d] dt   vision tokens of every tile (row-major)
+ * query_bank  [1 + n_bg][d]     dt   row 0 = query object t, rows 1..n_bg =
+ *                                    background phrases B_j; unit norm before
+ *                                    rounding to dt (the rounded values count)
+ * keep_count  > 0: keep the top min(keep_count, n_tiles) tiles by score;
+ *             == 0: keep every tile with u >= tau (tau is compared in float64)
+ * Outputs (all device):
+ * token_key   [n_tiles*n_v] f64  per-token margin of the unit token,
+ *                                r = (x.w)/|x| with w = t - mean_j B_j rounded
+ *                                to f32 (Eq. 1 is linear in the tile
+ *                                embedding); a fixed float64 summation order
+ *                                makes r reproducible bit for bit: elements in
+ *                                8-wide granules, granule g into accumulator
+ *                                g mod 4, ascending, then (a0+a2)+(a1+a3).
+ *                                All-zero token -> +0.
+ * token_sim   [n_tiles*n_v][1+n_bg] f32 cosine of each token to t and each
+ *                                B_j (MFMA relevance GEMM), or NULL to skip
+ * tile_score  [n_tiles] f64      s_i = mean of the tile's token margins: 64
+ *                                strided partial sums then a halving tree,
+ *                                divided by n_v
+ * tile_u      [n_tiles] f32      (s - min s)/(max s - min s) in float64,
+ *                                rounded to f32; all 1 when max == min
+ * tile_order  [n_tiles] i32      tile ids by (s descending, id ascending); the
+ *                                first *n_keep entries are the kept tiles
+ * n_keep      [1] i32            number of kept tiles
+ * Shape rules: 1 <= n_tiles <= 4096, 1 <= n_v <= 1024, d % 32 == 0,
+ * 32 <= d <= 16384, 0 <= n_bg <= 15, 0 <= tau (any double).
+ * workspace   >= rift_score_workspace_size(...) bytes, 256-byte aligned.
+ */
+RIFT_API rift_status rift_score_tiles(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
+                             int32_t d, const void* query_bank, int32_t n_bg,
+                             int32_t keep_count, double tau,
+                             double* token_key, float* token_sim, double* tile_score,
+                             float* tile_u, int32_t* tile_order, int32_t* n_keep,
+                             void* workspace, size_t ws_bytes, rift_stream stream);
+
+/* ------------------------------------------------------------------ Stage 2 */
+
+/*
+ * rift_assign_budgets -- [host only] per-tile token budgets from the discrete
+ * set C of Sec. 2.3 Stage 2, assigned by score rank: the kept tile of rank rho
+ * gets levels[j] for the tier j containing rho; tier j < n_levels-1 holds
+ * floor(n_keep * tier_num[j] / tier_den) tiles and the last tier the rest.
+ * levels    [host] n_levels budgets, strictly descending, each in [1, n_v]
+ * tier_num  [host] n_levels-1 numerators (>= 0; sum <= tier_den), or NULL for
+ *           the default {1, 3, 4}/16 (requires n_levels == 4)
+ * budgets   [host] out [n_keep];  total [host] out: sum of budgets (may be NULL)
+ */
+RIFT_API rift_status rift_assign_budgets(int32_t n_keep, int32_t n_v, const int32_t* levels,
+                                int32_t n_levels, const int32_t* tier_num, int32_t tier_den,
+                                int32_t* budgets, int64_t* total);
+
+/*
+ * rift_select_tokens -- VisionZip-style dominant-token retention (Sec. 2.3
+ * Stage 2) under per-tile budgets: for kept tile rho (id kept_tiles[rho]), keep
+ * the budgets[rho] tokens with the largest token_key, ties to the lower token
+ * index, and emit their indices in ascending order.
+ * token_key   [n_tiles*n_v] f64   from rift_score_tiles
+ * kept_tiles  [n_keep] i32        tile ids (e.g. the head of tile_order)
+ * budgets     [n_keep] i32        each in [0, n_v]
+ * sel_offsets [n_keep+1] i32 out  exclusive prefix sums of budgets
+ * sel_idx     [sel_capacity] i32 out   the kept indices, tile after tile
+ * status      [1] i32 out         0, or RIFT_ERR_BUDGET if a budget is out of
+ *                                 range, a tile id is out of range or the total
+ *                                 exceeds sel_capacity (then nothing is written
+ *                                 to sel_idx and all offsets are 0)
+ * Shape rules: 1 <= n_v <= 1024, 0 <= n_keep <= n_tiles <= 4096.
+ */
+RIFT_API rift_status rift_select_tokens(const double* token_key, int32_t n_tiles, int32_t n_v,
+                               const int32_t* kept_tiles, const int32_t* budgets,
+                               int32_t n_keep, int32_t* sel_offsets, int32_t* sel_idx,
+                               int64_t sel_capacity, int32_t* status, rift_stream stream);
+
+/*
+ * rift_compact -- pack every kept tile's prompt [n_sys system rows | selected
+ * vision rows of the tile, ascending | n_qry query rows] into one varlen batch.
+ * tokens   [n_tiles][n_v][d] dt;  sys_emb [n_sys][d] dt;  qry_emb [n_qry][d] dt
+ * kept_tiles, sel_offsets, sel_idx as produced for rift_select_tokens
+ * packed       [packed_rows][d] dt out, total rows
+ *              T = n_keep*(n_sys+n_qry) + sel_offsets[n_keep] must be <= packed_rows
+ * cu_seqlens   [n_keep+1] i32 out  prefix sums of sequence lengths
+ * position_ids [packed_rows] i32 out  0..L-1 within each sequence
+ * status       [1] i32 out  0, or RIFT_ERR_SHAPE if an index is out of range or
+ *              T > packed_rows (offending rows are not written)
+ * Shape rules: d * sizeof(dt) % 16 == 0; n_sys, n_qry >= 0.
+ */
+RIFT_API rift_status rift_compact(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
+                         int32_t d, const int32_t* kept_tiles, const int32_t* sel_offsets,
+                         const int32_t* sel_idx, int32_t n_keep, const void* sys_emb,
+                         int32_t n_sys, const void* qry_emb, int32_t n_qry, void* packed,
+                         int64_t packed_rows, int32_t* cu_seqlens, int32_t* position_ids,
+                         int32_t* status, rift_stream stream);
+
+/* ------------------------------------------------------------------ prefill */
+
+/* Weights of one decoder layer, nn.Linear layout [out][in], storage type
+ * cfg->dt: wq, wk, wv, wo [d][d]; w_gate, w_up [ffn][d]; w_down [d][ffn];
+ * RMSNorm gains g_attn, g_ffn [d]. */
+typedef struct {
+    const void* wq;
+    const void* wk;
+    const void* wv;
+    const void* wo;
+    const void* w_gate;
+    const void* w_up;
+    const void* w_down;
+    const void* g_attn;
+    const void* g_ffn;
+} rift_layer_weights;
+
+typedef struct {
+    int32_t d;          /* hidden size                       */
+    int32_t n_heads;    /* attention heads (no grouped KV)   */
+    int32_t head_dim;   /* n_heads * head_dim == d           */
+    int32_t ffn;        /* SwiGLU inner size                 */
+    int32_t n_layers;
+    float rms_eps;      /* RMSNorm epsilon                   */
+    float rope_base;    /* rotary base (10000 for LLaMA)     */
+    rift_dtype dt;      /* storage type of weights and activations */
+} rift_model_cfg;
+
+/* Workspace bytes rift_prefill needs for this model and batch. */
+RIFT_API size_t rift_prefill_workspace_size(const rift_model_cfg* cfg, int32_t total_tokens,
+                                   int32_t max_seqlen);
+
+/*
+ * rift_prefill -- prefill of n_seq independent prompts packed back to back
+ * (Sec. 2.1: prefill reads the whole input and builds the KV cache; each
+ * retained tile is its own call, Sec. 2.3).  Per layer, on each sequence:
+ *   h = RMSNorm(x) g_attn;  q,k,v = h Wq^T, h Wk^T, h Wv^T;
+ *   rotate-half RoPE on q, k (angle pos * base^(-2j/head_dim));
+ *   causal softmax attention within the sequence, scale 1/sqrt(head_dim);
+ *   x += o Wo^T;  h2 = RMSNorm(x) g_ffn;  x += (silu(h2 Wg^T) * (h2 Wu^T)) Wd^T.
+ * cfg, layers  [host] model shape and n_layers weight sets
+ * x_in         [total_tokens][d]: packed prompt tokens in cfg->dt, or, with
+ *              x_dt == RIFT_F32, a float32 residual stream (e.g. the output of
+ *              an earlier call); may alias hidden_out when x_dt == RIFT_F32
+ * cu_seqlens   [n_seq+1] i32, cu_seqlens[0] = 0, non-decreasing, last =
+ *              total_tokens, every length <= max_seqlen
+ * position_ids [total_tokens] i32, each in [0, max_seqlen)  (values outside
+ *              are clamped)
+ * hidden_out   [total_tokens][d] f32 out: residual stream after the last layer
+ *              (no final norm, no vocabulary projection)
+ * kv_cache     optional out [n_layers][2][total_tokens][d] cfg->dt: per layer
+ *              the rotated keys, then the values; NULL to skip
+ * Implemented: bf16 with head_dim == 128, d % 256 == 0, ffn % 128 == 0;
+ *              f32 with head_dim in {64, 128}, d % 64 == 0, ffn % 16 == 0.
+ * Shape rules: 1 <= max_seqlen <= 65536, total_tokens >= 0, n_seq >= 0.
+ */
+RIFT_API rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* layers,
+                         const void* x_in, rift_dtype x_dt, const int32_t* cu_seqlens,
+                         const int32_t* position_ids, int32_t n_seq, int32_t total_tokens,
+                         int32_t max_seqlen, float* hidden_out, void* kv_cache,
+                         void* workspace, size_t ws_bytes, rift_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RIFT_H */

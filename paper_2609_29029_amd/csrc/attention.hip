@@ -1,0 +1,243 @@
+// Varlen causal softmax attention of the packed prompts (each retained tile is
+// an independent sequence; Sec. 2.3 Stage 2).  Query i of a sequence attends
+// to keys 0..i of the same sequence, scale 1/sqrt(head_dim).
+//
+// bf16, head_dim 128, on MFMA.  One workgroup (4 waves) per (sequence, head,
+// 128-query block); wave w owns queries [32 w, 32 w + 32) of the block.  Keys
+// and values stream through LDS 64 at a time (K row-major, V transposed).  The
+// wave computes S^T = K Q^T (v_mfma_f32_32x32x16_bf16, M = keys, N = queries),
+// so each lane holds one query's scores in registers; the online softmax runs
+// in float32 (running max and sum per query); the unnormalised probabilities,
+// rounded to bf16, are already in the B-operand layout of O^T = V^T P^T.
+// Key blocks start at the sequence start, so a sequence's result does not
+// depend on how it is packed.
+//
+// The float32 path (small models) is a plain per-query loop.
+#include "launch.h"
+#include "rift_common.h"
+
+namespace rift {
+
+namespace {
+
+constexpr int HD = 128;
+constexpr int BQ = 128;
+constexpr int BKV = 64;
+constexpr int KPAD = HD + 8;   // K tile row stride (elements)
+constexpr int VPAD = BKV + 4;  // V^T tile row stride (elements)
+
+__global__ void __launch_bounds__(256)
+attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
+                 const bf16_t* __restrict__ v, bf16_t* __restrict__ o,
+                 const int* __restrict__ cu, int n_seq, int nqb, int H, float scale_log2) {
+    __shared__ __align__(16) bf16_t Ks[BKV * KPAD];
+    __shared__ __align__(16) bf16_t Vt[HD * VPAD];
+
+    const int bid = blockIdx.x;
+    const int qb = nqb - 1 - (bid % nqb);  // heaviest (last) query blocks first
+    const int rest = bid / nqb;
+    const int seq = rest % n_seq;
+    const int head = rest / n_seq;
+    const int s0 = cu[seq];
+    const int L = cu[seq + 1] - s0;
+    const int q0 = qb * BQ;
+    if (q0 >= L) return;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int h = lane >> 5;
+    const int col = lane & 31;
+    const int ld = H * HD;
+    const size_t head_off = (size_t)head * HD;
+
+    const int qw = q0 + wave * 32;            // first query of this wave
+    const int qidx = qw + col;                // this lane's query
+    const int q_eff = qidx < L ? qidx : L - 1;
+
+    // Q^T B-operand fragments: lane holds Q[query][16 kk + 8 h .. + 8]
+    bf16x8_t qf[8];
+    {
+        const bf16_t* qrow = q + (size_t)(s0 + q_eff) * ld + head_off + 8 * h;
+#pragma unroll
+        for (int kk = 0; kk < 8; ++kk) qf[kk] = *reinterpret_cast<const bf16x8_t*>(qrow + 16 * kk);
+    }
+
+    f32x16_t oacc[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[t][i] = 0.f;
+    float m_run = -INFINITY;
+    float l_run = 0.f;
+
+    const int kv_end = (q0 + BQ) < L ? (q0 + BQ) : L;
+    const int wave_last = (qw + 31) < (L - 1) ? (qw + 31) : (L - 1);
+
+    for (int kv0 = 0; kv0 < kv_end; kv0 += BKV) {
+        __syncthreads();
+        // stage K rows and V^T for keys kv0 .. kv0+63 (clamped to the sequence)
+#pragma unroll
+        for (int it = 0; it < 4; ++it) {
+            const int vec = tid + 256 * it;
+            const int rr = vec >> 4;
+            const int cc = (vec & 15) * 8;
+            int key = kv0 + rr;
+            key = key < L ? key : L - 1;
+            const size_t g = (size_t)(s0 + key) * ld + head_off + cc;
+            *reinterpret_cast<u32x4_t*>(Ks + rr * KPAD + cc) = *reinterpret_cast<const u32x4_t*>(k + g);
+            const u32x4_t vv = *reinterpret_cast<const u32x4_t*>(v + g);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                Vt[(cc + 2 * e) * VPAD + rr] = (bf16_t)(vv[e] & 0xFFFFu);
+                Vt[(cc + 2 * e + 1) * VPAD + rr] = (bf16_t)(vv[e] >> 16);
+            }
+        }
+        __syncthreads();
+        if (kv0 > wave_last) continue;  // every key of the block is after this wave's queries
+
+        // scores for two 32-key sub-blocks
+        float sc[2][16];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+            f32x16_t s;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) s[i] = 0.f;
+            const bf16_t* krow = Ks + (kb * 32 + col) * KPAD + 8 * h;
+#pragma unroll
+            for (int kk = 0; kk < 8; ++kk) {
+                const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(krow + 16 * kk);
+                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s, 0, 0, 0);
+            }
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int key = kv0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+                sc[kb][i] = (key <= q_eff) ? s[i] * scale_log2 : -INFINITY;
+            }
+        }
+        float bmax = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) bmax = fmaxf(bmax, sc[kb][i]);
+        bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
+        const float m_new = fmaxf(m_run, bmax);
+        const float alpha = exp2f(m_run - m_new);
+        float rsum = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const float pv = exp2f(sc[kb][i] - m_new);
+                sc[kb][i] = pv;
+                rsum += pv;
+            }
+        rsum += __shfl_xor(rsum, 32);
+        l_run = l_run * alpha + rsum;
+        m_run = m_new;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) oacc[t][i] *= alpha;
+
+        // O^T += V^T P^T.  For MFMA step ks of sub-block kb, lane half h holds
+        // keys {16 ks + 4 h + 0..3, 16 ks + 8 + 4 h + 0..3} in slots 0..7.
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                bf16x8_t pf;
+#pragma unroll
+                for (int jj = 0; jj < 8; ++jj) pf[jj] = (__bf16)sc[kb][8 * ks + jj];
+                const int kbase = kb * 32 + 16 * ks + 4 * h;
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const bf16_t* vrow = Vt + (t * 32 + col) * VPAD + kbase;
+                    const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
+                    const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 8);
+                    const u32x4_t vv = {lo.x, lo.y, hi.x, hi.y};
+                    oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vv),
+                                                                      pf, oacc[t], 0, 0, 0);
+                }
+            }
+    }
+
+    if (qidx >= L) return;
+    const float inv = 1.0f / l_run;
+    bf16_t* orow = o + (size_t)(s0 + qidx) * ld + head_off;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            const int dcol = t * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+            orow[dcol] = f32_to_bf16(oacc[t][i] * inv);
+        }
+}
+
+template <int D>
+__global__ void __launch_bounds__(128)
+attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
+                const float* __restrict__ v, float* __restrict__ o, const int* __restrict__ cu,
+                int n_seq, int H, float scale) {
+    const int seq = blockIdx.x % n_seq;
+    const int head = blockIdx.x / n_seq;
+    const int s0 = cu[seq];
+    const int L = cu[seq + 1] - s0;
+    const int ld = H * D;
+    for (int i = threadIdx.x; i < L; i += blockDim.x) {
+        const float* qi = q + (size_t)(s0 + i) * ld + head * D;
+        float acc[D];
+#pragma unroll
+        for (int c = 0; c < D; ++c) acc[c] = 0.f;
+        float m = -INFINITY, l = 0.f;
+        for (int j = 0; j <= i; ++j) {
+            const float* kj = k + (size_t)(s0 + j) * ld + head * D;
+            float s = 0.f;
+#pragma unroll
+            for (int c = 0; c < D; ++c) s = fmaf(qi[c], kj[c], s);
+            s *= scale;
+            const float mn = fmaxf(m, s);
+            const float a = expf(m - mn);
+            const float p = expf(s - mn);
+            l = l * a + p;
+            const float* vj = v + (size_t)(s0 + j) * ld + head * D;
+#pragma unroll
+            for (int c = 0; c < D; ++c) acc[c] = acc[c] * a + p * vj[c];
+            m = mn;
+        }
+        float* oi = o + (size_t)(s0 + i) * ld + head * D;
+#pragma unroll
+        for (int c = 0; c < D; ++c) oi[c] = acc[c] / l;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                                 uint16_t* o, const int* cu, int n_seq, int max_seqlen,
+                                 int n_heads, hipStream_t st) {
+    if (n_seq <= 0 || max_seqlen <= 0) return hipSuccess;
+    const int nqb = (max_seqlen + BQ - 1) / BQ;
+    const float scale_log2 = 1.4426950408889634f / sqrtf((float)HD);
+    const long long blocks = (long long)nqb * n_seq * n_heads;
+    hipLaunchKernelGGL(attn_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, st, q, k, v, o, cu,
+                       n_seq, nqb, n_heads, scale_log2);
+    return hipGetLastError();
+}
+
+hipError_t launch_attention_f32(const float* q, const float* k, const float* v, float* o,
+                                const int* cu, int n_seq, int max_seqlen, int n_heads, int hd,
+                                hipStream_t st) {
+    if (n_seq <= 0 || max_seqlen <= 0) return hipSuccess;
+    const float scale = 1.0f / sqrtf((float)hd);
+    const dim3 grid((unsigned)(n_seq * n_heads));
+    if (hd == 64)
+        hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(128), 0, st, q, k, v, o, cu, n_seq,
+                           n_heads, scale);
+    else
+        hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(128), 0, st, q, k, v, o, cu, n_seq,
+                           n_heads, scale);
+    return hipGetLastError();
+}
+
+}  // namespace rift

@@ -1,0 +1,353 @@
+// C ABI of the Rift hot path: argument validation, workspace carving and
+// kernel launches.  Nothing here allocates device memory or synchronises.
+#include <math.h>
+
+#include <mutex>
+
+#include "launch.h"
+#include "rift_common.h"
+
+namespace rift {
+hipError_t gemm_bf16_init_attributes();
+
+namespace {
+
+std::once_flag g_init_flag;
+hipError_t g_init_err = hipSuccess;
+
+template <typename K>
+hipError_t allow_lds(K* kernel, int bytes) {
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+}
+
+}  // namespace
+
+// score_tiles_kernel is defined in score.hip; its LDS need grows with d.
+hipError_t score_init_attributes();
+
+hipError_t init_kernel_attributes() {
+    std::call_once(g_init_flag, [] {
+        g_init_err = gemm_bf16_init_attributes();
+        if (g_init_err == hipSuccess) g_init_err = score_init_attributes();
+    });
+    return g_init_err;
+}
+
+}  // namespace rift
+
+using namespace rift;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+inline size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+inline bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & (kAlign - 1)) != 0; }
+
+inline size_t dt_bytes(rift_dtype dt) { return dt == RIFT_BF16 ? 2 : 4; }
+
+inline bool dt_valid(rift_dtype dt) { return dt == RIFT_BF16 || dt == RIFT_F32; }
+
+inline rift_status hip_status(hipError_t e) { return e == hipSuccess ? RIFT_OK : RIFT_ERR_HIP; }
+
+struct PrefillLayout {
+    size_t rope, h, q, k, v, a, gate2, total;
+};
+
+PrefillLayout prefill_layout(const rift_model_cfg& c, int64_t T, int64_t P) {
+    PrefillLayout L{};
+    const size_t e = dt_bytes(c.dt);
+    size_t off = 0;
+    L.rope = off;
+    off += align_up((size_t)P * (size_t)(c.head_dim / 2) * sizeof(float2));
+    L.h = off;
+    off += align_up((size_t)T * c.d * e);
+    L.q = off;
+    off += align_up((size_t)T * c.d * e);
+    L.k = off;
+    off += align_up((size_t)T * c.d * e);
+    L.v = off;
+    off += align_up((size_t)T * c.d * e);
+    L.a = off;
+    off += align_up((size_t)T * c.ffn * e);
+    L.gate2 = off;
+    if (c.dt == RIFT_F32) off += align_up((size_t)T * c.ffn * e);
+    L.total = off;
+    return L;
+}
+
+rift_status check_cfg(const rift_model_cfg* cfg) {
+    if (cfg == nullptr) return RIFT_ERR_NULL;
+    if (!dt_valid(cfg->dt)) return RIFT_ERR_DTYPE;
+    if (cfg->d <= 0 || cfg->n_heads <= 0 || cfg->head_dim <= 0 || cfg->ffn <= 0 ||
+        cfg->n_layers < 0 || (int64_t)cfg->n_heads * cfg->head_dim != cfg->d)
+        return RIFT_ERR_SHAPE;
+    if (!(cfg->rms_eps >= 0.0f) || !(cfg->rope_base > 0.0f)) return RIFT_ERR_SHAPE;
+    if (cfg->dt == RIFT_BF16) {
+        if (cfg->head_dim != 128 || cfg->d % 256 != 0 || cfg->ffn % 128 != 0)
+            return RIFT_ERR_UNSUPPORTED;
+        if ((uint64_t)cfg->d * cfg->ffn >= (1ull << 32)) return RIFT_ERR_UNSUPPORTED;
+    } else {
+        if ((cfg->head_dim != 64 && cfg->head_dim != 128) || cfg->d % 64 != 0 || cfg->ffn % 16 != 0)
+            return RIFT_ERR_UNSUPPORTED;
+    }
+    return RIFT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t rift_abi_version(void) { return RIFT_ABI_VERSION; }
+
+const char* rift_status_string(rift_status s) {
+    switch (s) {
+        case RIFT_OK: return "ok";
+        case RIFT_ERR_NULL: return "a required pointer is NULL";
+        case RIFT_ERR_SHAPE: return "a size breaks the shape rules of the call";
+        case RIFT_ERR_DTYPE: return "unknown or mismatched storage type";
+        case RIFT_ERR_BUDGET: return "budget, level or tier out of range";
+        case RIFT_ERR_WORKSPACE: return "workspace too small or not 256-byte aligned";
+        case RIFT_ERR_HIP: return "a HIP runtime call or kernel launch failed";
+        case RIFT_ERR_UNSUPPORTED: return "valid request outside what this build implements";
+    }
+    return "unknown status";
+}
+
+size_t rift_score_workspace_size(int32_t n_tiles, int32_t n_v, int32_t d) {
+    (void)n_tiles;
+    (void)n_v;
+    if (d <= 0) return 0;
+    return align_up((size_t)d * sizeof(float));
+}
+
+rift_status rift_score_tiles(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
+                             int32_t d, const void* query_bank, int32_t n_bg, int32_t keep_count,
+                             double tau, double* token_key, float* token_sim, double* tile_score,
+                             float* tile_u, int32_t* tile_order, int32_t* n_keep, void* workspace,
+                             size_t ws_bytes, rift_stream stream) {
+    if (tokens == nullptr || query_bank == nullptr || token_key == nullptr ||
+        tile_score == nullptr || tile_u == nullptr || tile_order == nullptr || n_keep == nullptr ||
+        workspace == nullptr)
+        return RIFT_ERR_NULL;
+    if (!dt_valid(dt)) return RIFT_ERR_DTYPE;
+    if (n_tiles < 1 || n_tiles > 4096 || n_v < 1 || n_v > 1024 || d < 32 || d > 16384 ||
+        d % 32 != 0 || n_bg < 0 || n_bg > 15 || keep_count < 0 || isnan(tau))
+        return RIFT_ERR_SHAPE;
+    if (misaligned(workspace) || ws_bytes < rift_score_workspace_size(n_tiles, n_v, d))
+        return RIFT_ERR_WORKSPACE;
+    if (init_kernel_attributes() != hipSuccess) return RIFT_ERR_HIP;
+    hipError_t e = launch_score(tokens, dt == RIFT_BF16, n_tiles, n_v, d, query_bank, n_bg,
+                                keep_count, tau, token_key, token_sim, tile_score, tile_u,
+                                tile_order, n_keep, static_cast<float*>(workspace),
+                                static_cast<hipStream_t>(stream));
+    return hip_status(e);
+}
+
+rift_status rift_assign_budgets(int32_t n_keep, int32_t n_v, const int32_t* levels,
+                                int32_t n_levels, const int32_t* tier_num, int32_t tier_den,
+                                int32_t* budgets, int64_t* total) {
+    static const int32_t kDefaultNum[3] = {1, 3, 4};
+    if (levels == nullptr || (n_keep > 0 && budgets == nullptr)) return RIFT_ERR_NULL;
+    if (n_keep < 0 || n_v < 1 || n_levels < 1 || n_levels > 64) return RIFT_ERR_SHAPE;
+    if (tier_num == nullptr) {
+        if (n_levels != 4) return RIFT_ERR_BUDGET;
+        tier_num = kDefaultNum;
+        tier_den = 16;
+    }
+    if (tier_den < 1) return RIFT_ERR_BUDGET;
+    int64_t num_sum = 0;
+    for (int j = 0; j < n_levels; ++j) {
+        if (levels[j] < 1 || levels[j] > n_v) return RIFT_ERR_BUDGET;
+        if (j > 0 && levels[j] >= levels[j - 1]) return RIFT_ERR_BUDGET;
+        if (j < n_levels - 1) {
+            if (tier_num[j] < 0) return RIFT_ERR_BUDGET;
+            num_sum += tier_num[j];
+        }
+    }
+    if (num_sum > tier_den) return RIFT_ERR_BUDGET;
+    int64_t rho = 0, sum = 0;
+    for (int j = 0; j < n_levels; ++j) {
+        int64_t cnt;
+        if (j < n_levels - 1) cnt = ((int64_t)n_keep * tier_num[j]) / tier_den;
+        else cnt = (int64_t)n_keep - rho;
+        for (int64_t c = 0; c < cnt; ++c) {
+            budgets[rho++] = levels[j];
+            sum += levels[j];
+        }
+    }
+    if (total != nullptr) *total = sum;
+    return RIFT_OK;
+}
+
+rift_status rift_select_tokens(const double* token_key, int32_t n_tiles, int32_t n_v,
+                               const int32_t* kept_tiles, const int32_t* budgets, int32_t n_keep,
+                               int32_t* sel_offsets, int32_t* sel_idx, int64_t sel_capacity,
+                               int32_t* status, rift_stream stream) {
+    if (sel_offsets == nullptr || status == nullptr) return RIFT_ERR_NULL;
+    if (n_keep > 0 && (token_key == nullptr || kept_tiles == nullptr || budgets == nullptr))
+        return RIFT_ERR_NULL;
+    if (sel_capacity > 0 && sel_idx == nullptr) return RIFT_ERR_NULL;
+    if (n_v < 1 || n_v > 1024 || n_tiles < 1 || n_tiles > 4096 || n_keep < 0 || n_keep > n_tiles ||
+        sel_capacity < 0)
+        return RIFT_ERR_SHAPE;
+    hipError_t e = launch_select(token_key, n_tiles, n_v, kept_tiles, budgets, n_keep, sel_offsets,
+                                 sel_idx, sel_capacity, status, static_cast<hipStream_t>(stream));
+    return hip_status(e);
+}
+
+rift_status rift_compact(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
+                         int32_t d, const int32_t* kept_tiles, const int32_t* sel_offsets,
+                         const int32_t* sel_idx, int32_t n_keep, const void* sys_emb,
+                         int32_t n_sys, const void* qry_emb, int32_t n_qry, void* packed,
+                         int64_t packed_rows, int32_t* cu_seqlens, int32_t* position_ids,
+                         int32_t* status, rift_stream stream) {
+    if (sel_offsets == nullptr || cu_seqlens == nullptr || status == nullptr) return RIFT_ERR_NULL;
+    if (n_keep > 0 && (tokens == nullptr || kept_tiles == nullptr)) return RIFT_ERR_NULL;
+    if (packed_rows > 0 && (packed == nullptr || position_ids == nullptr)) return RIFT_ERR_NULL;
+    if ((n_sys > 0 && sys_emb == nullptr) || (n_qry > 0 && qry_emb == nullptr)) return RIFT_ERR_NULL;
+    if (!dt_valid(dt)) return RIFT_ERR_DTYPE;
+    if (n_tiles < 1 || n_v < 1 || d < 1 || n_keep < 0 || n_sys < 0 || n_qry < 0 ||
+        packed_rows < 0 || ((size_t)d * dt_bytes(dt)) % 16 != 0 || packed_rows > (int64_t)INT32_MAX)
+        return RIFT_ERR_SHAPE;
+    hipError_t e = launch_compact(tokens, (int)dt_bytes(dt), n_tiles, n_v, d, kept_tiles,
+                                  sel_offsets, sel_idx, n_keep, sys_emb, n_sys, qry_emb, n_qry,
+                                  packed, packed_rows, cu_seqlens, position_ids, status,
+                                  static_cast<hipStream_t>(stream));
+    (void)sel_idx;
+    return hip_status(e);
+}
+
+size_t rift_prefill_workspace_size(const rift_model_cfg* cfg, int32_t total_tokens,
+                                   int32_t max_seqlen) {
+    if (check_cfg(cfg) != RIFT_OK || total_tokens < 0 || max_seqlen < 0) return 0;
+    return prefill_layout(*cfg, total_tokens, max_seqlen).total;
+}
+
+rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* layers,
+                         const void* x_in, rift_dtype x_dt, const int32_t* cu_seqlens,
+                         const int32_t* position_ids, int32_t n_seq, int32_t total_tokens,
+                         int32_t max_seqlen, float* hidden_out, void* kv_cache, void* workspace,
+                         size_t ws_bytes, rift_stream stream) {
+    rift_status cs = check_cfg(cfg);
+    if (cs != RIFT_OK) return cs;
+    const rift_model_cfg c = *cfg;
+    if (x_dt != c.dt && x_dt != RIFT_F32) return RIFT_ERR_DTYPE;
+    if (total_tokens < 0 || n_seq < 0 || max_seqlen < 1 || max_seqlen > 65536)
+        return RIFT_ERR_SHAPE;
+    if (c.dt == RIFT_BF16 && (uint64_t)total_tokens * (uint64_t)(c.d > c.ffn ? c.d : c.ffn) >=
+                                 (1ull << 32))
+        return RIFT_ERR_UNSUPPORTED;
+    if (total_tokens == 0) return RIFT_OK;
+    if (x_in == nullptr || cu_seqlens == nullptr || position_ids == nullptr ||
+        hidden_out == nullptr || workspace == nullptr || (c.n_layers > 0 && layers == nullptr))
+        return RIFT_ERR_NULL;
+    for (int l = 0; l < c.n_layers; ++l) {
+        const rift_layer_weights& w = layers[l];
+        if (!w.wq || !w.wk || !w.wv || !w.wo || !w.w_gate || !w.w_up || !w.w_down || !w.g_attn ||
+            !w.g_ffn)
+            return RIFT_ERR_NULL;
+    }
+    const PrefillLayout L = prefill_layout(c, total_tokens, max_seqlen);
+    if (misaligned(workspace) || ws_bytes < L.total) return RIFT_ERR_WORKSPACE;
+    if (init_kernel_attributes() != hipSuccess) return RIFT_ERR_HIP;
+
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    float2* rope = reinterpret_cast<float2*>(ws + L.rope);
+    const int T = total_tokens;
+    const int d = c.d;
+    const size_t td = (size_t)T * d;
+    const bool bf = c.dt == RIFT_BF16;
+    const size_t e = dt_bytes(c.dt);
+    hipError_t err = hipSuccess;
+#define RIFT_TRY(x)                        \
+    do {                                   \
+        err = (x);                         \
+        if (err != hipSuccess) return RIFT_ERR_HIP; \
+    } while (0)
+
+    if (c.n_layers == 0) {
+        if (x_dt == RIFT_F32) {
+            if (static_cast<const void*>(hidden_out) != x_in)
+                RIFT_TRY(launch_copy_f32(static_cast<const float*>(x_in), hidden_out, (long long)td, st));
+        } else {
+            RIFT_TRY(launch_to_f32(x_in, true, hidden_out, (long long)td, st));
+        }
+        return RIFT_OK;
+    }
+    RIFT_TRY(launch_rope_table(rope, max_seqlen, c.head_dim, c.rope_base, st));
+
+    for (int l = 0; l < c.n_layers; ++l) {
+        const rift_layer_weights& w = layers[l];
+        void* h = ws + L.h;
+        void* qb = ws + L.q;
+        void* kb = ws + L.k;
+        void* vb = ws + L.v;
+        if (kv_cache != nullptr) {
+            kb = static_cast<unsigned char*>(kv_cache) + (size_t)(2 * l) * td * e;
+            vb = static_cast<unsigned char*>(kv_cache) + (size_t)(2 * l + 1) * td * e;
+        }
+        // attention input norm; the first layer also lays down the f32 residual
+        if (l == 0) {
+            const bool in_bf16 = (x_dt == RIFT_BF16);
+            float* resid = (in_bf16 || static_cast<const void*>(hidden_out) != x_in) ? hidden_out : nullptr;
+            RIFT_TRY(launch_rmsnorm(x_in, in_bf16, resid, w.g_attn, bf, h, bf, T, d, c.rms_eps, st));
+        } else {
+            RIFT_TRY(launch_rmsnorm(hidden_out, false, nullptr, w.g_attn, bf, h, bf, T, d, c.rms_eps, st));
+        }
+        if (bf) {
+            QkvArgs qa{};
+            qa.a = static_cast<const uint16_t*>(h);
+            qa.wq = static_cast<const uint16_t*>(w.wq);
+            qa.wk = static_cast<const uint16_t*>(w.wk);
+            qa.wv = static_cast<const uint16_t*>(w.wv);
+            qa.q = static_cast<uint16_t*>(qb);
+            qa.k = static_cast<uint16_t*>(kb);
+            qa.v = static_cast<uint16_t*>(vb);
+            qa.rope = rope;
+            qa.pos = position_ids;
+            qa.n_pos = max_seqlen;
+            qa.M = T;
+            qa.d = d;
+            RIFT_TRY(launch_gemm_qkv_rope(qa, st));
+            // attention output reuses the h buffer (h is consumed by the QKV GEMM)
+            RIFT_TRY(launch_attention_bf16(static_cast<const uint16_t*>(qb), static_cast<const uint16_t*>(kb),
+                                           static_cast<const uint16_t*>(vb), static_cast<uint16_t*>(h),
+                                           cu_seqlens, n_seq, max_seqlen, c.n_heads, st));
+            RIFT_TRY(launch_gemm_resid(static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w.wo),
+                                       hidden_out, T, d, d, st));
+            RIFT_TRY(launch_rmsnorm(hidden_out, false, nullptr, w.g_ffn, true, h, true, T, d, c.rms_eps, st));
+            uint16_t* a = reinterpret_cast<uint16_t*>(ws + L.a);
+            RIFT_TRY(launch_gemm_swiglu(static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w.w_gate),
+                                        static_cast<const uint16_t*>(w.w_up), a, T, c.ffn, d, st));
+            RIFT_TRY(launch_gemm_resid(a, static_cast<const uint16_t*>(w.w_down), hidden_out, T, d, c.ffn, st));
+        } else {
+            float* hf = static_cast<float*>(h);
+            float* qf = static_cast<float*>(qb);
+            float* kf = static_cast<float*>(kb);
+            float* vf = static_cast<float*>(vb);
+            RIFT_TRY(launch_gemm_f32(hf, static_cast<const float*>(w.wq), qf, T, d, d, false, st));
+            RIFT_TRY(launch_gemm_f32(hf, static_cast<const float*>(w.wk), kf, T, d, d, false, st));
+            RIFT_TRY(launch_gemm_f32(hf, static_cast<const float*>(w.wv), vf, T, d, d, false, st));
+            RIFT_TRY(launch_rope_apply_f32(qf, rope, position_ids, max_seqlen, T, c.n_heads, c.head_dim, st));
+            RIFT_TRY(launch_rope_apply_f32(kf, rope, position_ids, max_seqlen, T, c.n_heads, c.head_dim, st));
+            RIFT_TRY(launch_attention_f32(qf, kf, vf, hf, cu_seqlens, n_seq, max_seqlen, c.n_heads,
+                                          c.head_dim, st));
+            RIFT_TRY(launch_gemm_f32(hf, static_cast<const float*>(w.wo), hidden_out, T, d, d, true, st));
+            RIFT_TRY(launch_rmsnorm(hidden_out, false, nullptr, w.g_ffn, false, hf, false, T, d, c.rms_eps, st));
+            float* gate = reinterpret_cast<float*>(ws + L.a);
+            float* up = reinterpret_cast<float*>(ws + L.gate2);
+            RIFT_TRY(launch_gemm_f32(hf, static_cast<const float*>(w.w_gate), gate, T, c.ffn, d, false, st));
+            RIFT_TRY(launch_gemm_f32(hf, static_cast<const float*>(w.w_up), up, T, c.ffn, d, false, st));
+            RIFT_TRY(launch_swiglu_f32(gate, up, gate, (long long)T * c.ffn, st));
+            RIFT_TRY(launch_gemm_f32(gate, static_cast<const float*>(w.w_down), hidden_out, T, d, c.ffn, true, st));
+        }
+    }
+#undef RIFT_TRY
+    return RIFT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,322 @@
+// bf16 GEMMs of the LLaMA decoder prefill on gfx950 MFMA, C = A B^T with A
+// [M][K] and B [N][K] both K-contiguous (activations and nn.Linear weights),
+// float32 accumulation, and the layer's elementwise work fused into the
+// epilogue:
+//   QKV   q|k|v = h [wq|wk|wv]^T, rotate-half RoPE on q and k, bf16 out
+//   RESID x += A B^T in float32 (attention output and FFN down projections)
+//   SWIGLU a = silu(h wg^T) * (h wu^T), bf16 out
+//
+// Tiling: a 256x256 output tile per workgroup of 4 waves (2x2), each wave a
+// 128x128 block of 4x4 v_mfma_f32_32x32x16_bf16 tiles (256 accumulator
+// registers).  K advances 64 at a time through two LDS stages of A and B tiles
+// (2 x 64 KB); the next stage's global loads are in flight while the current
+// stage feeds the MFMAs.  LDS rows are 128 bytes (64 bf16) split in 8 chunks
+// of 16 bytes; chunk c of row r is stored at position c ^ (r & 7), which keeps
+// the MFMA operand reads of 8 consecutive rows on distinct banks.
+//
+// Every output element is one fixed sequence of MFMA accumulations over K, no
+// matter which tile or batch row holds it, so a row's result does not depend on
+// what else is packed with it.
+//
+// Tile order: the hardware hands workgroup b to XCD b mod 8; each XCD gets a
+// contiguous range of tile ids, and tile ids walk 8 M-tiles per N-tile, so the
+// workgroups resident on one XCD share A and B panels in that XCD's L2.
+#include "launch.h"
+#include "rift_common.h"
+
+namespace rift {
+
+namespace {
+
+constexpr int BM = 256;
+constexpr int BN = 256;
+constexpr int BK = 64;
+constexpr int kGroupM = 8;
+constexpr int kTileElems = BM * BK;             // one operand tile (A or B), elements
+constexpr size_t kLdsBytes = 2 * 2 * kTileElems * sizeof(bf16_t);  // 128 KB
+
+enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+
+struct GemmParams {
+    const bf16_t* a;
+    const bf16_t* b0;
+    const bf16_t* b1;
+    const bf16_t* b2;
+    int M, N, K;
+    int d;            // QKV: width of each of q, k, v;  SWIGLU: ffn width
+    bf16_t* o0;
+    bf16_t* o1;
+    bf16_t* o2;
+    float* resid;
+    const float2* rope;
+    const int* pos;
+    int n_pos;
+};
+
+__device__ __forceinline__ void tile_coords(int bid, int num_m, int num_n, int& bm, int& bn) {
+    const int nt = num_m * num_n;
+    const int xcd = bid & 7;
+    const int slot = bid >> 3;
+    const int base = nt >> 3;
+    const int extra = nt & 7;
+    const int t = xcd * base + (xcd < extra ? xcd : extra) + slot;
+    const int group = t / (kGroupM * num_n);
+    const int first_m = group * kGroupM;
+    const int gm = (num_m - first_m) < kGroupM ? (num_m - first_m) : kGroupM;
+    const int in_group = t - group * kGroupM * num_n;
+    bm = first_m + in_group % gm;
+    bn = in_group / gm;
+}
+
+// B operand of tile bn: loader chunk j (0..7) covers tile rows (t>>3) + 32 j.
+// b_base gives the matrix that chunk j reads and b_row the row inside it.
+//   QKV:    one of wq | wk | wv per tile (d % 256 == 0), rows bn*256 + r - region*d
+//   SWIGLU: tile rows [0,64) gate, [64,128) up for output columns bn*128 + [0,64),
+//           rows [128,192) gate, [192,256) up for columns bn*128 + [64,128);
+//           with r = (t>>3) + 32 j that is gate for j in {0,1,4,5}, up otherwise
+//   RESID:  rows bn*256 + r
+template <int EPI>
+__device__ __forceinline__ const bf16_t* b_base(const GemmParams& p, int bn, int j) {
+    if constexpr (EPI == EPI_QKV) {
+        const int region = (bn * BN) / p.d;
+        return region == 0 ? p.b0 : (region == 1 ? p.b1 : p.b2);
+    } else if constexpr (EPI == EPI_SWIGLU) {
+        return ((j & 3) < 2) ? p.b0 : p.b1;
+    } else {
+        return p.b0;
+    }
+}
+
+template <int EPI>
+__device__ __forceinline__ int b_row(const GemmParams& p, int bn, int r) {
+    if constexpr (EPI == EPI_QKV) {
+        const int region = (bn * BN) / p.d;
+        return bn * BN + r - region * p.d;
+    } else if constexpr (EPI == EPI_SWIGLU) {
+        return bn * 128 + (r >> 7) * 64 + (r & 63);
+    } else {
+        return bn * BN + r;
+    }
+}
+
+template <int EPI>
+__global__ void __launch_bounds__(256, 1) gemm_bf16_kernel(GemmParams p) {
+    extern __shared__ __align__(16) bf16_t lds[];
+    const int num_m = (p.M + BM - 1) / BM;
+    const int num_n = (EPI == EPI_SWIGLU) ? p.d / 128 : p.N / BN;
+    int bm, bn;
+    tile_coords(blockIdx.x, num_m, num_n, bm, bn);
+    const int m0 = bm * BM;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave >> 1;
+    const int wn = wave & 1;
+
+    // Loader: thread t moves chunks t + 256 j (j = 0..7) of each operand tile;
+    // chunk id -> row = (t >> 3) + 32 j, logical chunk = t & 7.  Offsets are
+    // 32-bit element offsets from the operand base (every operand is < 4 GB).
+    const int ld_row = tid >> 3;
+    const int ld_lc = tid & 7;
+    uint32_t a_off[8], b_off[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int row = ld_row + 32 * j;
+        int ar = m0 + row;
+        ar = ar < p.M ? ar : p.M - 1;
+        a_off[j] = (uint32_t)ar * (uint32_t)p.K + ld_lc * 8;
+        b_off[j] = (uint32_t)b_row<EPI>(p, bn, row) * (uint32_t)p.K + ld_lc * 8;
+    }
+    // LDS position of this thread's chunk in row ld_row; rows + 32 j keep the
+    // same swizzle (32 j is a multiple of 8), so chunk j sits 32*64*j further.
+    const int lds_w = ld_row * BK + ((ld_lc ^ (ld_row & 7)) << 3);
+
+    f32x16_t acc[4][4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int n = 0; n < 4; ++n)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[m][n][i] = 0.f;
+
+    u32x4_t ra[8], rb[8];
+    const int nk = p.K / BK;
+
+    // prologue: stage 0
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        ra[j] = *reinterpret_cast<const u32x4_t*>(p.a + a_off[j]);
+        rb[j] = *reinterpret_cast<const u32x4_t*>(b_base<EPI>(p, bn, j) + b_off[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        *reinterpret_cast<u32x4_t*>(lds + lds_w + j * 32 * BK) = ra[j];
+        *reinterpret_cast<u32x4_t*>(lds + kTileElems + lds_w + j * 32 * BK) = rb[j];
+    }
+    __syncthreads();
+
+    // Operand reads: row wm*128 + m*32 + (lane & 31) has swizzle key lane & 7,
+    // so only the k sub-step changes the offset; m and n add 32*64 per step.
+    const int rd_a = (wm * 128 + (lane & 31)) * BK;
+    const int rd_b = (wn * 128 + (lane & 31)) * BK;
+    const int hsel = lane >> 5;
+    const int key = lane & 7;
+
+    for (int kt = 0; kt < nk; ++kt) {
+        const int cur = kt & 1;
+        const bool more = kt + 1 < nk;
+        if (more) {
+            const uint32_t koff = (uint32_t)(kt + 1) * BK;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                ra[j] = *reinterpret_cast<const u32x4_t*>(p.a + (a_off[j] + koff));
+                rb[j] = *reinterpret_cast<const u32x4_t*>(b_base<EPI>(p, bn, j) + (b_off[j] + koff));
+            }
+        }
+        const bf16_t* sA = lds + cur * 2 * kTileElems;
+        const bf16_t* sB = sA + kTileElems;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            const int sw = ((2 * kk + hsel) ^ key) << 3;
+            bf16x8_t af[4], bf[4];
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+                af[m] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + m * 32 * BK);
+#pragma unroll
+            for (int n = 0; n < 4; ++n)
+                bf[n] = *reinterpret_cast<const bf16x8_t*>(sB + rd_b + sw + n * 32 * BK);
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+#pragma unroll
+                for (int n = 0; n < 4; ++n)
+                    acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[m], bf[n], acc[m][n], 0, 0, 0);
+        }
+        if (more) {
+            bf16_t* dA = lds + (cur ^ 1) * 2 * kTileElems;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                *reinterpret_cast<u32x4_t*>(dA + lds_w + j * 32 * BK) = ra[j];
+                *reinterpret_cast<u32x4_t*>(dA + kTileElems + lds_w + j * 32 * BK) = rb[j];
+            }
+        }
+        __syncthreads();
+    }
+
+    // Epilogue.  acc[m][n][i] is row 8 (i/4) + 4 (lane/32) + (i%4) and column
+    // lane%32 of the 32x32 tile (m, n) of this wave.
+    const int col_in = lane & 31;
+    const int row_hi = 4 * (lane >> 5);
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            __builtin_amdgcn_sched_barrier(0);
+            const int row = m0 + wm * 128 + m * 32 + 8 * (i >> 2) + row_hi + (i & 3);
+            if (row >= p.M) continue;
+            if constexpr (EPI == EPI_RESID) {
+                float* dst = p.resid + (size_t)row * p.N + bn * BN + wn * 128 + col_in;
+#pragma unroll
+                for (int n = 0; n < 4; ++n) dst[n * 32] += acc[m][n][i];
+            } else if constexpr (EPI == EPI_SWIGLU) {
+                bf16_t* dst = p.o0 + (size_t)row * p.d + bn * 128 + wn * 64 + col_in;
+#pragma unroll
+                for (int n = 0; n < 2; ++n) {
+                    const float gt = acc[m][n][i];
+                    const float up = acc[m][n + 2][i];
+                    const float a = gt / (1.0f + expf(-gt)) * up;
+                    dst[n * 32] = f32_to_bf16(a);
+                }
+            } else {  // QKV
+                const int region = (bn * BN) / p.d;
+                const int head_col = (bn * BN - region * p.d) + wn * 128;  // first column of the head
+                bf16_t* out = (region == 0 ? p.o0 : (region == 1 ? p.o1 : p.o2)) +
+                              (size_t)row * p.d + head_col + col_in;
+                if (region == 2) {
+#pragma unroll
+                    for (int n = 0; n < 4; ++n) out[n * 32] = f32_to_bf16(acc[m][n][i]);
+                } else {
+                    int ps = p.pos[row];
+                    ps = ps < 0 ? 0 : (ps >= p.n_pos ? p.n_pos - 1 : ps);
+#pragma unroll
+                    for (int n = 0; n < 2; ++n) {
+                        const float2 cs = p.rope[(size_t)ps * 64 + n * 32 + col_in];
+                        const float x1 = acc[m][n][i];
+                        const float x2 = acc[m][n + 2][i];
+                        out[n * 32] = f32_to_bf16(x1 * cs.x - x2 * cs.y);
+                        out[n * 32 + 64] = f32_to_bf16(x2 * cs.x + x1 * cs.y);
+                    }
+                }
+            }
+        }
+    }
+}
+
+template <int EPI>
+hipError_t launch_gemm(const GemmParams& p, int num_n, hipStream_t st) {
+    const int num_m = (p.M + BM - 1) / BM;
+    if (p.M <= 0) return hipSuccess;
+    hipLaunchKernelGGL(gemm_bf16_kernel<EPI>, dim3(num_m * num_n), dim3(256), kLdsBytes, st, p);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t gemm_bf16_init_attributes() {
+    hipError_t e;
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<EPI_QKV>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
+    if (e != hipSuccess) return e;
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<EPI_RESID>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
+    if (e != hipSuccess) return e;
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<EPI_SWIGLU>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
+}
+
+hipError_t launch_gemm_qkv_rope(const QkvArgs& a, hipStream_t st) {
+    GemmParams p{};
+    p.a = a.a;
+    p.b0 = a.wq;
+    p.b1 = a.wk;
+    p.b2 = a.wv;
+    p.M = a.M;
+    p.N = 3 * a.d;
+    p.K = a.d;
+    p.d = a.d;
+    p.o0 = a.q;
+    p.o1 = a.k;
+    p.o2 = a.v;
+    p.rope = a.rope;
+    p.pos = a.pos;
+    p.n_pos = a.n_pos;
+    return launch_gemm<EPI_QKV>(p, p.N / BN, st);
+}
+
+hipError_t launch_gemm_resid(const uint16_t* a, const uint16_t* b, float* resid, int M, int N,
+                             int K, hipStream_t st) {
+    GemmParams p{};
+    p.a = a;
+    p.b0 = b;
+    p.M = M;
+    p.N = N;
+    p.K = K;
+    p.resid = resid;
+    return launch_gemm<EPI_RESID>(p, N / BN, st);
+}
+
+hipError_t launch_gemm_swiglu(const uint16_t* a, const uint16_t* wg, const uint16_t* wu,
+                              uint16_t* out, int M, int F, int K, hipStream_t st) {
+    GemmParams p{};
+    p.a = a;
+    p.b0 = wg;
+    p.b1 = wu;
+    p.M = M;
+    p.N = 2 * F;
+    p.K = K;
+    p.d = F;
+    p.o0 = out;
+    return launch_gemm<EPI_SWIGLU>(p, F / 128, st);
+}
+
+}  // namespace rift

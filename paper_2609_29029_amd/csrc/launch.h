@@ -1,0 +1,85 @@
+// Internal launchers of the Rift kernels (host side).  The C ABI in capi.hip
+// validates arguments and calls these; every launcher only enqueues work.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace rift {
+
+hipError_t launch_score(const void* tokens, bool bf16, int n_tiles, int n_v, int d,
+                        const void* qbank, int n_bg, int keep_count, double tau, double* token_key,
+                        float* token_sim, double* tile_score, float* tile_u, int* tile_order,
+                        int* n_keep, float* w32, hipStream_t st);
+
+hipError_t launch_select(const double* token_key, int n_tiles, int n_v, const int* kept,
+                         const int* budgets, int n_keep, int* sel_offsets, int* sel_idx,
+                         long long cap, int* status, hipStream_t st);
+
+hipError_t launch_compact(const void* tokens, int elem_bytes, int n_tiles, int n_v, int d,
+                          const int* kept, const int* offs, const int* sel, int n_keep,
+                          const void* sys, int n_sys, const void* qry, int n_qry, void* packed,
+                          long long cap, int* cu, int* pos_ids, int* status, hipStream_t st);
+
+// ---------------------------------------------------------------- prefill pieces
+// RoPE table: tab[p * (hd/2) + j] = (cos, sin)(p * base^(-2j/hd)), p < n_pos.
+hipError_t launch_rope_table(float2* tab, int n_pos, int hd, float base, hipStream_t st);
+
+// h = RMSNorm(x) * g, one row per wave.  x is f32 (x_bf16 == false) or bf16;
+// when resid != nullptr the f32 value of x is also stored there.  h is bf16
+// (h_bf16) or f32.
+hipError_t launch_rmsnorm(const void* x, bool x_bf16, float* resid, const void* g, bool g_bf16,
+                          void* h, bool h_bf16, int rows, int d, float eps, hipStream_t st);
+
+// bf16 MFMA GEMMs, C = A B^T (A [M][K], B rows [N][K], K contiguous).
+struct QkvArgs {
+    const uint16_t* a;  // h [M][d]
+    const uint16_t* wq;
+    const uint16_t* wk;
+    const uint16_t* wv;
+    uint16_t* q;  // [M][d]
+    uint16_t* k;
+    uint16_t* v;
+    const float2* rope;  // [n_pos][hd/2]
+    const int* pos;      // [M]
+    int n_pos;
+    int M, d;
+};
+hipError_t launch_gemm_qkv_rope(const QkvArgs& a, hipStream_t st);
+
+// resid[M][N] += A[M][K] B[N][K]^T  (attention output and FFN down projections)
+hipError_t launch_gemm_resid(const uint16_t* a, const uint16_t* b, float* resid, int M, int N,
+                             int K, hipStream_t st);
+
+// out[M][F] = silu(A Wg^T) * (A Wu^T), A [M][K], Wg, Wu [F][K]
+hipError_t launch_gemm_swiglu(const uint16_t* a, const uint16_t* wg, const uint16_t* wu,
+                              uint16_t* out, int M, int F, int K, hipStream_t st);
+
+// Varlen causal attention, bf16, head_dim 128.  q, k, v, o: [T][H*128].
+hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
+                                 uint16_t* o, const int* cu, int n_seq, int max_seqlen,
+                                 int n_heads, hipStream_t st);
+
+// ---------------------------------------------------------------- f32 path
+// C[M][N] = A[M][K] B[N][K]^T (+ C when accumulate)
+hipError_t launch_gemm_f32(const float* a, const float* b, float* c, int M, int N, int K,
+                           bool accumulate, hipStream_t st);
+// in-place rotate-half RoPE on x [M][H*hd] (f32)
+hipError_t launch_rope_apply_f32(float* x, const float2* rope, const int* pos, int n_pos, int M,
+                                 int n_heads, int hd, hipStream_t st);
+// a[M][F] = silu(g) * u  (f32, separate gate/up buffers; a may alias g)
+hipError_t launch_swiglu_f32(const float* g, const float* u, float* a, long long n,
+                             hipStream_t st);
+hipError_t launch_attention_f32(const float* q, const float* k, const float* v, float* o,
+                                const int* cu, int n_seq, int max_seqlen, int n_heads, int hd,
+                                hipStream_t st);
+// elementwise widening copy of a [rows][d] matrix into f32
+hipError_t launch_to_f32(const void* x, bool x_bf16, float* out, long long n, hipStream_t st);
+// copy f32 -> storage type (for KV-cache output of the f32 path / bf16 keys)
+hipError_t launch_copy_f32(const float* x, float* out, long long n, hipStream_t st);
+
+// kernels that need more than the default dynamic LDS are registered here
+hipError_t init_kernel_attributes();
+
+}  // namespace rift

@@ -1,0 +1,133 @@
+"""One Rift scene-query on the GPU: score -> budgets -> select -> compact ->
+prefill, enqueued on one stream through the C ABI.  Buffers are allocated once
+per plan (PyTorch as the allocator) and reused across queries.
+
+In keep-top-K mode the number of kept tiles, the budgets and the packed length
+are known on the host before the query runs, so the whole query is enqueued
+without a device-to-host copy.  Threshold mode (keep_count == 0) reads n_keep
+back once after scoring.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+from . import _lib as R
+
+
+@dataclass
+class PrefillShape:
+    d: int
+    n_heads: int
+    head_dim: int
+    ffn: int
+    n_layers: int
+    rms_eps: float = 1e-6
+    rope_base: float = 10000.0
+
+
+class SceneQuery:
+    """Device buffers and launch sequence of one scene-query shape.
+
+    tokens [n_tiles][n_v][d], qbank [1+M][d], sys [n_sys][d], qry [n_qry][d] and
+    every layer weight are device tensors of one storage dtype (bf16 or f32)."""
+
+    def __init__(self, tokens, qbank, sys_emb, qry_emb, layers: Sequence[dict],
+                 shape: PrefillShape, keep_count: int, tau: float, levels: Sequence[int],
+                 tier_num: Optional[Sequence[int]], tier_den: int, with_sims: bool = True,
+                 stream=None):
+        import torch
+        self.torch = torch
+        self.dev = tokens.device
+        self.tokens, self.qbank, self.sys, self.qry = tokens, qbank, sys_emb, qry_emb
+        self.layers = list(layers)
+        self.shape = shape
+        self.keep_count, self.tau = int(keep_count), float(tau)
+        self.levels, self.tier_num, self.tier_den = list(levels), tier_num, int(tier_den)
+        self.stream = stream
+        n_tiles, n_v, d = tokens.shape
+        self.n_tiles, self.n_v, self.d = n_tiles, n_v, d
+        nq = qbank.shape[0]
+        dev = self.dev
+        f64, f32, i32 = torch.float64, torch.float32, torch.int32
+        self.token_key = torch.empty(n_tiles * n_v, dtype=f64, device=dev)
+        self.token_sim = torch.empty(n_tiles * n_v, nq, dtype=f32, device=dev) if with_sims else None
+        self.tile_score = torch.empty(n_tiles, dtype=f64, device=dev)
+        self.tile_u = torch.empty(n_tiles, dtype=f32, device=dev)
+        self.tile_order = torch.empty(n_tiles, dtype=i32, device=dev)
+        self.n_keep_dev = torch.empty(1, dtype=i32, device=dev)
+        self.score_ws = torch.empty(max(256, R.rift_score_workspace_size(n_tiles, n_v, d)),
+                                    dtype=torch.uint8, device=dev)
+        self.sel_status = torch.empty(1, dtype=i32, device=dev)
+        self.cmp_status = torch.empty(1, dtype=i32, device=dev)
+        self.cfg = R.model_cfg(shape.d, shape.n_heads, shape.head_dim, shape.ffn, shape.n_layers,
+                               shape.rms_eps, shape.rope_base,
+                               R.RIFT_BF16 if tokens.dtype == torch.bfloat16 else R.RIFT_F32)
+        self._planned_keep = None
+        if self.keep_count > 0:
+            self._plan(min(self.keep_count, n_tiles))
+
+    # host-side plan for a given number of kept tiles
+    def _plan(self, n_keep: int) -> None:
+        torch = self.torch
+        if self._planned_keep == n_keep:
+            return
+        budgets, total = R.rift_assign_budgets(n_keep, self.n_v, self.levels, self.tier_num,
+                                               self.tier_den)
+        self.n_keep = n_keep
+        self.budgets_host = budgets
+        self.n_selected = total
+        fixed = self.sys.shape[0] + self.qry.shape[0]
+        self.total_tokens = n_keep * fixed + total
+        self.max_seqlen = fixed + (int(budgets.max()) if n_keep > 0 else 0)
+        dev = self.dev
+        self.budgets = torch.from_numpy(budgets).to(dev) if n_keep > 0 else \
+            torch.zeros(1, dtype=torch.int32, device=dev)
+        self.sel_offsets = torch.empty(n_keep + 1, dtype=torch.int32, device=dev)
+        self.sel_idx = torch.empty(max(1, total), dtype=torch.int32, device=dev)
+        T = self.total_tokens
+        self.packed = torch.empty(T, self.d, dtype=self.tokens.dtype, device=dev)
+        self.cu_seqlens = torch.empty(n_keep + 1, dtype=torch.int32, device=dev)
+        self.position_ids = torch.empty(T, dtype=torch.int32, device=dev)
+        self.hidden = torch.empty(T, self.d, dtype=torch.float32, device=dev)
+        ws = R.rift_prefill_workspace_size(self.cfg, T, max(1, self.max_seqlen))
+        self.prefill_ws = torch.empty(max(256, ws), dtype=torch.uint8, device=dev)
+        self._planned_keep = n_keep
+
+    def score(self) -> None:
+        R.rift_score_tiles(self.tokens, self.qbank, self.keep_count, self.tau, self.token_key,
+                           self.token_sim, self.tile_score, self.tile_u, self.tile_order,
+                           self.n_keep_dev, self.score_ws, self.stream)
+
+    def select(self) -> None:
+        R.rift_select_tokens(self.token_key, self.n_tiles, self.n_v, self.tile_order, self.budgets,
+                             self.n_keep, self.sel_offsets, self.sel_idx, self.sel_status,
+                             self.stream)
+
+    def compact(self) -> None:
+        R.rift_compact(self.tokens, self.tile_order, self.sel_offsets, self.sel_idx, self.n_keep,
+                       self.sys, self.qry, self.packed, self.cu_seqlens, self.position_ids,
+                       self.cmp_status, self.stream)
+
+    def prefill(self) -> None:
+        if self.total_tokens == 0:
+            return
+        R.rift_prefill(self.cfg, self.layers, self.packed, self.cu_seqlens, self.position_ids,
+                       self.n_keep, max(1, self.max_seqlen), self.hidden, self.prefill_ws,
+                       stream=self.stream)
+
+    def run(self) -> None:
+        """Enqueue the whole scene-query.  Threshold mode synchronises once to
+        read the number of kept tiles."""
+        self.score()
+        if self.keep_count == 0:
+            self.torch.cuda.current_stream().synchronize() if self.stream is None else \
+                self.stream.synchronize()
+            self._plan(int(self.n_keep_dev.item()))
+        self.select()
+        self.compact()
+        self.prefill()
+
+    def check_status(self) -> List[int]:
+        """Device status words of select and compact (synchronises)."""
+        return [int(self.sel_status.item()), int(self.cmp_status.item())]

@@ -1,0 +1,146 @@
+"""The C-ABI library on the CPU: it loads, exports every symbol include/rift.h
+declares, and its host-side logic (argument validation, budget assignment,
+workspace sizes) behaves as documented.  No kernel is launched here: every
+call below returns before any HIP call."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import rift_oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def R():
+    import paper_2609_29029_amd as R
+    if not R.lib_available():
+        from paper_2609_29029_amd.build import build
+        build()
+    R.load()
+    return R
+
+
+def declared_symbols():
+    with open(os.path.join(ROOT, "include", "rift.h")) as f:
+        text = f.read()
+    return re.findall(r"RIFT_API\s+[\w\s\*]+?\b(rift_\w+)\s*\(", text)
+
+
+def test_library_exports_every_declared_symbol(R):
+    L = R.load()
+    names = declared_symbols()
+    assert len(names) == 9
+    assert tuple(names) == R.EXPORTS
+    for n in names:
+        assert hasattr(L, n), n
+    assert L.rift_abi_version() == 1
+    assert L.rift_status_string(4).decode().startswith("budget")
+
+
+def test_only_abi_symbols_are_exported(R):
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", R.LIB_PATH], capture_output=True, text=True).stdout
+    text_syms = [ln.split()[-1] for ln in out.splitlines() if " T " in ln]
+    assert sorted(s for s in text_syms if s.startswith("rift_")) == sorted(R.EXPORTS)
+
+
+@pytest.mark.parametrize("K", [0, 1, 2, 7, 16, 31, 100, 400])
+def test_assign_budgets_matches_oracle(R, K):
+    lv, num, den = (576, 288, 144, 64), (1, 3, 4), 16
+    got, tot = R.rift_assign_budgets(K, 576, lv, num, den)
+    ref = O.assign_budgets(K, lv, num, den)
+    assert np.array_equal(got, ref) and tot == int(ref.sum())
+    got2, _ = R.rift_assign_budgets(K, 576, lv, None, 16)   # library default tiers
+    assert np.array_equal(got2, ref)
+
+
+def test_assign_budgets_rejects_bad_tables(R):
+    from paper_2609_29029_amd import RiftError
+    bad = [
+        dict(levels=[576, 576], tier_num=[1], tier_den=2),       # not strictly descending
+        dict(levels=[700, 64], tier_num=[1], tier_den=2),        # above n_v
+        dict(levels=[576, 0], tier_num=[1], tier_den=2),         # below 1
+        dict(levels=[576, 64], tier_num=[3], tier_den=2),        # fractions above 1
+        dict(levels=[576, 64], tier_num=[-1], tier_den=2),
+        dict(levels=[576, 64], tier_num=None, tier_den=16),      # default needs 4 levels
+        dict(levels=[576, 64], tier_num=[1], tier_den=0),
+    ]
+    for b in bad:
+        with pytest.raises(RiftError) as e:
+            R.rift_assign_budgets(8, 576, b["levels"], b["tier_num"], b["tier_den"])
+        assert e.value.status == 4
+    with pytest.raises(RiftError):
+        R.rift_assign_budgets(-1, 576, [64], [], 16)
+
+
+FAKE = 0x1000  # a non-NULL value; never dereferenced (validation fails first)
+
+
+def test_score_validation(R):
+    L = R.load()
+    args = dict(tokens=FAKE, dt=1, n_tiles=4, n_v=576, d=256, qb=FAKE, n_bg=15, keep=2, tau=0.37,
+                key=FAKE, sim=None, s=FAKE, u=FAKE, order=FAKE, nk=FAKE, ws=0x10000, wsb=1 << 20)
+
+    def call(**over):
+        a = dict(args, **over)
+        return L.rift_score_tiles(a["tokens"], a["dt"], a["n_tiles"], a["n_v"], a["d"], a["qb"], a["n_bg"],
+                                  a["keep"], a["tau"], a["key"], a["sim"], a["s"], a["u"], a["order"],
+                                  a["nk"], a["ws"], a["wsb"], None)
+    assert call(tokens=None) == 1
+    assert call(key=None) == 1
+    assert call(ws=None) == 1
+    assert call(dt=7) == 3
+    for bad in (dict(n_tiles=0), dict(n_tiles=4097), dict(n_v=0), dict(n_v=1025), dict(d=48),
+                dict(d=16416), dict(n_bg=16), dict(n_bg=-1), dict(keep=-1), dict(tau=float("nan"))):
+        assert call(**bad) == 2, bad
+    assert call(ws=0x10010) == 5              # misaligned workspace
+    assert call(wsb=16) == 5                  # too small
+    assert R.rift_score_workspace_size(4, 576, 4096) >= 4096 * 4
+
+
+def test_select_and_compact_validation(R):
+    L = R.load()
+    # select: NULL outputs, shapes
+    assert L.rift_select_tokens(FAKE, 4, 576, FAKE, FAKE, 2, None, FAKE, 10, FAKE, None) == 1
+    assert L.rift_select_tokens(FAKE, 4, 576, FAKE, FAKE, 2, FAKE, FAKE, 10, None, None) == 1
+    assert L.rift_select_tokens(None, 4, 576, FAKE, FAKE, 2, FAKE, FAKE, 10, FAKE, None) == 1
+    assert L.rift_select_tokens(FAKE, 4, 1025, FAKE, FAKE, 2, FAKE, FAKE, 10, FAKE, None) == 2
+    assert L.rift_select_tokens(FAKE, 4, 576, FAKE, FAKE, 5, FAKE, FAKE, 10, FAKE, None) == 2
+    assert L.rift_select_tokens(FAKE, 4, 576, FAKE, FAKE, 2, FAKE, None, 10, FAKE, None) == 1
+    # compact
+    c = L.rift_compact
+    assert c(FAKE, 1, 4, 576, 4096, FAKE, None, FAKE, 2, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 1
+    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, 2, None, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 1
+    assert c(FAKE, 9, 4, 576, 4096, FAKE, FAKE, FAKE, 2, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 3
+    assert c(FAKE, 1, 4, 576, 4, FAKE, FAKE, FAKE, 2, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 2
+    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, -1, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 2
+
+
+def test_prefill_validation_and_workspace(R):
+    L = R.load()
+    cfg = R.model_cfg(4096, 32, 128, 11008, 1, 1e-6, 10000.0, R.RIFT_BF16)
+    ws = R.rift_prefill_workspace_size(cfg, 22204, 643)
+    # rope table + h, q, k, v [T][d] + a [T][ffn], bf16
+    expect = 643 * 64 * 8 + 4 * 22204 * 4096 * 2 + 22204 * 11008 * 2
+    assert expect <= ws <= expect + 8 * 256
+    lw = (R.LayerWeights * 1)(R.LayerWeights(*([FAKE] * 9)))
+
+    def call(c, T=10, n_seq=1, max_len=10, x=FAKE, x_dt=1, wsb=1 << 40):
+        return L.rift_prefill(ctypes.byref(c), lw, x, x_dt, FAKE, FAKE, n_seq, T, max_len, FAKE, None,
+                              0x10000, wsb, None)
+    assert call(cfg, T=0) == 0                              # nothing to do
+    assert call(cfg, x=None) == 1
+    assert call(cfg, x_dt=5) == 3
+    assert call(cfg, max_len=0) == 2 and call(cfg, n_seq=-1) == 2
+    assert call(cfg, wsb=100) == 5
+    for bad in (R.model_cfg(4096, 64, 64, 11008, 1, 1e-6, 1e4, R.RIFT_BF16),    # bf16 needs head_dim 128
+                R.model_cfg(4160, 32, 130, 11008, 1, 1e-6, 1e4, R.RIFT_BF16),
+                R.model_cfg(256, 4, 64, 690, 1, 1e-6, 1e4, R.RIFT_F32)):        # ffn % 16
+        assert call(bad) == 7
+    assert call(R.model_cfg(4096, 31, 128, 11008, 1, 1e-6, 1e4, R.RIFT_BF16)) == 2
+    assert call(R.model_cfg(4096, 32, 128, 11008, 1, 1e-6, 1e4, 9)) == 3
+    assert R.rift_prefill_workspace_size(R.model_cfg(4096, 64, 64, 11008, 1, 1e-6, 1e4, R.RIFT_BF16), 10, 10) == 0

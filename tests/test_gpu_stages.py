@@ -1,0 +1,223 @@
+"""GPU parity of Stage 1 (score), Stage 2 (select) and compaction against the
+CPU oracle on the same seeded inputs.  Ranks, keys, token indices and packed
+buffers are compared bit for bit; normalised scores and cosines within 1e-3."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import rift_oracle as O
+from tests.rift_testlib import f64, oracle_stage1, torch_mod, upload, download_stored
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def R():
+    import paper_2609_29029_amd as R
+    torch = torch_mod()
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    R.load()
+    return R
+
+
+def run_score(R, tokens, qbank, keep_count, tau, sims=True):
+    torch = torch_mod()
+    n_tiles, n_v, d = tokens.shape
+    nq = qbank.shape[0]
+    out = dict(
+        token_key=torch.full((n_tiles * n_v,), float("nan"), dtype=torch.float64, device="cuda"),
+        token_sim=torch.full((n_tiles * n_v, nq), float("nan"), dtype=torch.float32, device="cuda") if sims else None,
+        tile_score=torch.empty(n_tiles, dtype=torch.float64, device="cuda"),
+        tile_u=torch.empty(n_tiles, dtype=torch.float32, device="cuda"),
+        tile_order=torch.empty(n_tiles, dtype=torch.int32, device="cuda"),
+        n_keep=torch.empty(1, dtype=torch.int32, device="cuda"))
+    ws = torch.empty(max(256, R.rift_score_workspace_size(n_tiles, n_v, d)), dtype=torch.uint8, device="cuda")
+    R.rift_score_tiles(tokens, qbank, keep_count, tau, out["token_key"], out["token_sim"],
+                       out["tile_score"], out["tile_u"], out["tile_order"], out["n_keep"], ws)
+    torch.cuda.synchronize()
+    return {k: (None if v is None else v.cpu().numpy()) for k, v in out.items()}
+
+
+def check_stage1(got, ref, X64, Q64, sims=True):
+    n_tiles, n_v = ref["r"].shape
+    key = got["token_key"].reshape(n_tiles, n_v)
+    assert np.array_equal(key, ref["r"]), f"keys differ: max |d| = {np.abs(key - ref['r']).max()}"
+    assert not np.any(np.signbit(key) & (key == 0))
+    assert np.array_equal(got["tile_score"], ref["s"])
+    assert list(got["tile_order"]) == list(ref["order"])
+    assert int(got["n_keep"][0]) == ref["n_keep"]
+    assert np.abs(got["tile_u"].astype(np.float64) - ref["u"]).max() <= 1e-3
+    assert np.array_equal(got["tile_u"], ref["u"].astype(np.float32))
+    if sims:
+        sim_ref = O.token_sims(X64.reshape(n_tiles * n_v, -1), Q64)
+        err = np.abs(got["token_sim"].astype(np.float64) - sim_ref).max()
+        assert err <= 1e-3, err
+
+
+@pytest.mark.parametrize("name", ["tiny", "one_tile", "scene8"])
+def test_score_parity(R, name):
+    w = synth.get(name)
+    sc = synth.make_scene(w)
+    got = run_score(R, upload(sc.tokens, w.dtype), upload(sc.qbank, w.dtype), w.keep_count, w.tau)
+    ref = oracle_stage1(sc, w.keep_count, w.tau)
+    check_stage1(got, ref, f64(sc.tokens, w.dtype), f64(sc.qbank, w.dtype))
+    if len(sc.planted):
+        # the planted query-aligned tiles rank at the top (sanity, not parity)
+        top = set(ref["order"][: len(sc.planted)])
+        assert top == set(int(t) for t in sc.planted)
+
+
+def test_score_threshold_mode(R):
+    w = synth.get("scene8")
+    sc = synth.make_scene(w)
+    got = run_score(R, upload(sc.tokens, w.dtype), upload(sc.qbank, w.dtype), 0, 0.37)
+    ref = oracle_stage1(sc, 0, 0.37)
+    check_stage1(got, ref, f64(sc.tokens, w.dtype), f64(sc.qbank, w.dtype))
+    assert ref["n_keep"] >= 1  # the top tile always has u = 1
+    got = run_score(R, upload(sc.tokens, w.dtype), upload(sc.qbank, w.dtype), 0, 1.5, sims=False)
+    assert int(got["n_keep"][0]) == 0
+
+
+@pytest.mark.parametrize("dtype,n_tiles,n_v,d,n_bg", [
+    ("f32", 3, 100, 64, 0),      # ragged token count, no background phrases
+    ("bf16", 5, 37, 512, 15),    # fewer tokens than one wave, ragged 16-blocks
+    ("bf16", 2, 1024, 256, 3),   # maximum tokens per tile
+    ("bf16", 9, 70, 96, 1),      # d not a multiple of 64
+])
+def test_score_edge_shapes(R, dtype, n_tiles, n_v, d, n_bg):
+    rng = np.random.default_rng(n_tiles * 1000 + n_v)
+    x32 = rng.standard_normal((n_tiles, n_v, d)).astype(np.float32)
+    x32[0, 3] = 0.0                       # an all-zero token scores +0
+    q = rng.standard_normal((1 + n_bg, d))
+    q = (q / np.linalg.norm(q, axis=1, keepdims=True)).astype(np.float32)
+    X, Q = synth.store(x32, dtype), synth.store(q, dtype)
+    got = run_score(R, upload(X, dtype), upload(Q, dtype), 2, 0.37)
+    X64, Q64 = f64(X, dtype), f64(Q, dtype)
+    ref = O.scene_query_stage1(X64, Q64, 2, 0.37)
+    check_stage1(got, ref, X64, Q64)
+    assert got["token_key"].reshape(n_tiles, n_v)[0, 3] == 0.0
+
+
+def test_score_equal_tiles(R):
+    """Identical tiles: max == min, so every u is 1 and ids break the ties."""
+    rng = np.random.default_rng(5)
+    tile = rng.standard_normal((64, 128)).astype(np.float32)
+    X = synth.store(np.stack([tile] * 6), "bf16")
+    q = rng.standard_normal((4, 128))
+    Q = synth.store((q / np.linalg.norm(q, axis=1, keepdims=True)).astype(np.float32), "bf16")
+    got = run_score(R, upload(X, "bf16"), upload(Q, "bf16"), 0, 0.99)
+    assert list(got["tile_order"]) == list(range(6))
+    assert np.all(got["tile_u"] == 1.0) and int(got["n_keep"][0]) == 6
+    assert np.all(got["tile_score"] == got["tile_score"][0])
+
+
+# ----------------------------------------------------------------------------- select
+def run_select(R, keys, kept, budgets, cap=None):
+    torch = torch_mod()
+    n_tiles, n_v = keys.shape
+    n_keep = len(kept)
+    total = int(np.clip(budgets, 0, n_v).sum()) if n_keep else 0
+    cap = total if cap is None else cap
+    key_d = torch.from_numpy(np.ascontiguousarray(keys.reshape(-1))).cuda()
+    kept_d = torch.tensor(list(kept) or [0], dtype=torch.int32, device="cuda")
+    bud_d = torch.tensor(list(budgets) or [0], dtype=torch.int32, device="cuda")
+    offs = torch.full((n_keep + 1,), -7, dtype=torch.int32, device="cuda")
+    sel = torch.full((max(1, cap),), -7, dtype=torch.int32, device="cuda")
+    status = torch.full((1,), -7, dtype=torch.int32, device="cuda")
+    R.rift_select_tokens(key_d, n_tiles, n_v, kept_d, bud_d, n_keep, offs, sel[:cap] if cap else sel[:0], status)
+    torch.cuda.synchronize()
+    return offs.cpu().numpy(), sel.cpu().numpy()[:cap], int(status.item())
+
+
+@pytest.mark.parametrize("ties", [False, True])
+def test_select_parity_random_keys(R, ties):
+    rng = np.random.default_rng(7 + ties)
+    n_tiles, n_v = 12, 576
+    keys = (rng.integers(-3, 4, size=(n_tiles, n_v)).astype(np.float64) if ties
+            else rng.standard_normal((n_tiles, n_v)))
+    kept = list(rng.permutation(n_tiles)[:9])
+    budgets = [576, 0, 1, 64, 144, 288, 575, 2, 300]
+    offs, sel, st = run_select(R, keys, kept, budgets)
+    r_offs, r_sel = O.select_tokens(keys, kept, budgets)
+    assert st == 0
+    assert np.array_equal(offs, r_offs) and np.array_equal(sel, r_sel)
+
+
+@pytest.mark.parametrize("n_v", [1, 5, 63, 64, 65, 333, 1024])
+def test_select_ragged_sizes(R, n_v):
+    rng = np.random.default_rng(n_v)
+    keys = rng.integers(0, 3, size=(3, n_v)).astype(np.float64)
+    budgets = [n_v, n_v // 2, min(n_v, 1)]
+    offs, sel, st = run_select(R, keys, [2, 0, 1], budgets)
+    r_offs, r_sel = O.select_tokens(keys, [2, 0, 1], budgets)
+    assert st == 0 and np.array_equal(offs, r_offs) and np.array_equal(sel, r_sel)
+
+
+def test_select_rejects_bad_budgets(R):
+    keys = np.zeros((2, 10))
+    for budgets, kept in (([11, 1], [0, 1]), ([-1, 1], [0, 1]), ([1, 1], [0, 2])):
+        offs, sel, st = run_select(R, keys, kept, budgets, cap=12)
+        assert st == 4 and np.all(offs == 0)              # RIFT_ERR_BUDGET
+        assert np.all(sel == -7)                          # nothing written
+    offs, sel, st = run_select(R, keys, [0, 1], [5, 5], cap=9)   # total above capacity
+    assert st == 4 and np.all(sel == -7)
+
+
+def test_select_empty(R):
+    offs, sel, st = run_select(R, np.zeros((2, 10)), [], [])
+    assert st == 0 and list(offs) == [0]
+
+
+# ----------------------------------------------------------------------------- compact
+def run_compact(R, X, dtype, kept, offs, sel, sysr, qry, rows=None):
+    torch = torch_mod()
+    n_keep = len(kept)
+    T = n_keep * (sysr.shape[0] + qry.shape[0]) + int(offs[-1])
+    rows = T if rows is None else rows
+    Xd = upload(X, dtype)
+    packed = torch.zeros(rows, X.shape[-1], dtype=Xd.dtype, device="cuda")
+    cu = torch.full((n_keep + 1,), -7, dtype=torch.int32, device="cuda")
+    pos = torch.full((rows,), -7, dtype=torch.int32, device="cuda")
+    st = torch.full((1,), -7, dtype=torch.int32, device="cuda")
+    kept_d = torch.tensor(list(kept) or [0], dtype=torch.int32, device="cuda")
+    offs_d = torch.tensor(list(offs), dtype=torch.int32, device="cuda")
+    sel_d = torch.tensor(list(sel) or [0], dtype=torch.int32, device="cuda")
+    R.rift_compact(Xd, kept_d, offs_d, sel_d, n_keep, upload(sysr, dtype), upload(qry, dtype),
+                   packed, cu, pos, st)
+    torch.cuda.synchronize()
+    return download_stored(packed, dtype), cu.cpu().numpy(), pos.cpu().numpy(), int(st.item())
+
+
+@pytest.mark.parametrize("name", ["tiny", "scene8"])
+def test_compact_parity(R, name):
+    w = synth.get(name)
+    sc = synth.make_scene(w)
+    ref = oracle_stage1(sc, w.keep_count, w.tau)
+    kept = list(ref["order"][: ref["n_keep"]])
+    budgets = O.assign_budgets(len(kept), w.levels, w.tier_num, w.tier_den)
+    offs, sel = O.select_tokens(ref["r"], kept, budgets)
+    packed, cu, pos, st = run_compact(R, sc.tokens, w.dtype, kept, offs, sel, sc.sys, sc.qry)
+    r_packed, r_cu, r_pos = O.compact(sc.tokens, kept, offs, sel, sc.sys, sc.qry)
+    assert st == 0
+    assert np.array_equal(packed, r_packed) and np.array_equal(cu, r_cu) and np.array_equal(pos, r_pos)
+
+
+def test_compact_edges(R):
+    rng = np.random.default_rng(3)
+    X = synth.store(rng.standard_normal((4, 20, 64)).astype(np.float32), "bf16")
+    sysr = synth.store(rng.standard_normal((3, 64)).astype(np.float32), "bf16")
+    qry = synth.store(rng.standard_normal((2, 64)).astype(np.float32), "bf16")
+    # zero-budget tile, full-budget tile
+    kept, offs, sel = [3, 1], np.array([0, 0, 20]), np.arange(20)
+    packed, cu, pos, st = run_compact(R, X, "bf16", kept, offs, sel, sysr, qry)
+    r = O.compact(X, kept, offs, sel, sysr, qry)
+    assert st == 0 and np.array_equal(packed, r[0]) and np.array_equal(cu, r[1]) and np.array_equal(pos, r[2])
+    # nothing kept
+    packed, cu, pos, st = run_compact(R, X, "bf16", [], np.array([0]), np.zeros(0, int), sysr, qry)
+    assert st == 0 and list(cu) == [0]
+    # capacity too small: status set, no row beyond capacity written
+    packed, cu, pos, st = run_compact(R, X, "bf16", kept, offs, sel, sysr, qry, rows=10)
+    assert st == 2
+    # token index out of range
+    packed, cu, pos, st = run_compact(R, X, "bf16", [0], np.array([0, 2]), np.array([1, 20]), sysr, qry)
+    assert st == 2
