@@ -1,0 +1,230 @@
+#!/usr/bin/env python3
+"""Throughput of the Rift hot path on one MI355X.
+
+One step = one whole scene-query: tile scoring and pruning (rift_score_tiles),
+per-tile token selection (rift_select_tokens), varlen compaction (rift_compact)
+and the decoder prefill of every retained prompt (rift_prefill), on synthetic
+inputs already resident in HBM.  The metric is retained vision tokens
+prefilled per second (sum of the per-tile budgets of one query, times steps,
+over the timed wall time), with milliseconds per scene-query alongside.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "retained vision tokens prefilled/sec + ms per 400-tile scene query, 1 GPU"
+PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+STAGES = ("qkv_rope", "attention", "out_proj", "gate_up_swiglu", "down_proj")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def stage_flops(T: int, d: int, ffn: int, seq_lens) -> dict:
+    """Algorithmic flops of one launch of each prefill stage (one layer)."""
+    attn = sum(2 * 2 * d * L * (L + 1) // 2 for L in seq_lens)  # QK^T and PV over the causal triangle
+    return {"qkv_rope": 2 * T * d * 3 * d, "attention": attn, "out_proj": 2 * T * d * d,
+            "gate_up_swiglu": 2 * T * d * 2 * ffn, "down_proj": 2 * T * ffn * d}
+
+
+def cpu_baseline(w, sc, seq_lens_by_tier, n_tiles_sample: int) -> dict:
+    """The oracle as it stands, on a bounded sample of the same workload:
+    Stage 1 and selection on `n_tiles_sample` tiles, and one decoder layer on
+    one prompt of each budget tier; extrapolated to the whole query."""
+    import synth
+    from oracle import rift_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()
+                            if i.get("user_api") == "blas"] or [1])
+    except Exception:  # pragma: no cover
+        blas_threads = 1
+    m = w.model
+    X = synth.to_f64(sc.tokens[:n_tiles_sample], w.dtype)
+    Q = synth.to_f64(sc.qbank, w.dtype)
+    t0 = time.perf_counter()
+    st = O.scene_query_stage1(X, Q, min(w.keep_count, n_tiles_sample), w.tau)
+    kept = list(st["order"][: st["n_keep"]])
+    O.select_tokens(st["r"], kept, [w.levels[0]] * len(kept))
+    t_stage1 = (time.perf_counter() - t0) * (w.n_tiles / n_tiles_sample)
+    W = {k: synth.to_f64(v, w.dtype) for k, v in synth.make_layer(w, 0).items()}
+    rng = np.random.default_rng(0)
+    t_prefill = 0.0
+    for L, count in seq_lens_by_tier:
+        x = rng.standard_normal((L, m.d))
+        t0 = time.perf_counter()
+        O.decoder_layer(x, W, m.n_heads, m.head_dim, m.rms_eps, m.rope_base, np.arange(L))
+        t_prefill += (time.perf_counter() - t0) * count * m.n_layers
+    total = t_stage1 + t_prefill
+    retained = sum(L - w.n_sys - w.n_qry for L, c in seq_lens_by_tier for _ in range(c))
+    return {"value": retained / total, "unit": "tokens/s", "cores": int(blas_threads),
+            "kind": "oracle",
+            "sample": (f"float64 NumPy oracle: Stage 1 + selection on {n_tiles_sample} of "
+                       f"{w.n_tiles} tiles, one decoder layer on one prompt per budget tier "
+                       f"(lengths {[L for L, _ in seq_lens_by_tier]}); extrapolated to "
+                       f"{w.n_tiles} tiles and {sum(c for _, c in seq_lens_by_tier)} prompts x "
+                       f"{m.n_layers} layers = {total:.1f} s per query; Stage 1 runs on one "
+                       f"thread, BLAS on {blas_threads}")}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="scene20_l32")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-tiles", type=int, default=8)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the Rift path here is a single-GPU build "
+              "(no collectives); run it with --gpus 1", file=sys.stderr)
+        return 2
+
+    import torch
+    import synth
+    from paper_2609_29029_amd.pipeline import PrefillShape, SceneQuery
+    import paper_2609_29029_amd as R
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    R.load()
+    w = synth.get(args.workload)
+    m = w.model
+    t_setup = time.perf_counter()
+    sc = synth.make_scene(w)
+
+    def up(a):
+        if w.dtype == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+    tokens, qbank, sysd, qryd = up(sc.tokens), up(sc.qbank), up(sc.sys), up(sc.qry)
+    layers = []
+    for l in range(m.n_layers):
+        W = synth.make_layer(w, l)
+        layers.append({k: up(v) for k, v in W.items()})
+        del W
+        if l % 8 == 7:
+            log(f"weights: {l + 1}/{m.n_layers} layers on device")
+    torch.cuda.synchronize()
+    log(f"setup {time.perf_counter() - t_setup:.1f} s")
+
+    q = SceneQuery(tokens, qbank, sysd, qryd, layers,
+                   PrefillShape(m.d, m.n_heads, m.head_dim, m.ffn, m.n_layers, m.rms_eps, m.rope_base),
+                   w.keep_count, w.tau, w.levels, w.tier_num, w.tier_den, with_sims=True)
+    T, n_ret = q.total_tokens, q.n_selected
+    budgets = [int(b) for b in q.budgets_host]
+    seq_lens = [w.n_sys + b + w.n_qry for b in budgets]
+
+    def E():
+        return torch.cuda.Event(enable_timing=True)
+
+    for i in range(args.warmup):
+        q.run()
+        torch.cuda.synchronize()
+        log(f"warmup {i + 1}/{args.warmup}")
+    assert q.check_status() == [0, 0]
+
+    K = args.steps
+    top = [[E() for _ in range(5)] for _ in range(K)]
+    lay = [[E() for _ in range(10 * m.n_layers)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(K):
+        ev = top[s]
+        ev[0].record()
+        q.score()
+        ev[1].record()
+        q.select()
+        ev[2].record()
+        q.compact()
+        ev[3].record()
+        q.prefill(events=lay[s])
+        ev[4].record()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    log(f"timed {K} steps: {(t1 - t0) * 1e3 / K:.2f} ms/step")
+
+    elapsed = t1 - t0
+    ms_step = elapsed * 1e3 / K
+    value = n_ret * K / elapsed
+
+    def med(xs):
+        return statistics.median(xs)
+
+    stage_ms = {"score": med([e[0].elapsed_time(e[1]) for e in top]),
+                "select": med([e[1].elapsed_time(e[2]) for e in top]),
+                "compact": med([e[2].elapsed_time(e[3]) for e in top]),
+                "prefill": med([e[3].elapsed_time(e[4]) for e in top])}
+    # per-launch average of each prefill stage over every layer of every step
+    per_launch = {}
+    for g, name in enumerate(STAGES):
+        ds = [lay[s][10 * l + 2 * g].elapsed_time(lay[s][10 * l + 2 * g + 1])
+              for s in range(K) for l in range(m.n_layers)]
+        per_launch[name] = sum(ds) / len(ds)
+    fl = stage_flops(T, m.d, m.ffn, seq_lens)
+    stage_roof = {n: {"ms": round(per_launch[n], 4),
+                      "tflops": round(fl[n] / (per_launch[n] * 1e-3) / 1e12, 1),
+                      "frac_bf16_peak": round(fl[n] / (per_launch[n] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+                  for n in STAGES}
+    dom = max(STAGES, key=lambda n: per_launch[n])
+    achieved = fl[dom] / (per_launch[dom] * 1e-3) / 1e12
+    prefill_flops = sum(fl.values()) * m.n_layers
+    # HBM-bound stages: algorithmic bytes
+    e = 2 if w.dtype == "bf16" else 4
+    score_bytes = w.n_tiles * w.n_v * m.d * e + w.n_tiles * w.n_v * (8 + 4 * (1 + w.n_bg))
+    compact_bytes = n_ret * m.d * e * 2 + q.n_keep * (w.n_sys + w.n_qry) * m.d * e + \
+        (w.n_sys + w.n_qry) * m.d * e
+    hbm = {"score_GBs": round(score_bytes / (stage_ms["score"] * 1e-3) / 1e9, 1),
+           "score_frac": round(score_bytes / (stage_ms["score"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+           "compact_GBs": round(compact_bytes / (stage_ms["compact"] * 1e-3) / 1e9, 1),
+           "compact_frac": round(compact_bytes / (stage_ms["compact"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "tokens/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": f"{w.name}: {w.n_tiles} tiles x {w.n_v} tokens, d={m.d}, keep "
+                               f"{w.keep_count}, budgets {list(w.levels)} by score rank, "
+                               f"{m.n_layers}-layer LLaMA-7B-shaped varlen prefill",
+                   "retained_vision_tokens": n_ret, "packed_tokens": T, "sequences": q.n_keep,
+                   "max_seqlen": q.max_seqlen, "prefill_tflop": round(prefill_flops / 1e12, 2)},
+        "roofline": {"bound": "mfma", "kernel": f"prefill {dom} (gemm_bf16_kernel)" if dom != "attention"
+                     else "attention", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None},
+        "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+        "prefill_stages": stage_roof,
+        "prefill_frac_bf16_peak": round(prefill_flops / (stage_ms["prefill"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "hbm": hbm,
+    }
+    if not args.no_cpu_baseline:
+        tiers = {}
+        for L in seq_lens:
+            tiers[L] = tiers.get(L, 0) + 1
+        t_cpu = time.perf_counter()
+        out["cpu_baseline"] = cpu_baseline(w, sc, sorted(tiers.items(), reverse=True),
+                                           args.cpu_sample_tiles)
+        log(f"cpu baseline {time.perf_counter() - t_cpu:.1f} s")
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -219,6 +219,12 @@ RIFT_API size_t rift_prefill_workspace_size(const rift_model_cfg* cfg, int32_t t
  *              (no final norm, no vocabulary projection)
  * kv_cache     optional out [n_layers][2][total_tokens][d] cfg->dt: per layer
  *              the rotated keys, then the values; NULL to skip
+ * events       optional [host] array of 10 * n_layers hipEvent_t (created by the
+ *              caller), or NULL.  For benchmarks: events[10 l + 2 g] and
+ *              events[10 l + 2 g + 1] are recorded on `stream` right before and
+ *              after stage g of layer l -- g = 0 QKV projection (+RoPE),
+ *              1 attention, 2 output projection, 3 gate/up projection (+SwiGLU),
+ *              4 down projection.
  * Implemented: bf16 with head_dim == 128, d % 256 == 0, ffn % 128 == 0;
  *              f32 with head_dim in {64, 128}, d % 64 == 0, ffn % 16 == 0.
  * Shape rules: 1 <= max_seqlen <= 65536, total_tokens >= 0, n_seq >= 0.
@@ -227,7 +233,8 @@ RIFT_API rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_we
                          const void* x_in, rift_dtype x_dt, const int32_t* cu_seqlens,
                          const int32_t* position_ids, int32_t n_seq, int32_t total_tokens,
                          int32_t max_seqlen, float* hidden_out, void* kv_cache,
-                         void* workspace, size_t ws_bytes, rift_stream stream);
+                         void* workspace, size_t ws_bytes, void* const* events,
+                         rift_stream stream);
 
 #ifdef __cplusplus
 }

@@ -80,7 +80,7 @@ def load() -> ctypes.CDLL:
     L.rift_prefill_workspace_size.argtypes = [ctypes.POINTER(ModelCfg), I32, I32]
     L.rift_prefill.restype = I32
     L.rift_prefill.argtypes = [ctypes.POINTER(ModelCfg), ctypes.POINTER(LayerWeights), P, I32, P, P,
-                               I32, I32, I32, P, P, P, SZ, P]
+                               I32, I32, I32, P, P, P, SZ, P, P]
     _lib = L
     return L
 
@@ -237,7 +237,9 @@ def layer_struct(w: dict) -> LayerWeights:
 
 def rift_prefill(cfg: ModelCfg, layers: Sequence[dict], x_in, cu_seqlens, position_ids,
                  n_seq: int, max_seqlen: int, hidden_out, workspace, kv_cache=None,
-                 stream=None) -> None:
+                 events=None, stream=None) -> None:
+    """events: optional list of 10 * n_layers torch.cuda.Event(enable_timing=True),
+    recorded around each per-layer stage (see include/rift.h)."""
     torch = _torch()
     T = x_in.shape[0]
     if len(layers) != cfg.n_layers:
@@ -251,8 +253,13 @@ def rift_prefill(cfg: ModelCfg, layers: Sequence[dict], x_in, cu_seqlens, positi
     _need(position_ids, torch.int32, (T,), "position_ids")
     _need(workspace, torch.uint8, None, "workspace")
     arr = (LayerWeights * max(1, len(layers)))(*[layer_struct(w) for w in layers])
+    ev = None
+    if events is not None:
+        if len(events) != 10 * cfg.n_layers:
+            raise ValueError("events needs 10 entries per layer")
+        ev = (ctypes.c_void_p * len(events))(*[int(e.cuda_event) for e in events])
     st = load().rift_prefill(ctypes.byref(cfg), arr, _ptr(x_in), _dt_code(x_in), _ptr(cu_seqlens),
                              _ptr(position_ids), int(n_seq), int(T), int(max_seqlen),
                              _ptr(hidden_out), _ptr(kv_cache), _ptr(workspace), workspace.numel(),
-                             _stream(stream))
+                             ev, _stream(stream))
     _check(st, "rift_prefill")

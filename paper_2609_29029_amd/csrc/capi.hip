@@ -230,7 +230,7 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
                          const void* x_in, rift_dtype x_dt, const int32_t* cu_seqlens,
                          const int32_t* position_ids, int32_t n_seq, int32_t total_tokens,
                          int32_t max_seqlen, float* hidden_out, void* kv_cache, void* workspace,
-                         size_t ws_bytes, rift_stream stream) {
+                         size_t ws_bytes, void* const* events, rift_stream stream) {
     rift_status cs = check_cfg(cfg);
     if (cs != RIFT_OK) return cs;
     const rift_model_cfg c = *cfg;
@@ -279,6 +279,11 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
         return RIFT_OK;
     }
     RIFT_TRY(launch_rope_table(rope, max_seqlen, c.head_dim, c.rope_base, st));
+    // benchmark hook: event pair around stage g of layer l
+    auto mark = [&](int l, int g, int end) -> hipError_t {
+        if (events == nullptr) return hipSuccess;
+        return hipEventRecord(static_cast<hipEvent_t>(events[10 * l + 2 * g + end]), st);
+    };
 
     for (int l = 0; l < c.n_layers; ++l) {
         const rift_layer_weights& w = layers[l];
@@ -312,38 +317,58 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
             qa.n_pos = max_seqlen;
             qa.M = T;
             qa.d = d;
+            RIFT_TRY(mark(l, 0, 0));
             RIFT_TRY(launch_gemm_qkv_rope(qa, st));
+            RIFT_TRY(mark(l, 0, 1));
             // attention output reuses the h buffer (h is consumed by the QKV GEMM)
+            RIFT_TRY(mark(l, 1, 0));
             RIFT_TRY(launch_attention_bf16(static_cast<const uint16_t*>(qb), static_cast<const uint16_t*>(kb),
                                            static_cast<const uint16_t*>(vb), static_cast<uint16_t*>(h),
                                            cu_seqlens, n_seq, max_seqlen, c.n_heads, st));
+            RIFT_TRY(mark(l, 1, 1));
+            RIFT_TRY(mark(l, 2, 0));
             RIFT_TRY(launch_gemm_resid(static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w.wo),
                                        hidden_out, T, d, d, st));
+            RIFT_TRY(mark(l, 2, 1));
             RIFT_TRY(launch_rmsnorm(hidden_out, false, nullptr, w.g_ffn, true, h, true, T, d, c.rms_eps, st));
             uint16_t* a = reinterpret_cast<uint16_t*>(ws + L.a);
+            RIFT_TRY(mark(l, 3, 0));
             RIFT_TRY(launch_gemm_swiglu(static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w.w_gate),
                                         static_cast<const uint16_t*>(w.w_up), a, T, c.ffn, d, st));
+            RIFT_TRY(mark(l, 3, 1));
+            RIFT_TRY(mark(l, 4, 0));
             RIFT_TRY(launch_gemm_resid(a, static_cast<const uint16_t*>(w.w_down), hidden_out, T, d, c.ffn, st));
+            RIFT_TRY(mark(l, 4, 1));
         } else {
             float* hf = static_cast<float*>(h);
             float* qf = static_cast<float*>(qb);
             float* kf = static_cast<float*>(kb);
             float* vf = static_cast<float*>(vb);
+            RIFT_TRY(mark(l, 0, 0));
             RIFT_TRY(launch_gemm_f32(hf, static_cast<const float*>(w.wq), qf, T, d, d, false, st));
             RIFT_TRY(launch_gemm_f32(hf, static_cast<const float*>(w.wk), kf, T, d, d, false, st));
             RIFT_TRY(launch_gemm_f32(hf, static_cast<const float*>(w.wv), vf, T, d, d, false, st));
             RIFT_TRY(launch_rope_apply_f32(qf, rope, position_ids, max_seqlen, T, c.n_heads, c.head_dim, st));
             RIFT_TRY(launch_rope_apply_f32(kf, rope, position_ids, max_seqlen, T, c.n_heads, c.head_dim, st));
+            RIFT_TRY(mark(l, 0, 1));
+            RIFT_TRY(mark(l, 1, 0));
             RIFT_TRY(launch_attention_f32(qf, kf, vf, hf, cu_seqlens, n_seq, max_seqlen, c.n_heads,
                                           c.head_dim, st));
+            RIFT_TRY(mark(l, 1, 1));
+            RIFT_TRY(mark(l, 2, 0));
             RIFT_TRY(launch_gemm_f32(hf, static_cast<const float*>(w.wo), hidden_out, T, d, d, true, st));
+            RIFT_TRY(mark(l, 2, 1));
             RIFT_TRY(launch_rmsnorm(hidden_out, false, nullptr, w.g_ffn, false, hf, false, T, d, c.rms_eps, st));
             float* gate = reinterpret_cast<float*>(ws + L.a);
             float* up = reinterpret_cast<float*>(ws + L.gate2);
+            RIFT_TRY(mark(l, 3, 0));
             RIFT_TRY(launch_gemm_f32(hf, static_cast<const float*>(w.w_gate), gate, T, c.ffn, d, false, st));
             RIFT_TRY(launch_gemm_f32(hf, static_cast<const float*>(w.w_up), up, T, c.ffn, d, false, st));
             RIFT_TRY(launch_swiglu_f32(gate, up, gate, (long long)T * c.ffn, st));
+            RIFT_TRY(mark(l, 3, 1));
+            RIFT_TRY(mark(l, 4, 0));
             RIFT_TRY(launch_gemm_f32(gate, static_cast<const float*>(w.w_down), hidden_out, T, d, c.ffn, true, st));
+            RIFT_TRY(mark(l, 4, 1));
         }
     }
 #undef RIFT_TRY

@@ -109,12 +109,12 @@ class SceneQuery:
                        self.sys, self.qry, self.packed, self.cu_seqlens, self.position_ids,
                        self.cmp_status, self.stream)
 
-    def prefill(self) -> None:
+    def prefill(self, events=None) -> None:
         if self.total_tokens == 0:
             return
         R.rift_prefill(self.cfg, self.layers, self.packed, self.cu_seqlens, self.position_ids,
                        self.n_keep, max(1, self.max_seqlen), self.hidden, self.prefill_ws,
-                       stream=self.stream)
+                       events=events, stream=self.stream)
 
     def run(self) -> None:
         """Enqueue the whole scene-query.  Threshold mode synchronises once to

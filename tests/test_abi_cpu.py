@@ -131,7 +131,7 @@ def test_prefill_validation_and_workspace(R):
 
     def call(c, T=10, n_seq=1, max_len=10, x=FAKE, x_dt=1, wsb=1 << 40):
         return L.rift_prefill(ctypes.byref(c), lw, x, x_dt, FAKE, FAKE, n_seq, T, max_len, FAKE, None,
-                              0x10000, wsb, None)
+                              0x10000, wsb, None, None)
     assert call(cfg, T=0) == 0                              # nothing to do
     assert call(cfg, x=None) == 1
     assert call(cfg, x_dt=5) == 3
