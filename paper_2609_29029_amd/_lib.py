@@ -257,6 +257,9 @@ def rift_prefill(cfg: ModelCfg, layers: Sequence[dict], x_in, cu_seqlens, positi
     if events is not None:
         if len(events) != 10 * cfg.n_layers:
             raise ValueError("events needs 10 entries per layer")
+        for e in events:          # torch creates the hipEvent on its first record()
+            if not e.cuda_event:
+                e.record()
         ev = (ctypes.c_void_p * len(events))(*[int(e.cuda_event) for e in events])
     st = load().rift_prefill(ctypes.byref(cfg), arr, _ptr(x_in), _dt_code(x_in), _ptr(cu_seqlens),
                              _ptr(position_ids), int(n_seq), int(T), int(max_seqlen),
