@@ -11,8 +11,8 @@
 // registers).  K advances 64 at a time through two LDS stages of A and B tiles
 // (2 x 64 KB); the next stage's global loads are in flight while the current
 // stage feeds the MFMAs.  LDS rows are 128 bytes (64 bf16) split in 8 chunks
-// of 16 bytes; chunk c of row r is stored at position c ^ (r & 7), which keeps
-// the MFMA operand reads of 8 consecutive rows on distinct banks.
+// of 16 bytes, stored in a row-dependent XOR order (swz below) that keeps the
+// MFMA operand reads on distinct banks.
 //
 // Every output element is one fixed sequence of MFMA accumulations over K, no
 // matter which tile or batch row holds it, so a row's result does not depend on
@@ -36,6 +36,26 @@ constexpr int kTileElems = BM * BK;             // one operand tile (A or B), el
 constexpr size_t kLdsBytes = 2 * 2 * kTileElems * sizeof(bf16_t);  // 128 KB
 
 enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+
+#ifndef RIFT_GEMM_DMA
+#define RIFT_GEMM_DMA 1
+#endif
+
+#ifndef RIFT_SWZ
+#define RIFT_SWZ 1
+#endif
+// LDS swizzle key of a tile row: chunk c of row r is stored at c ^ swz(r).
+// swz(r) = (r >> 1) ^ 4 (r & 1), mod 8, gives distinct positions to any 8
+// consecutive rows and to the 8 rows of equal parity among 16 consecutive
+// rows, so the 16-byte operand reads are conflict-free whether the LDS serves
+// 8 or 16 lanes per clock.
+__device__ __forceinline__ int swz(int r) {
+#if RIFT_SWZ
+    return ((r >> 1) ^ ((r & 1) << 2)) & 7;
+#else
+    return r & 7;
+#endif
+}
 
 struct GemmParams {
     const bf16_t* a;
@@ -87,6 +107,13 @@ __device__ __forceinline__ const bf16_t* b_base(const GemmParams& p, int bn, int
     }
 }
 
+// Matrix that B-tile row r (0..255) of tile bn is read from.
+template <int EPI>
+__device__ __forceinline__ const bf16_t* b_base_row(const GemmParams& p, int bn, int r) {
+    if constexpr (EPI == EPI_SWIGLU) return ((r & 127) < 64) ? p.b0 : p.b1;
+    else return b_base<EPI>(p, bn, 0);
+}
+
 template <int EPI>
 __device__ __forceinline__ int b_row(const GemmParams& p, int bn, int r) {
     if constexpr (EPI == EPI_QKV) {
@@ -99,112 +126,11 @@ __device__ __forceinline__ int b_row(const GemmParams& p, int bn, int r) {
     }
 }
 
+// Epilogue.  acc[m][n][i] is row 8 (i/4) + 4 (lane/32) + (i%4) and column
+// lane%32 of the 32x32 tile (m, n) of wave (wm, wn).
 template <int EPI>
-__global__ void __launch_bounds__(256, 1) gemm_bf16_kernel(GemmParams p) {
-    extern __shared__ __align__(16) bf16_t lds[];
-    const int num_m = (p.M + BM - 1) / BM;
-    const int num_n = (EPI == EPI_SWIGLU) ? p.d / 128 : p.N / BN;
-    int bm, bn;
-    tile_coords(blockIdx.x, num_m, num_n, bm, bn);
-    const int m0 = bm * BM;
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int wm = wave >> 1;
-    const int wn = wave & 1;
-
-    // Loader: thread t moves chunks t + 256 j (j = 0..7) of each operand tile;
-    // chunk id -> row = (t >> 3) + 32 j, logical chunk = t & 7.  Offsets are
-    // 32-bit element offsets from the operand base (every operand is < 4 GB).
-    const int ld_row = tid >> 3;
-    const int ld_lc = tid & 7;
-    uint32_t a_off[8], b_off[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const int row = ld_row + 32 * j;
-        int ar = m0 + row;
-        ar = ar < p.M ? ar : p.M - 1;
-        a_off[j] = (uint32_t)ar * (uint32_t)p.K + ld_lc * 8;
-        b_off[j] = (uint32_t)b_row<EPI>(p, bn, row) * (uint32_t)p.K + ld_lc * 8;
-    }
-    // LDS position of this thread's chunk in row ld_row; rows + 32 j keep the
-    // same swizzle (32 j is a multiple of 8), so chunk j sits 32*64*j further.
-    const int lds_w = ld_row * BK + ((ld_lc ^ (ld_row & 7)) << 3);
-
-    f32x16_t acc[4][4];
-#pragma unroll
-    for (int m = 0; m < 4; ++m)
-#pragma unroll
-        for (int n = 0; n < 4; ++n)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) acc[m][n][i] = 0.f;
-
-    u32x4_t ra[8], rb[8];
-    const int nk = p.K / BK;
-
-    // prologue: stage 0
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        ra[j] = *reinterpret_cast<const u32x4_t*>(p.a + a_off[j]);
-        rb[j] = *reinterpret_cast<const u32x4_t*>(b_base<EPI>(p, bn, j) + b_off[j]);
-    }
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        *reinterpret_cast<u32x4_t*>(lds + lds_w + j * 32 * BK) = ra[j];
-        *reinterpret_cast<u32x4_t*>(lds + kTileElems + lds_w + j * 32 * BK) = rb[j];
-    }
-    __syncthreads();
-
-    // Operand reads: row wm*128 + m*32 + (lane & 31) has swizzle key lane & 7,
-    // so only the k sub-step changes the offset; m and n add 32*64 per step.
-    const int rd_a = (wm * 128 + (lane & 31)) * BK;
-    const int rd_b = (wn * 128 + (lane & 31)) * BK;
-    const int hsel = lane >> 5;
-    const int key = lane & 7;
-
-    for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        const bool more = kt + 1 < nk;
-        if (more) {
-            const uint32_t koff = (uint32_t)(kt + 1) * BK;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                ra[j] = *reinterpret_cast<const u32x4_t*>(p.a + (a_off[j] + koff));
-                rb[j] = *reinterpret_cast<const u32x4_t*>(b_base<EPI>(p, bn, j) + (b_off[j] + koff));
-            }
-        }
-        const bf16_t* sA = lds + cur * 2 * kTileElems;
-        const bf16_t* sB = sA + kTileElems;
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-            const int sw = ((2 * kk + hsel) ^ key) << 3;
-            bf16x8_t af[4], bf[4];
-#pragma unroll
-            for (int m = 0; m < 4; ++m)
-                af[m] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + m * 32 * BK);
-#pragma unroll
-            for (int n = 0; n < 4; ++n)
-                bf[n] = *reinterpret_cast<const bf16x8_t*>(sB + rd_b + sw + n * 32 * BK);
-#pragma unroll
-            for (int m = 0; m < 4; ++m)
-#pragma unroll
-                for (int n = 0; n < 4; ++n)
-                    acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[m], bf[n], acc[m][n], 0, 0, 0);
-        }
-        if (more) {
-            bf16_t* dA = lds + (cur ^ 1) * 2 * kTileElems;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                *reinterpret_cast<u32x4_t*>(dA + lds_w + j * 32 * BK) = ra[j];
-                *reinterpret_cast<u32x4_t*>(dA + kTileElems + lds_w + j * 32 * BK) = rb[j];
-            }
-        }
-        __syncthreads();
-    }
-
-    // Epilogue.  acc[m][n][i] is row 8 (i/4) + 4 (lane/32) + (i%4) and column
-    // lane%32 of the 32x32 tile (m, n) of this wave.
+__device__ __forceinline__ void epilogue(const GemmParams& p, f32x16_t (&acc)[4][4], int m0, int bn,
+                                         int wm, int wn, int lane) {
     const int col_in = lane & 31;
     const int row_hi = 4 * (lane >> 5);
 #pragma unroll
@@ -253,10 +179,283 @@ __global__ void __launch_bounds__(256, 1) gemm_bf16_kernel(GemmParams p) {
 }
 
 template <int EPI>
+__global__ void __launch_bounds__(256, 1) gemm_bf16_kernel(GemmParams p) {
+    extern __shared__ __align__(16) bf16_t lds[];
+    const int num_m = (p.M + BM - 1) / BM;
+    const int num_n = (EPI == EPI_SWIGLU) ? p.d / 128 : p.N / BN;
+    int bm, bn;
+    tile_coords(blockIdx.x, num_m, num_n, bm, bn);
+    const int m0 = bm * BM;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int wm = wave >> 1;
+    const int wn = wave & 1;
+
+    // Loader: thread t moves chunks t + 256 j (j = 0..7) of each operand tile;
+    // chunk id -> row = (t >> 3) + 32 j, logical chunk = t & 7.  Offsets are
+    // 32-bit element offsets from the operand base (every operand is < 4 GB).
+    const int ld_row = tid >> 3;
+    const int ld_lc = tid & 7;
+    uint32_t a_off[8], b_off[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int row = ld_row + 32 * j;
+        int ar = m0 + row;
+        ar = ar < p.M ? ar : p.M - 1;
+        a_off[j] = (uint32_t)ar * (uint32_t)p.K + ld_lc * 8;
+        b_off[j] = (uint32_t)b_row<EPI>(p, bn, row) * (uint32_t)p.K + ld_lc * 8;
+    }
+    // LDS position of this thread's chunk in row ld_row; rows + 32 j keep the
+    // same swizzle key (32 j is a multiple of 16), so chunk j sits 32*64*j further.
+    const int lds_w = ld_row * BK + ((ld_lc ^ swz(ld_row)) << 3);
+
+    f32x16_t acc[4][4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int n = 0; n < 4; ++n)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[m][n][i] = 0.f;
+
+    u32x4_t ra[8], rb[8];
+    const int nk = p.K / BK;
+
+    // prologue: stage 0
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        ra[j] = *reinterpret_cast<const u32x4_t*>(p.a + a_off[j]);
+        rb[j] = *reinterpret_cast<const u32x4_t*>(b_base<EPI>(p, bn, j) + b_off[j]);
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        *reinterpret_cast<u32x4_t*>(lds + lds_w + j * 32 * BK) = ra[j];
+        *reinterpret_cast<u32x4_t*>(lds + kTileElems + lds_w + j * 32 * BK) = rb[j];
+    }
+    __syncthreads();
+
+    // Operand reads: row wm*128 + m*32 + (lane & 31) has swizzle key
+    // swz(lane & 31), so only the k sub-step changes the offset; m and n add
+    // 32*64 per step.
+    const int rd_a = (wm * 128 + (lane & 31)) * BK;
+    const int rd_b = (wn * 128 + (lane & 31)) * BK;
+    const int hsel = lane >> 5;
+    const int key = swz(lane & 31);
+
+    for (int kt = 0; kt < nk; ++kt) {
+        const int cur = kt & 1;
+        const bool more = kt + 1 < nk;
+        if (more) {
+            const uint32_t koff = (uint32_t)(kt + 1) * BK;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                ra[j] = *reinterpret_cast<const u32x4_t*>(p.a + (a_off[j] + koff));
+                rb[j] = *reinterpret_cast<const u32x4_t*>(b_base<EPI>(p, bn, j) + (b_off[j] + koff));
+            }
+        }
+        const bf16_t* sA = lds + cur * 2 * kTileElems;
+        const bf16_t* sB = sA + kTileElems;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            const int sw = ((2 * kk + hsel) ^ key) << 3;
+            bf16x8_t af[4], bf[4];
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+                af[m] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + m * 32 * BK);
+#pragma unroll
+            for (int n = 0; n < 4; ++n)
+                bf[n] = *reinterpret_cast<const bf16x8_t*>(sB + rd_b + sw + n * 32 * BK);
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+#pragma unroll
+                for (int n = 0; n < 4; ++n)
+                    acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[m], bf[n], acc[m][n], 0, 0, 0);
+        }
+        if (more) {
+            bf16_t* dA = lds + (cur ^ 1) * 2 * kTileElems;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                *reinterpret_cast<u32x4_t*>(dA + lds_w + j * 32 * BK) = ra[j];
+                *reinterpret_cast<u32x4_t*>(dA + kTileElems + lds_w + j * 32 * BK) = rb[j];
+            }
+        }
+        __syncthreads();
+    }
+
+    epilogue<EPI>(p, acc, m0, bn, wm, wn, lane);
+}
+
+// ---------------------------------------------------------------------------
+// Variant with a 4-stage LDS ring filled by global_load_lds_dwordx4 (LDS DMA).
+// K advances 32 per stage; a stage holds the A and B tiles (256 rows x 64
+// bytes each, 32 KB).  Loads for stage k+3 are issued right after the barrier
+// that opens stage k, so each load has about three stages of MFMA work to land;
+// no registers stage the data.  Rows are 64 bytes (4 chunks of 16 bytes);
+// chunk c of row r sits at position c ^ swz4(r), which keeps the operand reads
+// of any 8 consecutive rows, and of the 4 rows r, r+4, r+8, r+12, on distinct
+// banks.  The loads are issued with inline assembly and the waits are explicit
+// (s_waitcnt vmcnt before every barrier), because the compiler would otherwise
+// wait for every outstanding LDS DMA before each LDS read.
+constexpr int BK2 = 32;
+constexpr int NST = 4;
+constexpr int kStageElems = 2 * BM * BK2;   // A tile then B tile
+
+__device__ __forceinline__ int swz4(int r) { return ((r >> 2) ^ (r & 2)) & 3; }
+
+// 16 bytes per lane from global memory to LDS address lds_addr + 16 * lane.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :: "s"(lds_addr), "v"(g) : "memory", "m0");
+}
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
+template <int N>
+__device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory"); }
+
+template <int EPI>
+__global__ void __launch_bounds__(256, 1) gemm_bf16_dma_kernel(GemmParams p) {
+    __shared__ __align__(16) bf16_t lds[NST * kStageElems];
+    const int num_m = (p.M + BM - 1) / BM;
+    const int num_n = (EPI == EPI_SWIGLU) ? p.d / 128 : p.N / BN;
+    int bm, bn;
+    tile_coords(blockIdx.x, num_m, num_n, bm, bn);
+    const int m0 = bm * BM;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 1;
+    const int wn = wave & 1;
+
+    // DMA sources: instruction j (0..3) of this wave moves tile rows
+    // 16 (4 wave + j) + (lane >> 2); the lane fetches logical chunk cl.
+    const int rsub = lane >> 2;
+    const int cl = (lane & 3) ^ swz4(rsub);
+    const bf16_t* asrc[4];
+    const bf16_t* bsrc[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int row = 16 * (4 * wave + j) + rsub;
+        int ar = m0 + row;
+        ar = ar < p.M ? ar : p.M - 1;
+        asrc[j] = p.a + (size_t)ar * p.K + cl * 8;
+        bsrc[j] = b_base_row<EPI>(p, bn, row) + (size_t)b_row<EPI>(p, bn, row) * p.K + cl * 8;
+    }
+    const uint32_t ring = (uint32_t)(uintptr_t)lds;
+    auto issue = [&](int stage, int kt) {
+        const uint32_t sb = ring + (uint32_t)stage * (kStageElems * 2) + (uint32_t)wave * 4096u;
+        const size_t ko = (size_t)kt * BK2;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dma16(asrc[j] + ko, sb + j * 1024u);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dma16(bsrc[j] + ko, sb + BM * BK2 * 2 + j * 1024u);
+    };
+
+    f32x16_t acc[4][4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int n = 0; n < 4; ++n)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[m][n][i] = 0.f;
+
+    const int nk = p.K / BK2;
+    for (int s = 0; s < 3 && s < nk; ++s) issue(s, s);
+
+    // operand reads: row & 15 == lane & 15 for every (m, n), so one swizzle key
+    const int rd_a = (wm * 128 + (lane & 31)) * BK2;
+    const int rd_b = BM * BK2 + (wn * 128 + (lane & 31)) * BK2;
+    const int key = swz4(lane & 15);
+    const int hsel = lane >> 5;
+    const int sw0 = ((0 + hsel) ^ key) << 3;   // k sub-step 0: logical chunks 0, 1
+    const int sw1 = ((2 + hsel) ^ key) << 3;   // k sub-step 1: logical chunks 2, 3
+
+    bf16x8_t a0[4], b0[4], a1[4], b1[4];
+    auto read = [&](bf16x8_t (&af)[4], bf16x8_t (&bf)[4], int stage, int sw) {
+        const bf16_t* sA = lds + stage * kStageElems;
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+            af[m] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + m * 32 * BK2);
+#pragma unroll
+        for (int n = 0; n < 4; ++n)
+            bf[n] = *reinterpret_cast<const bf16x8_t*>(sA + rd_b + sw + n * 32 * BK2);
+    };
+    auto mma = [&](const bf16x8_t (&af)[4], const bf16x8_t (&bf)[4]) {
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+#pragma unroll
+            for (int n = 0; n < 4; ++n)
+                acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[m], bf[n], acc[m][n], 0, 0, 0);
+    };
+    // Wait until this wave's DMA for stage s has landed, given that the
+    // stages after s up to min(s + 2, nk - 1) have been issued, then barrier.
+    auto open_stage = [&](int s) {
+        const int after = nk - 1 - s;
+        if (after >= 2) asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)" ::: "memory");
+        else if (after == 1) asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)" ::: "memory");
+        else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+        wg_barrier();
+    };
+
+    // Software pipeline: sub-step 1 of stage kt is read while sub-step 0
+    // computes; stage kt+1 opens (wait, barrier, DMA of stage kt+4 into the
+    // buffer stage kt used) between the two MFMA groups, and its sub-step 0 is
+    // read while sub-step 1 of stage kt computes.
+    open_stage(0);
+    if (nk > 3) issue(3, 3);
+    read(a0, b0, 0, sw0);
+    int kt = 0;
+    // steady state, branch-free: when stage kt+1 opens, stages kt+2 and kt+3
+    // are in flight (16 DMA instructions per lane), and stage kt+4 exists
+    // Each phase issues its 8 LDS reads between its first 8 MFMAs (MFMA first,
+    // so the wait for the previous phase's operands never waits for the new
+    // reads); sched_barrier keeps MFMAs from moving across the phases.
+    auto interleave = [] {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);       // the other 8 MFMAs
+    };
+    for (; kt + 4 < nk; ++kt) {
+        const int cur = kt & (NST - 1);
+        read(a1, b1, cur, sw1);
+        mma(a0, b0);
+        interleave();
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)" ::: "memory");
+        wg_barrier();
+        issue(cur, kt + 4);
+        __builtin_amdgcn_sched_barrier(0);
+        read(a0, b0, (kt + 1) & (NST - 1), sw0);
+        mma(a1, b1);
+        interleave();
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    // last stages
+    for (; kt < nk; ++kt) {
+        const int cur = kt & (NST - 1);
+        read(a1, b1, cur, sw1);
+        mma(a0, b0);
+        if (kt + 1 < nk) {
+            open_stage(kt + 1);
+            read(a0, b0, (kt + 1) & (NST - 1), sw0);
+        }
+        mma(a1, b1);
+    }
+    epilogue<EPI>(p, acc, m0, bn, wm, wn, lane);
+}
+
+template <int EPI>
 hipError_t launch_gemm(const GemmParams& p, int num_n, hipStream_t st) {
     const int num_m = (p.M + BM - 1) / BM;
     if (p.M <= 0) return hipSuccess;
+#if RIFT_GEMM_DMA
+    hipLaunchKernelGGL(gemm_bf16_dma_kernel<EPI>, dim3(num_m * num_n), dim3(256), 0, st, p);
+#else
     hipLaunchKernelGGL(gemm_bf16_kernel<EPI>, dim3(num_m * num_n), dim3(256), kLdsBytes, st, p);
+#endif
     return hipGetLastError();
 }
 
