@@ -8,18 +8,11 @@
 #include "rift_common.h"
 
 namespace rift {
-hipError_t gemm_bf16_init_attributes();
 
 namespace {
 
 std::once_flag g_init_flag;
 hipError_t g_init_err = hipSuccess;
-
-template <typename K>
-hipError_t allow_lds(K* kernel, int bytes) {
-    return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
-                               hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-}
 
 }  // namespace
 
@@ -28,8 +21,7 @@ hipError_t score_init_attributes();
 
 hipError_t init_kernel_attributes() {
     std::call_once(g_init_flag, [] {
-        g_init_err = gemm_bf16_init_attributes();
-        if (g_init_err == hipSuccess) g_init_err = score_init_attributes();
+        g_init_err = score_init_attributes();
     });
     return g_init_err;
 }

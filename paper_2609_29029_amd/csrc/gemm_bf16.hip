@@ -8,11 +8,8 @@
 //
 // Tiling: a 256x256 output tile per workgroup of 4 waves (2x2), each wave a
 // 128x128 block of 4x4 v_mfma_f32_32x32x16_bf16 tiles (256 accumulator
-// registers).  K advances 64 at a time through two LDS stages of A and B tiles
-// (2 x 64 KB); the next stage's global loads are in flight while the current
-// stage feeds the MFMAs.  LDS rows are 128 bytes (64 bf16) split in 8 chunks
-// of 16 bytes, stored in a row-dependent XOR order (swz below) that keeps the
-// MFMA operand reads on distinct banks.
+// registers).  K advances 32 per stage through a ring of four LDS stages
+// (128 KB) that LDS DMA fills three stages ahead (see the kernel).
 //
 // Every output element is one fixed sequence of MFMA accumulations over K, no
 // matter which tile or batch row holds it, so a row's result does not depend on
@@ -30,32 +27,9 @@ namespace {
 
 constexpr int BM = 256;
 constexpr int BN = 256;
-constexpr int BK = 64;
 constexpr int kGroupM = 8;
-constexpr int kTileElems = BM * BK;             // one operand tile (A or B), elements
-constexpr size_t kLdsBytes = 2 * 2 * kTileElems * sizeof(bf16_t);  // 128 KB
 
 enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
-
-#ifndef RIFT_GEMM_DMA
-#define RIFT_GEMM_DMA 1
-#endif
-
-#ifndef RIFT_SWZ
-#define RIFT_SWZ 1
-#endif
-// LDS swizzle key of a tile row: chunk c of row r is stored at c ^ swz(r).
-// swz(r) = (r >> 1) ^ 4 (r & 1), mod 8, gives distinct positions to any 8
-// consecutive rows and to the 8 rows of equal parity among 16 consecutive
-// rows, so the 16-byte operand reads are conflict-free whether the LDS serves
-// 8 or 16 lanes per clock.
-__device__ __forceinline__ int swz(int r) {
-#if RIFT_SWZ
-    return ((r >> 1) ^ ((r & 1) << 2)) & 7;
-#else
-    return r & 7;
-#endif
-}
 
 struct GemmParams {
     const bf16_t* a;
@@ -88,30 +62,22 @@ __device__ __forceinline__ void tile_coords(int bid, int num_m, int num_n, int& 
     bn = in_group / gm;
 }
 
-// B operand of tile bn: loader chunk j (0..7) covers tile rows (t>>3) + 32 j.
-// b_base gives the matrix that chunk j reads and b_row the row inside it.
-//   QKV:    one of wq | wk | wv per tile (d % 256 == 0), rows bn*256 + r - region*d
+// B operand of tile bn, row r (0..255): b_base_row is the matrix it is read
+// from and b_row the row inside that matrix.
+//   QKV:    one of wq | wk | wv per tile (d % 256 == 0), row bn*256 + r - region*d
 //   SWIGLU: tile rows [0,64) gate, [64,128) up for output columns bn*128 + [0,64),
-//           rows [128,192) gate, [192,256) up for columns bn*128 + [64,128);
-//           with r = (t>>3) + 32 j that is gate for j in {0,1,4,5}, up otherwise
-//   RESID:  rows bn*256 + r
+//           rows [128,192) gate, [192,256) up for columns bn*128 + [64,128)
+//   RESID:  row bn*256 + r
 template <int EPI>
-__device__ __forceinline__ const bf16_t* b_base(const GemmParams& p, int bn, int j) {
+__device__ __forceinline__ const bf16_t* b_base_row(const GemmParams& p, int bn, int r) {
     if constexpr (EPI == EPI_QKV) {
         const int region = (bn * BN) / p.d;
         return region == 0 ? p.b0 : (region == 1 ? p.b1 : p.b2);
     } else if constexpr (EPI == EPI_SWIGLU) {
-        return ((j & 3) < 2) ? p.b0 : p.b1;
+        return ((r & 127) < 64) ? p.b0 : p.b1;
     } else {
         return p.b0;
     }
-}
-
-// Matrix that B-tile row r (0..255) of tile bn is read from.
-template <int EPI>
-__device__ __forceinline__ const bf16_t* b_base_row(const GemmParams& p, int bn, int r) {
-    if constexpr (EPI == EPI_SWIGLU) return ((r & 127) < 64) ? p.b0 : p.b1;
-    else return b_base<EPI>(p, bn, 0);
 }
 
 template <int EPI>
@@ -127,50 +93,86 @@ __device__ __forceinline__ int b_row(const GemmParams& p, int bn, int r) {
 }
 
 // Epilogue.  acc[m][n][i] is row 8 (i/4) + 4 (lane/32) + (i%4) and column
-// lane%32 of the 32x32 tile (m, n) of wave (wm, wn).
+// lane%32 of the 32x32 tile (m, n) of wave (wm, wn).  Rows are handled 32 at a
+// time (one m) so that every global load of a block is in flight at once.
+// pos_lds holds the clamped position of each of the tile's 256 rows (QKV).
 template <int EPI>
 __device__ __forceinline__ void epilogue(const GemmParams& p, f32x16_t (&acc)[4][4], int m0, int bn,
-                                         int wm, int wn, int lane) {
+                                         int wm, int wn, int lane, const int* pos_lds) {
     const int col_in = lane & 31;
     const int row_hi = 4 * (lane >> 5);
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
+        __builtin_amdgcn_sched_barrier(0);
+        const int r0 = wm * 128 + m * 32 + row_hi;   // tile row of i = 0
+        if constexpr (EPI == EPI_RESID) {
+            float old[16][4];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            __builtin_amdgcn_sched_barrier(0);
-            const int row = m0 + wm * 128 + m * 32 + 8 * (i >> 2) + row_hi + (i & 3);
-            if (row >= p.M) continue;
-            if constexpr (EPI == EPI_RESID) {
+            for (int i = 0; i < 16; ++i) {
+                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
+                const float* src = p.resid + (size_t)(row < p.M ? row : p.M - 1) * p.N +
+                                   bn * BN + wn * 128 + col_in;
+#pragma unroll
+                for (int n = 0; n < 4; ++n) old[i][n] = src[n * 32];
+            }
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
+                if (row >= p.M) continue;
                 float* dst = p.resid + (size_t)row * p.N + bn * BN + wn * 128 + col_in;
 #pragma unroll
-                for (int n = 0; n < 4; ++n) dst[n * 32] += acc[m][n][i];
-            } else if constexpr (EPI == EPI_SWIGLU) {
+                for (int n = 0; n < 4; ++n) dst[n * 32] = old[i][n] + acc[m][n][i];
+            }
+        } else if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
+                if (row >= p.M) continue;
                 bf16_t* dst = p.o0 + (size_t)row * p.d + bn * 128 + wn * 64 + col_in;
 #pragma unroll
                 for (int n = 0; n < 2; ++n) {
                     const float gt = acc[m][n][i];
                     const float up = acc[m][n + 2][i];
-                    const float a = gt / (1.0f + expf(-gt)) * up;
-                    dst[n * 32] = f32_to_bf16(a);
+                    dst[n * 32] = f32_to_bf16(gt / (1.0f + expf(-gt)) * up);
                 }
-            } else {  // QKV
-                const int region = (bn * BN) / p.d;
-                const int head_col = (bn * BN - region * p.d) + wn * 128;  // first column of the head
-                bf16_t* out = (region == 0 ? p.o0 : (region == 1 ? p.o1 : p.o2)) +
-                              (size_t)row * p.d + head_col + col_in;
-                if (region == 2) {
+            }
+        } else {  // QKV
+            const int region = (bn * BN) / p.d;
+            const int head_col = (bn * BN - region * p.d) + wn * 128;  // first column of the head
+            bf16_t* outb = (region == 0 ? p.o0 : (region == 1 ? p.o1 : p.o2)) + head_col + col_in;
+            if (region == 2) {
 #pragma unroll
-                    for (int n = 0; n < 4; ++n) out[n * 32] = f32_to_bf16(acc[m][n][i]);
-                } else {
-                    int ps = p.pos[row];
-                    ps = ps < 0 ? 0 : (ps >= p.n_pos ? p.n_pos - 1 : ps);
+                for (int i = 0; i < 16; ++i) {
+                    const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
+                    if (row >= p.M) continue;
 #pragma unroll
-                    for (int n = 0; n < 2; ++n) {
-                        const float2 cs = p.rope[(size_t)ps * 64 + n * 32 + col_in];
-                        const float x1 = acc[m][n][i];
-                        const float x2 = acc[m][n + 2][i];
-                        out[n * 32] = f32_to_bf16(x1 * cs.x - x2 * cs.y);
-                        out[n * 32 + 64] = f32_to_bf16(x2 * cs.x + x1 * cs.y);
+                    for (int n = 0; n < 4; ++n) outb[(size_t)row * p.d + n * 32] = f32_to_bf16(acc[m][n][i]);
+                }
+            } else {
+#pragma unroll
+                for (int half = 0; half < 2; ++half) {   // 8 rows at a time
+                    __builtin_amdgcn_sched_barrier(0);
+                    float2 cs[8][2];
+#pragma unroll
+                    for (int ii = 0; ii < 8; ++ii) {
+                        const int i = 8 * half + ii;
+                        const int ps = pos_lds[r0 + 8 * (i >> 2) + (i & 3)];
+#pragma unroll
+                        for (int n = 0; n < 2; ++n) cs[ii][n] = p.rope[(size_t)ps * 64 + n * 32 + col_in];
+                    }
+#pragma unroll
+                    for (int ii = 0; ii < 8; ++ii) {
+                        const int i = 8 * half + ii;
+                        const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
+                        if (row >= p.M) continue;
+                        bf16_t* out = outb + (size_t)row * p.d;
+#pragma unroll
+                        for (int n = 0; n < 2; ++n) {
+                            const float x1 = acc[m][n][i];
+                            const float x2 = acc[m][n + 2][i];
+                            out[n * 32] = f32_to_bf16(x1 * cs[ii][n].x - x2 * cs[ii][n].y);
+                            out[n * 32 + 64] = f32_to_bf16(x2 * cs[ii][n].x + x1 * cs[ii][n].y);
+                        }
                     }
                 }
             }
@@ -178,116 +180,8 @@ __device__ __forceinline__ void epilogue(const GemmParams& p, f32x16_t (&acc)[4]
     }
 }
 
-template <int EPI>
-__global__ void __launch_bounds__(256, 1) gemm_bf16_kernel(GemmParams p) {
-    extern __shared__ __align__(16) bf16_t lds[];
-    const int num_m = (p.M + BM - 1) / BM;
-    const int num_n = (EPI == EPI_SWIGLU) ? p.d / 128 : p.N / BN;
-    int bm, bn;
-    tile_coords(blockIdx.x, num_m, num_n, bm, bn);
-    const int m0 = bm * BM;
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int wm = wave >> 1;
-    const int wn = wave & 1;
-
-    // Loader: thread t moves chunks t + 256 j (j = 0..7) of each operand tile;
-    // chunk id -> row = (t >> 3) + 32 j, logical chunk = t & 7.  Offsets are
-    // 32-bit element offsets from the operand base (every operand is < 4 GB).
-    const int ld_row = tid >> 3;
-    const int ld_lc = tid & 7;
-    uint32_t a_off[8], b_off[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const int row = ld_row + 32 * j;
-        int ar = m0 + row;
-        ar = ar < p.M ? ar : p.M - 1;
-        a_off[j] = (uint32_t)ar * (uint32_t)p.K + ld_lc * 8;
-        b_off[j] = (uint32_t)b_row<EPI>(p, bn, row) * (uint32_t)p.K + ld_lc * 8;
-    }
-    // LDS position of this thread's chunk in row ld_row; rows + 32 j keep the
-    // same swizzle key (32 j is a multiple of 16), so chunk j sits 32*64*j further.
-    const int lds_w = ld_row * BK + ((ld_lc ^ swz(ld_row)) << 3);
-
-    f32x16_t acc[4][4];
-#pragma unroll
-    for (int m = 0; m < 4; ++m)
-#pragma unroll
-        for (int n = 0; n < 4; ++n)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) acc[m][n][i] = 0.f;
-
-    u32x4_t ra[8], rb[8];
-    const int nk = p.K / BK;
-
-    // prologue: stage 0
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        ra[j] = *reinterpret_cast<const u32x4_t*>(p.a + a_off[j]);
-        rb[j] = *reinterpret_cast<const u32x4_t*>(b_base<EPI>(p, bn, j) + b_off[j]);
-    }
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        *reinterpret_cast<u32x4_t*>(lds + lds_w + j * 32 * BK) = ra[j];
-        *reinterpret_cast<u32x4_t*>(lds + kTileElems + lds_w + j * 32 * BK) = rb[j];
-    }
-    __syncthreads();
-
-    // Operand reads: row wm*128 + m*32 + (lane & 31) has swizzle key
-    // swz(lane & 31), so only the k sub-step changes the offset; m and n add
-    // 32*64 per step.
-    const int rd_a = (wm * 128 + (lane & 31)) * BK;
-    const int rd_b = (wn * 128 + (lane & 31)) * BK;
-    const int hsel = lane >> 5;
-    const int key = swz(lane & 31);
-
-    for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        const bool more = kt + 1 < nk;
-        if (more) {
-            const uint32_t koff = (uint32_t)(kt + 1) * BK;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                ra[j] = *reinterpret_cast<const u32x4_t*>(p.a + (a_off[j] + koff));
-                rb[j] = *reinterpret_cast<const u32x4_t*>(b_base<EPI>(p, bn, j) + (b_off[j] + koff));
-            }
-        }
-        const bf16_t* sA = lds + cur * 2 * kTileElems;
-        const bf16_t* sB = sA + kTileElems;
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-            const int sw = ((2 * kk + hsel) ^ key) << 3;
-            bf16x8_t af[4], bf[4];
-#pragma unroll
-            for (int m = 0; m < 4; ++m)
-                af[m] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + m * 32 * BK);
-#pragma unroll
-            for (int n = 0; n < 4; ++n)
-                bf[n] = *reinterpret_cast<const bf16x8_t*>(sB + rd_b + sw + n * 32 * BK);
-#pragma unroll
-            for (int m = 0; m < 4; ++m)
-#pragma unroll
-                for (int n = 0; n < 4; ++n)
-                    acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[m], bf[n], acc[m][n], 0, 0, 0);
-        }
-        if (more) {
-            bf16_t* dA = lds + (cur ^ 1) * 2 * kTileElems;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                *reinterpret_cast<u32x4_t*>(dA + lds_w + j * 32 * BK) = ra[j];
-                *reinterpret_cast<u32x4_t*>(dA + kTileElems + lds_w + j * 32 * BK) = rb[j];
-            }
-        }
-        __syncthreads();
-    }
-
-    epilogue<EPI>(p, acc, m0, bn, wm, wn, lane);
-}
-
 // ---------------------------------------------------------------------------
-// Variant with a 4-stage LDS ring filled by global_load_lds_dwordx4 (LDS DMA).
+// Main loop: a 4-stage LDS ring filled by global_load_lds_dwordx4 (LDS DMA).
 // K advances 32 per stage; a stage holds the A and B tiles (256 rows x 64
 // bytes each, 32 KB).  Loads for stage k+3 are issued right after the barrier
 // that opens stage k, so each load has about three stages of MFMA work to land;
@@ -315,6 +209,7 @@ __device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(%0)" :
 template <int EPI>
 __global__ void __launch_bounds__(256, 1) gemm_bf16_dma_kernel(GemmParams p) {
     __shared__ __align__(16) bf16_t lds[NST * kStageElems];
+    __shared__ int pos_lds[BM];   // QKV: clamped position of each tile row
     const int num_m = (p.M + BM - 1) / BM;
     const int num_n = (EPI == EPI_SWIGLU) ? p.d / 128 : p.N / BN;
     int bm, bn;
@@ -358,6 +253,13 @@ __global__ void __launch_bounds__(256, 1) gemm_bf16_dma_kernel(GemmParams p) {
         for (int n = 0; n < 4; ++n)
 #pragma unroll
             for (int i = 0; i < 16; ++i) acc[m][n][i] = 0.f;
+
+    if constexpr (EPI == EPI_QKV) {
+        int r = m0 + tid;
+        r = r < p.M ? r : p.M - 1;
+        int ps = p.pos[r];
+        pos_lds[tid] = ps < 0 ? 0 : (ps >= p.n_pos ? p.n_pos - 1 : ps);
+    }   // read only after the main loop's barriers
 
     const int nk = p.K / BK2;
     for (int s = 0; s < 3 && s < nk; ++s) issue(s, s);
@@ -444,34 +346,18 @@ __global__ void __launch_bounds__(256, 1) gemm_bf16_dma_kernel(GemmParams p) {
         }
         mma(a1, b1);
     }
-    epilogue<EPI>(p, acc, m0, bn, wm, wn, lane);
+    epilogue<EPI>(p, acc, m0, bn, wm, wn, lane, pos_lds);
 }
 
 template <int EPI>
 hipError_t launch_gemm(const GemmParams& p, int num_n, hipStream_t st) {
     const int num_m = (p.M + BM - 1) / BM;
     if (p.M <= 0) return hipSuccess;
-#if RIFT_GEMM_DMA
     hipLaunchKernelGGL(gemm_bf16_dma_kernel<EPI>, dim3(num_m * num_n), dim3(256), 0, st, p);
-#else
-    hipLaunchKernelGGL(gemm_bf16_kernel<EPI>, dim3(num_m * num_n), dim3(256), kLdsBytes, st, p);
-#endif
     return hipGetLastError();
 }
 
 }  // namespace
-
-hipError_t gemm_bf16_init_attributes() {
-    hipError_t e;
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<EPI_QKV>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
-    if (e != hipSuccess) return e;
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<EPI_RESID>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
-    if (e != hipSuccess) return e;
-    return hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_bf16_kernel<EPI_SWIGLU>),
-                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsBytes);
-}
 
 hipError_t launch_gemm_qkv_rope(const QkvArgs& a, hipStream_t st) {
     GemmParams p{};
