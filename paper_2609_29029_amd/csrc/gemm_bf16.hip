@@ -18,6 +18,8 @@
 // Tile order: the hardware hands workgroup b to XCD b mod 8; each XCD gets a
 // contiguous range of tile ids, and tile ids walk 8 M-tiles per N-tile, so the
 // workgroups resident on one XCD share A and B panels in that XCD's L2.
+#include <type_traits>
+
 #include "launch.h"
 #include "rift_common.h"
 
@@ -30,6 +32,10 @@ constexpr int BN = 256;
 constexpr int kGroupM = 8;
 
 enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
+
+#ifndef RIFT_GEMM_K64
+#define RIFT_GEMM_K64 1
+#endif
 
 struct GemmParams {
     const bf16_t* a;
@@ -309,31 +315,49 @@ __global__ void __launch_bounds__(256, 1) gemm_bf16_dma_kernel(GemmParams p) {
     int kt = 0;
     // steady state, branch-free: when stage kt+1 opens, stages kt+2 and kt+3
     // are in flight (16 DMA instructions per lane), and stage kt+4 exists
-    // Each phase issues its 8 LDS reads between its first 8 MFMAs (MFMA first,
-    // so the wait for the previous phase's operands never waits for the new
-    // reads); sched_barrier keeps MFMAs from moving across the phases.
-    auto interleave = [] {
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);       // the other 8 MFMAs
+    // Steady state.  Each phase runs 16 MFMAs; in the shadow of each of its
+    // first 8 MFMAs it issues one LDS read for the next phase (and, in phase 2,
+    // one DMA instruction for stage kt+4), so neither reads nor DMA issue
+    // stall the MFMA pipe.  Reads come in the order a[0], b[0..3], a[1..3], the
+    // order in which the next phase's MFMAs need them.  sched_barrier pins the
+    // order.
+    auto read_one = [&](bf16x8_t (&af)[4], bf16x8_t (&bf)[4], int stage, int sw, int q) {
+        const bf16_t* sA = lds + stage * kStageElems;
+        if (q == 0) af[0] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw);
+        else if (q <= 4) bf[q - 1] = *reinterpret_cast<const bf16x8_t*>(sA + rd_b + sw + (q - 1) * 32 * BK2);
+        else af[q - 4] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + (q - 4) * 32 * BK2);
     };
+    const uint32_t ring_wave = ring + (uint32_t)wave * 4096u;
     for (; kt + 4 < nk; ++kt) {
         const int cur = kt & (NST - 1);
-        read(a1, b1, cur, sw1);
-        mma(a0, b0);
-        interleave();
+        const int nxt = (kt + 1) & (NST - 1);
         __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            acc[q >> 2][q & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[q >> 2], b0[q & 3],
+                                                                          acc[q >> 2][q & 3], 0, 0, 0);
+            if (q < 8) read_one(a1, b1, cur, sw1, q);
+            __builtin_amdgcn_sched_barrier(0);
+        }
         asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)" ::: "memory");
         wg_barrier();
-        issue(cur, kt + 4);
+        // a1/b1 are complete (lgkmcnt(0) above); an empty asm that redefines
+        // them tells the compiler so, and keeps it from waiting on the reads
+        // issued below before using them
+#pragma unroll
+        for (int m = 0; m < 4; ++m) asm volatile("" : "+v"(a1[m]), "+v"(b1[m]));
         __builtin_amdgcn_sched_barrier(0);
-        read(a0, b0, (kt + 1) & (NST - 1), sw0);
-        mma(a1, b1);
-        interleave();
-        __builtin_amdgcn_sched_barrier(0);
+        const uint32_t sb = ring_wave + (uint32_t)cur * (kStageElems * 2);
+        const size_t ko = (size_t)(kt + 4) * BK2;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            acc[q >> 2][q & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[q >> 2], b1[q & 3],
+                                                                          acc[q >> 2][q & 3], 0, 0, 0);
+            if (q < 4) dma16(asrc[q] + ko, sb + q * 1024u);
+            else if (q < 8) dma16(bsrc[q - 4] + ko, sb + BM * BK2 * 2 + (q - 4) * 1024u);
+            if (q < 8) read_one(a0, b0, nxt, sw0, q);
+            __builtin_amdgcn_sched_barrier(0);
+        }
     }
     // last stages
     for (; kt < nk; ++kt) {
@@ -349,11 +373,153 @@ __global__ void __launch_bounds__(256, 1) gemm_bf16_dma_kernel(GemmParams p) {
     epilogue<EPI>(p, acc, m0, bn, wm, wn, lane, pos_lds);
 }
 
+// ---------------------------------------------------------------------------
+// Main loop, 64-deep stages: two LDS buffers of 64 KB (A and B tiles, rows of
+// 128 bytes = one cache line of a K-contiguous operand row, so every LDS DMA
+// request reads whole lines).  Within a stage the four 16-deep sub-steps each
+// run 16 MFMAs while the next sub-step's operands are read from LDS.  The
+// barrier sits before sub-step 3: by then stage kt+1 has landed and every wave
+// has read the whole of stage kt, so sub-step 3 also issues the DMA of stage
+// kt+2 into the buffer stage kt used (one instruction per MFMA), about 64
+// MFMAs before it is needed.  LDS rows hold 8 chunks of 16 bytes; chunk c of
+// row r sits at c ^ swz8(r), conflict-free for the operand reads.
+constexpr int BK3 = 64;
+constexpr int kStage3 = 2 * BM * BK3;   // elements per stage (A then B)
+
+__device__ __forceinline__ int swz8(int r) { return ((r >> 1) ^ ((r & 1) << 2)) & 7; }
+
+template <int EPI>
+__global__ void __launch_bounds__(256, 1) gemm_bf16_k64_kernel(GemmParams p) {
+    __shared__ __align__(16) bf16_t lds[2 * kStage3];
+    __shared__ int pos_lds[BM];   // QKV: clamped position of each tile row
+    const int num_m = (p.M + BM - 1) / BM;
+    const int num_n = (EPI == EPI_SWIGLU) ? p.d / 128 : p.N / BN;
+    int bm, bn;
+    tile_coords(blockIdx.x, num_m, num_n, bm, bn);
+    const int m0 = bm * BM;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 1;
+    const int wn = wave & 1;
+
+    // DMA: instruction j (0..7) of this wave moves tile rows 8 (8 wave + j) +
+    // (lane >> 3), lane fetching logical chunk (lane & 7) ^ swz8(row).
+    const bf16_t* asrc[8];
+    const bf16_t* bsrc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int row = 8 * (8 * wave + j) + (lane >> 3);
+        const int c = (lane & 7) ^ swz8(row);
+        int ar = m0 + row;
+        ar = ar < p.M ? ar : p.M - 1;
+        asrc[j] = p.a + (size_t)ar * p.K + c * 8;
+        bsrc[j] = b_base_row<EPI>(p, bn, row) + (size_t)b_row<EPI>(p, bn, row) * p.K + c * 8;
+    }
+    const uint32_t ring_wave = (uint32_t)(uintptr_t)lds + (uint32_t)wave * 8192u;
+    auto dma_one = [&](int buf, int kt, int q) {   // q = 0..15: A chunks 0..7 then B chunks 0..7
+        const uint32_t sb = ring_wave + (uint32_t)buf * (kStage3 * 2);
+        const size_t ko = (size_t)kt * BK3;
+        if (q < 8) dma16(asrc[q] + ko, sb + q * 1024u);
+        else dma16(bsrc[q - 8] + ko, sb + BM * BK3 * 2 + (q - 8) * 1024u);
+    };
+
+    if constexpr (EPI == EPI_QKV) {
+        int r = m0 + tid;
+        r = r < p.M ? r : p.M - 1;
+        int ps = p.pos[r];
+        pos_lds[tid] = ps < 0 ? 0 : (ps >= p.n_pos ? p.n_pos - 1 : ps);
+    }
+
+    f32x16_t acc[4][4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int n = 0; n < 4; ++n)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[m][n][i] = 0.f;
+
+    const int nk = p.K / BK3;
+    const int rd_a = (wm * 128 + (lane & 31)) * BK3;
+    const int rd_b = BM * BK3 + (wn * 128 + (lane & 31)) * BK3;
+    const int key = swz8(lane & 15);
+    const int hsel = lane >> 5;
+    // logical chunk of sub-step kk for this lane: 2 kk + hsel
+    auto swk = [&](int kk) { return ((2 * kk + hsel) ^ key) << 3; };
+    bf16x8_t fa[2][4], fb[2][4];
+    // one LDS read (order a[0], b[0..3], a[1..3]) of sub-step kk of buffer buf
+    auto read_one = [&](int slot, int buf, int kk, int q) {
+        const bf16_t* sA = lds + buf * kStage3;
+        const int sw = swk(kk);
+        if (q == 0) fa[slot][0] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw);
+        else if (q <= 4) fb[slot][q - 1] = *reinterpret_cast<const bf16x8_t*>(sA + rd_b + sw + (q - 1) * 32 * BK3);
+        else fa[slot][q - 4] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + (q - 4) * 32 * BK3);
+    };
+    auto mfma_one = [&](int slot, int q) {
+        acc[q >> 2][q & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][q >> 2], fb[slot][q & 3],
+                                                                      acc[q >> 2][q & 3], 0, 0, 0);
+    };
+
+    // prologue: stage 0 (and stage 1 when it exists) in flight, stage 0 landed
+#pragma unroll
+    for (int q = 0; q < 16; ++q) dma_one(0, 0, q);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    wg_barrier();
+    if (nk > 1) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) dma_one(1, 1, q);
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) read_one(0, 0, 0, q);
+
+    // one stage; kDma / kMore say whether stage kt+2 gets loaded and whether
+    // sub-step 0 of stage kt+1 gets read (both true except in the last two)
+    auto stage = [&](int kt, auto kDma, auto kMore) {
+        const int cur = kt & 1;
+#pragma unroll
+        for (int kk = 0; kk < 3; ++kk) {
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                mfma_one(kk & 1, q);
+                if (q < 8) read_one((kk + 1) & 1, cur, kk + 1, q);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        // stage kt+1 landed (its DMA is the only one outstanding) and every
+        // wave has read all of stage kt
+        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+        wg_barrier();
+#pragma unroll
+        for (int m = 0; m < 4; ++m) asm volatile("" : "+v"(fa[1][m]), "+v"(fb[1][m]));
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            mfma_one(1, q);
+            if constexpr (decltype(kDma)::value) dma_one(cur, kt + 2, q);
+            if constexpr (decltype(kMore)::value) { if (q < 8) read_one(0, cur ^ 1, 0, q); }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    using T_ = std::true_type;
+    using F_ = std::false_type;
+    int kt = 0;
+    for (; kt + 2 < nk; ++kt) stage(kt, T_{}, T_{});
+    if (kt + 1 < nk) stage(kt++, F_{}, T_{});
+    stage(kt, F_{}, F_{});
+    epilogue<EPI>(p, acc, m0, bn, wm, wn, lane, pos_lds);
+}
+
 template <int EPI>
 hipError_t launch_gemm(const GemmParams& p, int num_n, hipStream_t st) {
     const int num_m = (p.M + BM - 1) / BM;
     if (p.M <= 0) return hipSuccess;
+#if RIFT_GEMM_K64
+    hipLaunchKernelGGL(gemm_bf16_k64_kernel<EPI>, dim3(num_m * num_n), dim3(256), 0, st, p);
+#else
     hipLaunchKernelGGL(gemm_bf16_dma_kernel<EPI>, dim3(num_m * num_n), dim3(256), 0, st, p);
+#endif
     return hipGetLastError();
 }
 
