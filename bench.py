@@ -41,10 +41,11 @@ def stage_flops(T: int, d: int, ffn: int, seq_lens) -> dict:
             "gate_up_swiglu": 2 * T * d * 2 * ffn, "down_proj": 2 * T * ffn * d}
 
 
-def cpu_baseline(w, sc, seq_lens_by_tier, n_tiles_sample: int) -> dict:
+def cpu_baseline(w, sc, seq_lens_by_tier, n_tiles_sample: int, n_layers_sample: int) -> dict:
     """The oracle as it stands, on a bounded sample of the same workload:
-    Stage 1 and selection on `n_tiles_sample` tiles, and one decoder layer on
-    one prompt of each budget tier; extrapolated to the whole query."""
+    Stage 1 and selection on `n_tiles_sample` tiles, and `n_layers_sample`
+    decoder layers on one prompt of each budget tier; extrapolated to the whole
+    query (every layer costs the same)."""
     import synth
     from oracle import rift_oracle as O
     try:
@@ -64,17 +65,19 @@ def cpu_baseline(w, sc, seq_lens_by_tier, n_tiles_sample: int) -> dict:
     W = {k: synth.to_f64(v, w.dtype) for k, v in synth.make_layer(w, 0).items()}
     rng = np.random.default_rng(0)
     t_prefill = 0.0
+    n_ls = max(1, min(n_layers_sample, m.n_layers))
     for L, count in seq_lens_by_tier:
         x = rng.standard_normal((L, m.d))
         t0 = time.perf_counter()
-        O.decoder_layer(x, W, m.n_heads, m.head_dim, m.rms_eps, m.rope_base, np.arange(L))
-        t_prefill += (time.perf_counter() - t0) * count * m.n_layers
+        for _ in range(n_ls):
+            x = O.decoder_layer(x, W, m.n_heads, m.head_dim, m.rms_eps, m.rope_base, np.arange(L))
+        t_prefill += (time.perf_counter() - t0) * count * m.n_layers / n_ls
     total = t_stage1 + t_prefill
     retained = sum(L - w.n_sys - w.n_qry for L, c in seq_lens_by_tier for _ in range(c))
     return {"value": retained / total, "unit": "tokens/s", "cores": int(blas_threads),
             "kind": "oracle",
             "sample": (f"float64 NumPy oracle: Stage 1 + selection on {n_tiles_sample} of "
-                       f"{w.n_tiles} tiles, one decoder layer on one prompt per budget tier "
+                       f"{w.n_tiles} tiles, {n_ls} decoder layers on one prompt per budget tier "
                        f"(lengths {[L for L, _ in seq_lens_by_tier]}); extrapolated to "
                        f"{w.n_tiles} tiles and {sum(c for _, c in seq_lens_by_tier)} prompts x "
                        f"{m.n_layers} layers = {total:.1f} s per query; Stage 1 runs on one "
@@ -88,7 +91,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="scene20_l32")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-tiles", type=int, default=8)
+    ap.add_argument("--cpu-sample-tiles", type=int, default=64)
+    ap.add_argument("--cpu-sample-layers", type=int, default=4)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the Rift path here is a single-GPU build "
@@ -220,7 +224,7 @@ def main() -> int:
             tiers[L] = tiers.get(L, 0) + 1
         t_cpu = time.perf_counter()
         out["cpu_baseline"] = cpu_baseline(w, sc, sorted(tiers.items(), reverse=True),
-                                           args.cpu_sample_tiles)
+                                           args.cpu_sample_tiles, args.cpu_sample_layers)
         log(f"cpu baseline {time.perf_counter() - t_cpu:.1f} s")
     print(json.dumps(out), flush=True)
     return 0

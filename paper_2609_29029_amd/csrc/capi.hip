@@ -80,7 +80,7 @@ rift_status check_cfg(const rift_model_cfg* cfg) {
     if (cfg->dt == RIFT_BF16) {
         if (cfg->head_dim != 128 || cfg->d % 256 != 0 || cfg->ffn % 128 != 0)
             return RIFT_ERR_UNSUPPORTED;
-        if ((uint64_t)cfg->d * cfg->ffn >= (1ull << 32)) return RIFT_ERR_UNSUPPORTED;
+        if ((uint64_t)cfg->d * cfg->ffn >= (1ull << 31)) return RIFT_ERR_UNSUPPORTED;
     } else {
         if ((cfg->head_dim != 64 && cfg->head_dim != 128) || cfg->d % 64 != 0 || cfg->ffn % 16 != 0)
             return RIFT_ERR_UNSUPPORTED;
@@ -229,8 +229,9 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
     if (x_dt != c.dt && x_dt != RIFT_F32) return RIFT_ERR_DTYPE;
     if (total_tokens < 0 || n_seq < 0 || max_seqlen < 1 || max_seqlen > 65536)
         return RIFT_ERR_SHAPE;
+    // the bf16 GEMMs address operands with 32-bit byte offsets
     if (c.dt == RIFT_BF16 && (uint64_t)total_tokens * (uint64_t)(c.d > c.ffn ? c.d : c.ffn) >=
-                                 (1ull << 32))
+                                 (1ull << 31))
         return RIFT_ERR_UNSUPPORTED;
     if (total_tokens == 0) return RIFT_OK;
     if (x_in == nullptr || cu_seqlens == nullptr || position_ids == nullptr ||

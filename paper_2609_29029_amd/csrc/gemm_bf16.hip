@@ -36,6 +36,9 @@ enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
 #ifndef RIFT_GEMM_K64
 #define RIFT_GEMM_K64 1
 #endif
+#ifndef RIFT_GEMM_W8
+#define RIFT_GEMM_W8 1
+#endif
 
 struct GemmParams {
     const bf16_t* a;
@@ -206,7 +209,18 @@ __device__ __forceinline__ int swz4(int r) { return ((r >> 2) ^ (r & 2)) & 3; }
 // 16 bytes per lane from global memory to LDS address lds_addr + 16 * lane.
 __device__ __forceinline__ void dma16(const void* g, uint32_t lds_addr) {
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
-                 :: "s"(lds_addr), "v"(g) : "memory", "m0");
+                 :: "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(g) : "memory", "m0");
+}
+// Same, saddr form: 64-bit wave-uniform base plus a 32-bit per-lane byte
+// offset (the hardware adds them; offsets stay below 2^31 by the host checks).
+__device__ __forceinline__ void dma16s(const void* base, uint32_t voff, uint32_t lds_addr) {
+    const uint64_t b = (uint64_t)(uintptr_t)base;
+    // readfirstlane returns a signed int: go through uint32_t so the low word is
+    // zero-extended (sign extension would corrupt the upper half of the address)
+    const uint64_t ub = (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b) |
+                        ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32)) << 32);
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :: "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(ub) : "memory", "m0");
 }
 __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 template <int N>
@@ -511,11 +525,215 @@ __global__ void __launch_bounds__(256, 1) gemm_bf16_k64_kernel(GemmParams p) {
     epilogue<EPI>(p, acc, m0, bn, wm, wn, lane, pos_lds);
 }
 
+// ---------------------------------------------------------------------------
+// Eight-wave variant (two waves per SIMD, so one wave's LDS or DMA issue
+// stalls are covered by the other's MFMAs).  Same tile, stages and order of
+// accumulation; waves are 2 (M) x 4 (N), each 128 rows x 64 columns, its two
+// 32-column blocks at tile columns c0 and c0 + 64 with
+// c0 = 128 (wn >> 1) + 32 (wn & 1), so the RoPE pairs (j, j + 64) of a head and
+// the gate/up pairs of SwiGLU sit in the same lane.
+__device__ __forceinline__ int w8_c0(int wn) { return 128 * (wn >> 1) + 32 * (wn & 1); }
+
+template <int EPI>
+__device__ __forceinline__ void epilogue_w8(const GemmParams& p, f32x16_t (&acc)[4][2], int m0, int bn,
+                                            int wm, int wn, int lane, const int* pos_lds) {
+    const int col_in = lane & 31;
+    const int row_hi = 4 * (lane >> 5);
+    const int c0 = w8_c0(wn);
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+        __builtin_amdgcn_sched_barrier(0);
+        const int r0 = wm * 128 + m * 32 + row_hi;   // tile row of i = 0
+        if constexpr (EPI == EPI_RESID) {
+            float old[16][2];
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
+                const float* src = p.resid + (size_t)(row < p.M ? row : p.M - 1) * p.N + bn * BN + c0 + col_in;
+#pragma unroll
+                for (int n = 0; n < 2; ++n) old[i][n] = src[n * 64];
+            }
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
+                if (row >= p.M) continue;
+                float* dst = p.resid + (size_t)row * p.N + bn * BN + c0 + col_in;
+#pragma unroll
+                for (int n = 0; n < 2; ++n) dst[n * 64] = old[i][n] + acc[m][n][i];
+            }
+        } else if constexpr (EPI == EPI_SWIGLU) {
+            const int oc = bn * 128 + 64 * (wn >> 1) + 32 * (wn & 1) + col_in;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
+                if (row >= p.M) continue;
+                const float gt = acc[m][0][i];
+                const float up = acc[m][1][i];
+                p.o0[(size_t)row * p.d + oc] = f32_to_bf16(gt / (1.0f + expf(-gt)) * up);
+            }
+        } else {  // QKV
+            const int region = (bn * BN) / p.d;
+            const int j = 32 * (wn & 1) + col_in;                                     // 0..63 in the head
+            bf16_t* outb = (region == 0 ? p.o0 : (region == 1 ? p.o1 : p.o2)) +
+                           (bn * BN - region * p.d) + 128 * (wn >> 1) + j;
+            if (region == 2) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
+                    if (row >= p.M) continue;
+#pragma unroll
+                    for (int n = 0; n < 2; ++n) outb[(size_t)row * p.d + n * 64] = f32_to_bf16(acc[m][n][i]);
+                }
+            } else {
+                float2 cs[16];
+#pragma unroll
+                for (int i = 0; i < 16; ++i) cs[i] = p.rope[(size_t)pos_lds[r0 + 8 * (i >> 2) + (i & 3)] * 64 + j];
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
+                    if (row >= p.M) continue;
+                    const float x1 = acc[m][0][i];
+                    const float x2 = acc[m][1][i];
+                    bf16_t* out = outb + (size_t)row * p.d;
+                    out[0] = f32_to_bf16(x1 * cs[i].x - x2 * cs[i].y);
+                    out[64] = f32_to_bf16(x2 * cs[i].x + x1 * cs[i].y);
+                }
+            }
+        }
+    }
+}
+
+template <int EPI>
+__global__ void __launch_bounds__(512, 1) gemm_bf16_w8_kernel(GemmParams p) {
+    __shared__ __align__(16) bf16_t lds[2 * kStage3];
+    __shared__ int pos_lds[BM];   // QKV: clamped position of each tile row
+    const int num_m = (p.M + BM - 1) / BM;
+    const int num_n = (EPI == EPI_SWIGLU) ? p.d / 128 : p.N / BN;
+    int bm, bn;
+    tile_coords(blockIdx.x, num_m, num_n, bm, bn);
+    const int m0 = bm * BM;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 2;
+    const int wn = wave & 3;
+
+    // DMA: instruction j (0..3) of this wave moves A-tile rows 8 (4 wave + j) +
+    // (lane >> 3) and instruction 4 + j the same B-tile rows.
+    // Per-lane byte offsets are fixed for the whole K loop; the stage's K
+    // offset goes into the wave-uniform base.
+    uint32_t aoff[4], boff[4];
+    const bf16_t* bbase[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int row = 8 * (4 * wave + j) + (lane >> 3);
+        const int c = (lane & 7) ^ swz8(row);
+        int ar = m0 + row;
+        ar = ar < p.M ? ar : p.M - 1;
+        aoff[j] = ((uint32_t)ar * (uint32_t)p.K + (uint32_t)c * 8u) * 2u;
+        boff[j] = ((uint32_t)b_row<EPI>(p, bn, row) * (uint32_t)p.K + (uint32_t)c * 8u) * 2u;
+        bbase[j] = b_base_row<EPI>(p, bn, 8 * (4 * wave + j));   // one matrix per 8-row group
+    }
+    const uint32_t ring_wave = (uint32_t)(uintptr_t)lds + (uint32_t)wave * 4096u;
+    auto dma_one = [&](int buf, int kt, int q) {   // q = 0..7: A chunks 0..3 then B chunks 0..3
+        const uint32_t sb = ring_wave + (uint32_t)buf * (kStage3 * 2);
+        const size_t ko = (size_t)kt * BK3;
+        if (q < 4) dma16s(p.a + ko, aoff[q], sb + q * 1024u);
+        else dma16s(bbase[q - 4] + ko, boff[q - 4], sb + BM * BK3 * 2 + (q - 4) * 1024u);
+    };
+
+    if constexpr (EPI == EPI_QKV) {
+        if (tid < BM) {
+            int r = m0 + tid;
+            r = r < p.M ? r : p.M - 1;
+            int ps = p.pos[r];
+            pos_lds[tid] = ps < 0 ? 0 : (ps >= p.n_pos ? p.n_pos - 1 : ps);
+        }
+    }
+
+    f32x16_t acc[4][2];
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int n = 0; n < 2; ++n)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[m][n][i] = 0.f;
+
+    const int nk = p.K / BK3;
+    const int rd_a = (wm * 128 + (lane & 31)) * BK3;
+    const int rd_b = BM * BK3 + (w8_c0(wn) + (lane & 31)) * BK3;
+    const int key = swz8(lane & 15);
+    const int hsel = lane >> 5;
+    auto swk = [&](int kk) { return ((2 * kk + hsel) ^ key) << 3; };
+    bf16x8_t fa[2][4], fb[2][2];
+    // one LDS read (order a[0], b[0], b[1], a[1..3]) of sub-step kk of buffer buf
+    auto read_one = [&](int slot, int buf, int kk, int q) {
+        const bf16_t* sA = lds + buf * kStage3;
+        const int sw = swk(kk);
+        if (q == 0) fa[slot][0] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw);
+        else if (q <= 2) fb[slot][q - 1] = *reinterpret_cast<const bf16x8_t*>(sA + rd_b + sw + (q - 1) * 64 * BK3);
+        else fa[slot][q - 2] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + (q - 2) * 32 * BK3);
+    };
+    auto mfma_one = [&](int slot, int q) {   // q = 0..7: (m, n) = (q >> 1, q & 1)
+        acc[q >> 1][q & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][q >> 1], fb[slot][q & 1],
+                                                                      acc[q >> 1][q & 1], 0, 0, 0);
+    };
+
+#pragma unroll
+    for (int q = 0; q < 8; ++q) dma_one(0, 0, q);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    wg_barrier();
+    if (nk > 1) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) dma_one(1, 1, q);
+    }
+#pragma unroll
+    for (int q = 0; q < 6; ++q) read_one(0, 0, 0, q);
+
+    auto stage = [&](int kt, auto kDma, auto kMore) {
+        const int cur = kt & 1;
+#pragma unroll
+        for (int kk = 0; kk < 3; ++kk) {
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                mfma_one(kk & 1, q);
+                if (q < 6) read_one((kk + 1) & 1, cur, kk + 1, q);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+        wg_barrier();
+#pragma unroll
+        for (int m = 0; m < 4; ++m) asm volatile("" : "+v"(fa[1][m]));
+#pragma unroll
+        for (int n = 0; n < 2; ++n) asm volatile("" : "+v"(fb[1][n]));
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            mfma_one(1, q);
+            if constexpr (decltype(kDma)::value) dma_one(cur, kt + 2, q);
+            if constexpr (decltype(kMore)::value) { if (q < 6) read_one(0, cur ^ 1, 0, q); }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
+    using T_ = std::true_type;
+    using F_ = std::false_type;
+    int kt = 0;
+    for (; kt + 2 < nk; ++kt) stage(kt, T_{}, T_{});
+    if (kt + 1 < nk) stage(kt++, F_{}, T_{});
+    stage(kt, F_{}, F_{});
+    epilogue_w8<EPI>(p, acc, m0, bn, wm, wn, lane, pos_lds);
+}
+
 template <int EPI>
 hipError_t launch_gemm(const GemmParams& p, int num_n, hipStream_t st) {
     const int num_m = (p.M + BM - 1) / BM;
     if (p.M <= 0) return hipSuccess;
-#if RIFT_GEMM_K64
+#if RIFT_GEMM_W8
+    hipLaunchKernelGGL(gemm_bf16_w8_kernel<EPI>, dim3(num_m * num_n), dim3(512), 0, st, p);
+#elif RIFT_GEMM_K64
     hipLaunchKernelGGL(gemm_bf16_k64_kernel<EPI>, dim3(num_m * num_n), dim3(256), 0, st, p);
 #else
     hipLaunchKernelGGL(gemm_bf16_dma_kernel<EPI>, dim3(num_m * num_n), dim3(256), 0, st, p);

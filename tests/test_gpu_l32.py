@@ -1,0 +1,91 @@
+"""The 400-tile scene through the full 32-layer LLaMA-7B-shaped stack.
+
+bf16 rounding compounds over 32 layers, so hidden states are gated per layer,
+teacher-forced: the oracle runs layer l on the GPU's own input to layer l, for
+sampled layers and prompts, and each must stay within 2e-2 (rowwise max
+relative error).  The 32-layer call must equal the chain of 32 one-layer calls
+bit for bit, and the end-to-end error against a float64 32-layer run is
+reported."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import rift_oracle as O
+from tests.rift_testlib import (f64, oracle_layer_weights, oracle_stage1, rowwise_rel_err,
+                                torch_mod, upload, upload_layer, download_stored)
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+CHECK_LAYERS = (0, 1, 15, 31)
+
+
+def test_scene20_l32_per_layer_teacher_forced():
+    import paper_2609_29029_amd as R
+    torch = torch_mod()
+    assert torch.cuda.is_available()
+    R.load()
+    w = synth.get("scene20_l32")
+    m = w.model
+    sc = synth.make_scene(w)
+    ref = oracle_stage1(sc, w.keep_count, w.tau)
+    kept = list(ref["order"][: ref["n_keep"]])
+    budgets = O.assign_budgets(len(kept), w.levels, w.tier_num, w.tier_den)
+    offs, sel = O.select_tokens(ref["r"], kept, budgets)
+    packed, cu, pos = O.compact(sc.tokens, kept, offs, sel, sc.sys, sc.qry)
+    T, d = packed.shape
+    L = int(np.diff(cu).max())
+    lens = np.diff(cu)
+    seqs = [int(np.argmin(lens)), int(np.argmax(lens))]
+
+    host_layers = {}
+    dev_layers = []
+    for l in range(m.n_layers):
+        W = synth.make_layer(w, l)
+        if l in CHECK_LAYERS:
+            host_layers[l] = W
+        dev_layers.append(upload_layer(W, w.dtype))
+        del W
+
+    cfg1 = R.model_cfg(m.d, m.n_heads, m.head_dim, m.ffn, 1, m.rms_eps, m.rope_base, R.RIFT_BF16)
+    cfg32 = R.model_cfg(m.d, m.n_heads, m.head_dim, m.ffn, m.n_layers, m.rms_eps, m.rope_base, R.RIFT_BF16)
+    ws = torch.empty(R.rift_prefill_workspace_size(cfg32, T, L), dtype=torch.uint8, device="cuda")
+    x = upload(packed, w.dtype)
+    cu_d, pos_d = torch.from_numpy(cu).cuda(), torch.from_numpy(pos).cuda()
+
+    # layer-by-layer chain; keep the inputs of the checked layers
+    cur = torch.empty(T, d, dtype=torch.float32, device="cuda")
+    inputs = {0: f64(packed, w.dtype)}
+    for l in range(m.n_layers):
+        R.rift_prefill(cfg1, [dev_layers[l]], x if l == 0 else cur, cu_d, pos_d, len(kept), L, cur, ws)
+        if l + 1 in CHECK_LAYERS:
+            torch.cuda.synchronize()
+            inputs[l + 1] = cur.cpu().numpy().astype(np.float64)
+        if l in CHECK_LAYERS:
+            torch.cuda.synchronize()
+            out = cur.cpu().numpy().astype(np.float64)
+            Wo = oracle_layer_weights(host_layers[l], w.dtype)
+            for i in seqs:
+                s0, s1 = cu[i], cu[i + 1]
+                y = O.decoder_layer(inputs[l][s0:s1], Wo, m.n_heads, m.head_dim, m.rms_eps, m.rope_base, pos[s0:s1])
+                err = rowwise_rel_err(out[s0:s1], y)
+                print(f"layer {l} seq {i} (L={s1 - s0}): teacher-forced rel err {err:.3e}")
+                assert err <= 2e-2, (l, i, err)
+    chain = cur.clone()
+
+    # the 32-layer call equals the chain bit for bit
+    full = torch.empty(T, d, dtype=torch.float32, device="cuda")
+    R.rift_prefill(cfg32, dev_layers, x, cu_d, pos_d, len(kept), L, full, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(full, chain)
+
+    # end-to-end against float64, reported (bf16 storage compounds over 32 layers)
+    i = seqs[0]
+    s0, s1 = cu[i], cu[i + 1]
+    xs = f64(packed[s0:s1], w.dtype)
+    for l in range(m.n_layers):
+        Wl = host_layers.get(l)
+        Wo = oracle_layer_weights(Wl if Wl is not None else synth.make_layer(w, l), w.dtype)
+        xs = O.decoder_layer(xs, Wo, m.n_heads, m.head_dim, m.rms_eps, m.rope_base, pos[s0:s1])
+    e2e = rowwise_rel_err(full.cpu().numpy()[s0:s1].astype(np.float64), xs)
+    print(f"end-to-end 32-layer rel err on seq {i} (L={s1 - s0}): {e2e:.3e} (reported, not gated)")
+    assert np.isfinite(e2e)
