@@ -91,8 +91,10 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="scene20_l32")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-tiles", type=int, default=64)
-    ap.add_argument("--cpu-sample-layers", type=int, default=4)
+    ap.add_argument("--cpu-sample-tiles", type=int, default=128)
+    ap.add_argument("--cpu-sample-layers", type=int, default=12)
+    ap.add_argument("--traffic-calibration", action="store_true",
+                    help="also run a 1 GiB copy kernel (for HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the Rift path here is a single-GPU build "
@@ -143,7 +145,8 @@ def main() -> int:
         q.run()
         torch.cuda.synchronize()
         log(f"warmup {i + 1}/{args.warmup}")
-    assert q.check_status() == [0, 0]
+    if args.warmup:
+        assert q.check_status() == [0, 0]
 
     K = args.steps
     top = [[E() for _ in range(5)] for _ in range(K)]
@@ -164,6 +167,16 @@ def main() -> int:
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     log(f"timed {K} steps: {(t1 - t0) * 1e3 / K:.2f} ms/step")
+    assert q.check_status() == [0, 0]
+    if args.traffic_calibration:
+        # a plain copy of known size (1 GiB read, 1 GiB written) whose FETCH_SIZE and
+        # WRITE_SIZE readings scale the counters of the prefill kernels to bytes
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+        log("traffic calibration copy: 1 GiB read + 1 GiB written")
 
     elapsed = t1 - t0
     ms_step = elapsed * 1e3 / K

@@ -6,10 +6,14 @@
 //   RESID x += A B^T in float32 (attention output and FFN down projections)
 //   SWIGLU a = silu(h wg^T) * (h wu^T), bf16 out
 //
-// Tiling: a 256x256 output tile per workgroup of 4 waves (2x2), each wave a
-// 128x128 block of 4x4 v_mfma_f32_32x32x16_bf16 tiles (256 accumulator
-// registers).  K advances 32 per stage through a ring of four LDS stages
-// (128 KB) that LDS DMA fills three stages ahead (see the kernel).
+// Tiling: a 256x256 output tile per workgroup of 8 waves (2 in M x 4 in N),
+// each wave a 128x64 block of 4x2 v_mfma_f32_32x32x16_bf16 tiles.  K advances
+// 64 per stage through two LDS buffers of 64 KB that LDS DMA (global_load_lds)
+// fills a stage ahead.  Two main loops share that layout: the eight-wave loop
+// (every wave reads its operands for the next 16-deep sub-step while it runs
+// the MFMAs of the current one) and the ping-pong loop (the two waves on a
+// SIMD alternate between a whole stage of MFMAs and the LDS reads of the next
+// stage).  The last tiles of a GEMM can run as 256x128 halves on 4 waves.
 //
 // Every output element is one fixed sequence of MFMA accumulations over K, no
 // matter which tile or batch row holds it, so a row's result does not depend on
@@ -33,12 +37,6 @@ constexpr int kGroupM = 8;
 
 enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2 };
 
-#ifndef RIFT_GEMM_K64
-#define RIFT_GEMM_K64 1
-#endif
-#ifndef RIFT_GEMM_W8
-#define RIFT_GEMM_W8 1
-#endif
 
 struct GemmParams {
     const bf16_t* a;
@@ -54,15 +52,25 @@ struct GemmParams {
     const float2* rope;
     const int* pos;
     int n_pos;
+    int num_m, num_n;   // 256x256 output tiles
+    int n_full;         // tiles 0 .. n_full-1 (grouped order) run as whole tiles,
+                        // the rest as two 256x128 halves each
 };
 
-__device__ __forceinline__ void tile_coords(int bid, int num_m, int num_n, int& bm, int& bn) {
-    const int nt = num_m * num_n;
+// Workgroup bid of a launch of `count` workgroups -> its index in that launch,
+// so that the hardware's round-robin of workgroups over the 8 XCDs gives each
+// XCD a contiguous range of indices.
+__device__ __forceinline__ int xcd_remap(int bid, int count) {
     const int xcd = bid & 7;
     const int slot = bid >> 3;
-    const int base = nt >> 3;
-    const int extra = nt & 7;
-    const int t = xcd * base + (xcd < extra ? xcd : extra) + slot;
+    const int base = count >> 3;
+    const int extra = count & 7;
+    return xcd * base + (xcd < extra ? xcd : extra) + slot;
+}
+
+// Tile t of the grouped order: 8 M-tiles per N-tile, so tiles with nearby t
+// share A and B panels.
+__device__ __forceinline__ void group_coords(int t, int num_m, int num_n, int& bm, int& bn) {
     const int group = t / (kGroupM * num_n);
     const int first_m = group * kGroupM;
     const int gm = (num_m - first_m) < kGroupM ? (num_m - first_m) : kGroupM;
@@ -77,11 +85,21 @@ __device__ __forceinline__ void tile_coords(int bid, int num_m, int num_n, int& 
 //   SWIGLU: tile rows [0,64) gate, [64,128) up for output columns bn*128 + [0,64),
 //           rows [128,192) gate, [192,256) up for columns bn*128 + [64,128)
 //   RESID:  row bn*256 + r
+// One of three pointers by a wave-uniform index, as selects on values (an
+// indexed read of the kernel-argument struct would put it in scratch memory).
+template <typename T>
+__device__ __forceinline__ T* pick3(int i, T* x, T* y, T* z) {
+    const uintptr_t a = (uintptr_t)x, b = (uintptr_t)y, c = (uintptr_t)z;
+    uintptr_t r = i == 1 ? b : a;
+    r = i == 2 ? c : r;
+    return (T*)r;
+}
+
 template <int EPI>
 __device__ __forceinline__ const bf16_t* b_base_row(const GemmParams& p, int bn, int r) {
     if constexpr (EPI == EPI_QKV) {
-        const int region = (bn * BN) / p.d;
-        return region == 0 ? p.b0 : (region == 1 ? p.b1 : p.b2);
+        const int region = __builtin_amdgcn_readfirstlane((bn * BN) / p.d);
+        return pick3(region, p.b0, p.b1, p.b2);
     } else if constexpr (EPI == EPI_SWIGLU) {
         return ((r & 127) < 64) ? p.b0 : p.b1;
     } else {
@@ -101,116 +119,6 @@ __device__ __forceinline__ int b_row(const GemmParams& p, int bn, int r) {
     }
 }
 
-// Epilogue.  acc[m][n][i] is row 8 (i/4) + 4 (lane/32) + (i%4) and column
-// lane%32 of the 32x32 tile (m, n) of wave (wm, wn).  Rows are handled 32 at a
-// time (one m) so that every global load of a block is in flight at once.
-// pos_lds holds the clamped position of each of the tile's 256 rows (QKV).
-template <int EPI>
-__device__ __forceinline__ void epilogue(const GemmParams& p, f32x16_t (&acc)[4][4], int m0, int bn,
-                                         int wm, int wn, int lane, const int* pos_lds) {
-    const int col_in = lane & 31;
-    const int row_hi = 4 * (lane >> 5);
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-        __builtin_amdgcn_sched_barrier(0);
-        const int r0 = wm * 128 + m * 32 + row_hi;   // tile row of i = 0
-        if constexpr (EPI == EPI_RESID) {
-            float old[16][4];
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
-                const float* src = p.resid + (size_t)(row < p.M ? row : p.M - 1) * p.N +
-                                   bn * BN + wn * 128 + col_in;
-#pragma unroll
-                for (int n = 0; n < 4; ++n) old[i][n] = src[n * 32];
-            }
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
-                if (row >= p.M) continue;
-                float* dst = p.resid + (size_t)row * p.N + bn * BN + wn * 128 + col_in;
-#pragma unroll
-                for (int n = 0; n < 4; ++n) dst[n * 32] = old[i][n] + acc[m][n][i];
-            }
-        } else if constexpr (EPI == EPI_SWIGLU) {
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
-                if (row >= p.M) continue;
-                bf16_t* dst = p.o0 + (size_t)row * p.d + bn * 128 + wn * 64 + col_in;
-#pragma unroll
-                for (int n = 0; n < 2; ++n) {
-                    const float gt = acc[m][n][i];
-                    const float up = acc[m][n + 2][i];
-                    dst[n * 32] = f32_to_bf16(gt / (1.0f + expf(-gt)) * up);
-                }
-            }
-        } else {  // QKV
-            const int region = (bn * BN) / p.d;
-            const int head_col = (bn * BN - region * p.d) + wn * 128;  // first column of the head
-            bf16_t* outb = (region == 0 ? p.o0 : (region == 1 ? p.o1 : p.o2)) + head_col + col_in;
-            if (region == 2) {
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
-                    if (row >= p.M) continue;
-#pragma unroll
-                    for (int n = 0; n < 4; ++n) outb[(size_t)row * p.d + n * 32] = f32_to_bf16(acc[m][n][i]);
-                }
-            } else {
-#pragma unroll
-                for (int half = 0; half < 2; ++half) {   // 8 rows at a time
-                    __builtin_amdgcn_sched_barrier(0);
-                    float2 cs[8][2];
-#pragma unroll
-                    for (int ii = 0; ii < 8; ++ii) {
-                        const int i = 8 * half + ii;
-                        const int ps = pos_lds[r0 + 8 * (i >> 2) + (i & 3)];
-#pragma unroll
-                        for (int n = 0; n < 2; ++n) cs[ii][n] = p.rope[(size_t)ps * 64 + n * 32 + col_in];
-                    }
-#pragma unroll
-                    for (int ii = 0; ii < 8; ++ii) {
-                        const int i = 8 * half + ii;
-                        const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
-                        if (row >= p.M) continue;
-                        bf16_t* out = outb + (size_t)row * p.d;
-#pragma unroll
-                        for (int n = 0; n < 2; ++n) {
-                            const float x1 = acc[m][n][i];
-                            const float x2 = acc[m][n + 2][i];
-                            out[n * 32] = f32_to_bf16(x1 * cs[ii][n].x - x2 * cs[ii][n].y);
-                            out[n * 32 + 64] = f32_to_bf16(x2 * cs[ii][n].x + x1 * cs[ii][n].y);
-                        }
-                    }
-                }
-            }
-        }
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Main loop: a 4-stage LDS ring filled by global_load_lds_dwordx4 (LDS DMA).
-// K advances 32 per stage; a stage holds the A and B tiles (256 rows x 64
-// bytes each, 32 KB).  Loads for stage k+3 are issued right after the barrier
-// that opens stage k, so each load has about three stages of MFMA work to land;
-// no registers stage the data.  Rows are 64 bytes (4 chunks of 16 bytes);
-// chunk c of row r sits at position c ^ swz4(r), which keeps the operand reads
-// of any 8 consecutive rows, and of the 4 rows r, r+4, r+8, r+12, on distinct
-// banks.  The loads are issued with inline assembly and the waits are explicit
-// (s_waitcnt vmcnt before every barrier), because the compiler would otherwise
-// wait for every outstanding LDS DMA before each LDS read.
-constexpr int BK2 = 32;
-constexpr int NST = 4;
-constexpr int kStageElems = 2 * BM * BK2;   // A tile then B tile
-
-__device__ __forceinline__ int swz4(int r) { return ((r >> 2) ^ (r & 2)) & 3; }
-
-// 16 bytes per lane from global memory to LDS address lds_addr + 16 * lane.
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds_addr) {
-    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
-                 :: "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(g) : "memory", "m0");
-}
 // Same, saddr form: 64-bit wave-uniform base plus a 32-bit per-lane byte
 // offset (the hardware adds them; offsets stay below 2^31 by the host checks).
 __device__ __forceinline__ void dma16s(const void* base, uint32_t voff, uint32_t lds_addr) {
@@ -223,312 +131,19 @@ __device__ __forceinline__ void dma16s(const void* base, uint32_t voff, uint32_t
                  :: "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(ub) : "memory", "m0");
 }
 __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
-template <int N>
-__device__ __forceinline__ void vm_wait() { asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory"); }
-
-template <int EPI>
-__global__ void __launch_bounds__(256, 1) gemm_bf16_dma_kernel(GemmParams p) {
-    __shared__ __align__(16) bf16_t lds[NST * kStageElems];
-    __shared__ int pos_lds[BM];   // QKV: clamped position of each tile row
-    const int num_m = (p.M + BM - 1) / BM;
-    const int num_n = (EPI == EPI_SWIGLU) ? p.d / 128 : p.N / BN;
-    int bm, bn;
-    tile_coords(blockIdx.x, num_m, num_n, bm, bn);
-    const int m0 = bm * BM;
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave >> 1;
-    const int wn = wave & 1;
-
-    // DMA sources: instruction j (0..3) of this wave moves tile rows
-    // 16 (4 wave + j) + (lane >> 2); the lane fetches logical chunk cl.
-    const int rsub = lane >> 2;
-    const int cl = (lane & 3) ^ swz4(rsub);
-    const bf16_t* asrc[4];
-    const bf16_t* bsrc[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int row = 16 * (4 * wave + j) + rsub;
-        int ar = m0 + row;
-        ar = ar < p.M ? ar : p.M - 1;
-        asrc[j] = p.a + (size_t)ar * p.K + cl * 8;
-        bsrc[j] = b_base_row<EPI>(p, bn, row) + (size_t)b_row<EPI>(p, bn, row) * p.K + cl * 8;
-    }
-    const uint32_t ring = (uint32_t)(uintptr_t)lds;
-    auto issue = [&](int stage, int kt) {
-        const uint32_t sb = ring + (uint32_t)stage * (kStageElems * 2) + (uint32_t)wave * 4096u;
-        const size_t ko = (size_t)kt * BK2;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) dma16(asrc[j] + ko, sb + j * 1024u);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) dma16(bsrc[j] + ko, sb + BM * BK2 * 2 + j * 1024u);
-    };
-
-    f32x16_t acc[4][4];
-#pragma unroll
-    for (int m = 0; m < 4; ++m)
-#pragma unroll
-        for (int n = 0; n < 4; ++n)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) acc[m][n][i] = 0.f;
-
-    if constexpr (EPI == EPI_QKV) {
-        int r = m0 + tid;
-        r = r < p.M ? r : p.M - 1;
-        int ps = p.pos[r];
-        pos_lds[tid] = ps < 0 ? 0 : (ps >= p.n_pos ? p.n_pos - 1 : ps);
-    }   // read only after the main loop's barriers
-
-    const int nk = p.K / BK2;
-    for (int s = 0; s < 3 && s < nk; ++s) issue(s, s);
-
-    // operand reads: row & 15 == lane & 15 for every (m, n), so one swizzle key
-    const int rd_a = (wm * 128 + (lane & 31)) * BK2;
-    const int rd_b = BM * BK2 + (wn * 128 + (lane & 31)) * BK2;
-    const int key = swz4(lane & 15);
-    const int hsel = lane >> 5;
-    const int sw0 = ((0 + hsel) ^ key) << 3;   // k sub-step 0: logical chunks 0, 1
-    const int sw1 = ((2 + hsel) ^ key) << 3;   // k sub-step 1: logical chunks 2, 3
-
-    bf16x8_t a0[4], b0[4], a1[4], b1[4];
-    auto read = [&](bf16x8_t (&af)[4], bf16x8_t (&bf)[4], int stage, int sw) {
-        const bf16_t* sA = lds + stage * kStageElems;
-#pragma unroll
-        for (int m = 0; m < 4; ++m)
-            af[m] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + m * 32 * BK2);
-#pragma unroll
-        for (int n = 0; n < 4; ++n)
-            bf[n] = *reinterpret_cast<const bf16x8_t*>(sA + rd_b + sw + n * 32 * BK2);
-    };
-    auto mma = [&](const bf16x8_t (&af)[4], const bf16x8_t (&bf)[4]) {
-#pragma unroll
-        for (int m = 0; m < 4; ++m)
-#pragma unroll
-            for (int n = 0; n < 4; ++n)
-                acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[m], bf[n], acc[m][n], 0, 0, 0);
-    };
-    // Wait until this wave's DMA for stage s has landed, given that the
-    // stages after s up to min(s + 2, nk - 1) have been issued, then barrier.
-    auto open_stage = [&](int s) {
-        const int after = nk - 1 - s;
-        if (after >= 2) asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)" ::: "memory");
-        else if (after == 1) asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)" ::: "memory");
-        else asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
-        wg_barrier();
-    };
-
-    // Software pipeline: sub-step 1 of stage kt is read while sub-step 0
-    // computes; stage kt+1 opens (wait, barrier, DMA of stage kt+4 into the
-    // buffer stage kt used) between the two MFMA groups, and its sub-step 0 is
-    // read while sub-step 1 of stage kt computes.
-    open_stage(0);
-    if (nk > 3) issue(3, 3);
-    read(a0, b0, 0, sw0);
-    int kt = 0;
-    // steady state, branch-free: when stage kt+1 opens, stages kt+2 and kt+3
-    // are in flight (16 DMA instructions per lane), and stage kt+4 exists
-    // Steady state.  Each phase runs 16 MFMAs; in the shadow of each of its
-    // first 8 MFMAs it issues one LDS read for the next phase (and, in phase 2,
-    // one DMA instruction for stage kt+4), so neither reads nor DMA issue
-    // stall the MFMA pipe.  Reads come in the order a[0], b[0..3], a[1..3], the
-    // order in which the next phase's MFMAs need them.  sched_barrier pins the
-    // order.
-    auto read_one = [&](bf16x8_t (&af)[4], bf16x8_t (&bf)[4], int stage, int sw, int q) {
-        const bf16_t* sA = lds + stage * kStageElems;
-        if (q == 0) af[0] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw);
-        else if (q <= 4) bf[q - 1] = *reinterpret_cast<const bf16x8_t*>(sA + rd_b + sw + (q - 1) * 32 * BK2);
-        else af[q - 4] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + (q - 4) * 32 * BK2);
-    };
-    const uint32_t ring_wave = ring + (uint32_t)wave * 4096u;
-    for (; kt + 4 < nk; ++kt) {
-        const int cur = kt & (NST - 1);
-        const int nxt = (kt + 1) & (NST - 1);
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            acc[q >> 2][q & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[q >> 2], b0[q & 3],
-                                                                          acc[q >> 2][q & 3], 0, 0, 0);
-            if (q < 8) read_one(a1, b1, cur, sw1, q);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)" ::: "memory");
-        wg_barrier();
-        // a1/b1 are complete (lgkmcnt(0) above); an empty asm that redefines
-        // them tells the compiler so, and keeps it from waiting on the reads
-        // issued below before using them
-#pragma unroll
-        for (int m = 0; m < 4; ++m) asm volatile("" : "+v"(a1[m]), "+v"(b1[m]));
-        __builtin_amdgcn_sched_barrier(0);
-        const uint32_t sb = ring_wave + (uint32_t)cur * (kStageElems * 2);
-        const size_t ko = (size_t)(kt + 4) * BK2;
-#pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            acc[q >> 2][q & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[q >> 2], b1[q & 3],
-                                                                          acc[q >> 2][q & 3], 0, 0, 0);
-            if (q < 4) dma16(asrc[q] + ko, sb + q * 1024u);
-            else if (q < 8) dma16(bsrc[q - 4] + ko, sb + BM * BK2 * 2 + (q - 4) * 1024u);
-            if (q < 8) read_one(a0, b0, nxt, sw0, q);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    }
-    // last stages
-    for (; kt < nk; ++kt) {
-        const int cur = kt & (NST - 1);
-        read(a1, b1, cur, sw1);
-        mma(a0, b0);
-        if (kt + 1 < nk) {
-            open_stage(kt + 1);
-            read(a0, b0, (kt + 1) & (NST - 1), sw0);
-        }
-        mma(a1, b1);
-    }
-    epilogue<EPI>(p, acc, m0, bn, wm, wn, lane, pos_lds);
-}
 
 // ---------------------------------------------------------------------------
-// Main loop, 64-deep stages: two LDS buffers of 64 KB (A and B tiles, rows of
-// 128 bytes = one cache line of a K-contiguous operand row, so every LDS DMA
-// request reads whole lines).  Within a stage the four 16-deep sub-steps each
-// run 16 MFMAs while the next sub-step's operands are read from LDS.  The
-// barrier sits before sub-step 3: by then stage kt+1 has landed and every wave
-// has read the whole of stage kt, so sub-step 3 also issues the DMA of stage
-// kt+2 into the buffer stage kt used (one instruction per MFMA), about 64
-// MFMAs before it is needed.  LDS rows hold 8 chunks of 16 bytes; chunk c of
+// Stages are 64 deep: two LDS buffers of 64 KB (A and B tiles, rows of 128
+// bytes = one cache line of a K-contiguous operand row, so every LDS DMA
+// request reads whole lines).  LDS rows hold 8 chunks of 16 bytes; chunk c of
 // row r sits at c ^ swz8(r), conflict-free for the operand reads.
 constexpr int BK3 = 64;
 constexpr int kStage3 = 2 * BM * BK3;   // elements per stage (A then B)
 
 __device__ __forceinline__ int swz8(int r) { return ((r >> 1) ^ ((r & 1) << 2)) & 7; }
 
-template <int EPI>
-__global__ void __launch_bounds__(256, 1) gemm_bf16_k64_kernel(GemmParams p) {
-    __shared__ __align__(16) bf16_t lds[2 * kStage3];
-    __shared__ int pos_lds[BM];   // QKV: clamped position of each tile row
-    const int num_m = (p.M + BM - 1) / BM;
-    const int num_n = (EPI == EPI_SWIGLU) ? p.d / 128 : p.N / BN;
-    int bm, bn;
-    tile_coords(blockIdx.x, num_m, num_n, bm, bn);
-    const int m0 = bm * BM;
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave >> 1;
-    const int wn = wave & 1;
-
-    // DMA: instruction j (0..7) of this wave moves tile rows 8 (8 wave + j) +
-    // (lane >> 3), lane fetching logical chunk (lane & 7) ^ swz8(row).
-    const bf16_t* asrc[8];
-    const bf16_t* bsrc[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const int row = 8 * (8 * wave + j) + (lane >> 3);
-        const int c = (lane & 7) ^ swz8(row);
-        int ar = m0 + row;
-        ar = ar < p.M ? ar : p.M - 1;
-        asrc[j] = p.a + (size_t)ar * p.K + c * 8;
-        bsrc[j] = b_base_row<EPI>(p, bn, row) + (size_t)b_row<EPI>(p, bn, row) * p.K + c * 8;
-    }
-    const uint32_t ring_wave = (uint32_t)(uintptr_t)lds + (uint32_t)wave * 8192u;
-    auto dma_one = [&](int buf, int kt, int q) {   // q = 0..15: A chunks 0..7 then B chunks 0..7
-        const uint32_t sb = ring_wave + (uint32_t)buf * (kStage3 * 2);
-        const size_t ko = (size_t)kt * BK3;
-        if (q < 8) dma16(asrc[q] + ko, sb + q * 1024u);
-        else dma16(bsrc[q - 8] + ko, sb + BM * BK3 * 2 + (q - 8) * 1024u);
-    };
-
-    if constexpr (EPI == EPI_QKV) {
-        int r = m0 + tid;
-        r = r < p.M ? r : p.M - 1;
-        int ps = p.pos[r];
-        pos_lds[tid] = ps < 0 ? 0 : (ps >= p.n_pos ? p.n_pos - 1 : ps);
-    }
-
-    f32x16_t acc[4][4];
-#pragma unroll
-    for (int m = 0; m < 4; ++m)
-#pragma unroll
-        for (int n = 0; n < 4; ++n)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) acc[m][n][i] = 0.f;
-
-    const int nk = p.K / BK3;
-    const int rd_a = (wm * 128 + (lane & 31)) * BK3;
-    const int rd_b = BM * BK3 + (wn * 128 + (lane & 31)) * BK3;
-    const int key = swz8(lane & 15);
-    const int hsel = lane >> 5;
-    // logical chunk of sub-step kk for this lane: 2 kk + hsel
-    auto swk = [&](int kk) { return ((2 * kk + hsel) ^ key) << 3; };
-    bf16x8_t fa[2][4], fb[2][4];
-    // one LDS read (order a[0], b[0..3], a[1..3]) of sub-step kk of buffer buf
-    auto read_one = [&](int slot, int buf, int kk, int q) {
-        const bf16_t* sA = lds + buf * kStage3;
-        const int sw = swk(kk);
-        if (q == 0) fa[slot][0] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw);
-        else if (q <= 4) fb[slot][q - 1] = *reinterpret_cast<const bf16x8_t*>(sA + rd_b + sw + (q - 1) * 32 * BK3);
-        else fa[slot][q - 4] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + (q - 4) * 32 * BK3);
-    };
-    auto mfma_one = [&](int slot, int q) {
-        acc[q >> 2][q & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][q >> 2], fb[slot][q & 3],
-                                                                      acc[q >> 2][q & 3], 0, 0, 0);
-    };
-
-    // prologue: stage 0 (and stage 1 when it exists) in flight, stage 0 landed
-#pragma unroll
-    for (int q = 0; q < 16; ++q) dma_one(0, 0, q);
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    wg_barrier();
-    if (nk > 1) {
-#pragma unroll
-        for (int q = 0; q < 16; ++q) dma_one(1, 1, q);
-    }
-#pragma unroll
-    for (int q = 0; q < 8; ++q) read_one(0, 0, 0, q);
-
-    // one stage; kDma / kMore say whether stage kt+2 gets loaded and whether
-    // sub-step 0 of stage kt+1 gets read (both true except in the last two)
-    auto stage = [&](int kt, auto kDma, auto kMore) {
-        const int cur = kt & 1;
-#pragma unroll
-        for (int kk = 0; kk < 3; ++kk) {
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int q = 0; q < 16; ++q) {
-                mfma_one(kk & 1, q);
-                if (q < 8) read_one((kk + 1) & 1, cur, kk + 1, q);
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        }
-        // stage kt+1 landed (its DMA is the only one outstanding) and every
-        // wave has read all of stage kt
-        asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
-        wg_barrier();
-#pragma unroll
-        for (int m = 0; m < 4; ++m) asm volatile("" : "+v"(fa[1][m]), "+v"(fb[1][m]));
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            mfma_one(1, q);
-            if constexpr (decltype(kDma)::value) dma_one(cur, kt + 2, q);
-            if constexpr (decltype(kMore)::value) { if (q < 8) read_one(0, cur ^ 1, 0, q); }
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    };
-    using T_ = std::true_type;
-    using F_ = std::false_type;
-    int kt = 0;
-    for (; kt + 2 < nk; ++kt) stage(kt, T_{}, T_{});
-    if (kt + 1 < nk) stage(kt++, F_{}, T_{});
-    stage(kt, F_{}, F_{});
-    epilogue<EPI>(p, acc, m0, bn, wm, wn, lane, pos_lds);
-}
-
 // ---------------------------------------------------------------------------
-// Eight-wave variant (two waves per SIMD, so one wave's LDS or DMA issue
-// stalls are covered by the other's MFMAs).  Same tile, stages and order of
-// accumulation; waves are 2 (M) x 4 (N), each 128 rows x 64 columns, its two
+// Wave layout: 2 (M) x 4 (N) waves, each 128 rows x 64 columns, its two
 // 32-column blocks at tile columns c0 and c0 + 64 with
 // c0 = 128 (wn >> 1) + 32 (wn & 1), so the RoPE pairs (j, j + 64) of a head and
 // the gate/up pairs of SwiGLU sit in the same lane.
@@ -572,10 +187,9 @@ __device__ __forceinline__ void epilogue_w8(const GemmParams& p, f32x16_t (&acc)
                 p.o0[(size_t)row * p.d + oc] = f32_to_bf16(gt / (1.0f + expf(-gt)) * up);
             }
         } else {  // QKV
-            const int region = (bn * BN) / p.d;
+            const int region = __builtin_amdgcn_readfirstlane((bn * BN) / p.d);
             const int j = 32 * (wn & 1) + col_in;                                     // 0..63 in the head
-            bf16_t* outb = (region == 0 ? p.o0 : (region == 1 ? p.o1 : p.o2)) +
-                           (bn * BN - region * p.d) + 128 * (wn >> 1) + j;
+            bf16_t* outb = pick3(region, p.o0, p.o1, p.o2) + (bn * BN - region * p.d) + 128 * (wn >> 1) + j;
             if (region == 2) {
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
@@ -603,52 +217,81 @@ __device__ __forceinline__ void epilogue_w8(const GemmParams& p, f32x16_t (&acc)
     }
 }
 
-template <int EPI>
-__global__ void __launch_bounds__(512, 1) gemm_bf16_w8_kernel(GemmParams p) {
+// Eight-wave main loop (two waves per SIMD, so one wave's LDS or DMA issue
+// stalls are covered by the other's MFMAs).  Within a stage the four 16-deep
+// sub-steps each run 8 MFMAs while the next sub-step's operands are read from
+// LDS.  The barrier sits before sub-step 3: by then stage kt+1 has landed and
+// every wave has read the whole of stage kt, so sub-step 3 also issues the DMA
+// of stage kt+2 into the buffer stage kt used, a stage before it is needed.
+//
+// HALF: a workgroup of 4 waves computes one half (128 columns, h = 0 or 1) of
+// a 256x256 tile, as waves (wm, 2h + (wave & 1)) of the whole-tile layout would;
+// only those 128 B rows are loaded.  Used for the last tiles of a GEMM so that
+// the final round over the CUs is half as long.
+template <int EPI, bool HALF>
+__global__ void __launch_bounds__(HALF ? 256 : 512, 1) gemm_bf16_w8_kernel(GemmParams p) {
     __shared__ __align__(16) bf16_t lds[2 * kStage3];
     __shared__ int pos_lds[BM];   // QKV: clamped position of each tile row
-    const int num_m = (p.M + BM - 1) / BM;
-    const int num_n = (EPI == EPI_SWIGLU) ? p.d / 128 : p.N / BN;
-    int bm, bn;
-    tile_coords(blockIdx.x, num_m, num_n, bm, bn);
+    int bm, bn, h = 0;
+    if constexpr (HALF) {
+        const int i = xcd_remap(blockIdx.x, 2 * (p.num_m * p.num_n - p.n_full));
+        h = i & 1;
+        group_coords(p.n_full + (i >> 1), p.num_m, p.num_n, bm, bn);
+    } else {
+        group_coords(xcd_remap(blockIdx.x, p.n_full), p.num_m, p.num_n, bm, bn);
+    }
     const int m0 = bm * BM;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave >> 2;
-    const int wn = wave & 3;
+    const int wm = HALF ? (wave >> 1) : (wave >> 2);
+    const int wn = HALF ? (2 * h + (wave & 1)) : (wave & 3);
 
-    // DMA: instruction j (0..3) of this wave moves A-tile rows 8 (4 wave + j) +
-    // (lane >> 3) and instruction 4 + j the same B-tile rows.
+    // DMA.  Whole tile: instruction j (0..3) of this wave moves A-tile rows
+    // 8 (4 wave + j) + (lane >> 3) and instruction 4 + j the same B-tile rows.
+    // Half tile: instructions 0..7 move A rows 8 (8 wave + j) + (lane >> 3),
+    // instructions 8..11 B rows 128 h + 8 (4 wave + j) + (lane >> 3).
     // Per-lane byte offsets are fixed for the whole K loop; the stage's K
-    // offset goes into the wave-uniform base.
-    uint32_t aoff[4], boff[4];
-    const bf16_t* bbase[4];
+    // offset goes into the wave-uniform base.  LDS rows sit at the same place
+    // in both modes.
+    constexpr int NA = HALF ? 8 : 4;
+    constexpr int NB = 4;
+    constexpr int NQ = NA + NB;
+    uint32_t aoff[NA], boff[NB];
+    const bf16_t* bbase[NB];
+    int arow0[NA], brow0[NB];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int row = 8 * (4 * wave + j) + (lane >> 3);
+    for (int j = 0; j < NA; ++j) {
+        arow0[j] = 8 * (NA * wave + j);
+        const int row = arow0[j] + (lane >> 3);
         const int c = (lane & 7) ^ swz8(row);
         int ar = m0 + row;
         ar = ar < p.M ? ar : p.M - 1;
         aoff[j] = ((uint32_t)ar * (uint32_t)p.K + (uint32_t)c * 8u) * 2u;
-        boff[j] = ((uint32_t)b_row<EPI>(p, bn, row) * (uint32_t)p.K + (uint32_t)c * 8u) * 2u;
-        bbase[j] = b_base_row<EPI>(p, bn, 8 * (4 * wave + j));   // one matrix per 8-row group
     }
-    const uint32_t ring_wave = (uint32_t)(uintptr_t)lds + (uint32_t)wave * 4096u;
-    auto dma_one = [&](int buf, int kt, int q) {   // q = 0..7: A chunks 0..3 then B chunks 0..3
-        const uint32_t sb = ring_wave + (uint32_t)buf * (kStage3 * 2);
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        brow0[j] = 128 * h + 8 * (4 * wave + j);
+        const int row = brow0[j] + (lane >> 3);
+        const int c = (lane & 7) ^ swz8(row);
+        boff[j] = ((uint32_t)b_row<EPI>(p, bn, row) * (uint32_t)p.K + (uint32_t)c * 8u) * 2u;
+        bbase[j] = b_base_row<EPI>(p, bn, brow0[j]);   // one matrix per 8-row group
+    }
+    const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
+    auto dma_one = [&](int buf, int kt, int q) {   // q = 0..NQ-1: A chunks then B chunks
+        const uint32_t sb = lds0 + (uint32_t)buf * (kStage3 * 2);
         const size_t ko = (size_t)kt * BK3;
-        if (q < 4) dma16s(p.a + ko, aoff[q], sb + q * 1024u);
-        else dma16s(bbase[q - 4] + ko, boff[q - 4], sb + BM * BK3 * 2 + (q - 4) * 1024u);
+        if (q < NA) dma16s(p.a + ko, aoff[q], sb + (uint32_t)arow0[q] * 128u);
+        else dma16s(bbase[q - NA] + ko, boff[q - NA], sb + BM * BK3 * 2 + (uint32_t)brow0[q - NA] * 128u);
     };
 
     if constexpr (EPI == EPI_QKV) {
-        if (tid < BM) {
-            int r = m0 + tid;
+        for (int i = tid; i < BM; i += (HALF ? 256 : 512)) {
+            int r = m0 + i;
             r = r < p.M ? r : p.M - 1;
             int ps = p.pos[r];
-            pos_lds[tid] = ps < 0 ? 0 : (ps >= p.n_pos ? p.n_pos - 1 : ps);
+            pos_lds[i] = ps < 0 ? 0 : (ps >= p.n_pos ? p.n_pos - 1 : ps);
         }
     }
 
@@ -681,12 +324,12 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_w8_kernel(GemmParams p) {
     };
 
 #pragma unroll
-    for (int q = 0; q < 8; ++q) dma_one(0, 0, q);
+    for (int q = 0; q < NQ; ++q) dma_one(0, 0, q);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     wg_barrier();
     if (nk > 1) {
 #pragma unroll
-        for (int q = 0; q < 8; ++q) dma_one(1, 1, q);
+        for (int q = 0; q < NQ; ++q) dma_one(1, 1, q);
     }
 #pragma unroll
     for (int q = 0; q < 6; ++q) read_one(0, 0, 0, q);
@@ -713,7 +356,10 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_w8_kernel(GemmParams p) {
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
             mfma_one(1, q);
-            if constexpr (decltype(kDma)::value) dma_one(cur, kt + 2, q);
+            if constexpr (decltype(kDma)::value) {
+                dma_one(cur, kt + 2, q);
+                if (q + 8 < NQ) dma_one(cur, kt + 2, q + 8);
+            }
             if constexpr (decltype(kMore)::value) { if (q < 6) read_one(0, cur ^ 1, 0, q); }
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -727,17 +373,204 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_w8_kernel(GemmParams p) {
     epilogue_w8<EPI>(p, acc, m0, bn, wm, wn, lane, pos_lds);
 }
 
+// ---------------------------------------------------------------------------
+// Ping-pong variant.  Same tile, LDS stages, wave sub-tiles and order of
+// accumulation as the eight-wave kernel, but the two waves that share a SIMD
+// take turns: while one issues the 32 MFMAs of a whole 64-deep stage from
+// registers, the other reads its operands for the next stage from LDS, and a
+// workgroup barrier separates the turns.  Waves 0-3 (rows 0-127 of the tile)
+// run one turn ahead of waves 4-7 (rows 128-255); the hardware places waves w
+// and w + 4 of a 512-thread workgroup on the same SIMD, so every SIMD holds one
+// wave of each group and its MFMA pipe is fed by one of them at every moment.
+//
+// Turn t (each ends with a barrier of all eight waves):
+//   group 0: t = 2j   reads stage j          t = 2j+1  MFMAs of stage j
+//   group 1: t = 2j+1 reads stage j          t = 2j+2  MFMAs of stage j
+// Stage j sits in buffer j mod 2 and is last read in turn 2j+1, so the LDS
+// DMA of stage j+2 is issued in turn 2j+2 (group 0 while reading stage j+1,
+// group 1 between its MFMAs of stage j) and every wave waits for its own DMA
+// at the end of turn 2j+3, before group 0 reads stage j+2.
 template <int EPI>
-hipError_t launch_gemm(const GemmParams& p, int num_n, hipStream_t st) {
-    const int num_m = (p.M + BM - 1) / BM;
+__global__ void __launch_bounds__(512, 1) gemm_bf16_pp_kernel(GemmParams p) {
+    __shared__ __align__(16) bf16_t lds[2 * kStage3];
+    __shared__ int pos_lds[BM];   // QKV: clamped position of each tile row
+    int bm, bn;
+    group_coords(xcd_remap(blockIdx.x, p.n_full), p.num_m, p.num_n, bm, bn);
+    const int m0 = bm * BM;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 2;   // also the group
+    const int wn = wave & 3;
+
+    // DMA: as the eight-wave kernel (instruction j moves A rows and B rows
+    // 8 (4 wave + j) + (lane >> 3) of the stage).
+    uint32_t aoff[4], boff[4];
+    const bf16_t* bbase[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int row = 8 * (4 * wave + j) + (lane >> 3);
+        const int c = (lane & 7) ^ swz8(row);
+        int ar = m0 + row;
+        ar = ar < p.M ? ar : p.M - 1;
+        aoff[j] = ((uint32_t)ar * (uint32_t)p.K + (uint32_t)c * 8u) * 2u;
+        boff[j] = ((uint32_t)b_row<EPI>(p, bn, row) * (uint32_t)p.K + (uint32_t)c * 8u) * 2u;
+        bbase[j] = b_base_row<EPI>(p, bn, 8 * (4 * wave + j));
+    }
+    const uint32_t ring_wave = (uint32_t)(uintptr_t)lds + (uint32_t)wave * 4096u;
+    auto dma_one = [&](int kt, int q) {   // q = 0..7: A chunks 0..3 then B chunks 0..3
+        const uint32_t sb = ring_wave + (uint32_t)(kt & 1) * (kStage3 * 2);
+        const size_t ko = (size_t)kt * BK3;
+        if (q < 4) dma16s(p.a + ko, aoff[q], sb + q * 1024u);
+        else dma16s(bbase[q - 4] + ko, boff[q - 4], sb + BM * BK3 * 2 + (q - 4) * 1024u);
+    };
+
+    if constexpr (EPI == EPI_QKV) {
+        if (tid < BM) {
+            int r = m0 + tid;
+            r = r < p.M ? r : p.M - 1;
+            int ps = p.pos[r];
+            pos_lds[tid] = ps < 0 ? 0 : (ps >= p.n_pos ? p.n_pos - 1 : ps);
+        }
+    }
+
+    f32x16_t acc[4][2];
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int n = 0; n < 2; ++n)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[m][n][i] = 0.f;
+
+    const int nk = p.K / BK3;
+    const int rd_a = (wm * 128 + (lane & 31)) * BK3;
+    const int rd_b = BM * BK3 + (w8_c0(wn) + (lane & 31)) * BK3;
+    const int key = swz8(lane & 15);
+    const int hsel = lane >> 5;
+    bf16x8_t fa[4][4], fb[4][2];   // [k sub-step][m or n]: one whole stage
+    auto read_one = [&](int kt, int r) {   // r = 0..23: sub-step r / 6, operand r % 6
+        const bf16_t* sA = lds + (kt & 1) * kStage3;
+        const int kk = r / 6, q = r % 6;
+        const int sw = ((2 * kk + hsel) ^ key) << 3;
+        if (q < 4) fa[kk][q] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + q * 32 * BK3);
+        else fb[kk][q - 4] = *reinterpret_cast<const bf16x8_t*>(sA + rd_b + sw + (q - 4) * 64 * BK3);
+    };
+    auto mfma_one = [&](int i) {   // i = 0..31: sub-step i / 8, (m, n) = ((i >> 1) & 3, i & 1)
+        const int kk = i >> 3, m = (i >> 1) & 3, n = i & 1;
+        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk][m], fb[kk][n], acc[m][n], 0, 0, 0);
+    };
+    auto turn_end = [&]() {
+        __builtin_amdgcn_sched_barrier(0);
+        wg_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    // reads of stage kt; with kDma, this wave's share of the DMA of stage kt + 1
+    auto read_turn = [&](int kt, auto kDma) {
+#pragma unroll
+        for (int r = 0; r < 24; ++r) {
+            read_one(kt, r);
+            if constexpr (decltype(kDma)::value) { if (r % 3 == 2) dma_one(kt + 1, r / 3); }
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    };
+    // MFMAs of stage kt; with kDma, this wave's share of the DMA of stage kt + 2
+    auto mfma_turn = [&](int kt, auto kDma) {
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int i = 0; i < 32; ++i) {
+            mfma_one(i);
+            if constexpr (decltype(kDma)::value) { if ((i & 3) == 3) dma_one(kt + 2, i >> 2); }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        __builtin_amdgcn_s_setprio(0);
+    };
+    using T_ = std::true_type;
+    using F_ = std::false_type;
+
+    // prologue: stages 0 and 1 in flight, wait for stage 0
+#pragma unroll
+    for (int q = 0; q < 8; ++q) dma_one(0, q);
+    if (nk > 1) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) dma_one(1, q);
+        asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    } else {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+    turn_end();
+
+    if (wm == 0) {
+        // stage 1 was issued by the prologue; stages 2 .. nk-1 here
+        auto step = [&](int kt, auto kDma) {
+            read_turn(kt, kDma);
+            turn_end();
+            mfma_turn(kt, F_{});
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            turn_end();
+        };
+        step(0, F_{});
+        int kt = 1;
+        for (; kt + 1 < nk; ++kt) step(kt, T_{});
+        if (kt < nk) step(kt, F_{});
+    } else {
+        turn_end();
+        auto step = [&](int kt, auto kDma) {
+            read_turn(kt, F_{});
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            turn_end();
+            mfma_turn(kt, kDma);
+        };
+        int kt = 0;
+        for (; kt + 2 < nk; ++kt) {
+            step(kt, T_{});
+            turn_end();
+        }
+        if (kt + 1 < nk) {
+            step(kt++, F_{});
+            turn_end();
+        }
+        step(kt, F_{});
+    }
+    epilogue_w8<EPI>(p, acc, m0, bn, wm, wn, lane, pos_lds);
+}
+
+int cu_count() {
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    if (cache[dev] == 0) {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+        cache[dev] = n;
+    }
+    return cache[dev];
+}
+
+// Whole 256x256 tiles first (ping-pong kernel for the QKV and gate/up GEMMs,
+// eight-wave kernel for the residual ones), then, if the tiles of the last
+// round over the CUs fill at most half of it, those tiles as two 256x128
+// halves each, so that round takes about half as long.  Every output element
+// is accumulated in the same order by all three kernels.
+template <int EPI>
+hipError_t launch_gemm(GemmParams p, int num_n, hipStream_t st) {
     if (p.M <= 0) return hipSuccess;
-#if RIFT_GEMM_W8
-    hipLaunchKernelGGL(gemm_bf16_w8_kernel<EPI>, dim3(num_m * num_n), dim3(512), 0, st, p);
-#elif RIFT_GEMM_K64
-    hipLaunchKernelGGL(gemm_bf16_k64_kernel<EPI>, dim3(num_m * num_n), dim3(256), 0, st, p);
-#else
-    hipLaunchKernelGGL(gemm_bf16_dma_kernel<EPI>, dim3(num_m * num_n), dim3(256), 0, st, p);
-#endif
+    p.num_m = (p.M + BM - 1) / BM;
+    p.num_n = num_n;
+    const int nt = p.num_m * num_n;
+    const int cus = cu_count();
+    const int rem = nt % cus;
+    p.n_full = (2 * rem <= cus) ? nt - rem : nt;
+    if (p.n_full > 0) {
+        if constexpr (EPI == EPI_RESID)
+            hipLaunchKernelGGL((gemm_bf16_w8_kernel<EPI, false>), dim3(p.n_full), dim3(512), 0, st, p);
+        else
+            hipLaunchKernelGGL(gemm_bf16_pp_kernel<EPI>, dim3(p.n_full), dim3(512), 0, st, p);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (nt > p.n_full)
+        hipLaunchKernelGGL((gemm_bf16_w8_kernel<EPI, true>), dim3(2 * (nt - p.n_full)), dim3(256), 0, st, p);
     return hipGetLastError();
 }
 
