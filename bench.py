@@ -28,6 +28,22 @@ METRIC = "retained vision tokens prefilled/sec + ms per 400-tile scene query, 1 
 PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 STAGES = ("qkv_rope", "attention", "out_proj", "gate_up_swiglu", "down_proj")
+KERNEL_NAMES = {"qkv_rope": "QKV+RoPE GEMM (gemm_bf16_pp_kernel<0> + half-tile tail)",
+                "attention": "varlen causal attention (attn_bf16_kernel)",
+                "out_proj": "output projection + residual (gemm_bf16_w8_kernel<1> + half-tile tail)",
+                "gate_up_swiglu": "gate/up+SwiGLU GEMM (gemm_bf16_pp_kernel<2> + half-tile tail)",
+                "down_proj": "down projection + residual (gemm_bf16_w8_kernel<1> + half-tile tail)"}
+GEMM_SRC = os.path.join(ROOT, "paper_2609_29029_amd", "csrc", "gemm_bf16.hip")
+
+# HBM traffic of one gate/up+SwiGLU launch at the 400-tile workload (whole tiles
+# and the half-tile tail together), from two rocprofv3 --pmc runs of this
+# script with --traffic-calibration (FETCH_SIZE, then WRITE_SIZE), each scaled
+# by what the counter reads for the 1 GiB calibration copy (FETCH_SIZE reads
+# half the bytes, WRITE_SIZE all of them).  Valid only for the GEMM source it
+# was measured on, identified by its SHA-256; otherwise reported as null.
+TRAFFIC = {"stage": "gate_up_swiglu",
+           "gemm_src_sha256": "58ec944c843f14a1d631e206da91a465c9cdc8ce9c2d1d891f82210c7c3c1544",
+           "bytes": 7.0914e9}
 
 
 def log(*a):
@@ -92,7 +108,7 @@ def main() -> int:
     ap.add_argument("--workload", default="scene20_l32")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tiles", type=int, default=128)
-    ap.add_argument("--cpu-sample-layers", type=int, default=12)
+    ap.add_argument("--cpu-sample-layers", type=int, default=16)
     ap.add_argument("--traffic-calibration", action="store_true",
                     help="also run a 1 GiB copy kernel (for HBM counter calibration)")
     args = ap.parse_args()
@@ -201,6 +217,11 @@ def main() -> int:
                       "frac_bf16_peak": round(fl[n] / (per_launch[n] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
                   for n in STAGES}
     dom = max(STAGES, key=lambda n: per_launch[n])
+    import hashlib
+    with open(GEMM_SRC, "rb") as f:
+        src_sha = hashlib.sha256(f.read()).hexdigest()
+    traffic = (TRAFFIC["bytes"] if dom == TRAFFIC["stage"] and src_sha == TRAFFIC["gemm_src_sha256"]
+               and w.name == "scene20_l32" else None)
     achieved = fl[dom] / (per_launch[dom] * 1e-3) / 1e12
     prefill_flops = sum(fl.values()) * m.n_layers
     # HBM-bound stages: algorithmic bytes
@@ -222,10 +243,9 @@ def main() -> int:
                                f"{m.n_layers}-layer LLaMA-7B-shaped varlen prefill",
                    "retained_vision_tokens": n_ret, "packed_tokens": T, "sequences": q.n_keep,
                    "max_seqlen": q.max_seqlen, "prefill_tflop": round(prefill_flops / 1e12, 2)},
-        "roofline": {"bound": "mfma", "kernel": f"prefill {dom} (gemm_bf16_kernel)" if dom != "attention"
-                     else "attention", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+        "roofline": {"bound": "mfma", "kernel": KERNEL_NAMES[dom], "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None},
+                     "traffic": traffic},
         "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
         "prefill_stages": stage_roof,
         "prefill_frac_bf16_peak": round(prefill_flops / (stage_ms["prefill"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),

@@ -69,6 +69,58 @@ rmsnorm_kernel(const void* __restrict__ x, float* __restrict__ resid, const void
     }
 }
 
+// Same operation with the row held in registers (d = 256 NCH): every load of
+// the row is issued before the first use, the row is read from memory once,
+// and the squares are summed in the same lane-strided order as above.
+template <bool XBF16, bool GBF16, bool HBF16, int NCH>
+__global__ void __launch_bounds__(256)
+rmsnorm_reg_kernel(const void* __restrict__ x, float* __restrict__ resid, const void* __restrict__ g,
+                   void* __restrict__ h, int rows, float eps) {
+    constexpr int d = 256 * NCH;
+    const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (row >= rows) return;
+    const size_t base = (size_t)row * d + lane * 4;
+    f32x4_t v[NCH];
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        if constexpr (XBF16) {
+            const uint2 w = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(x) + base + 256 * c);
+            v[c] = f32x4_t{bf16_lo(w.x), bf16_hi(w.x), bf16_lo(w.y), bf16_hi(w.y)};
+        } else {
+            v[c] = __builtin_nontemporal_load(reinterpret_cast<const f32x4_t*>(static_cast<const float*>(x) + base + 256 * c));
+        }
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) ss += v[c][0] * v[c][0] + v[c][1] * v[c][1] + v[c][2] * v[c][2] + v[c][3] * v[c][3];
+    ss = wave_sum(ss);
+    const float inv = 1.0f / sqrtf(ss / (float)d + eps);
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        const int i = lane * 4 + 256 * c;
+        if (resid != nullptr) *reinterpret_cast<f32x4_t*>(resid + base + 256 * c) = v[c];
+        float gv[4];
+        if constexpr (GBF16) {
+            const uint2 w = *reinterpret_cast<const uint2*>(static_cast<const bf16_t*>(g) + i);
+            gv[0] = bf16_lo(w.x); gv[1] = bf16_hi(w.x); gv[2] = bf16_lo(w.y); gv[3] = bf16_hi(w.y);
+        } else {
+            const f32x4_t w = *reinterpret_cast<const f32x4_t*>(static_cast<const float*>(g) + i);
+            gv[0] = w[0]; gv[1] = w[1]; gv[2] = w[2]; gv[3] = w[3];
+        }
+        const float y0 = v[c][0] * inv * gv[0], y1 = v[c][1] * inv * gv[1];
+        const float y2 = v[c][2] * inv * gv[2], y3 = v[c][3] * inv * gv[3];
+        if constexpr (HBF16) {
+            uint2 o;
+            o.x = (uint32_t)f32_to_bf16(y0) | ((uint32_t)f32_to_bf16(y1) << 16);
+            o.y = (uint32_t)f32_to_bf16(y2) | ((uint32_t)f32_to_bf16(y3) << 16);
+            *reinterpret_cast<uint2*>(static_cast<bf16_t*>(h) + base + 256 * c) = o;
+        } else {
+            *reinterpret_cast<f32x4_t*>(static_cast<float*>(h) + base + 256 * c) = f32x4_t{y0, y1, y2, y3};
+        }
+    }
+}
+
 // C[M][N] = A[M][K] B[N][K]^T (+ C).  64x64 tile, 16x16 threads of 4x4 outputs.
 __global__ void __launch_bounds__(256)
 gemm_f32_kernel(const float* __restrict__ A, const float* __restrict__ B, float* __restrict__ C,
@@ -174,6 +226,25 @@ hipError_t launch_rmsnorm(const void* x, bool x_bf16, float* resid, const void* 
                           void* h, bool h_bf16, int rows, int d, float eps, hipStream_t st) {
     if (rows <= 0) return hipSuccess;
     const dim3 grid(blocks_for(rows, 4)), blk(256);
+#define RIFT_RMS_REG(NCH)                                                                              \
+    if (d == 256 * NCH) {                                                                              \
+        if (x_bf16 && g_bf16 && h_bf16)                                                                \
+            hipLaunchKernelGGL((rmsnorm_reg_kernel<true, true, true, NCH>), grid, blk, 0, st, x, resid, g, h, rows, eps); \
+        else if (!x_bf16 && g_bf16 && h_bf16)                                                          \
+            hipLaunchKernelGGL((rmsnorm_reg_kernel<false, true, true, NCH>), grid, blk, 0, st, x, resid, g, h, rows, eps); \
+        else if (!x_bf16 && !g_bf16 && !h_bf16)                                                        \
+            hipLaunchKernelGGL((rmsnorm_reg_kernel<false, false, false, NCH>), grid, blk, 0, st, x, resid, g, h, rows, eps); \
+        else                                                                                           \
+            return hipErrorInvalidValue;                                                               \
+        return hipGetLastError();                                                                      \
+    }
+    RIFT_RMS_REG(1)
+    RIFT_RMS_REG(2)
+    RIFT_RMS_REG(4)
+    RIFT_RMS_REG(8)
+    RIFT_RMS_REG(16)
+    RIFT_RMS_REG(32)
+#undef RIFT_RMS_REG
     if (x_bf16 && g_bf16 && h_bf16)
         hipLaunchKernelGGL((rmsnorm_kernel<true, true, true>), grid, blk, 0, st, x, resid, g, h, rows, d, eps);
     else if (!x_bf16 && g_bf16 && h_bf16)
