@@ -156,9 +156,12 @@ RIFT_API rift_status rift_select_tokens(const double* token_key, int32_t n_tiles
  *              T = n_keep*(n_sys+n_qry) + sel_offsets[n_keep] must be <= packed_rows
  * cu_seqlens   [n_keep+1] i32 out  prefix sums of sequence lengths
  * position_ids [packed_rows] i32 out  0..L-1 within each sequence
- * status       [1] i32 out  0, or RIFT_ERR_SHAPE if an index is out of range or
- *              T > packed_rows (offending rows are not written)
- * Shape rules: d * sizeof(dt) % 16 == 0; n_sys, n_qry >= 0.
+ * status       [1] i32 out  0, or RIFT_ERR_SHAPE if a tile id or selected index is
+ *              out of range, a budget (sel_offsets step) is outside [0, n_v],
+ *              sel_offsets[0] != 0 or T > packed_rows; a bad tile id, budget,
+ *              first offset or total stops every row from being written, a bad
+ *              selected index only its own row
+ * Shape rules: d * sizeof(dt) % 16 == 0; n_sys, n_qry >= 0; 0 <= n_keep <= 65535.
  */
 RIFT_API rift_status rift_compact(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
                          int32_t d, const int32_t* kept_tiles, const int32_t* sel_offsets,

@@ -4,11 +4,13 @@
 //
 // bf16, head_dim 128, on MFMA.  One workgroup (4 waves) per (sequence, head,
 // 128-query block); wave w owns queries [32 w, 32 w + 32) of the block.  Keys
-// and values stream through LDS 64 at a time (K row-major, V transposed).  The
-// wave computes S^T = K Q^T (v_mfma_f32_32x32x16_bf16, M = keys, N = queries),
-// so each lane holds one query's scores in registers; the online softmax runs
-// in float32 (running max and sum per query); the unnormalised probabilities,
-// rounded to bf16, are already in the B-operand layout of O^T = V^T P^T.
+// and values stream through two LDS buffers 64 at a time, both row-major; the
+// next block's rows are loaded into registers while the current one is used.
+// The wave computes S^T = K Q^T (v_mfma_f32_32x32x16_bf16, M = keys,
+// N = queries), so each lane holds one query's scores in registers; the online
+// softmax runs in float32 (running max and sum per query); the unnormalised
+// probabilities, rounded to bf16, are already in the B-operand layout of
+// O^T = V^T P^T, whose A operand (V^T) comes from transposing LDS reads.
 // Key blocks start at the sequence start, so a sequence's result does not
 // depend on how it is packed.
 //
@@ -23,15 +25,24 @@ namespace {
 constexpr int HD = 128;
 constexpr int BQ = 128;
 constexpr int BKV = 64;
-constexpr int KPAD = HD + 8;   // K tile row stride (elements)
-constexpr int VPAD = BKV + 4;  // V^T tile row stride (elements)
+constexpr int KPAD = HD + 8;    // K tile row stride (elements): 272 B, b128 reads of 32 rows 2-way
+constexpr int VPAD = HD + 32;   // V tile row stride (elements): 320 B, transposing reads 2-way
 
-__global__ void __launch_bounds__(256)
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
+
+// ds_read_b64_tr_b16: lane i of each 16-lane group g gets, in component j, the
+// 16-bit element at (address passed by lane 16 g + 4 j + i / 4) + i % 4.
+__device__ __forceinline__ v4s_t lds_read_tr16(const bf16_t* p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)(p));
+}
+
+__global__ void __launch_bounds__(256, 2)
 attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
                  const bf16_t* __restrict__ v, bf16_t* __restrict__ o,
                  const int* __restrict__ cu, int n_seq, int nqb, int H, float scale_log2) {
-    __shared__ __align__(16) bf16_t Ks[BKV * KPAD];
-    __shared__ __align__(16) bf16_t Vt[HD * VPAD];
+    __shared__ __align__(16) bf16_t Ks[2][BKV * KPAD];
+    __shared__ __align__(16) bf16_t Vs[2][BKV * VPAD];
 
     const int bid = blockIdx.x;
     const int qb = nqb - 1 - (bid % nqb);  // heaviest (last) query blocks first
@@ -72,94 +83,119 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
     float l_run = 0.f;
 
     const int kv_end = (q0 + BQ) < L ? (q0 + BQ) : L;
+    const int nkv = (kv_end + BKV - 1) / BKV;
     const int wave_last = (qw + 31) < (L - 1) ? (qw + 31) : (L - 1);
 
-    for (int kv0 = 0; kv0 < kv_end; kv0 += BKV) {
-        __syncthreads();
-        // stage K rows and V^T for keys kv0 .. kv0+63 (clamped to the sequence)
+    // K and V rows of a key block (clamped to the sequence): thread moves
+    // 16 bytes of rows rr = (tid + 256 it) / 16 of both, into registers first
+    u32x4_t kr[4], vr[4];
+    auto load_block = [&](int kv0) {
+#pragma unroll
+        for (int it = 0; it < 4; ++it) {
+            const int vec = tid + 256 * it;
+            int key = kv0 + (vec >> 4);
+            key = key < L ? key : L - 1;
+            const size_t g = (size_t)(s0 + key) * ld + head_off + (vec & 15) * 8;
+            kr[it] = *reinterpret_cast<const u32x4_t*>(k + g);
+            vr[it] = *reinterpret_cast<const u32x4_t*>(v + g);
+        }
+    };
+    auto store_block = [&](int buf) {
 #pragma unroll
         for (int it = 0; it < 4; ++it) {
             const int vec = tid + 256 * it;
             const int rr = vec >> 4;
             const int cc = (vec & 15) * 8;
-            int key = kv0 + rr;
-            key = key < L ? key : L - 1;
-            const size_t g = (size_t)(s0 + key) * ld + head_off + cc;
-            *reinterpret_cast<u32x4_t*>(Ks + rr * KPAD + cc) = *reinterpret_cast<const u32x4_t*>(k + g);
-            const u32x4_t vv = *reinterpret_cast<const u32x4_t*>(v + g);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                Vt[(cc + 2 * e) * VPAD + rr] = (bf16_t)(vv[e] & 0xFFFFu);
-                Vt[(cc + 2 * e + 1) * VPAD + rr] = (bf16_t)(vv[e] >> 16);
-            }
+            *reinterpret_cast<u32x4_t*>(&Ks[buf][rr * KPAD + cc]) = kr[it];
+            *reinterpret_cast<u32x4_t*>(&Vs[buf][rr * VPAD + cc]) = vr[it];
         }
-        __syncthreads();
-        if (kv0 > wave_last) continue;  // every key of the block is after this wave's queries
+    };
 
-        // scores for two 32-key sub-blocks
-        float sc[2][16];
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            f32x16_t s;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) s[i] = 0.f;
-            const bf16_t* krow = Ks + (kb * 32 + col) * KPAD + 8 * h;
-#pragma unroll
-            for (int kk = 0; kk < 8; ++kk) {
-                const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(krow + 16 * kk);
-                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s, 0, 0, 0);
-            }
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int key = kv0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-                sc[kb][i] = (key <= q_eff) ? s[i] * scale_log2 : -INFINITY;
-            }
-        }
-        float bmax = -INFINITY;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) bmax = fmaxf(bmax, sc[kb][i]);
-        bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
-        const float m_new = fmaxf(m_run, bmax);
-        const float alpha = exp2f(m_run - m_new);
-        float rsum = 0.f;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const float pv = exp2f(sc[kb][i] - m_new);
-                sc[kb][i] = pv;
-                rsum += pv;
-            }
-        rsum += __shfl_xor(rsum, 32);
-        l_run = l_run * alpha + rsum;
-        m_run = m_new;
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) oacc[t][i] *= alpha;
+    // transposing-read addresses of this lane as a source lane: group g,
+    // component j, quad u -> key 4 (g >> 1) + j (+ 8), dims 16 (g & 1) + 4 u
+    const int tg = lane >> 4, tj = (lane >> 2) & 3, tu = lane & 3;
+    const int v_off = (4 * (tg >> 1) + tj) * VPAD + 16 * (tg & 1) + 4 * tu;
 
-        // O^T += V^T P^T.  For MFMA step ks of sub-block kb, lane half h holds
-        // keys {16 ks + 4 h + 0..3, 16 ks + 8 + 4 h + 0..3} in slots 0..7.
+    load_block(0);
+    store_block(0);
+    __syncthreads();
+    for (int kb_i = 0; kb_i < nkv; ++kb_i) {
+        const int kv0 = kb_i * BKV;
+        const int cur = kb_i & 1;
+        if (kb_i + 1 < nkv) load_block(kv0 + BKV);
+        if (kv0 <= wave_last) {
+            // scores for two 32-key sub-blocks
+            float sc[2][16];
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+            for (int kb = 0; kb < 2; ++kb) {
+                f32x16_t s;
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-                bf16x8_t pf;
+                for (int i = 0; i < 16; ++i) s[i] = 0.f;
+                const bf16_t* krow = &Ks[cur][(kb * 32 + col) * KPAD + 8 * h];
 #pragma unroll
-                for (int jj = 0; jj < 8; ++jj) pf[jj] = (__bf16)sc[kb][8 * ks + jj];
-                const int kbase = kb * 32 + 16 * ks + 4 * h;
+                for (int kk = 0; kk < 8; ++kk) {
+                    const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(krow + 16 * kk);
+                    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s, 0, 0, 0);
+                }
 #pragma unroll
-                for (int t = 0; t < 4; ++t) {
-                    const bf16_t* vrow = Vt + (t * 32 + col) * VPAD + kbase;
-                    const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
-                    const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 8);
-                    const u32x4_t vv = {lo.x, lo.y, hi.x, hi.y};
-                    oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vv),
-                                                                      pf, oacc[t], 0, 0, 0);
+                for (int i = 0; i < 16; ++i) {
+                    const int key = kv0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+                    sc[kb][i] = (key <= q_eff) ? s[i] * scale_log2 : -INFINITY;
                 }
             }
+            float bmax = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) bmax = fmaxf(bmax, sc[kb][i]);
+            bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
+            const float m_new = fmaxf(m_run, bmax);
+            const float alpha = exp2f(m_run - m_new);
+            float rsum = 0.f;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const float pv = exp2f(sc[kb][i] - m_new);
+                    sc[kb][i] = pv;
+                    rsum += pv;
+                }
+            rsum += __shfl_xor(rsum, 32);
+            l_run = l_run * alpha + rsum;
+            m_run = m_new;
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) oacc[t][i] *= alpha;
+
+            // O^T += V^T P^T.  MFMA step ks of sub-block kb contracts keys
+            // 16 ks + 4 h + {0..3} (slots 0..3) and 16 ks + 8 + 4 h + {0..3}
+            // (slots 4..7) of lane half h: the P values this lane holds, and two
+            // transposing reads of the row-major V tile give the same keys.
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) {
+                    bf16x8_t pf;
+#pragma unroll
+                    for (int jj = 0; jj < 8; ++jj) pf[jj] = (__bf16)sc[kb][8 * ks + jj];
+                    const bf16_t* vb = &Vs[cur][(kb * 32 + 16 * ks) * VPAD + v_off];
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        const v4s_t lo = lds_read_tr16(vb + 32 * t);
+                        const v4s_t hi = lds_read_tr16(vb + 32 * t + 8 * VPAD);
+                        const u32x4_t vv = {__builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 0, 1)),
+                                            __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 2, 3)),
+                                            __builtin_bit_cast(uint32_t, __builtin_shufflevector(hi, hi, 0, 1)),
+                                            __builtin_bit_cast(uint32_t, __builtin_shufflevector(hi, hi, 2, 3))};
+                        oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vv),
+                                                                          pf, oacc[t], 0, 0, 0);
+                    }
+                }
+        }
+        // the other buffer was last read before the previous barrier
+        if (kb_i + 1 < nkv) store_block(cur ^ 1);
+        __syncthreads();
     }
 
     if (qidx >= L) return;

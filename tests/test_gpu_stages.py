@@ -221,3 +221,6 @@ def test_compact_edges(R):
     # token index out of range
     packed, cu, pos, st = run_compact(R, X, "bf16", [0], np.array([0, 2]), np.array([1, 20]), sysr, qry)
     assert st == 2
+    # a budget (offset step) larger than n_v
+    packed, cu, pos, st = run_compact(R, X, "bf16", [0], np.array([0, 21]), np.arange(21) % 20, sysr, qry)
+    assert st == 2
