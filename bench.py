@@ -100,6 +100,90 @@ def cpu_baseline(w, sc, seq_lens_by_tier, n_tiles_sample: int, n_layers_sample: 
                        f"thread, BLAS on {blas_threads}")}
 
 
+def exhaustive_run(R, torch, w, tokens, qbank, sysd, qryd, layers, cfg, chunk: int = 50) -> dict:
+    """Every tile kept at the full budget n_v: the no-pruning baseline the
+    paper compares against.  Same kernels; the prefill runs as consecutive
+    calls of `chunk` prompts each (all prompts have the same length), since one
+    call is limited to T * max(d, ffn) < 2^31.  Timed once with HIP events on
+    the current stream."""
+    n, nv, d = tokens.shape
+    dev = tokens.device
+    f64, f32, i32 = torch.float64, torch.float32, torch.int32
+    nq = qbank.shape[0]
+    fixed = sysd.shape[0] + qryd.shape[0]
+    L = nv + fixed
+    T = n * L
+    key = torch.empty(n * nv, dtype=f64, device=dev)
+    sim = torch.empty(n * nv, nq, dtype=f32, device=dev)
+    score = torch.empty(n, dtype=f64, device=dev)
+    u = torch.empty(n, dtype=f32, device=dev)
+    order = torch.empty(n, dtype=i32, device=dev)
+    nkeep = torch.empty(1, dtype=i32, device=dev)
+    sws = torch.empty(max(256, R.rift_score_workspace_size(n, nv, d)), dtype=torch.uint8, device=dev)
+    budgets = torch.full((n,), nv, dtype=i32, device=dev)
+    offs = torch.empty(n + 1, dtype=i32, device=dev)
+    sel = torch.empty(n * nv, dtype=i32, device=dev)
+    st1 = torch.empty(1, dtype=i32, device=dev)
+    packed = torch.empty(T, d, dtype=tokens.dtype, device=dev)
+    cu = torch.empty(n + 1, dtype=i32, device=dev)
+    pos = torch.empty(T, dtype=i32, device=dev)
+    st2 = torch.empty(1, dtype=i32, device=dev)
+    chunks = [(c, min(n, c + chunk)) for c in range(0, n, chunk)]
+    cu_c = {m: torch.arange(0, m + 1, dtype=i32, device=dev) * L for m in {b - a for a, b in chunks}}
+    ws = torch.empty(R.rift_prefill_workspace_size(cfg, chunk * L, L), dtype=torch.uint8, device=dev)
+    hid = torch.empty(chunk * L, d, dtype=f32, device=dev)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    R.rift_score_tiles(tokens, qbank, n, 0.0, key, sim, score, u, order, nkeep, sws)
+    R.rift_select_tokens(key, n, nv, order, budgets, n, offs, sel, st1)
+    R.rift_compact(tokens, order, offs, sel, n, sysd, qryd, packed, cu, pos, st2)
+    for a, b in chunks:
+        m = b - a
+        R.rift_prefill(cfg, layers, packed[a * L:b * L], cu_c[m], pos[a * L:b * L], m, L,
+                       hid[:m * L], ws)
+    e1.record()
+    torch.cuda.synchronize()
+    assert int(st1.item()) == 0 and int(st2.item()) == 0
+    ms = e0.elapsed_time(e1)
+    m = w.model
+    fl = stage_flops(T, m.d, m.ffn, [L] * n)
+    tflop = sum(fl.values()) * m.n_layers / 1e12
+    del packed, ws, hid, sim
+    return {"ms": round(ms, 2), "packed_tokens": T, "prompts": n, "prefill_calls": len(chunks),
+            "tflop": round(tflop, 1), "frac_bf16_peak": round(tflop / (ms * 1e-3) / PEAK_BF16_TFLOPS, 4)}
+
+
+def select_batched(R, torch, token_key, order, budgets, n_tiles, n_v, n_keep, copies=64, reps=10) -> dict:
+    """rift_select_tokens over `copies` scene-queries' keys at once (one call),
+    for a bandwidth-meaningful number; median of `reps` timed calls."""
+    dev = token_key.device
+    keys = token_key.repeat(copies)
+    kept = torch.cat([order[:n_keep] + c * n_tiles for c in range(copies)]).contiguous()
+    b = budgets[:n_keep].repeat(copies).contiguous()
+    total = int(b.sum().item())
+    offs = torch.empty(copies * n_keep + 1, dtype=torch.int32, device=dev)
+    sel = torch.empty(total, dtype=torch.int32, device=dev)
+    st = torch.empty(1, dtype=torch.int32, device=dev)
+    for _ in range(2):
+        R.rift_select_tokens(keys, copies * n_tiles, n_v, kept, b, copies * n_keep, offs, sel, st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        R.rift_select_tokens(keys, copies * n_tiles, n_v, kept, b, copies * n_keep, offs, sel, st)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    us = statistics.median(ts) * 1e3
+    nbytes = copies * n_keep * n_v * 8 + total * 4 + copies * n_keep * 12
+    return {"queries": copies, "kept_tiles": copies * n_keep, "us": round(us, 1),
+            "GBs": round(nbytes / (us * 1e-6) / 1e9, 1),
+            "frac_hbm": round(nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -109,6 +193,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tiles", type=int, default=128)
     ap.add_argument("--cpu-sample-layers", type=int, default=16)
+    ap.add_argument("--no-exhaustive", action="store_true",
+                    help="skip the every-tile, full-budget comparison run")
     ap.add_argument("--traffic-calibration", action="store_true",
                     help="also run a 1 GiB copy kernel (for HBM counter calibration)")
     args = ap.parse_args()
@@ -201,6 +287,7 @@ def main() -> int:
     def med(xs):
         return statistics.median(xs)
 
+    stage_ms_total = med([e[0].elapsed_time(e[4]) for e in top])
     stage_ms = {"score": med([e[0].elapsed_time(e[1]) for e in top]),
                 "select": med([e[1].elapsed_time(e[2]) for e in top]),
                 "compact": med([e[2].elapsed_time(e[3]) for e in top]),
@@ -251,6 +338,16 @@ def main() -> int:
         "prefill_frac_bf16_peak": round(prefill_flops / (stage_ms["prefill"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "hbm": hbm,
     }
+    out["packed_tokens_per_s"] = round(T * K / elapsed, 1)
+    out["select_batched"] = select_batched(R, torch, q.token_key, q.tile_order, q.budgets, w.n_tiles,
+                                           w.n_v, q.n_keep)
+    if not args.no_exhaustive:
+        log("exhaustive run (every tile at the full budget) ...")
+        ex = exhaustive_run(R, torch, w, tokens, qbank, sysd, qryd, layers, q.cfg)
+        ex["rift_ms_over_exhaustive_ms"] = round(stage_ms_total / ex["ms"], 4)
+        ex["latency_reduction"] = round(1 - stage_ms_total / ex["ms"], 4)
+        out["exhaustive"] = ex
+        log(f"exhaustive: {ex['ms']:.1f} ms")
     if not args.no_cpu_baseline:
         tiers = {}
         for L in seq_lens:

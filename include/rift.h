@@ -140,7 +140,8 @@ RIFT_API rift_status rift_assign_budgets(int32_t n_keep, int32_t n_v, const int3
  *                                 range, a tile id is out of range or the total
  *                                 exceeds sel_capacity (then nothing is written
  *                                 to sel_idx and all offsets are 0)
- * Shape rules: 1 <= n_v <= 1024, 0 <= n_keep <= n_tiles <= 4096.
+ * Shape rules: 1 <= n_v <= 1024, n_tiles >= 1, n_tiles * n_v <= INT32_MAX,
+ *              0 <= n_keep <= n_tiles, sel_capacity <= INT32_MAX.
  */
 RIFT_API rift_status rift_select_tokens(const double* token_key, int32_t n_tiles, int32_t n_v,
                                const int32_t* kept_tiles, const int32_t* budgets,

@@ -182,8 +182,8 @@ rift_status rift_select_tokens(const double* token_key, int32_t n_tiles, int32_t
     if (n_keep > 0 && (token_key == nullptr || kept_tiles == nullptr || budgets == nullptr))
         return RIFT_ERR_NULL;
     if (sel_capacity > 0 && sel_idx == nullptr) return RIFT_ERR_NULL;
-    if (n_v < 1 || n_v > 1024 || n_tiles < 1 || n_tiles > 4096 || n_keep < 0 || n_keep > n_tiles ||
-        sel_capacity < 0)
+    if (n_v < 1 || n_v > 1024 || n_tiles < 1 || (int64_t)n_tiles * n_v > (int64_t)INT32_MAX ||
+        n_keep < 0 || n_keep > n_tiles || sel_capacity < 0 || sel_capacity > (int64_t)INT32_MAX)
         return RIFT_ERR_SHAPE;
     hipError_t e = launch_select(token_key, n_tiles, n_v, kept_tiles, budgets, n_keep, sel_offsets,
                                  sel_idx, sel_capacity, status, static_cast<hipStream_t>(stream));

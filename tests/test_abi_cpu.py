@@ -111,6 +111,8 @@ def test_select_and_compact_validation(R):
     assert L.rift_select_tokens(FAKE, 4, 1025, FAKE, FAKE, 2, FAKE, FAKE, 10, FAKE, None) == 2
     assert L.rift_select_tokens(FAKE, 4, 576, FAKE, FAKE, 5, FAKE, FAKE, 10, FAKE, None) == 2
     assert L.rift_select_tokens(FAKE, 4, 576, FAKE, FAKE, 2, FAKE, None, 10, FAKE, None) == 1
+    assert L.rift_select_tokens(FAKE, 1 << 22, 1024, FAKE, FAKE, 2, FAKE, FAKE, 10, FAKE, None) == 2
+    assert L.rift_select_tokens(FAKE, 4, 576, FAKE, FAKE, 2, FAKE, FAKE, 1 << 31, FAKE, None) == 2
     # compact
     c = L.rift_compact
     assert c(FAKE, 1, 4, 576, 4096, FAKE, None, FAKE, 2, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 1
