@@ -143,6 +143,19 @@ def test_select_parity_random_keys(R, ties):
     assert np.array_equal(offs, r_offs) and np.array_equal(sel, r_sel)
 
 
+def test_select_signed_zeros_and_extremes(R):
+    """-0.0 and +0.0 compare equal (ties go to the lower index); negative,
+    subnormal and huge keys keep their order."""
+    rng = np.random.default_rng(11)
+    vals = np.array([-0.0, 0.0, 5e-324, -5e-324, 1e300, -1e300, 1.0, -1.0, 2.0 ** -1074, 0.5])
+    keys = rng.choice(vals, size=(6, 300))
+    kept = [5, 0, 3, 1]
+    budgets = [1, 150, 299, 37]
+    offs, sel, st = run_select(R, keys, kept, budgets)
+    r_offs, r_sel = O.select_tokens(keys, kept, budgets)
+    assert st == 0 and np.array_equal(offs, r_offs) and np.array_equal(sel, r_sel)
+
+
 @pytest.mark.parametrize("n_v", [1, 5, 63, 64, 65, 333, 1024])
 def test_select_ragged_sizes(R, n_v):
     rng = np.random.default_rng(n_v)
