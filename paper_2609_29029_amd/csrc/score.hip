@@ -1,8 +1,10 @@
 // Stage 1 of Rift (Sec. 2.3, Eq. 1; Listing 1; App. B Step 3) on gfx950.
 //
 //   prep_w       w = t - (1/M) sum_j B_j in float64, rounded to float32.
-//   score_tiles  one workgroup per tile, one wave per 64 tokens.  A single pass
-//                over the tile's tokens computes, per token,
+//   score_tiles  one workgroup per tile of up to 10 waves, a wave per 64-token
+//                group (every 10th group beyond 640 tokens); each token row is
+//                read a whole 128-byte line at a time, a line ahead of its use.
+//                A single pass over the tile's tokens computes, per token,
 //                  * the float64 ranking key r = (x.w)/|x| on the VALUs, in the
 //                    fixed granule order (8-wide granules, granule g into
 //                    accumulator g mod 4, then (a0+a2)+(a1+a3));
@@ -43,7 +45,7 @@ __global__ void prep_w_kernel(const void* __restrict__ qbank, int is_bf16, int d
 }
 
 template <bool kBf16>
-__global__ void __launch_bounds__(1024)
+__global__ void __launch_bounds__(640)
 score_tiles_kernel(const void* __restrict__ tokens, int n_v, int d,
                    const void* __restrict__ qbank, int nq, const float* __restrict__ w32,
                    double* __restrict__ token_key, float* __restrict__ token_sim,
@@ -61,11 +63,14 @@ score_tiles_kernel(const void* __restrict__ tokens, int n_v, int d,
     for (int i = threadIdx.x; i < d; i += blockDim.x) w_lds[i] = w32[i];
     __syncthreads();
 
+    const int n_groups = (n_v + 63) >> 6;       // 64 tokens per group
+    const int n_waves = blockDim.x >> 6;
+    for (int grp = wave; grp < n_groups; grp += n_waves) {
     int tok[4];
     size_t row_off[4];
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
-        tok[b] = wave * 64 + b * 16 + r;
+        tok[b] = grp * 64 + b * 16 + r;
         int t_clamped = tok[b] < n_v ? tok[b] : n_v - 1;
         row_off[b] = ((size_t)tile * n_v + t_clamped) * (size_t)d;
     }
@@ -81,42 +86,49 @@ score_tiles_kernel(const void* __restrict__ tokens, int n_v, int d,
     if constexpr (kBf16) {
         const bf16_t* X = static_cast<const bf16_t*>(tokens);
         const bf16_t* Q = static_cast<const bf16_t*>(qbank);
-        u32x4_t xc[4], xn[4], qc, qn;
+        // ring of four register sets.  Two consecutive steps cover the two
+        // halves of each token row's 128-byte lines, so their loads are issued
+        // together, a line ahead: at even s, the loads of steps s + 2, s + 3.
+        u32x4_t xs[4][4], qs[4];
+        auto load = [&](int st, int slot) {
+            const int k = st * 32 + q * 8;
 #pragma unroll
-        for (int b = 0; b < 4; ++b) xc[b] = *reinterpret_cast<const u32x4_t*>(X + row_off[b] + q * 8);
-        qc = *reinterpret_cast<const u32x4_t*>(Q + q_off + q * 8);
-        for (int s = 0; s < steps; ++s) {
-            const int k = s * 32 + q * 8;
-            if (s + 1 < steps) {
+            for (int b = 0; b < 4; ++b) xs[slot][b] = *reinterpret_cast<const u32x4_t*>(X + row_off[b] + k);
+            qs[slot] = *reinterpret_cast<const u32x4_t*>(Q + q_off + k);
+        };
 #pragma unroll
-                for (int b = 0; b < 4; ++b)
-                    xn[b] = *reinterpret_cast<const u32x4_t*>(X + row_off[b] + k + 32);
-                qn = *reinterpret_cast<const u32x4_t*>(Q + q_off + k + 32);
-            }
-            const f32x4_t w0 = *reinterpret_cast<const f32x4_t*>(w_lds + k);
-            const f32x4_t w1 = *reinterpret_cast<const f32x4_t*>(w_lds + k + 4);
-            const double wd[8] = {(double)w0[0], (double)w0[1], (double)w0[2], (double)w0[3],
-                                  (double)w1[0], (double)w1[1], (double)w1[2], (double)w1[3]};
-            const bf16x8_t qa = __builtin_bit_cast(bf16x8_t, qc);
+        for (int j = 0; j < 2; ++j)
+            if (j < steps) load(j, j);
+        for (int s0 = 0; s0 < steps; s0 += 4) {
 #pragma unroll
-            for (int b = 0; b < 4; ++b) {
-                const u32x4_t x = xc[b];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const double x0 = (double)bf16_lo(x[e]);
-                    const double x1 = (double)bf16_hi(x[e]);
-                    n2[b] = fma(x0, x0, n2[b]);
-                    g[b] = fma(x0, wd[2 * e], g[b]);
-                    n2[b] = fma(x1, x1, n2[b]);
-                    g[b] = fma(x1, wd[2 * e + 1], g[b]);
+            for (int j = 0; j < 4; ++j) {
+                const int s = s0 + j;
+                if (s >= steps) break;
+                if ((j & 1) == 0) {
+                    if (s + 2 < steps) load(s + 2, (j + 2) & 3);
+                    if (s + 3 < steps) load(s + 3, (j + 3) & 3);
                 }
-                acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, __builtin_bit_cast(bf16x8_t, x),
-                                                                 acc[b], 0, 0, 0);
-            }
-            if (s + 1 < steps) {
+                const int k = s * 32 + q * 8;
+                const f32x4_t w0 = *reinterpret_cast<const f32x4_t*>(w_lds + k);
+                const f32x4_t w1 = *reinterpret_cast<const f32x4_t*>(w_lds + k + 4);
+                const double wd[8] = {(double)w0[0], (double)w0[1], (double)w0[2], (double)w0[3],
+                                      (double)w1[0], (double)w1[1], (double)w1[2], (double)w1[3]};
+                const bf16x8_t qa = __builtin_bit_cast(bf16x8_t, qs[j]);
 #pragma unroll
-                for (int b = 0; b < 4; ++b) xc[b] = xn[b];
-                qc = qn;
+                for (int b = 0; b < 4; ++b) {
+                    const u32x4_t x = xs[j][b];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const double x0 = (double)bf16_lo(x[e]);
+                        const double x1 = (double)bf16_hi(x[e]);
+                        n2[b] = fma(x0, x0, n2[b]);
+                        g[b] = fma(x0, wd[2 * e], g[b]);
+                        n2[b] = fma(x1, x1, n2[b]);
+                        g[b] = fma(x1, wd[2 * e + 1], g[b]);
+                    }
+                    acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, __builtin_bit_cast(bf16x8_t, x),
+                                                                     acc[b], 0, 0, 0);
+                }
             }
         }
     } else {
@@ -173,6 +185,7 @@ score_tiles_kernel(const void* __restrict__ tokens, int n_v, int d,
             }
         }
     }
+    }   // token groups
     __syncthreads();
 
     // Tile score: 64 strided partial sums of r, halving tree, divide by n_v.
@@ -248,8 +261,9 @@ hipError_t launch_score(const void* tokens, bool bf16, int n_tiles, int n_v, int
                         int* n_keep, float* w32, hipStream_t st) {
     hipLaunchKernelGGL(prep_w_kernel, dim3((d + 255) / 256), dim3(256), 0, st, qbank, bf16 ? 1 : 0,
                        d, n_bg, w32);
-    const int waves = (n_v + 63) / 64;
-    const size_t lds = (size_t)d * sizeof(float) + (size_t)waves * 64 * sizeof(double);
+    const int groups = (n_v + 63) / 64;
+    const int waves = groups < 10 ? groups : 10;   // a wave takes every 10th group beyond 640 tokens
+    const size_t lds = (size_t)d * sizeof(float) + (size_t)groups * 64 * sizeof(double);
     if (bf16) {
         hipLaunchKernelGGL(score_tiles_kernel<true>, dim3(n_tiles), dim3(waves * 64), lds, st,
                            tokens, n_v, d, qbank, 1 + n_bg, w32, token_key, token_sim, tile_score);
