@@ -149,54 +149,68 @@ __device__ __forceinline__ int swz8(int r) { return ((r >> 1) ^ ((r & 1) << 2)) 
 // the gate/up pairs of SwiGLU sit in the same lane.
 __device__ __forceinline__ int w8_c0(int wn) { return 128 * (wn >> 1) + 32 * (wn & 1); }
 
-template <int EPI>
-__device__ __forceinline__ void epilogue_w8(const GemmParams& p, f32x16_t (&acc)[4][2], int m0, int bn,
-                                            int wm, int wn, int lane, const int* pos_lds) {
+// Epilogue through LDS.  After the main loop the stage buffers are free: each
+// wave writes its outputs (SiLU(gate)*up, RoPE'd q/k, v, or the raw product for
+// the residual GEMMs) into a row-major tile in LDS, then every thread of the
+// workgroup moves 16 contiguous bytes of a row, so global stores (and the
+// residual loads) are whole cache lines.  acc[m][n][i] is row
+// 8 (i/4) + 4 (lane/32) + (i%4) of the 32x32 block (m, n) of wave (wm, wn),
+// column lane%32; the block's tile columns are c0 + 64 n + lane%32.  A half-tile
+// workgroup (HALF) holds logical tile columns [128 h, 128 h + 128).
+constexpr int kStagingBytes = 256 * (256 + 8) * 2;   // largest staging tile (QKV)
+
+template <int EPI, bool HALF>
+__device__ __forceinline__ void epilogue_staged(const GemmParams& p, f32x16_t (&acc)[4][2], int m0, int bn,
+                                                int h, int wm, int wn, int lane, const int* pos_lds,
+                                                unsigned char* stage) {
+    constexpr int NT = HALF ? 256 : 512;
+    const int tid = threadIdx.x;
     const int col_in = lane & 31;
     const int row_hi = 4 * (lane >> 5);
-    const int c0 = w8_c0(wn);
+    const int cbase = HALF ? 128 * h : 0;
+    __syncthreads();   // every wave is done with the stage buffers
+    if constexpr (EPI == EPI_SWIGLU) {
+        constexpr int OC = HALF ? 64 : 128;   // outputs per row of this workgroup
+        constexpr int LD = OC + 8;
+        bf16_t* S = reinterpret_cast<bf16_t*>(stage);
+        const int sc = 64 * (wn >> 1) + 32 * (wn & 1) + col_in - (HALF ? 64 * h : 0);
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
-        __builtin_amdgcn_sched_barrier(0);
-        const int r0 = wm * 128 + m * 32 + row_hi;   // tile row of i = 0
-        if constexpr (EPI == EPI_RESID) {
-            float old[16][2];
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
-                const float* src = p.resid + (size_t)(row < p.M ? row : p.M - 1) * p.N + bn * BN + c0 + col_in;
-#pragma unroll
-                for (int n = 0; n < 2; ++n) old[i][n] = src[n * 64];
-            }
+        for (int m = 0; m < 4; ++m)
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
-                if (row >= p.M) continue;
-                float* dst = p.resid + (size_t)row * p.N + bn * BN + c0 + col_in;
-#pragma unroll
-                for (int n = 0; n < 2; ++n) dst[n * 64] = old[i][n] + acc[m][n][i];
-            }
-        } else if constexpr (EPI == EPI_SWIGLU) {
-            const int oc = bn * 128 + 64 * (wn >> 1) + 32 * (wn & 1) + col_in;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
-                if (row >= p.M) continue;
+                const int r = wm * 128 + m * 32 + 8 * (i >> 2) + row_hi + (i & 3);
                 const float gt = acc[m][0][i];
                 const float up = acc[m][1][i];
-                p.o0[(size_t)row * p.d + oc] = f32_to_bf16(gt / (1.0f + expf(-gt)) * up);
+                S[r * LD + sc] = f32_to_bf16(gt / (1.0f + expf(-gt)) * up);
             }
-        } else {  // QKV
-            const int region = __builtin_amdgcn_readfirstlane((bn * BN) / p.d);
-            const int j = 32 * (wn & 1) + col_in;                                     // 0..63 in the head
-            bf16_t* outb = pick3(region, p.o0, p.o1, p.o2) + (bn * BN - region * p.d) + 128 * (wn >> 1) + j;
+        __syncthreads();
+        constexpr int VPR = OC / 8;
+        bf16_t* out = p.o0 + bn * 128 + (HALF ? 64 * h : 0);
+        for (int v = tid; v < 256 * VPR; v += NT) {
+            const int r = v / VPR;
+            const int cv = (v % VPR) * 8;
+            const int row = m0 + r;
+            if (row < p.M)
+                *reinterpret_cast<u32x4_t*>(out + (size_t)row * p.d + cv) =
+                    *reinterpret_cast<const u32x4_t*>(S + r * LD + cv);
+        }
+    } else if constexpr (EPI == EPI_QKV) {
+        constexpr int OC = HALF ? 128 : 256;
+        constexpr int LD = OC + 8;
+        bf16_t* S = reinterpret_cast<bf16_t*>(stage);
+        const int region = __builtin_amdgcn_readfirstlane((bn * BN) / p.d);
+        const int j = 32 * (wn & 1) + col_in;            // 0..63 within the head
+        const int sc = 128 * (wn >> 1) + j - cbase;      // staging column of j; j + 64 at sc + 64
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            __builtin_amdgcn_sched_barrier(0);
+            const int r0 = wm * 128 + m * 32 + row_hi;
             if (region == 2) {
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
-                    const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
-                    if (row >= p.M) continue;
-#pragma unroll
-                    for (int n = 0; n < 2; ++n) outb[(size_t)row * p.d + n * 64] = f32_to_bf16(acc[m][n][i]);
+                    const int r = r0 + 8 * (i >> 2) + (i & 3);
+                    S[r * LD + sc] = f32_to_bf16(acc[m][0][i]);
+                    S[r * LD + sc + 64] = f32_to_bf16(acc[m][1][i]);
                 }
             } else {
                 float2 cs[16];
@@ -204,15 +218,57 @@ __device__ __forceinline__ void epilogue_w8(const GemmParams& p, f32x16_t (&acc)
                 for (int i = 0; i < 16; ++i) cs[i] = p.rope[(size_t)pos_lds[r0 + 8 * (i >> 2) + (i & 3)] * 64 + j];
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
-                    const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
-                    if (row >= p.M) continue;
+                    const int r = r0 + 8 * (i >> 2) + (i & 3);
                     const float x1 = acc[m][0][i];
                     const float x2 = acc[m][1][i];
-                    bf16_t* out = outb + (size_t)row * p.d;
-                    out[0] = f32_to_bf16(x1 * cs[i].x - x2 * cs[i].y);
-                    out[64] = f32_to_bf16(x2 * cs[i].x + x1 * cs[i].y);
+                    S[r * LD + sc] = f32_to_bf16(x1 * cs[i].x - x2 * cs[i].y);
+                    S[r * LD + sc + 64] = f32_to_bf16(x2 * cs[i].x + x1 * cs[i].y);
                 }
             }
+        }
+        __syncthreads();
+        constexpr int VPR = OC / 8;
+        bf16_t* out = pick3(region, p.o0, p.o1, p.o2) + (bn * BN - region * p.d) + cbase;
+        for (int v = tid; v < 256 * VPR; v += NT) {
+            const int r = v / VPR;
+            const int cv = (v % VPR) * 8;
+            const int row = m0 + r;
+            if (row < p.M)
+                *reinterpret_cast<u32x4_t*>(out + (size_t)row * p.d + cv) =
+                    *reinterpret_cast<const u32x4_t*>(S + r * LD + cv);
+        }
+    } else {   // RESID: x += A B^T in float32, 128 rows (one wm) at a time
+        constexpr int OC = HALF ? 128 : 256;
+        constexpr int LD = OC + 4;
+        float* S = reinterpret_cast<float*>(stage);
+        const int sc = w8_c0(wn) - cbase + col_in;
+        constexpr int VPR = OC / 4;
+        float* base = p.resid + bn * BN + cbase;
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            if (wm == half) {
+#pragma unroll
+                for (int m = 0; m < 4; ++m)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        const int rr = m * 32 + 8 * (i >> 2) + row_hi + (i & 3);
+                        S[rr * LD + sc] = acc[m][0][i];
+                        S[rr * LD + sc + 64] = acc[m][1][i];
+                    }
+            }
+            __syncthreads();
+            for (int v = tid; v < 128 * VPR; v += NT) {
+                const int rr = v / VPR;
+                const int cv = (v % VPR) * 4;
+                const int row = m0 + half * 128 + rr;
+                if (row < p.M) {
+                    f32x4_t* dst = reinterpret_cast<f32x4_t*>(base + (size_t)row * p.N + cv);
+                    const f32x4_t old = *dst;
+                    const f32x4_t add = *reinterpret_cast<const f32x4_t*>(S + rr * LD + cv);
+                    *dst = f32x4_t{old[0] + add[0], old[1] + add[1], old[2] + add[2], old[3] + add[3]};
+                }
+            }
+            __syncthreads();
         }
     }
 }
@@ -230,7 +286,7 @@ __device__ __forceinline__ void epilogue_w8(const GemmParams& p, f32x16_t (&acc)
 // the final round over the CUs is half as long.
 template <int EPI, bool HALF>
 __global__ void __launch_bounds__(HALF ? 256 : 512, 1) gemm_bf16_w8_kernel(GemmParams p) {
-    __shared__ __align__(16) bf16_t lds[2 * kStage3];
+    __shared__ __align__(16) bf16_t lds[kStagingBytes / 2];   // two stages, then the epilogue tile
     __shared__ int pos_lds[BM];   // QKV: clamped position of each tile row
     int bm, bn, h = 0;
     if constexpr (HALF) {
@@ -370,7 +426,7 @@ __global__ void __launch_bounds__(HALF ? 256 : 512, 1) gemm_bf16_w8_kernel(GemmP
     for (; kt + 2 < nk; ++kt) stage(kt, T_{}, T_{});
     if (kt + 1 < nk) stage(kt++, F_{}, T_{});
     stage(kt, F_{}, F_{});
-    epilogue_w8<EPI>(p, acc, m0, bn, wm, wn, lane, pos_lds);
+    epilogue_staged<EPI, HALF>(p, acc, m0, bn, h, wm, wn, lane, pos_lds, reinterpret_cast<unsigned char*>(lds));
 }
 
 // ---------------------------------------------------------------------------
@@ -392,7 +448,7 @@ __global__ void __launch_bounds__(HALF ? 256 : 512, 1) gemm_bf16_w8_kernel(GemmP
 // at the end of turn 2j+3, before group 0 reads stage j+2.
 template <int EPI>
 __global__ void __launch_bounds__(512, 1) gemm_bf16_pp_kernel(GemmParams p) {
-    __shared__ __align__(16) bf16_t lds[2 * kStage3];
+    __shared__ __align__(16) bf16_t lds[kStagingBytes / 2];   // two stages, then the epilogue tile
     __shared__ int pos_lds[BM];   // QKV: clamped position of each tile row
     int bm, bn;
     group_coords(xcd_remap(blockIdx.x, p.n_full), p.num_m, p.num_n, bm, bn);
@@ -532,7 +588,7 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_pp_kernel(GemmParams p) {
         }
         step(kt, F_{});
     }
-    epilogue_w8<EPI>(p, acc, m0, bn, wm, wn, lane, pos_lds);
+    epilogue_staged<EPI, false>(p, acc, m0, bn, 0, wm, wn, lane, pos_lds, reinterpret_cast<unsigned char*>(lds));
 }
 
 int cu_count() {
