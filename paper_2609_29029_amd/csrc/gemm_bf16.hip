@@ -149,15 +149,16 @@ __device__ __forceinline__ int swz8(int r) { return ((r >> 1) ^ ((r & 1) << 2)) 
 // the gate/up pairs of SwiGLU sit in the same lane.
 __device__ __forceinline__ int w8_c0(int wn) { return 128 * (wn >> 1) + 32 * (wn & 1); }
 
-// Epilogue through LDS.  After the main loop the stage buffers are free: each
-// wave writes its outputs (SiLU(gate)*up, RoPE'd q/k, v, or the raw product for
-// the residual GEMMs) into a row-major tile in LDS, then every thread of the
-// workgroup moves 16 contiguous bytes of a row, so global stores (and the
-// residual loads) are whole cache lines.  acc[m][n][i] is row
+// Epilogue.  For the bf16 outputs the stage buffers, free after the main loop,
+// hold the tile: each wave writes its outputs (SiLU(gate)*up, RoPE'd q/k, v)
+// into a row-major tile in LDS, then every thread of the workgroup moves 16
+// contiguous bytes of a row, so global stores are whole row segments.  The
+// residual GEMMs read, add and write float32 straight from the lanes (32
+// consecutive columns per instruction).  acc[m][n][i] is row
 // 8 (i/4) + 4 (lane/32) + (i%4) of the 32x32 block (m, n) of wave (wm, wn),
 // column lane%32; the block's tile columns are c0 + 64 n + lane%32.  A half-tile
 // workgroup (HALF) holds logical tile columns [128 h, 128 h + 128).
-constexpr int kStagingBytes = 256 * (256 + 8) * 2;   // largest staging tile (QKV)
+constexpr int kStagingBytes = 256 * (256 + 8) * 2;   // largest staging tile (QKV, bf16)
 
 template <int EPI, bool HALF>
 __device__ __forceinline__ void epilogue_staged(const GemmParams& p, f32x16_t (&acc)[4][2], int m0, int bn,
@@ -181,7 +182,10 @@ __device__ __forceinline__ void epilogue_staged(const GemmParams& p, f32x16_t (&
                 const int r = wm * 128 + m * 32 + 8 * (i >> 2) + row_hi + (i & 3);
                 const float gt = acc[m][0][i];
                 const float up = acc[m][1][i];
-                S[r * LD + sc] = f32_to_bf16(gt / (1.0f + expf(-gt)) * up);
+                // silu(g) = g / (1 + e^-g) with the hardware exp2 and reciprocal
+                // (about 1 ulp each; the result is rounded to bf16)
+                const float e = __builtin_amdgcn_exp2f(gt * -1.4426950408889634f);
+                S[r * LD + sc] = f32_to_bf16(gt * __builtin_amdgcn_rcpf(1.0f + e) * up);
             }
         __syncthreads();
         constexpr int VPR = OC / 8;
@@ -237,39 +241,31 @@ __device__ __forceinline__ void epilogue_staged(const GemmParams& p, f32x16_t (&
                 *reinterpret_cast<u32x4_t*>(out + (size_t)row * p.d + cv) =
                     *reinterpret_cast<const u32x4_t*>(S + r * LD + cv);
         }
-    } else {   // RESID: x += A B^T in float32, 128 rows (one wm) at a time
-        constexpr int OC = HALF ? 128 : 256;
-        constexpr int LD = OC + 4;
-        float* S = reinterpret_cast<float*>(stage);
-        const int sc = w8_c0(wn) - cbase + col_in;
-        constexpr int VPR = OC / 4;
-        float* base = p.resid + bn * BN + cbase;
+    } else {   // RESID: x += A B^T in float32, read-modify-write straight from the lanes
+        const int c0 = w8_c0(wn);
 #pragma unroll
-        for (int half = 0; half < 2; ++half) {
-            if (wm == half) {
+        for (int m = 0; m < 4; ++m) {
+            __builtin_amdgcn_sched_barrier(0);
+            const int r0 = wm * 128 + m * 32 + row_hi;
+            float old[16][2];
 #pragma unroll
-                for (int m = 0; m < 4; ++m)
+            for (int i = 0; i < 16; ++i) {
+                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
+                const float* src = p.resid + (size_t)(row < p.M ? row : p.M - 1) * p.N + bn * BN + c0 + col_in;
 #pragma unroll
-                    for (int i = 0; i < 16; ++i) {
-                        const int rr = m * 32 + 8 * (i >> 2) + row_hi + (i & 3);
-                        S[rr * LD + sc] = acc[m][0][i];
-                        S[rr * LD + sc + 64] = acc[m][1][i];
-                    }
+                for (int n = 0; n < 2; ++n) old[i][n] = src[n * 64];
             }
-            __syncthreads();
-            for (int v = tid; v < 128 * VPR; v += NT) {
-                const int rr = v / VPR;
-                const int cv = (v % VPR) * 4;
-                const int row = m0 + half * 128 + rr;
-                if (row < p.M) {
-                    f32x4_t* dst = reinterpret_cast<f32x4_t*>(base + (size_t)row * p.N + cv);
-                    const f32x4_t old = *dst;
-                    const f32x4_t add = *reinterpret_cast<const f32x4_t*>(S + rr * LD + cv);
-                    *dst = f32x4_t{old[0] + add[0], old[1] + add[1], old[2] + add[2], old[3] + add[3]};
-                }
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
+                if (row >= p.M) continue;
+                float* dst = p.resid + (size_t)row * p.N + bn * BN + c0 + col_in;
+#pragma unroll
+                for (int n = 0; n < 2; ++n) dst[n * 64] = old[i][n] + acc[m][n][i];
             }
-            __syncthreads();
         }
+        (void)stage;
+        (void)cbase;
     }
 }
 
