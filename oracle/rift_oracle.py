@@ -35,6 +35,16 @@ Readings of points the paper leaves open (each is listed in the design doc):
       0..L-1; RMSNorm gains 1; rotate-half RoPE; attention scale 1/sqrt(hd);
       the output is the residual stream after the last layer, before any
       final norm.
+  R8  Optional score smoothing (Listing 1's note; App. B Step 3): each tile's
+      score is averaged with those of its m most visually similar tiles.  The
+      tile's embedding for similarity is its summed unit-normalised tokens,
+      E_i = fp32(sum over t ascending of x_t * (1/sqrt(n2_t))) with n2_t =
+      cdot(x_t, x_t) and the product then the sum each rounded (no fusion);
+      similarity is the cosine G_ij / sqrt(G_ii G_jj) of the canonical dot
+      products G = cdot(E_i, E_j) (0 when a norm is 0); the neighbours are the
+      m largest similarities over j != i, ties to the lower j; the smoothed
+      score is (s_i + sum of the neighbours' s in neighbour order) / (1 + m),
+      and u and the ranking use it.  Off unless asked for (m = 0).
 """
 from __future__ import annotations
 
@@ -313,12 +323,78 @@ def prefill(packed: np.ndarray, cu_seqlens: np.ndarray, position_ids: np.ndarray
 # ============================================================================ whole query
 
 
-def scene_query_stage1(tokens: np.ndarray, qbank: np.ndarray, keep_count: int, tau: float):
+def scene_query_stage1(tokens: np.ndarray, qbank: np.ndarray, keep_count: int, tau: float,
+                       knn_m: int = 0):
     """Stage 1 of one scene-query on float64 inputs: keys, tile scores, u,
-    order, n_keep (Sec. 2.3 Stage 1)."""
+    order, n_keep (Sec. 2.3 Stage 1); with knn_m > 0 the scores are first
+    smoothed over each tile's knn_m most similar tiles (reading R8)."""
     w32 = query_direction(qbank)
     r = np.stack([token_keys(tokens[i], w32) for i in range(tokens.shape[0])])
-    s = tile_scores(r)
+    s_raw = tile_scores(r)
+    out = {"w32": w32, "r": r, "s_raw": s_raw}
+    s = s_raw
+    if knn_m > 0:
+        inv = np.stack([token_inv_norms(tokens[i]) for i in range(tokens.shape[0])])
+        E = tile_embeddings(tokens, inv)
+        cos = tile_similarity(E)
+        s, nbrs = knn_smooth(s_raw, cos, knn_m)
+        out.update({"inv": inv, "E": E, "cos": cos, "nbrs": nbrs})
     u = normalise(s)
     order, n_keep = rank_and_keep(s, u, keep_count, tau)
-    return {"w32": w32, "r": r, "s": s, "u": u, "order": order, "n_keep": n_keep}
+    out.update({"s": s, "u": u, "order": order, "n_keep": n_keep})
+    return out
+
+
+# ------------------------------------------------------- optional smoothing (R8)
+
+
+def token_inv_norms(x: np.ndarray) -> np.ndarray:
+    """1/sqrt(n2) per token with n2 = cdot(x, x), correctly rounded square root
+    and divide; 0 for an all-zero token.  x: [..., d]."""
+    n2 = cdot(x, x)
+    with np.errstate(divide="ignore"):
+        inv = 1.0 / np.sqrt(n2)
+    return np.where(n2 == 0.0, 0.0, inv)
+
+
+def tile_embeddings(tokens: np.ndarray, inv: np.ndarray) -> np.ndarray:
+    """E_i = fp32(sum over tokens t, ascending, of x_t * inv_t), every product
+    and every addition rounded to float64 on its own (reading R8).
+    tokens: [n_tiles, n_v, d] float64; inv: [n_tiles, n_v].  Returns float64
+    holding float32 values."""
+    P = np.zeros((tokens.shape[0], tokens.shape[2]), dtype=np.float64)
+    for t in range(tokens.shape[1]):
+        P = P + tokens[:, t, :] * inv[:, t:t + 1]
+    return P.astype(np.float32).astype(np.float64)
+
+
+def tile_similarity(E: np.ndarray) -> np.ndarray:
+    """Cosine of every pair of tile embeddings from the canonical dot
+    products: G_ij / sqrt(G_ii * G_jj), 0 where that denominator is 0."""
+    n = E.shape[0]
+    G = np.empty((n, n), dtype=np.float64)
+    for j in range(n):
+        G[:, j] = cdot(E, E[j])
+    g = np.diag(G).copy()
+    den = np.sqrt(g[:, None] * g[None, :])
+    with np.errstate(invalid="ignore", divide="ignore"):
+        cos = G / den
+    return np.where(den == 0.0, 0.0, cos)
+
+
+def knn_smooth(s: np.ndarray, cos: np.ndarray, m: int):
+    """Smoothed scores and neighbour lists: the m (at most n - 1) largest
+    cos[i, j] over j != i, ties to the lower j; s'_i = (s_i + s_j1 + ... +
+    s_jm) / (1 + m), added in that order (reading R8)."""
+    n = s.shape[0]
+    m_eff = min(m, n - 1)
+    out = np.empty(n, dtype=np.float64)
+    nbrs = []
+    for i in range(n):
+        js = sorted((j for j in range(n) if j != i), key=lambda j: (-cos[i, j], j))[:m_eff]
+        acc = float(s[i])
+        for j in js:
+            acc = acc + float(s[j])
+        out[i] = acc / (1 + m_eff)
+        nbrs.append(js)
+    return out, nbrs

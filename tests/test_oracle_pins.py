@@ -381,3 +381,79 @@ def test_decoder_layer_vs_transformers_llama():
     got = O.decoder_layer(x, W, m.n_heads, m.head_dim, m.rms_eps, m.rope_base, np.arange(L))
     err = np.abs(got - ref).max(axis=1) / np.abs(ref).max(axis=1)
     assert err.max() < 1e-6, err.max()
+
+
+# ----------------------------------------------------------------------------- score smoothing (R8)
+def _grouped_scene(rng, n_groups=3, per_group=4, n_v=16, d=64):
+    """Tiles whose tokens lie close to one of n_groups orthogonal directions."""
+    base = np.zeros((n_groups, d))
+    for g in range(n_groups):
+        base[g, 8 * g] = 3.0
+    tiles = []
+    for g in range(n_groups):
+        for _ in range(per_group):
+            tiles.append(base[g] + 0.05 * rng.standard_normal((n_v, d)))
+    return np.stack(tiles).astype(np.float32).astype(np.float64)
+
+
+def test_knn_neighbours_are_the_group_and_score_is_the_group_mean():
+    rng = np.random.default_rng(21)
+    X = _grouped_scene(rng)
+    inv = np.stack([O.token_inv_norms(X[i]) for i in range(X.shape[0])])
+    cos = O.tile_similarity(O.tile_embeddings(X, inv))
+    s = rng.standard_normal(X.shape[0])
+    sm, nbrs = O.knn_smooth(s, cos, 3)
+    for i in range(X.shape[0]):
+        group = set(range(4 * (i // 4), 4 * (i // 4) + 4)) - {i}
+        assert set(nbrs[i]) == group
+        assert abs(sm[i] - s[4 * (i // 4):4 * (i // 4) + 4].mean()) <= 1e-15 * 4
+
+
+def test_knn_off_and_constant_scores():
+    rng = np.random.default_rng(22)
+    X = rng.standard_normal((5, 64, 32)).astype(np.float32).astype(np.float64)
+    Q = rng.standard_normal((16, 32)).astype(np.float32).astype(np.float64)
+    a = O.scene_query_stage1(X, Q, 2, 0.0)
+    b = O.scene_query_stage1(X, Q, 2, 0.0, knn_m=0)
+    assert np.array_equal(a["s"], b["s"]) and np.array_equal(a["s"], a["s_raw"])
+    cos = rng.uniform(-1, 1, size=(5, 5))
+    sm, _ = O.knn_smooth(np.full(5, 0.375), cos, 3)
+    assert np.all(sm == 0.375)
+
+
+def test_tile_similarity_against_normalised_dot_products():
+    rng = np.random.default_rng(23)
+    X = rng.standard_normal((7, 20, 64)).astype(np.float32).astype(np.float64)
+    inv = np.stack([O.token_inv_norms(X[i]) for i in range(7)])
+    E = O.tile_embeddings(X, inv)
+    # the embedding is the sum of unit tokens, up to float32 rounding
+    unit = X / np.linalg.norm(X, axis=2, keepdims=True)
+    assert np.allclose(E, unit.sum(axis=1), rtol=1e-6, atol=1e-6)
+    cos = O.tile_similarity(E)
+    En = E / np.linalg.norm(E, axis=1, keepdims=True)
+    assert np.allclose(cos, En @ En.T, rtol=0, atol=1e-13)
+    assert np.array_equal(cos, cos.T)
+    assert np.allclose(np.diag(cos), 1.0, atol=1e-15)
+
+
+def test_knn_ties_go_to_the_lower_tile_and_permutation_equivariance():
+    rng = np.random.default_rng(24)
+    X = rng.standard_normal((6, 12, 32)).astype(np.float32).astype(np.float64)
+    X[4] = X[2]                       # tiles 2 and 4 identical: equal similarity to everyone
+    inv = np.stack([O.token_inv_norms(X[i]) for i in range(6)])
+    cos = O.tile_similarity(O.tile_embeddings(X, inv))
+    s = rng.standard_normal(6)
+    _, nbrs = O.knn_smooth(s, cos, 5)
+    for i in (0, 1, 3, 5):
+        assert nbrs[i].index(2) < nbrs[i].index(4)
+    # relabelling tiles relabels the result (random tiles, no ties)
+    Y = rng.standard_normal((6, 12, 32)).astype(np.float32).astype(np.float64)
+    perm = rng.permutation(6)
+    invY = np.stack([O.token_inv_norms(Y[i]) for i in range(6)])
+    cY = O.tile_similarity(O.tile_embeddings(Y, invY))
+    smY, _ = O.knn_smooth(s, cY, 3)
+    Yp = Y[perm]
+    invP = np.stack([O.token_inv_norms(Yp[i]) for i in range(6)])
+    cP = O.tile_similarity(O.tile_embeddings(Yp, invP))
+    smP, _ = O.knn_smooth(s[perm], cP, 3)
+    assert np.array_equal(smP, smY[perm])
