@@ -154,6 +154,33 @@ def exhaustive_run(R, torch, w, tokens, qbank, sysd, qryd, layers, cfg, chunk: i
             "tflop": round(tflop, 1), "frac_bf16_peak": round(tflop / (ms * 1e-3) / PEAK_BF16_TFLOPS, 4)}
 
 
+def knn_score_timing(R, torch, tokens, qbank, keep_count, m=6, reps=10) -> dict:
+    """The scoring call with the optional smoothing over each tile's m most
+    similar tiles (median of `reps` calls), for comparison with the plain
+    scoring stage the scene-query uses."""
+    n, nv, d = tokens.shape
+    dev = tokens.device
+    key = torch.empty(n * nv, dtype=torch.float64, device=dev)
+    sim = torch.empty(n * nv, qbank.shape[0], dtype=torch.float32, device=dev)
+    s = torch.empty(n, dtype=torch.float64, device=dev)
+    u = torch.empty(n, dtype=torch.float32, device=dev)
+    order = torch.empty(n, dtype=torch.int32, device=dev)
+    nk = torch.empty(1, dtype=torch.int32, device=dev)
+    ws = torch.empty(R.rift_score_workspace_size(n, nv, d, m), dtype=torch.uint8, device=dev)
+    call = lambda: R.rift_score_tiles(tokens, qbank, keep_count, 0.0, key, sim, s, u, order, nk, ws, knn_m=m)
+    call()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        call()
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    return {"m": m, "score_ms": round(statistics.median(ts), 4)}
+
+
 def select_batched(R, torch, token_key, order, budgets, n_tiles, n_v, n_keep, copies=64, reps=10) -> dict:
     """rift_select_tokens over `copies` scene-queries' keys at once (one call),
     for a bandwidth-meaningful number; median of `reps` timed calls."""
@@ -339,6 +366,9 @@ def main() -> int:
         "hbm": hbm,
     }
     out["packed_tokens_per_s"] = round(T * K / elapsed, 1)
+    kn = knn_score_timing(R, torch, tokens, qbank, w.keep_count)
+    kn["extra_ms_over_plain_score"] = round(kn["score_ms"] - stage_ms["score"], 4)
+    out["knn_smoothing"] = kn
     out["select_batched"] = select_batched(R, torch, q.token_key, q.tile_order, q.budgets, w.n_tiles,
                                            w.n_v, q.n_keep)
     if not args.no_exhaustive:

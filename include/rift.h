@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define RIFT_ABI_VERSION 1
+#define RIFT_ABI_VERSION 2
 
 #if defined(__GNUC__) || defined(__clang__)
 #define RIFT_API __attribute__((visibility("default")))
@@ -67,8 +67,10 @@ RIFT_API const char* rift_status_string(rift_status s);
 
 /* ------------------------------------------------------------------ Stage 1 */
 
-/* Workspace bytes rift_score_tiles needs for a scene of this shape. */
-RIFT_API size_t rift_score_workspace_size(int32_t n_tiles, int32_t n_v, int32_t d);
+/* Workspace bytes rift_score_tiles needs for a scene of this shape and knn_m
+ * (0 if the call does not smooth; a smoothing call needs about
+ * 8 n_tiles (n_v + n_tiles) + 4 n_tiles d bytes more). */
+RIFT_API size_t rift_score_workspace_size(int32_t n_tiles, int32_t n_v, int32_t d, int32_t knn_m);
 
 /*
  * rift_score_tiles -- Stage 1 of Sec. 2.3: Eq. 1 background-margin relevance,
@@ -80,6 +82,15 @@ RIFT_API size_t rift_score_workspace_size(int32_t n_tiles, int32_t n_v, int32_t 
  *                                    rounding to dt (the rounded values count)
  * keep_count  > 0: keep the top min(keep_count, n_tiles) tiles by score;
  *             == 0: keep every tile with u >= tau (tau is compared in float64)
+ * knn_m       0: no smoothing.  > 0: before normalisation each tile score is
+ *             averaged with the scores of its knn_m most visually similar tiles
+ *             (Listing 1's note "smoothed with its 6 most similar tiles";
+ *             App. B Step 3).  The tile embedding is the float32-rounded sum of
+ *             its unit tokens, accumulated over tokens in ascending order with
+ *             each product and sum rounded on its own; similarity is the cosine
+ *             of the canonical dot products; neighbours are the knn_m (at most
+ *             n_tiles - 1) largest over the other tiles, ties to the lower id;
+ *             s' = (s + neighbour scores in neighbour order) / (1 + knn_m).
  * Outputs (all device):
  * token_key   [n_tiles*n_v] f64  per-token margin of the unit token,
  *                                r = (x.w)/|x| with w = t - mean_j B_j rounded
@@ -93,19 +104,20 @@ RIFT_API size_t rift_score_workspace_size(int32_t n_tiles, int32_t n_v, int32_t 
  *                                B_j (MFMA relevance GEMM), or NULL to skip
  * tile_score  [n_tiles] f64      s_i = mean of the tile's token margins: 64
  *                                strided partial sums then a halving tree,
- *                                divided by n_v
+ *                                divided by n_v; the smoothed score when
+ *                                knn_m > 0 (the score u and the order use)
  * tile_u      [n_tiles] f32      (s - min s)/(max s - min s) in float64,
  *                                rounded to f32; all 1 when max == min
  * tile_order  [n_tiles] i32      tile ids by (s descending, id ascending); the
  *                                first *n_keep entries are the kept tiles
  * n_keep      [1] i32            number of kept tiles
  * Shape rules: 1 <= n_tiles <= 4096, 1 <= n_v <= 1024, d % 32 == 0,
- * 32 <= d <= 16384, 0 <= n_bg <= 15, 0 <= tau (any double).
+ * 32 <= d <= 16384, 0 <= n_bg <= 15, 0 <= tau (any double), knn_m >= 0.
  * workspace   >= rift_score_workspace_size(...) bytes, 256-byte aligned.
  */
 RIFT_API rift_status rift_score_tiles(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
                              int32_t d, const void* query_bank, int32_t n_bg,
-                             int32_t keep_count, double tau,
+                             int32_t keep_count, double tau, int32_t knn_m,
                              double* token_key, float* token_sim, double* tile_score,
                              float* tile_u, int32_t* tile_order, int32_t* n_keep,
                              void* workspace, size_t ws_bytes, rift_stream stream);

@@ -67,9 +67,9 @@ def load() -> ctypes.CDLL:
     L.rift_status_string.restype = ctypes.c_char_p
     L.rift_status_string.argtypes = [I32]
     L.rift_score_workspace_size.restype = SZ
-    L.rift_score_workspace_size.argtypes = [I32, I32, I32]
+    L.rift_score_workspace_size.argtypes = [I32, I32, I32, I32]
     L.rift_score_tiles.restype = I32
-    L.rift_score_tiles.argtypes = [P, I32, I32, I32, I32, P, I32, I32, F64, P, P, P, P, P, P, P, SZ, P]
+    L.rift_score_tiles.argtypes = [P, I32, I32, I32, I32, P, I32, I32, F64, I32, P, P, P, P, P, P, P, SZ, P]
     L.rift_assign_budgets.restype = I32
     L.rift_assign_budgets.argtypes = [I32, I32, P, I32, P, I32, P, P]
     L.rift_select_tokens.restype = I32
@@ -134,12 +134,13 @@ def _need(t, dtype, shape=None, name="tensor"):
 
 
 # ----------------------------------------------------------------------------- Stage 1
-def rift_score_workspace_size(n_tiles: int, n_v: int, d: int) -> int:
-    return int(load().rift_score_workspace_size(n_tiles, n_v, d))
+def rift_score_workspace_size(n_tiles: int, n_v: int, d: int, knn_m: int = 0) -> int:
+    return int(load().rift_score_workspace_size(n_tiles, n_v, d, knn_m))
 
 
 def rift_score_tiles(tokens, query_bank, keep_count: int, tau: float, token_key, token_sim,
-                     tile_score, tile_u, tile_order, n_keep, workspace, stream=None) -> None:
+                     tile_score, tile_u, tile_order, n_keep, workspace, stream=None,
+                     knn_m: int = 0) -> None:
     torch = _torch()
     n_tiles, n_v, d = tokens.shape
     nq = query_bank.shape[0]
@@ -155,7 +156,7 @@ def rift_score_tiles(tokens, query_bank, keep_count: int, tau: float, token_key,
     _need(n_keep, torch.int32, (1,), "n_keep")
     _need(workspace, torch.uint8, None, "workspace")
     st = load().rift_score_tiles(_ptr(tokens), dt, n_tiles, n_v, d, _ptr(query_bank), nq - 1,
-                                 int(keep_count), float(tau), _ptr(token_key), _ptr(token_sim),
+                                 int(keep_count), float(tau), int(knn_m), _ptr(token_key), _ptr(token_sim),
                                  _ptr(tile_score), _ptr(tile_u), _ptr(tile_order), _ptr(n_keep),
                                  _ptr(workspace), workspace.numel(), _stream(stream))
     _check(st, "rift_score_tiles")

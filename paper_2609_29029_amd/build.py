@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "librift.so")
 BUILD = os.path.join(HERE, "_build")
 
-SOURCES = ["score.hip", "select.hip", "compact.hip", "prefill_misc.hip", "gemm_bf16.hip",
+SOURCES = ["score.hip", "knn.hip", "select.hip", "compact.hip", "prefill_misc.hip", "gemm_bf16.hip",
            "attention.hip", "capi.hip"]
 
 ARCH = "gfx950"

@@ -108,32 +108,60 @@ const char* rift_status_string(rift_status s) {
     return "unknown status";
 }
 
-size_t rift_score_workspace_size(int32_t n_tiles, int32_t n_v, int32_t d) {
-    (void)n_tiles;
-    (void)n_v;
-    if (d <= 0) return 0;
-    return align_up((size_t)d * sizeof(float));
+namespace {
+// score workspace: w (float32 [d]); with smoothing, then inverse token norms
+// (float64 [n_tiles n_v]), tile embeddings (float32 [n_tiles][d]), their
+// dot products (float64 [n_tiles][n_tiles]) and the smoothed scores.
+struct ScoreLayout {
+    size_t w, inv, emb, gram, smooth, total;
+};
+ScoreLayout score_layout(int32_t n_tiles, int32_t n_v, int32_t d, int32_t knn_m) {
+    ScoreLayout L{};
+    size_t off = 0;
+    L.w = off;
+    off += align_up((size_t)d * sizeof(float));
+    if (knn_m > 0) {
+        L.inv = off;
+        off += align_up((size_t)n_tiles * n_v * sizeof(double));
+        L.emb = off;
+        off += align_up((size_t)n_tiles * d * sizeof(float));
+        L.gram = off;
+        off += align_up((size_t)n_tiles * n_tiles * sizeof(double));
+        L.smooth = off;
+        off += align_up((size_t)n_tiles * sizeof(double));
+    }
+    L.total = off;
+    return L;
+}
+}  // namespace
+
+size_t rift_score_workspace_size(int32_t n_tiles, int32_t n_v, int32_t d, int32_t knn_m) {
+    if (d <= 0 || n_tiles <= 0 || n_v <= 0 || knn_m < 0) return 0;
+    return score_layout(n_tiles, n_v, d, knn_m).total;
 }
 
 rift_status rift_score_tiles(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
                              int32_t d, const void* query_bank, int32_t n_bg, int32_t keep_count,
-                             double tau, double* token_key, float* token_sim, double* tile_score,
-                             float* tile_u, int32_t* tile_order, int32_t* n_keep, void* workspace,
-                             size_t ws_bytes, rift_stream stream) {
+                             double tau, int32_t knn_m, double* token_key, float* token_sim,
+                             double* tile_score, float* tile_u, int32_t* tile_order, int32_t* n_keep,
+                             void* workspace, size_t ws_bytes, rift_stream stream) {
     if (tokens == nullptr || query_bank == nullptr || token_key == nullptr ||
         tile_score == nullptr || tile_u == nullptr || tile_order == nullptr || n_keep == nullptr ||
         workspace == nullptr)
         return RIFT_ERR_NULL;
     if (!dt_valid(dt)) return RIFT_ERR_DTYPE;
     if (n_tiles < 1 || n_tiles > 4096 || n_v < 1 || n_v > 1024 || d < 32 || d > 16384 ||
-        d % 32 != 0 || n_bg < 0 || n_bg > 15 || keep_count < 0 || isnan(tau))
+        d % 32 != 0 || n_bg < 0 || n_bg > 15 || keep_count < 0 || isnan(tau) || knn_m < 0)
         return RIFT_ERR_SHAPE;
-    if (misaligned(workspace) || ws_bytes < rift_score_workspace_size(n_tiles, n_v, d))
-        return RIFT_ERR_WORKSPACE;
+    const ScoreLayout L = score_layout(n_tiles, n_v, d, knn_m);
+    if (misaligned(workspace) || ws_bytes < L.total) return RIFT_ERR_WORKSPACE;
     if (init_kernel_attributes() != hipSuccess) return RIFT_ERR_HIP;
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
     hipError_t e = launch_score(tokens, dt == RIFT_BF16, n_tiles, n_v, d, query_bank, n_bg,
-                                keep_count, tau, token_key, token_sim, tile_score, tile_u,
-                                tile_order, n_keep, static_cast<float*>(workspace),
+                                keep_count, tau, knn_m, token_key, token_sim, tile_score, tile_u,
+                                tile_order, n_keep, reinterpret_cast<float*>(ws + L.w),
+                                reinterpret_cast<double*>(ws + L.inv), reinterpret_cast<float*>(ws + L.emb),
+                                reinterpret_cast<double*>(ws + L.gram), reinterpret_cast<double*>(ws + L.smooth),
                                 static_cast<hipStream_t>(stream));
     return hip_status(e);
 }

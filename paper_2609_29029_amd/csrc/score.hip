@@ -49,7 +49,7 @@ __global__ void __launch_bounds__(640)
 score_tiles_kernel(const void* __restrict__ tokens, int n_v, int d,
                    const void* __restrict__ qbank, int nq, const float* __restrict__ w32,
                    double* __restrict__ token_key, float* __restrict__ token_sim,
-                   double* __restrict__ tile_score) {
+                   double* __restrict__ tile_score, double* __restrict__ inv_out) {
     extern __shared__ __align__(16) unsigned char smem[];
     float* w_lds = reinterpret_cast<float*>(smem);
     double* r_lds = reinterpret_cast<double*>(smem + (size_t)d * sizeof(float));
@@ -174,6 +174,7 @@ score_tiles_kernel(const void* __restrict__ tokens, int n_v, int d,
         if (valid && q == 0) {
             token_key[key_base + tok[b]] = key;
             r_lds[tok[b]] = key;
+            if (inv_out != nullptr) inv_out[key_base + tok[b]] = (nn == 0.0) ? 0.0 : 1.0 / sqrt(nn);
         }
         if (token_sim != nullptr && valid) {
             const float inv = (nn > 0.0) ? (float)(1.0 / sqrt(nn)) : 0.0f;
@@ -208,7 +209,8 @@ __device__ __forceinline__ bool precedes(double ka, int ia, double kb, int ib) {
 
 __global__ void __launch_bounds__(1024)
 rank_tiles_kernel(const double* __restrict__ s, int n, int keep_count, double tau,
-                  float* __restrict__ u_out, int* __restrict__ order, int* __restrict__ n_keep) {
+                  float* __restrict__ u_out, int* __restrict__ order, int* __restrict__ n_keep,
+                  double* __restrict__ s_copy) {
     __shared__ double key[4096];
     __shared__ int id[4096];
     __shared__ int kept;
@@ -217,6 +219,7 @@ rank_tiles_kernel(const double* __restrict__ s, int n, int keep_count, double ta
     for (int i = threadIdx.x; i < N; i += blockDim.x) {
         key[i] = i < n ? s[i] : -INFINITY;
         id[i] = i;
+        if (s_copy != nullptr && i < n) s_copy[i] = s[i];
     }
     if (threadIdx.x == 0) kept = 0;
     __syncthreads();
@@ -256,23 +259,34 @@ rank_tiles_kernel(const double* __restrict__ s, int n, int keep_count, double ta
 }
 
 hipError_t launch_score(const void* tokens, bool bf16, int n_tiles, int n_v, int d,
-                        const void* qbank, int n_bg, int keep_count, double tau, double* token_key,
-                        float* token_sim, double* tile_score, float* tile_u, int* tile_order,
-                        int* n_keep, float* w32, hipStream_t st) {
+                        const void* qbank, int n_bg, int keep_count, double tau, int knn_m,
+                        double* token_key, float* token_sim, double* tile_score, float* tile_u,
+                        int* tile_order, int* n_keep, float* w32, double* inv, float* emb,
+                        double* gram, double* s_smooth, hipStream_t st) {
     hipLaunchKernelGGL(prep_w_kernel, dim3((d + 255) / 256), dim3(256), 0, st, qbank, bf16 ? 1 : 0,
                        d, n_bg, w32);
     const int groups = (n_v + 63) / 64;
     const int waves = groups < 10 ? groups : 10;   // a wave takes every 10th group beyond 640 tokens
     const size_t lds = (size_t)d * sizeof(float) + (size_t)groups * 64 * sizeof(double);
+    double* inv_out = knn_m > 0 ? inv : nullptr;
     if (bf16) {
         hipLaunchKernelGGL(score_tiles_kernel<true>, dim3(n_tiles), dim3(waves * 64), lds, st,
-                           tokens, n_v, d, qbank, 1 + n_bg, w32, token_key, token_sim, tile_score);
+                           tokens, n_v, d, qbank, 1 + n_bg, w32, token_key, token_sim, tile_score, inv_out);
     } else {
         hipLaunchKernelGGL(score_tiles_kernel<false>, dim3(n_tiles), dim3(waves * 64), lds, st,
-                           tokens, n_v, d, qbank, 1 + n_bg, w32, token_key, token_sim, tile_score);
+                           tokens, n_v, d, qbank, 1 + n_bg, w32, token_key, token_sim, tile_score, inv_out);
     }
-    hipLaunchKernelGGL(rank_tiles_kernel, dim3(1), dim3(1024), 0, st, tile_score, n_tiles,
-                       keep_count, tau, tile_u, tile_order, n_keep);
+    const double* s_rank = tile_score;
+    double* s_copy = nullptr;
+    if (knn_m > 0) {
+        const hipError_t e = launch_knn_smooth(tokens, bf16, n_tiles, n_v, d, inv, emb, gram, tile_score,
+                                               knn_m, s_smooth, st);
+        if (e != hipSuccess) return e;
+        s_rank = s_smooth;
+        s_copy = tile_score;   // the output tile score is the one the ranking used
+    }
+    hipLaunchKernelGGL(rank_tiles_kernel, dim3(1), dim3(1024), 0, st, s_rank, n_tiles,
+                       keep_count, tau, tile_u, tile_order, n_keep, s_copy);
     return hipGetLastError();
 }
 

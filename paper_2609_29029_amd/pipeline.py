@@ -35,7 +35,7 @@ class SceneQuery:
     def __init__(self, tokens, qbank, sys_emb, qry_emb, layers: Sequence[dict],
                  shape: PrefillShape, keep_count: int, tau: float, levels: Sequence[int],
                  tier_num: Optional[Sequence[int]], tier_den: int, with_sims: bool = True,
-                 stream=None):
+                 stream=None, knn_m: int = 0):
         import torch
         self.torch = torch
         self.dev = tokens.device
@@ -45,6 +45,7 @@ class SceneQuery:
         self.keep_count, self.tau = int(keep_count), float(tau)
         self.levels, self.tier_num, self.tier_den = list(levels), tier_num, int(tier_den)
         self.stream = stream
+        self.knn_m = int(knn_m)
         n_tiles, n_v, d = tokens.shape
         self.n_tiles, self.n_v, self.d = n_tiles, n_v, d
         nq = qbank.shape[0]
@@ -56,7 +57,7 @@ class SceneQuery:
         self.tile_u = torch.empty(n_tiles, dtype=f32, device=dev)
         self.tile_order = torch.empty(n_tiles, dtype=i32, device=dev)
         self.n_keep_dev = torch.empty(1, dtype=i32, device=dev)
-        self.score_ws = torch.empty(max(256, R.rift_score_workspace_size(n_tiles, n_v, d)),
+        self.score_ws = torch.empty(max(256, R.rift_score_workspace_size(n_tiles, n_v, d, self.knn_m)),
                                     dtype=torch.uint8, device=dev)
         self.sel_status = torch.empty(1, dtype=i32, device=dev)
         self.cmp_status = torch.empty(1, dtype=i32, device=dev)
@@ -97,7 +98,7 @@ class SceneQuery:
     def score(self) -> None:
         R.rift_score_tiles(self.tokens, self.qbank, self.keep_count, self.tau, self.token_key,
                            self.token_sim, self.tile_score, self.tile_u, self.tile_order,
-                           self.n_keep_dev, self.score_ws, self.stream)
+                           self.n_keep_dev, self.score_ws, self.stream, knn_m=self.knn_m)
 
     def select(self) -> None:
         R.rift_select_tokens(self.token_key, self.n_tiles, self.n_v, self.tile_order, self.budgets,

@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol(R):
     assert tuple(names) == R.EXPORTS
     for n in names:
         assert hasattr(L, n), n
-    assert L.rift_abi_version() == 1
+    assert L.rift_abi_version() == 2
     assert L.rift_status_string(4).decode().startswith("budget")
 
 
@@ -82,24 +82,30 @@ FAKE = 0x1000  # a non-NULL value; never dereferenced (validation fails first)
 
 def test_score_validation(R):
     L = R.load()
-    args = dict(tokens=FAKE, dt=1, n_tiles=4, n_v=576, d=256, qb=FAKE, n_bg=15, keep=2, tau=0.37,
+    args = dict(tokens=FAKE, dt=1, n_tiles=4, n_v=576, d=256, qb=FAKE, n_bg=15, keep=2, tau=0.37, knn=0,
                 key=FAKE, sim=None, s=FAKE, u=FAKE, order=FAKE, nk=FAKE, ws=0x10000, wsb=1 << 20)
 
     def call(**over):
         a = dict(args, **over)
         return L.rift_score_tiles(a["tokens"], a["dt"], a["n_tiles"], a["n_v"], a["d"], a["qb"], a["n_bg"],
-                                  a["keep"], a["tau"], a["key"], a["sim"], a["s"], a["u"], a["order"],
+                                  a["keep"], a["tau"], a["knn"], a["key"], a["sim"], a["s"], a["u"], a["order"],
                                   a["nk"], a["ws"], a["wsb"], None)
     assert call(tokens=None) == 1
     assert call(key=None) == 1
     assert call(ws=None) == 1
     assert call(dt=7) == 3
     for bad in (dict(n_tiles=0), dict(n_tiles=4097), dict(n_v=0), dict(n_v=1025), dict(d=48),
-                dict(d=16416), dict(n_bg=16), dict(n_bg=-1), dict(keep=-1), dict(tau=float("nan"))):
+                dict(d=16416), dict(n_bg=16), dict(n_bg=-1), dict(keep=-1), dict(tau=float("nan")),
+                dict(knn=-1)):
         assert call(**bad) == 2, bad
     assert call(ws=0x10010) == 5              # misaligned workspace
     assert call(wsb=16) == 5                  # too small
     assert R.rift_score_workspace_size(4, 576, 4096) >= 4096 * 4
+    # smoothing needs inverse norms, embeddings, their dot products and the smoothed scores
+    need = R.rift_score_workspace_size(4, 576, 256, 6)
+    assert need >= 256 * 4 + 4 * 576 * 8 + 4 * 256 * 4 + 4 * 4 * 8 + 4 * 8
+    assert call(knn=6, wsb=need - 1) == 5
+    assert R.rift_score_workspace_size(4, 576, 4096, -1) == 0
 
 
 def test_select_and_compact_validation(R):

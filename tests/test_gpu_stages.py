@@ -20,7 +20,7 @@ def R():
     return R
 
 
-def run_score(R, tokens, qbank, keep_count, tau, sims=True):
+def run_score(R, tokens, qbank, keep_count, tau, sims=True, knn_m=0):
     torch = torch_mod()
     n_tiles, n_v, d = tokens.shape
     nq = qbank.shape[0]
@@ -31,9 +31,9 @@ def run_score(R, tokens, qbank, keep_count, tau, sims=True):
         tile_u=torch.empty(n_tiles, dtype=torch.float32, device="cuda"),
         tile_order=torch.empty(n_tiles, dtype=torch.int32, device="cuda"),
         n_keep=torch.empty(1, dtype=torch.int32, device="cuda"))
-    ws = torch.empty(max(256, R.rift_score_workspace_size(n_tiles, n_v, d)), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(max(256, R.rift_score_workspace_size(n_tiles, n_v, d, knn_m)), dtype=torch.uint8, device="cuda")
     R.rift_score_tiles(tokens, qbank, keep_count, tau, out["token_key"], out["token_sim"],
-                       out["tile_score"], out["tile_u"], out["tile_order"], out["n_keep"], ws)
+                       out["tile_score"], out["tile_u"], out["tile_order"], out["n_keep"], ws, knn_m=knn_m)
     torch.cuda.synchronize()
     return {k: (None if v is None else v.cpu().numpy()) for k, v in out.items()}
 
@@ -65,6 +65,42 @@ def test_score_parity(R, name):
         # the planted query-aligned tiles rank at the top (sanity, not parity)
         top = set(ref["order"][: len(sc.planted)])
         assert top == set(int(t) for t in sc.planted)
+
+
+@pytest.mark.parametrize("name,m", [("tiny", 1), ("tiny", 6), ("scene8", 6), ("scene8", 3), ("one_tile", 6)])
+def test_score_knn_smoothing_parity(R, name, m):
+    """Optional smoothing over the m most similar tiles: smoothed scores, u,
+    order and kept count bit for bit (keys as without smoothing)."""
+    w = synth.get(name)
+    sc = synth.make_scene(w)
+    X64, Q64 = f64(sc.tokens, w.dtype), f64(sc.qbank, w.dtype)
+    got = run_score(R, upload(sc.tokens, w.dtype), upload(sc.qbank, w.dtype), w.keep_count, w.tau, knn_m=m)
+    ref = O.scene_query_stage1(X64, Q64, w.keep_count, w.tau, knn_m=m)
+    check_stage1(got, ref, X64, Q64)
+    # threshold mode on the smoothed scores
+    got = run_score(R, upload(sc.tokens, w.dtype), upload(sc.qbank, w.dtype), 0, 0.37, sims=False, knn_m=m)
+    ref = O.scene_query_stage1(X64, Q64, 0, 0.37, knn_m=m)
+    check_stage1(got, ref, X64, Q64, sims=False)
+
+
+def test_score_knn_grouped_tiles(R):
+    """Tiles built around three orthogonal directions: each tile's neighbours
+    are the rest of its group, so with m = 3 its score is its group's mean."""
+    rng = np.random.default_rng(21)
+    d, n_v = 64, 64
+    base = np.zeros((3, d))
+    for g in range(3):
+        base[g, 8 * g] = 3.0
+    X = np.stack([base[i // 4] + 0.05 * rng.standard_normal((n_v, d)) for i in range(12)])
+    X = synth.store(X.astype(np.float32), "f32")
+    Q = synth.store(rng.standard_normal((16, d)).astype(np.float32), "f32")
+    X64, Q64 = f64(X, "f32"), f64(Q, "f32")
+    got = run_score(R, upload(X, "f32"), upload(Q, "f32"), 4, 0.0, sims=False, knn_m=3)
+    ref = O.scene_query_stage1(X64, Q64, 4, 0.0, knn_m=3)
+    check_stage1(got, ref, X64, Q64, sims=False)
+    raw = ref["s_raw"]
+    for i in range(12):
+        assert abs(got["tile_score"][i] - raw[4 * (i // 4):4 * (i // 4) + 4].mean()) <= 1e-15 * 4
 
 
 def test_score_threshold_mode(R):
@@ -237,3 +273,16 @@ def test_compact_edges(R):
     # a budget (offset step) larger than n_v
     packed, cu, pos, st = run_compact(R, X, "bf16", [0], np.array([0, 21]), np.arange(21) % 20, sysr, qry)
     assert st == 2
+
+
+@pytest.mark.slow
+def test_score_knn_smoothing_full_size(R):
+    """The 400-tile scene with 6-neighbour smoothing, every score and rank bit
+    for bit."""
+    w = synth.get("scene20")
+    sc = synth.make_scene(w)
+    X64, Q64 = f64(sc.tokens, w.dtype), f64(sc.qbank, w.dtype)
+    got = run_score(R, upload(sc.tokens, w.dtype), upload(sc.qbank, w.dtype), w.keep_count, w.tau,
+                    sims=False, knn_m=6)
+    ref = O.scene_query_stage1(X64, Q64, w.keep_count, w.tau, knn_m=6)
+    check_stage1(got, ref, X64, Q64, sims=False)
