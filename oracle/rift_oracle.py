@@ -45,6 +45,12 @@ Readings of points the paper leaves open (each is listed in the design doc):
       m largest similarities over j != i, ties to the lower j; the smoothed
       score is (s_i + sum of the neighbours' s in neighbour order) / (1 + m),
       and u and the ranking use it.  Off unless asked for (m = 0).
+  R9  Optional utility budgets (Eq. 2): U_i(c) = p_i a+_c + (1 - p_i) a-_c
+      - lambda E_c evaluated in float64 as ((p a+) + ((1 - p) a-)) - (lambda
+      E) with every operation rounded on its own; the budget is the c of
+      largest U, ties to the smaller c.  p_i, the trained predictor's
+      probability that the tile holds the object, is out of scope: callers
+      pass it (the pipeline passes the tile's normalised score u_i).
 """
 from __future__ import annotations
 
@@ -193,6 +199,22 @@ def assign_budgets(n_keep: int, levels: Sequence[int], tier_num: Sequence[int],
     out: List[int] = []
     for lvl, c in zip(levels, counts):
         out.extend([int(lvl)] * c)
+    return np.array(out, dtype=np.int32)
+
+
+def utility_budgets(p: Sequence[float], levels: Sequence[int], alpha_pos: Sequence[float],
+                    alpha_neg: Sequence[float], energy: Sequence[float], lam: float) -> np.ndarray:
+    """Eq. 2 budget per tile (reading R9): the candidate c of largest
+    U(c) = p a+_c + (1 - p) a-_c - lambda E_c, ties to the smaller c."""
+    out = []
+    for pi in p:
+        pi = float(pi)
+        best_c, best_u = None, None
+        for c, ap, an, e in zip(levels, alpha_pos, alpha_neg, energy):
+            u = ((pi * float(ap)) + ((1.0 - pi) * float(an))) - (float(lam) * float(e))
+            if best_u is None or u > best_u or (u == best_u and int(c) < best_c):
+                best_c, best_u = int(c), u
+        out.append(best_c)
     return np.array(out, dtype=np.int32)
 
 

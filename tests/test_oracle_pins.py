@@ -457,3 +457,39 @@ def test_knn_ties_go_to_the_lower_tile_and_permutation_equivariance():
     cP = O.tile_similarity(O.tile_embeddings(Yp, invP))
     smP, _ = O.knn_smooth(s[perm], cP, 3)
     assert np.array_equal(smP, smY[perm])
+
+
+# ----------------------------------------------------------------------------- utility budgets (R9)
+# Stand-in accuracy and energy tables over the paper's budget set for LLaVA-1.5
+# (Sec. 2.3 Stage 2): accuracy on object tiles grows with the budget, accuracy
+# on empty tiles barely moves, energy is proportional to the budget.
+C5 = [576, 432, 288, 144, 72]
+AP = [0.92, 0.90, 0.85, 0.74, 0.58]
+AN = [0.95, 0.95, 0.94, 0.93, 0.91]
+EN = [c / 576 for c in C5]
+
+
+def test_utility_budgets_hand_worked():
+    # p = 1: U = a+ - 0.1 E = 0.82, 0.825, 0.80, 0.715, 0.5675 -> 432
+    # p = 0: U = a- - 0.1 E = 0.85, 0.875, 0.89, 0.905, 0.8975 -> 144
+    assert list(O.utility_budgets([1.0, 0.0], C5, AP, AN, EN, 0.1)) == [432, 144]
+    # no energy cost: the most accurate budget for the object tile, for an empty tile the
+    # first of the equal-accuracy 576 / 432 pair by size (the smaller)
+    assert list(O.utility_budgets([1.0, 0.0], C5, AP, AN, EN, 0.0)) == [576, 432]
+    # energy dominates: the smallest budget for everyone
+    assert list(O.utility_budgets([1.0, 0.5, 0.0], C5, AP, AN, EN, 100.0)) == [72, 72, 72]
+
+
+def test_utility_budgets_ties_and_order_independence():
+    # equal utilities everywhere -> the smallest budget, whatever the listing order
+    flat = [0.5] * 5
+    assert list(O.utility_budgets([0.3], C5, flat, flat, [0.0] * 5, 1.0)) == [72]
+    perm = [3, 0, 4, 1, 2]
+    a = O.utility_budgets([0.0, 0.25, 0.5, 0.75, 1.0], C5, AP, AN, EN, 0.1)
+    b = O.utility_budgets([0.0, 0.25, 0.5, 0.75, 1.0], [C5[i] for i in perm], [AP[i] for i in perm],
+                          [AN[i] for i in perm], [EN[i] for i in perm], 0.1)
+    assert np.array_equal(a, b)
+    # the budget never shrinks as p grows when a+ - a- grows with the budget
+    p = np.linspace(0, 1, 101)
+    bud = O.utility_budgets(p, C5, AP, AN, EN, 0.1)
+    assert np.all(np.diff(bud) >= 0)
