@@ -139,6 +139,29 @@ RIFT_API rift_status rift_assign_budgets(int32_t n_keep, int32_t n_v, const int3
                                 int32_t* budgets, int64_t* total);
 
 /*
+ * rift_assign_budgets_utility -- [host only] the elastic-prefill policy of
+ * Eq. 2 (Sec. 2.3 Stage 2): for each kept tile the budget c of the candidate
+ * set maximising U(c) = p a+_c + (1 - p) a-_c - lambda E_c, where p is the
+ * probability that the tile holds the object (the paper's trained predictor is
+ * outside this library: the caller supplies p), a+_c / a-_c the profiled answer
+ * accuracy with / without the object and E_c the profiled energy of budget c.
+ * U is evaluated in float64 as ((p a+) + ((1 - p) a-)) - (lambda E), each
+ * operation rounded on its own; ties go to the smaller budget.
+ * levels     [host] n_c candidate budgets, each in [1, n_v], any order
+ * alpha_pos, alpha_neg, energy  [host] n_c finite values, same order
+ * lambda     finite accuracy-energy trade-off
+ * p          [host] n_keep values in [0, 1] (f32)
+ * budgets    [host] out [n_keep];  total [host] out: sum of budgets (may be NULL)
+ * Errors: RIFT_ERR_NULL, RIFT_ERR_SHAPE (n_keep < 0, n_v < 1, n_c outside
+ * [1, 64]), RIFT_ERR_BUDGET (a value out of range or not finite).
+ */
+RIFT_API rift_status rift_assign_budgets_utility(int32_t n_keep, int32_t n_v, int32_t n_c,
+                                        const int32_t* levels, const double* alpha_pos,
+                                        const double* alpha_neg, const double* energy,
+                                        double lambda, const float* p, int32_t* budgets,
+                                        int64_t* total);
+
+/*
  * rift_select_tokens -- VisionZip-style dominant-token retention (Sec. 2.3
  * Stage 2) under per-tile budgets: for kept tile rho (id kept_tiles[rho]), keep
  * the budgets[rho] tokens with the largest token_key, ties to the lower token

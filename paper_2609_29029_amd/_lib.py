@@ -24,7 +24,8 @@ RIFT_BF16 = 1
 
 # Every symbol include/rift.h declares, in declaration order.
 EXPORTS = ("rift_abi_version", "rift_status_string", "rift_score_workspace_size",
-           "rift_score_tiles", "rift_assign_budgets", "rift_select_tokens", "rift_compact",
+           "rift_score_tiles", "rift_assign_budgets", "rift_assign_budgets_utility",
+           "rift_select_tokens", "rift_compact",
            "rift_prefill_workspace_size", "rift_prefill")
 
 
@@ -72,6 +73,8 @@ def load() -> ctypes.CDLL:
     L.rift_score_tiles.argtypes = [P, I32, I32, I32, I32, P, I32, I32, F64, I32, P, P, P, P, P, P, P, SZ, P]
     L.rift_assign_budgets.restype = I32
     L.rift_assign_budgets.argtypes = [I32, I32, P, I32, P, I32, P, P]
+    L.rift_assign_budgets_utility.restype = I32
+    L.rift_assign_budgets_utility.argtypes = [I32, I32, I32, P, P, P, P, F64, P, P, P]
     L.rift_select_tokens.restype = I32
     L.rift_select_tokens.argtypes = [P, I32, I32, P, P, I32, P, P, I64, P, P]
     L.rift_compact.restype = I32
@@ -178,6 +181,26 @@ def rift_assign_budgets(n_keep: int, n_v: int, levels: Sequence[int],
                                     out.ctypes.data, ctypes.byref(tot))
     _check(st, "rift_assign_budgets")
     return out[:n_keep].copy(), int(tot.value)
+
+
+def rift_assign_budgets_utility(p, levels: Sequence[int], alpha_pos: Sequence[float],
+                                alpha_neg: Sequence[float], energy: Sequence[float], lam: float,
+                                n_v: int):
+    """Host-only call (Eq. 2); p: per-tile probabilities (float32).  Returns
+    (budgets as int32 numpy array, total)."""
+    import numpy as np
+    pv = np.ascontiguousarray(p, dtype=np.float32)
+    lv = np.ascontiguousarray(levels, dtype=np.int32)
+    ap = np.ascontiguousarray(alpha_pos, dtype=np.float64)
+    an = np.ascontiguousarray(alpha_neg, dtype=np.float64)
+    en = np.ascontiguousarray(energy, dtype=np.float64)
+    out = np.zeros(max(1, pv.size), dtype=np.int32)
+    tot = ctypes.c_int64(0)
+    st = load().rift_assign_budgets_utility(int(pv.size), int(n_v), int(lv.size), lv.ctypes.data,
+                                            ap.ctypes.data, an.ctypes.data, en.ctypes.data, float(lam),
+                                            pv.ctypes.data, out.ctypes.data, ctypes.byref(tot))
+    _check(st, "rift_assign_budgets_utility")
+    return out[:pv.size].copy(), int(tot.value)
 
 
 def rift_select_tokens(token_key, n_tiles: int, n_v: int, kept_tiles, budgets, n_keep: int,

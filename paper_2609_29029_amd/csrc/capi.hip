@@ -2,6 +2,8 @@
 // kernel launches.  Nothing here allocates device memory or synchronises.
 #include <math.h>
 
+#include <cmath>
+
 #include <mutex>
 
 #include "launch.h"
@@ -197,6 +199,43 @@ rift_status rift_assign_budgets(int32_t n_keep, int32_t n_v, const int32_t* leve
             budgets[rho++] = levels[j];
             sum += levels[j];
         }
+    }
+    if (total != nullptr) *total = sum;
+    return RIFT_OK;
+}
+
+rift_status rift_assign_budgets_utility(int32_t n_keep, int32_t n_v, int32_t n_c,
+                                        const int32_t* levels, const double* alpha_pos,
+                                        const double* alpha_neg, const double* energy, double lambda,
+                                        const float* p, int32_t* budgets, int64_t* total) {
+#pragma clang fp contract(off)
+    if (levels == nullptr || alpha_pos == nullptr || alpha_neg == nullptr || energy == nullptr)
+        return RIFT_ERR_NULL;
+    if (n_keep > 0 && (p == nullptr || budgets == nullptr)) return RIFT_ERR_NULL;
+    if (n_keep < 0 || n_v < 1 || n_c < 1 || n_c > 64) return RIFT_ERR_SHAPE;
+    if (!std::isfinite(lambda)) return RIFT_ERR_BUDGET;
+    for (int c = 0; c < n_c; ++c) {
+        if (levels[c] < 1 || levels[c] > n_v) return RIFT_ERR_BUDGET;
+        if (!std::isfinite(alpha_pos[c]) || !std::isfinite(alpha_neg[c]) || !std::isfinite(energy[c]))
+            return RIFT_ERR_BUDGET;
+    }
+    for (int i = 0; i < n_keep; ++i)
+        if (!(p[i] >= 0.0f && p[i] <= 1.0f)) return RIFT_ERR_BUDGET;
+    int64_t sum = 0;
+    for (int i = 0; i < n_keep; ++i) {
+        const double pi = (double)p[i];
+        int best_c = 0;
+        double best_u = 0.0;
+        for (int c = 0; c < n_c; ++c) {
+            // each operation rounded on its own (no contraction in this function)
+            const double u = ((pi * alpha_pos[c]) + ((1.0 - pi) * alpha_neg[c])) - (lambda * energy[c]);
+            if (c == 0 || u > best_u || (u == best_u && levels[c] < best_c)) {
+                best_c = levels[c];
+                best_u = u;
+            }
+        }
+        budgets[i] = best_c;
+        sum += best_c;
     }
     if (total != nullptr) *total = sum;
     return RIFT_OK;

@@ -2,10 +2,12 @@
 prefill, enqueued on one stream through the C ABI.  Buffers are allocated once
 per plan (PyTorch as the allocator) and reused across queries.
 
-In keep-top-K mode the number of kept tiles, the budgets and the packed length
-are known on the host before the query runs, so the whole query is enqueued
-without a device-to-host copy.  Threshold mode (keep_count == 0) reads n_keep
-back once after scoring.
+In keep-top-K mode with rank-tier budgets the number of kept tiles, the
+budgets and the packed length are known on the host before the query runs, so
+the whole query is enqueued without a device-to-host copy.  Threshold mode
+(keep_count == 0) reads n_keep back once after scoring; the Eq. 2 utility
+policy reads the kept tiles' normalised scores back once (they stand in for the
+object probability p) and assigns budgets on the host.
 """
 from __future__ import annotations
 
@@ -35,7 +37,7 @@ class SceneQuery:
     def __init__(self, tokens, qbank, sys_emb, qry_emb, layers: Sequence[dict],
                  shape: PrefillShape, keep_count: int, tau: float, levels: Sequence[int],
                  tier_num: Optional[Sequence[int]], tier_den: int, with_sims: bool = True,
-                 stream=None, knn_m: int = 0):
+                 stream=None, knn_m: int = 0, utility: Optional[dict] = None):
         import torch
         self.torch = torch
         self.dev = tokens.device
@@ -46,6 +48,8 @@ class SceneQuery:
         self.levels, self.tier_num, self.tier_den = list(levels), tier_num, int(tier_den)
         self.stream = stream
         self.knn_m = int(knn_m)
+        # utility: dict(levels, alpha_pos, alpha_neg, energy, lam) for the Eq. 2 policy
+        self.utility = utility
         n_tiles, n_v, d = tokens.shape
         self.n_tiles, self.n_v, self.d = n_tiles, n_v, d
         nq = qbank.shape[0]
@@ -65,16 +69,22 @@ class SceneQuery:
                                shape.rms_eps, shape.rope_base,
                                R.RIFT_BF16 if tokens.dtype == torch.bfloat16 else R.RIFT_F32)
         self._planned_keep = None
-        if self.keep_count > 0:
+        self._cap = (0, 0)
+        if self.keep_count > 0 and utility is None:
             self._plan(min(self.keep_count, n_tiles))
 
-    # host-side plan for a given number of kept tiles
-    def _plan(self, n_keep: int) -> None:
+    # host-side plan for a given number of kept tiles (and budgets, in utility mode)
+    def _plan(self, n_keep: int, budgets=None) -> None:
+        import numpy as np
         torch = self.torch
-        if self._planned_keep == n_keep:
-            return
-        budgets, total = R.rift_assign_budgets(n_keep, self.n_v, self.levels, self.tier_num,
-                                               self.tier_den)
+        if budgets is None:
+            if self._planned_keep == n_keep:
+                return
+            budgets, total = R.rift_assign_budgets(n_keep, self.n_v, self.levels, self.tier_num,
+                                                   self.tier_den)
+        else:
+            budgets = np.ascontiguousarray(budgets, dtype=np.int32)
+            total = int(budgets.sum())
         self.n_keep = n_keep
         self.budgets_host = budgets
         self.n_selected = total
@@ -84,15 +94,28 @@ class SceneQuery:
         dev = self.dev
         self.budgets = torch.from_numpy(budgets).to(dev) if n_keep > 0 else \
             torch.zeros(1, dtype=torch.int32, device=dev)
-        self.sel_offsets = torch.empty(n_keep + 1, dtype=torch.int32, device=dev)
-        self.sel_idx = torch.empty(max(1, total), dtype=torch.int32, device=dev)
-        T = self.total_tokens
-        self.packed = torch.empty(T, self.d, dtype=self.tokens.dtype, device=dev)
-        self.cu_seqlens = torch.empty(n_keep + 1, dtype=torch.int32, device=dev)
-        self.position_ids = torch.empty(T, dtype=torch.int32, device=dev)
-        self.hidden = torch.empty(T, self.d, dtype=torch.float32, device=dev)
-        ws = R.rift_prefill_workspace_size(self.cfg, T, max(1, self.max_seqlen))
-        self.prefill_ws = torch.empty(max(256, ws), dtype=torch.uint8, device=dev)
+        # buffers grow to the largest plan seen and are reused
+        T, P = self.total_tokens, max(1, self.max_seqlen)
+        if n_keep + 1 > self._cap[0] or T > self._cap[1] or self._planned_keep is None:
+            cap_keep = max(n_keep + 1, self._cap[0])
+            cap_T = max(T, self._cap[1], 1)
+            self.sel_offsets_all = torch.empty(cap_keep, dtype=torch.int32, device=dev)
+            self.cu_seqlens_all = torch.empty(cap_keep, dtype=torch.int32, device=dev)
+            self.sel_idx = torch.empty(max(1, cap_T), dtype=torch.int32, device=dev)
+            self.packed_all = torch.empty(cap_T, self.d, dtype=self.tokens.dtype, device=dev)
+            self.position_all = torch.empty(cap_T, dtype=torch.int32, device=dev)
+            self.hidden_all = torch.empty(cap_T, self.d, dtype=torch.float32, device=dev)
+            self._cap = (cap_keep, cap_T)
+            self._ws_cap = 0
+        self.sel_offsets = self.sel_offsets_all[:n_keep + 1]
+        self.cu_seqlens = self.cu_seqlens_all[:n_keep + 1]
+        self.packed = self.packed_all[:T]
+        self.position_ids = self.position_all[:T]
+        self.hidden = self.hidden_all[:T]
+        ws = max(256, R.rift_prefill_workspace_size(self.cfg, T, P))
+        if ws > getattr(self, "_ws_cap", 0):
+            self.prefill_ws = torch.empty(ws, dtype=torch.uint8, device=dev)
+            self._ws_cap = ws
         self._planned_keep = n_keep
 
     def score(self) -> None:
@@ -102,8 +125,8 @@ class SceneQuery:
 
     def select(self) -> None:
         R.rift_select_tokens(self.token_key, self.n_tiles, self.n_v, self.tile_order, self.budgets,
-                             self.n_keep, self.sel_offsets, self.sel_idx, self.sel_status,
-                             self.stream)
+                             self.n_keep, self.sel_offsets, self.sel_idx[:max(1, self.n_selected)],
+                             self.sel_status, self.stream)
 
     def compact(self) -> None:
         R.rift_compact(self.tokens, self.tile_order, self.sel_offsets, self.sel_idx, self.n_keep,
@@ -117,14 +140,28 @@ class SceneQuery:
                        self.n_keep, max(1, self.max_seqlen), self.hidden, self.prefill_ws,
                        events=events, stream=self.stream)
 
+    def plan_utility(self) -> None:
+        """Eq. 2 budgets for the kept tiles, with each tile's normalised score u
+        as its object probability p (reads the scores back)."""
+        ut = self.utility
+        n_keep = int(self.n_keep_dev.item())
+        order = self.tile_order[:n_keep].long()
+        p = self.tile_u[order].cpu().numpy()
+        budgets, _ = R.rift_assign_budgets_utility(p, ut["levels"], ut["alpha_pos"], ut["alpha_neg"],
+                                                   ut["energy"], ut["lam"], self.n_v)
+        self._plan(n_keep, budgets)
+
     def run(self) -> None:
-        """Enqueue the whole scene-query.  Threshold mode synchronises once to
-        read the number of kept tiles."""
+        """Enqueue the whole scene-query.  Threshold mode and the utility
+        policy synchronise once after scoring."""
         self.score()
-        if self.keep_count == 0:
+        if self.keep_count == 0 or self.utility is not None:
             self.torch.cuda.current_stream().synchronize() if self.stream is None else \
                 self.stream.synchronize()
-            self._plan(int(self.n_keep_dev.item()))
+            if self.utility is not None:
+                self.plan_utility()
+            else:
+                self._plan(int(self.n_keep_dev.item()))
         self.select()
         self.compact()
         self.prefill()

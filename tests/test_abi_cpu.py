@@ -33,7 +33,7 @@ def declared_symbols():
 def test_library_exports_every_declared_symbol(R):
     L = R.load()
     names = declared_symbols()
-    assert len(names) == 9
+    assert len(names) == 10
     assert tuple(names) == R.EXPORTS
     for n in names:
         assert hasattr(L, n), n
@@ -152,3 +152,28 @@ def test_prefill_validation_and_workspace(R):
     assert call(R.model_cfg(4096, 31, 128, 11008, 1, 1e-6, 1e4, R.RIFT_BF16)) == 2
     assert call(R.model_cfg(4096, 32, 128, 11008, 1, 1e-6, 1e4, 9)) == 3
     assert R.rift_prefill_workspace_size(R.model_cfg(4096, 64, 64, 11008, 1, 1e-6, 1e4, R.RIFT_BF16), 10, 10) == 0
+
+
+def test_utility_budgets_match_oracle(R):
+    from oracle import rift_oracle as O
+    C5 = [576, 432, 288, 144, 72]
+    AP = [0.92, 0.90, 0.85, 0.74, 0.58]
+    AN = [0.95, 0.95, 0.94, 0.93, 0.91]
+    EN = [c / 576 for c in C5]
+    rng = np.random.default_rng(31)
+    p = np.concatenate([[0.0, 1.0, 0.5], rng.uniform(0, 1, 200)]).astype(np.float32)
+    for lam in (0.0, 0.1, 0.37, 100.0):
+        b, tot = R.rift_assign_budgets_utility(p, C5, AP, AN, EN, lam, 576)
+        ref = O.utility_budgets(p.astype(np.float64), C5, AP, AN, EN, lam)
+        assert np.array_equal(b, ref) and tot == int(ref.sum())
+    # validation
+    L = R.load()
+    import ctypes
+    with pytest.raises(R.RiftError):
+        R.rift_assign_budgets_utility([1.5], C5, AP, AN, EN, 0.1, 576)
+    with pytest.raises(R.RiftError):
+        R.rift_assign_budgets_utility([0.5], [577] + C5[1:], AP, AN, EN, 0.1, 576)
+    with pytest.raises(R.RiftError):
+        R.rift_assign_budgets_utility([0.5], C5, AP, AN, EN, float("inf"), 576)
+    b, tot = R.rift_assign_budgets_utility([], C5, AP, AN, EN, 0.1, 576)
+    assert b.size == 0 and tot == 0

@@ -182,3 +182,49 @@ def test_scene20_full_size(R):
     errs = [rowwise_rel_err(hid[cu[i]:cu[i + 1]], ys[i]) for i in seqs]
     print(f"scene20: prefill rowwise rel err {errs}")
     assert max(errs) <= TOL["bf16"]
+
+
+# Eq. 2 stand-in tables over the paper's budget set for LLaVA-1.5 (Sec. 2.3 Stage 2)
+UTIL = dict(levels=[576, 432, 288, 144, 72], alpha_pos=[0.92, 0.90, 0.85, 0.74, 0.58],
+            alpha_neg=[0.95, 0.95, 0.94, 0.93, 0.91], energy=[c / 576 for c in (576, 432, 288, 144, 72)],
+            lam=0.1)
+
+
+@pytest.mark.parametrize("knn_m", [0, 6])
+def test_scene_query_utility_budgets(R, knn_m):
+    """The Eq. 2 utility policy with p = u (and optionally smoothed scores):
+    budgets, selection and packing bit for bit, prefill within tolerance."""
+    from paper_2609_29029_amd.pipeline import SceneQuery
+    torch = torch_mod()
+    w = synth.get("scene8")
+    sc = synth.make_scene(w)
+    W = synth.make_layer(w, 0)
+    q = SceneQuery(upload(sc.tokens, w.dtype), upload(sc.qbank, w.dtype), upload(sc.sys, w.dtype),
+                   upload(sc.qry, w.dtype), [upload_layer(W, w.dtype)], plan_shape(w), w.keep_count, w.tau,
+                   w.levels, w.tier_num, w.tier_den, knn_m=knn_m, utility=UTIL)
+    q.run()
+    torch.cuda.synchronize()
+    assert q.check_status() == [0, 0]
+    X64, Q64 = f64(sc.tokens, w.dtype), f64(sc.qbank, w.dtype)
+    ref = O.scene_query_stage1(X64, Q64, w.keep_count, w.tau, knn_m=knn_m)
+    kept = list(ref["order"][: ref["n_keep"]])
+    p = ref["u"][kept].astype(np.float32).astype(np.float64)
+    budgets = O.utility_budgets(p, UTIL["levels"], UTIL["alpha_pos"], UTIL["alpha_neg"], UTIL["energy"],
+                                UTIL["lam"])
+    assert np.array_equal(q.budgets_host, budgets)
+    if knn_m == 0:
+        assert len(set(budgets.tolist())) > 1    # the policy is elastic on this scene
+    offs, sel = O.select_tokens(ref["r"], kept, budgets)
+    packed, cu, pos = O.compact(sc.tokens, kept, offs, sel, sc.sys, sc.qry)
+    assert np.array_equal(q.tile_order.cpu().numpy(), ref["order"])
+    assert np.array_equal(q.sel_offsets.cpu().numpy(), offs)
+    assert np.array_equal(q.sel_idx.cpu().numpy()[: len(sel)], sel)
+    assert np.array_equal(download_stored(q.packed, w.dtype), packed)
+    assert np.array_equal(q.cu_seqlens.cpu().numpy(), cu)
+    m = w.model
+    seqs = pick_sequences(cu, 4)
+    hid = q.hidden.cpu().numpy().astype(np.float64)
+    ys = O.prefill(f64(packed, w.dtype), cu, pos, [oracle_layer_weights(W, w.dtype)], m.n_heads, m.head_dim,
+                   m.rms_eps, m.rope_base, seqs)
+    errs = [rowwise_rel_err(hid[cu[i]:cu[i + 1]], ys[i]) for i in seqs]
+    assert max(errs) <= TOL[w.dtype], errs
