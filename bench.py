@@ -181,6 +181,35 @@ def knn_score_timing(R, torch, tokens, qbank, keep_count, m=6, reps=10) -> dict:
     return {"m": m, "score_ms": round(statistics.median(ts), 4)}
 
 
+# Eq. 2 stand-in tables over the paper's budget set for LLaVA-1.5 (accuracy with
+# and without the object, energy proportional to the budget); the probability
+# p of each kept tile is its normalised score u.
+UTILITY = dict(levels=[576, 432, 288, 144, 72], alpha_pos=[0.92, 0.90, 0.85, 0.74, 0.58],
+               alpha_neg=[0.95, 0.95, 0.94, 0.93, 0.91],
+               energy=[c / 576 for c in (576, 432, 288, 144, 72)], lam=0.1)
+
+
+def utility_run(R, torch, w, tokens, qbank, sysd, qryd, layers, q, reps=3) -> dict:
+    """The scene-query with Eq. 2 utility budgets instead of the rank tiers
+    (one read-back of the kept tiles' scores after scoring); wall time per
+    query including that synchronisation."""
+    from paper_2609_29029_amd.pipeline import SceneQuery
+    uq = SceneQuery(tokens, qbank, sysd, qryd, layers, q.shape, w.keep_count, w.tau, w.levels,
+                    w.tier_num, w.tier_den, with_sims=True, utility=UTILITY)
+    uq.run()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        uq.run()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / reps
+    assert uq.check_status() == [0, 0]
+    levels, counts = np.unique(uq.budgets_host, return_counts=True)
+    return {"ms_per_query": round(ms, 2), "retained_vision_tokens": int(uq.n_selected),
+            "tokens_per_s": round(uq.n_selected / (ms * 1e-3), 1),
+            "budgets": {int(l): int(c) for l, c in zip(levels, counts)}}
+
+
 def select_batched(R, torch, token_key, order, budgets, n_tiles, n_v, n_keep, copies=64, reps=10) -> dict:
     """rift_select_tokens over `copies` scene-queries' keys at once (one call),
     for a bandwidth-meaningful number; median of `reps` timed calls."""
@@ -369,6 +398,7 @@ def main() -> int:
     kn = knn_score_timing(R, torch, tokens, qbank, w.keep_count)
     kn["extra_ms_over_plain_score"] = round(kn["score_ms"] - stage_ms["score"], 4)
     out["knn_smoothing"] = kn
+    out["utility_policy"] = utility_run(R, torch, w, tokens, qbank, sysd, qryd, layers, q)
     out["select_batched"] = select_batched(R, torch, q.token_key, q.tile_order, q.budgets, w.n_tiles,
                                            w.n_v, q.n_keep)
     if not args.no_exhaustive:
