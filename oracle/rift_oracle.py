@@ -17,7 +17,7 @@ satellite imagery for efficient VLM inference on edge"):
   * Sec. 2.1 and Sec. 2.3 Stage 2 -- each retained tile is an independent
     prompt that the LLaVA-1.5-7B (LLaMA-7B-shaped) decoder prefills.
 
-Readings of points the paper leaves open (each is listed in the design doc):
+Readings of points the paper leaves open (numbered as in the design notes):
   R1  V_i is the mean of the tile's unit-normalised vision tokens, so the tile
       score is the mean over tokens of the per-token Eq. 1 margin.
   R2  Eq. 1 is linear in V_i, so the margin is V_i . w with
@@ -26,15 +26,12 @@ Readings of points the paper leaves open (each is listed in the design doc):
       so that the same decisions are reproducible bit for bit.
   R4  Tile order is (score descending, tile id ascending); min-max with
       max == min gives u = 1 for every tile.
-  R5  Token importance for VisionZip's "dominant tokens" is the per-token
+  R5  Retention by threshold keeps u >= tau (Listing 1, App. B Step 3).
+  R6  Token importance for VisionZip's "dominant tokens" is the per-token
       margin; ties go to the lower token index; kept tokens stay in ascending
       index order.
-  R6  Budgets by score rank: tiers of floor(K*num_j/den) kept tiles per level,
+  R7  Budgets by score rank: tiers of floor(K*num_j/den) kept tiles per level,
       the last level takes the rest.
-  R7  Each prompt is [system | kept vision tokens | query text] with positions
-      0..L-1; RMSNorm gains 1; rotate-half RoPE; attention scale 1/sqrt(hd);
-      the output is the residual stream after the last layer, before any
-      final norm.
   R8  Optional score smoothing (Listing 1's note; App. B Step 3): each tile's
       score is averaged with those of its m most visually similar tiles.  The
       tile's embedding for similarity is its summed unit-normalised tokens,
@@ -45,7 +42,12 @@ Readings of points the paper leaves open (each is listed in the design doc):
       m largest similarities over j != i, ties to the lower j; the smoothed
       score is (s_i + sum of the neighbours' s in neighbour order) / (1 + m),
       and u and the ranking use it.  Off unless asked for (m = 0).
-  R9  Optional utility budgets (Eq. 2): U_i(c) = p_i a+_c + (1 - p_i) a-_c
+  R9  Each prompt is [system | kept vision tokens | query text] with positions
+      0..L-1.
+  R10 RMSNorm gains 1; rotate-half RoPE; attention scale 1/sqrt(hd); the
+      output is the residual stream after the last layer, before any final
+      norm.
+  R13 Optional utility budgets (Eq. 2): U_i(c) = p_i a+_c + (1 - p_i) a-_c
       - lambda E_c evaluated in float64 as ((p a+) + ((1 - p) a-)) - (lambda
       E) with every operation rounded on its own; the budget is the c of
       largest U, ties to the smaller c.  p_i, the trained predictor's
@@ -184,7 +186,7 @@ def rank_and_keep(s: np.ndarray, u: np.ndarray, keep_count: int, tau: float
 
 def tier_counts(n_keep: int, n_levels: int, tier_num: Sequence[int], tier_den: int
                 ) -> List[int]:
-    """Kept tiles per budget level (reading R6): level j < last gets
+    """Kept tiles per budget level (reading R7): level j < last gets
     floor(K * num_j / den), the last level the remainder."""
     counts = [(n_keep * int(tier_num[j])) // int(tier_den) for j in range(n_levels - 1)]
     counts.append(n_keep - sum(counts))
@@ -193,7 +195,7 @@ def tier_counts(n_keep: int, n_levels: int, tier_num: Sequence[int], tier_den: i
 
 def assign_budgets(n_keep: int, levels: Sequence[int], tier_num: Sequence[int],
                    tier_den: int) -> np.ndarray:
-    """Budget of kept rank rho (reading R6): higher-ranked tiles get the larger
+    """Budget of kept rank rho (reading R7): higher-ranked tiles get the larger
     levels of the discrete set C (Sec. 2.3 Stage 2)."""
     counts = tier_counts(n_keep, len(levels), tier_num, tier_den)
     out: List[int] = []
@@ -204,7 +206,7 @@ def assign_budgets(n_keep: int, levels: Sequence[int], tier_num: Sequence[int],
 
 def utility_budgets(p: Sequence[float], levels: Sequence[int], alpha_pos: Sequence[float],
                     alpha_neg: Sequence[float], energy: Sequence[float], lam: float) -> np.ndarray:
-    """Eq. 2 budget per tile (reading R9): the candidate c of largest
+    """Eq. 2 budget per tile (reading R13): the candidate c of largest
     U(c) = p a+_c + (1 - p) a-_c - lambda E_c, ties to the smaller c."""
     out = []
     for pi in p:
@@ -221,7 +223,7 @@ def utility_budgets(p: Sequence[float], levels: Sequence[int], alpha_pos: Sequen
 def select_tokens(r: np.ndarray, kept: Sequence[int], budgets: Sequence[int]
                   ) -> Tuple[np.ndarray, np.ndarray]:
     """For each kept tile, its `budget` most important tokens by (key
-    descending, index ascending), emitted in ascending index order (reading R5;
+    descending, index ascending), emitted in ascending index order (reading R6;
     VisionZip's dominant-token retention, Sec. 2.3 Stage 2).
     Returns (sel_offsets [K+1], sel_idx [sum budgets])."""
     r = np.asarray(r, dtype=np.float64)
@@ -241,7 +243,7 @@ def compact(x: np.ndarray, kept: Sequence[int], sel_offsets: np.ndarray,
             sel_idx: np.ndarray, sys: np.ndarray, qry: np.ndarray
             ) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
     """Packed varlen batch: sequence rho = [sys | x[kept[rho], sel] | qry]
-    (reading R7), cu_seqlens = prefix sums of lengths, position ids 0..L-1 per
+    (reading R9), cu_seqlens = prefix sums of lengths, position ids 0..L-1 per
     sequence.  Works on any element type (it only moves rows)."""
     rows = []
     cu = [0]
@@ -271,7 +273,7 @@ def rmsnorm(x: np.ndarray, g: np.ndarray, eps: float) -> np.ndarray:
 
 
 def rope(x: np.ndarray, positions: np.ndarray, base: float) -> np.ndarray:
-    """Rotate-half rotary embedding (reading R7) on x: [L, H, hd].  Pair
+    """Rotate-half rotary embedding (reading R10) on x: [L, H, hd].  Pair
     (j, j + hd/2) turns by angle pos * base^(-2j/hd)."""
     hd = x.shape[-1]
     half = hd // 2

@@ -459,7 +459,7 @@ def test_knn_ties_go_to_the_lower_tile_and_permutation_equivariance():
     assert np.array_equal(smP, smY[perm])
 
 
-# ----------------------------------------------------------------------------- utility budgets (R9)
+# ----------------------------------------------------------------------------- utility budgets (R13)
 # Stand-in accuracy and energy tables over the paper's budget set for LLaVA-1.5
 # (Sec. 2.3 Stage 2): accuracy on object tiles grows with the budget, accuracy
 # on empty tiles barely moves, energy is proportional to the budget.
