@@ -228,3 +228,42 @@ def test_scene_query_utility_budgets(R, knn_m):
                    m.rms_eps, m.rope_base, seqs)
     errs = [rowwise_rel_err(hid[cu[i]:cu[i + 1]], ys[i]) for i in seqs]
     assert max(errs) <= TOL[w.dtype], errs
+
+
+@pytest.mark.parametrize("lens", [[1], [17], [40, 3], [300], [129, 1, 255, 64]])
+def test_prefill_small_and_ragged_batches(R, lens):
+    """bf16 prefill of batches whose GEMMs are a few partial tiles (every tile
+    then runs in the half-width path, M below one 256-row tile or ragged), one
+    LLaMA-7B layer, against the oracle; and a batch's sequences equal the same
+    sequences prefilled alone, bit for bit."""
+    torch = torch_mod()
+    w = synth.get("scene8")
+    m = w.model
+    rng = np.random.default_rng(sum(lens))
+    W = synth.make_layer(w, 0)
+    Wd = upload_layer(W, w.dtype)
+    cfg = R.model_cfg(m.d, m.n_heads, m.head_dim, m.ffn, 1, m.rms_eps, m.rope_base, R.RIFT_BF16)
+    x = synth.store(rng.standard_normal((sum(lens), m.d)).astype(np.float32), "bf16")
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    pos = np.concatenate([np.arange(l) for l in lens]).astype(np.int32)
+
+    def run(xs, cus, poss):
+        T = xs.shape[0]
+        L = int(np.diff(cus).max())
+        ws = torch.empty(R.rift_prefill_workspace_size(cfg, T, L), dtype=torch.uint8, device="cuda")
+        out = torch.empty(T, m.d, dtype=torch.float32, device="cuda")
+        R.rift_prefill(cfg, [Wd], upload(xs, "bf16"), torch.from_numpy(cus).cuda(),
+                       torch.from_numpy(poss).cuda(), len(cus) - 1, L, out, ws)
+        torch.cuda.synchronize()
+        return out.cpu().numpy().astype(np.float64)
+
+    hid = run(x, cu, pos)
+    ys = O.prefill(f64(x, "bf16"), cu, pos, [oracle_layer_weights(W, w.dtype)], m.n_heads, m.head_dim,
+                   m.rms_eps, m.rope_base, list(range(len(lens))))
+    for i in range(len(lens)):
+        err = rowwise_rel_err(hid[cu[i]:cu[i + 1]], ys[i])
+        assert err <= TOL["bf16"], (i, err)
+    if len(lens) > 1:
+        for i in range(len(lens)):
+            alone = run(x[cu[i]:cu[i + 1]], np.array([0, lens[i]], dtype=np.int32), np.arange(lens[i], dtype=np.int32))
+            assert np.array_equal(alone, hid[cu[i]:cu[i + 1]])
