@@ -6,15 +6,18 @@
 //                   exclusive prefix sums sel_offsets (each thread sums a
 //                   contiguous run, then one scan over the threads) and the
 //                   status word.
-//   select_topk     one wave per kept tile, keys in registers: an 8-pass radix
-//                   select (8-bit digits, histogram in the wave's own LDS
-//                   slice) finds the budget-th pair in (descending key,
-//                   ascending index) order, then ballot prefix counts write the
-//                   chosen indices in ascending order.
+//   select_topk     one wave per kept tile, keys in registers: a radix select
+//                   (8-bit digits from the top, histogram in the wave's own
+//                   LDS slice; it stops once the bin that holds the
+//                   budget-th key is taken whole) finds the budget-th pair in
+//                   (descending key, ascending index) order, then ballot
+//                   prefix counts write the chosen indices in ascending order.
 #include "launch.h"
 #include "rift_common.h"
 
 namespace rift {
+
+constexpr int kOffBatch = 8;
 
 __global__ void __launch_bounds__(1024)
 select_offsets_kernel(const int* __restrict__ kept, const int* __restrict__ budgets, int n_keep,
@@ -27,18 +30,30 @@ select_offsets_kernel(const int* __restrict__ kept, const int* __restrict__ budg
     const int wave = tid >> 6;
     if (tid == 0) bad = 0;
     __syncthreads();
-    // thread t owns budgets [t per, (t + 1) per): validate and sum them
+    // thread t owns budgets [t per, (t + 1) per): validate and sum them, in
+    // batches of kOffBatch whose loads are all issued before the first is used
     const int per = (n_keep + 1023) / 1024;
     const int i0 = tid * per;
+    const int i1 = min(i0 + per, n_keep);
     long long mine = 0;
-    for (int j = 0; j < per; ++j) {
-        const int i = i0 + j;
-        if (i >= n_keep) break;
-        const int b = budgets[i];
-        const int t = kept[i];
-        if (b < 0 || b > n_v || t < 0 || t >= n_tiles) atomicOr(&bad, 1);
-        mine += b < 0 ? 0 : (b > n_v ? n_v : b);
+    bool bad_mine = false;
+    for (int j0 = i0; j0 < i1; j0 += kOffBatch) {
+        int bv[kOffBatch], tv[kOffBatch];
+#pragma unroll
+        for (int j = 0; j < kOffBatch; ++j) {
+            const int i = min(j0 + j, i1 - 1);
+            bv[j] = budgets[i];
+            tv[j] = kept[i];
+        }
+#pragma unroll
+        for (int j = 0; j < kOffBatch; ++j) {
+            if (j0 + j >= i1) break;
+            const int b = bv[j], t = tv[j];
+            bad_mine |= b < 0 || b > n_v || t < 0 || t >= n_tiles;
+            mine += b < 0 ? 0 : (b > n_v ? n_v : b);
+        }
     }
+    if (bad_mine) atomicOr(&bad, 1);
     // exclusive scan over threads: within the wave, then across the 16 waves
     long long incl = mine;
 #pragma unroll
@@ -59,12 +74,16 @@ select_offsets_kernel(const int* __restrict__ kept, const int* __restrict__ budg
         for (int i = tid; i <= n_keep; i += blockDim.x) offs[i] = 0;
     } else {
         long long run = base + incl - mine;
-        for (int j = 0; j < per; ++j) {
-            const int i = i0 + j;
-            if (i >= n_keep) break;
-            offs[i] = (int)run;
-            const int b = budgets[i];
-            run += b < 0 ? 0 : (b > n_v ? n_v : b);
+        for (int j0 = i0; j0 < i1; j0 += kOffBatch) {
+            int bv[kOffBatch];
+#pragma unroll
+            for (int j = 0; j < kOffBatch; ++j) bv[j] = budgets[min(j0 + j, i1 - 1)];
+#pragma unroll
+            for (int j = 0; j < kOffBatch; ++j) {
+                if (j0 + j >= i1) break;
+                offs[j0 + j] = (int)run;
+                run += bv[j];   // validated above: 0 <= bv[j] <= n_v
+            }
         }
         if (tid == 0) offs[n_keep] = (int)total;
     }
@@ -80,34 +99,57 @@ __device__ __forceinline__ uint64_t desc_bits(double x) {
     return ~asc;
 }
 
-constexpr int kSelMaxPerLane = 16;   // n_v <= 1024
 
+// Inclusive prefix sum over the 64 lanes of a wave with DPP moves: shifts by
+// 1, 2, 4 and 8 inside each row of 16 lanes (lanes shifted in from outside
+// the row contribute 0), then the last lane of row 0 is added to row 1 and row
+// 3 gets row 2's, and finally lane 31 is added to rows 2 and 3.
+__device__ __forceinline__ unsigned wave_incl_scan(unsigned v) {
+    v += (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false);   // row_shr:1
+    v += (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false);   // row_shr:2
+    v += (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);   // row_shr:4
+    v += (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false);   // row_shr:8
+    v += (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false);   // row_bcast:15
+    v += (unsigned)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false);   // row_bcast:31
+    return v;
+}
+
+// NE: keys per lane the kernel is built for (n_v <= 64 NE); 9 covers a 24 x 24
+// token tile, 16 the largest n_v (1024).
+template <int NE>
 __global__ void __launch_bounds__(256)
 select_topk_kernel(const double* __restrict__ token_key, int n_v, int n_keep,
                    const int* __restrict__ kept, const int* __restrict__ offs,
                    const int* __restrict__ status, int* __restrict__ sel_idx) {
     __shared__ unsigned hist_all[4][256];
-    if (*status != 0) return;
     const int wave = threadIdx.x >> 6;
     const int lane = threadIdx.x & 63;
     const int rho = blockIdx.x * 4 + wave;
     if (rho >= n_keep) return;
+    // the status word, this tile's offsets and its id are loaded together
+    const int bad = *status;
     const int off = offs[rho];
-    const int budget = offs[rho + 1] - off;
+    const int off_end = offs[rho + 1];
+    const int tile = kept[rho];
+    if (bad != 0) return;
+    const int budget = off_end - off;
     if (budget <= 0) return;
     if (budget >= n_v) {
         for (int i = lane; i < n_v; i += 64) sel_idx[off + i] = i;
         return;
     }
     unsigned* hist = hist_all[wave];
-    const double* kt = token_key + (size_t)kept[rho] * n_v;
+    const double* kt = token_key + (size_t)tile * n_v;
     const int ne = (n_v + 63) >> 6;   // elements per lane; element e of lane l is index 64 e + l
-    uint64_t u[kSelMaxPerLane];
+    // every load in bounds (index clamped to the last key), none behind a branch,
+    // so the wave waits for its keys once
+    double raw[NE];
 #pragma unroll
-    for (int e = 0; e < kSelMaxPerLane; ++e) {
-        const int i = 64 * e + lane;
-        u[e] = (e < ne && i < n_v) ? desc_bits(kt[i]) : ~0ull;   // padding sorts last
-    }
+    for (int e = 0; e < NE; ++e) raw[e] = kt[min(64 * e + lane, n_v - 1)];
+    uint64_t u[NE];
+#pragma unroll
+    for (int e = 0; e < NE; ++e)
+        u[e] = (64 * e + lane < n_v) ? desc_bits(raw[e]) : ~0ull;   // padding sorts last
     // the budget-th smallest value T of u over the valid elements, digit by digit
     uint64_t prefix = 0, mask = 0;
     int k = budget;
@@ -116,7 +158,7 @@ select_topk_kernel(const double* __restrict__ token_key, int n_v, int n_keep,
         for (int j = 0; j < 4; ++j) hist[4 * lane + j] = 0;
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
-        for (int e = 0; e < kSelMaxPerLane; ++e) {
+        for (int e = 0; e < NE; ++e) {
             const int i = 64 * e + lane;
             if (e < ne && i < n_v && (u[e] & mask) == prefix)
                 atomicAdd(&hist[(unsigned)(u[e] >> shift) & 255u], 1u);
@@ -126,13 +168,7 @@ select_topk_kernel(const double* __restrict__ token_key, int n_v, int n_keep,
 #pragma unroll
         for (int j = 0; j < 4; ++j) c[j] = hist[4 * lane + j];
         const unsigned mine = c[0] + c[1] + c[2] + c[3];
-        unsigned incl = mine;
-#pragma unroll
-        for (int sft = 1; sft < 64; sft <<= 1) {
-            const unsigned o = __shfl_up(incl, sft);
-            if (lane >= sft) incl += o;
-        }
-        unsigned before = incl - mine;   // count in bins < 4 lane
+        unsigned before = wave_incl_scan(mine) - mine;   // count in bins < 4 lane
         int hit = -1;
         unsigned hit_before = 0;
 #pragma unroll
@@ -143,24 +179,32 @@ select_topk_kernel(const double* __restrict__ token_key, int n_v, int n_keep,
             }
             before += c[j];
         }
+        unsigned hit_count = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (hit == 4 * lane + j) hit_count = c[j];
         const uint64_t hits = __ballot(hit >= 0);
         const int src = __builtin_ctzll(hits);   // exactly one lane holds the digit
-        const int digit = __shfl(hit, src);
-        k -= (int)__shfl(hit_before, src);
+        const int digit = __builtin_amdgcn_readlane(hit, src);
+        k -= (int)__builtin_amdgcn_readlane(hit_before, src);
         prefix |= (uint64_t)digit << shift;
         mask |= 255ull << shift;
+        // every candidate left in the bin is taken: the digits below no longer matter
+        if ((int)__builtin_amdgcn_readlane(hit_count, src) == k) break;
     }
-    // take every u < T, and the first k (by index) of u == T; write ascending
+    // take every u whose masked value is below the prefix, and the first k (by
+    // index) of those equal to it; write ascending
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     int eq_seen = 0, written = 0;
 #pragma unroll
-    for (int e = 0; e < kSelMaxPerLane; ++e) {
+    for (int e = 0; e < NE; ++e) {
         if (e >= ne) break;
         const int i = 64 * e + lane;
         const bool valid = i < n_v;
-        const bool eq = valid && u[e] == prefix;
+        const uint64_t um = u[e] & mask;
+        const bool eq = valid && um == prefix;
         const uint64_t eqm = __ballot(eq);
-        const bool take = valid && (u[e] < prefix || (eq && eq_seen + __popcll(eqm & below) < k));
+        const bool take = valid && (um < prefix || (eq && eq_seen + __popcll(eqm & below) < k));
         eq_seen += __popcll(eqm);
         const uint64_t tm = __ballot(take);
         if (take) sel_idx[off + written + __popcll(tm & below)] = i;
@@ -174,8 +218,12 @@ hipError_t launch_select(const double* token_key, int n_tiles, int n_v, const in
     hipLaunchKernelGGL(select_offsets_kernel, dim3(1), dim3(1024), 0, st, kept, budgets, n_keep,
                        n_tiles, n_v, cap, sel_offsets, status);
     if (n_keep > 0)
-        hipLaunchKernelGGL(select_topk_kernel, dim3((n_keep + 3) / 4), dim3(256), 0, st, token_key, n_v,
-                           n_keep, kept, sel_offsets, status, sel_idx);
+        if (n_v <= 64 * 9)
+            hipLaunchKernelGGL(select_topk_kernel<9>, dim3((n_keep + 3) / 4), dim3(256), 0, st, token_key,
+                               n_v, n_keep, kept, sel_offsets, status, sel_idx);
+        else
+            hipLaunchKernelGGL(select_topk_kernel<16>, dim3((n_keep + 3) / 4), dim3(256), 0, st, token_key,
+                               n_v, n_keep, kept, sel_offsets, status, sel_idx);
     return hipGetLastError();
 }
 
