@@ -100,12 +100,13 @@ def cpu_baseline(w, sc, seq_lens_by_tier, n_tiles_sample: int, n_layers_sample: 
                        f"thread, BLAS on {blas_threads}")}
 
 
-def exhaustive_run(R, torch, w, tokens, qbank, sysd, qryd, layers, cfg, chunk: int = 50) -> dict:
+def exhaustive_setup(R, torch, w, tokens, qbank, sysd, qryd, layers, cfg, chunk: int = 50):
     """Every tile kept at the full budget n_v: the no-pruning baseline the
     paper compares against.  Same kernels; the prefill runs as consecutive
     calls of `chunk` prompts each (all prompts have the same length), since one
-    call is limited to T * max(d, ffn) < 2^31.  Timed once with HIP events on
-    the current stream."""
+    call is limited to T * max(d, ffn) < 2^31.  Returns a function that enqueues
+    one whole exhaustive query on the current stream and returns its status
+    words, and the query's shape."""
     n, nv, d = tokens.shape
     dev = tokens.device
     f64, f32, i32 = torch.float64, torch.float32, torch.int32
@@ -132,26 +133,135 @@ def exhaustive_run(R, torch, w, tokens, qbank, sysd, qryd, layers, cfg, chunk: i
     cu_c = {m: torch.arange(0, m + 1, dtype=i32, device=dev) * L for m in {b - a for a, b in chunks}}
     ws = torch.empty(R.rift_prefill_workspace_size(cfg, chunk * L, L), dtype=torch.uint8, device=dev)
     hid = torch.empty(chunk * L, d, dtype=f32, device=dev)
+
+    def run():
+        R.rift_score_tiles(tokens, qbank, n, 0.0, key, sim, score, u, order, nkeep, sws)
+        R.rift_select_tokens(key, n, nv, order, budgets, n, offs, sel, st1)
+        R.rift_compact(tokens, order, offs, sel, n, sysd, qryd, packed, cu, pos, st2)
+        for a, b in chunks:
+            m = b - a
+            R.rift_prefill(cfg, layers, packed[a * L:b * L], cu_c[m], pos[a * L:b * L], m, L,
+                           hid[:m * L], ws)
+        return st1, st2
+
+    return run, {"packed_tokens": T, "prompts": n, "prefill_calls": len(chunks), "seq_len": L}
+
+
+def exhaustive_run(run, shape, w, torch) -> dict:
+    """One exhaustive query, timed with HIP events on the current stream."""
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
-    R.rift_score_tiles(tokens, qbank, n, 0.0, key, sim, score, u, order, nkeep, sws)
-    R.rift_select_tokens(key, n, nv, order, budgets, n, offs, sel, st1)
-    R.rift_compact(tokens, order, offs, sel, n, sysd, qryd, packed, cu, pos, st2)
-    for a, b in chunks:
-        m = b - a
-        R.rift_prefill(cfg, layers, packed[a * L:b * L], cu_c[m], pos[a * L:b * L], m, L,
-                       hid[:m * L], ws)
+    st1, st2 = run()
     e1.record()
     torch.cuda.synchronize()
     assert int(st1.item()) == 0 and int(st2.item()) == 0
     ms = e0.elapsed_time(e1)
     m = w.model
+    T, L, n = shape["packed_tokens"], shape["seq_len"], shape["prompts"]
     fl = stage_flops(T, m.d, m.ffn, [L] * n)
     tflop = sum(fl.values()) * m.n_layers / 1e12
-    del packed, ws, hid, sim
-    return {"ms": round(ms, 2), "packed_tokens": T, "prompts": n, "prefill_calls": len(chunks),
+    return {"ms": round(ms, 2), "packed_tokens": T, "prompts": n, "prefill_calls": shape["prefill_calls"],
             "tflop": round(tflop, 1), "frac_bf16_peak": round(tflop / (ms * 1e-3) / PEAK_BF16_TFLOPS, 4)}
+
+
+class EnergyMeter:
+    """Board energy of the GPU from its own accumulator (amdsmi): the counter
+    advances in units of `counter_resolution` microjoules and carries the
+    timestamp of its last update.  The average power of a workload is the
+    difference of two updates that both fall while it runs, over the time
+    between them; the poller thread records every update it sees."""
+
+    def __init__(self, torch):
+        import amdsmi
+        self.smi = amdsmi
+        amdsmi.amdsmi_init()
+        hs = amdsmi.amdsmi_get_processor_handles()
+        bus = torch.cuda.get_device_properties(0).pci_bus_id
+        pick = [h for h in hs if int(amdsmi.amdsmi_get_gpu_device_bdf(h).split(":")[1], 16) == bus]
+        if len(pick) != 1:
+            raise RuntimeError(f"no unique amdsmi device on PCI bus {bus:#x} ({len(hs)} devices)")
+        self.h = pick[0]
+
+    def read(self):
+        e = self.smi.amdsmi_get_energy_count(self.h)
+        return e["energy_accumulator"] * e["counter_resolution"] * 1e-6, e["timestamp"] * 1e-9
+
+    def average_power(self, work, min_seconds: float, min_updates: int = 4) -> dict:
+        """Call work() back to back until the counter has updated at least
+        `min_updates` times over at least `min_seconds` since the first update
+        seen after the loop began; returns watts, the span and the number of
+        work() calls per second of wall time."""
+        import threading
+        ups, stop = [], threading.Event()
+
+        def poll():
+            last = None
+            while not stop.is_set():
+                j, t = self.read()
+                if t != last:
+                    ups.append((j, t))
+                    last = t
+                time.sleep(0.005)
+
+        th = threading.Thread(target=poll, daemon=True)
+        th.start()
+        while not ups:
+            time.sleep(0.001)
+        t0 = time.perf_counter()
+        calls = 0
+        while True:
+            work()
+            calls += 1
+            inside = ups[1:]   # ups[0] was read before the loop began
+            if len(inside) >= min_updates and inside[-1][1] - inside[0][1] >= min_seconds:
+                break
+        wall = time.perf_counter() - t0
+        stop.set()
+        th.join()
+        (j0, s0), (j1, s1) = inside[0], inside[-1]
+        return {"watts": (j1 - j0) / (s1 - s0), "span_s": s1 - s0, "updates": len(inside),
+                "calls": calls, "wall_s_per_call": wall / calls}
+
+    def close(self):
+        self.smi.amdsmi_shut_down()
+
+
+def energy_run(torch, rift_query, ex_run, rift_ms, ex_ms, min_seconds: float) -> dict:
+    """Energy per scene-query, Rift against exhaustive: each workload runs back
+    to back (one synchronisation per query) while the board's energy counter
+    gives its average power; energy per query = average power x wall time per
+    query in that loop.  Idle power (no work) is reported for context."""
+    try:
+        meter = EnergyMeter(torch)
+    except Exception as exc:   # amdsmi missing or the device not visible to it
+        return {"error": repr(exc)[:200]}
+    try:
+        def rift():
+            rift_query()
+            torch.cuda.synchronize()
+
+        def ex():
+            ex_run()
+            torch.cuda.synchronize()
+
+        idle = meter.average_power(lambda: time.sleep(0.05), min_seconds=2.0, min_updates=3)
+        pr = meter.average_power(rift, min_seconds)
+        pe = meter.average_power(ex, min_seconds)
+    finally:
+        meter.close()
+    e_r = pr["watts"] * pr["wall_s_per_call"]
+    e_e = pe["watts"] * pe["wall_s_per_call"]
+    return {"method": "amdsmi energy accumulator: average board power between counter updates "
+                      "while the workload runs back to back, times wall time per query",
+            "idle_W": round(idle["watts"], 1),
+            "rift": {"W": round(pr["watts"], 1), "wall_ms_per_query": round(pr["wall_s_per_call"] * 1e3, 2),
+                     "device_ms_per_query": round(rift_ms, 2), "J_per_query": round(e_r, 2),
+                     "queries": pr["calls"], "span_s": round(pr["span_s"], 2)},
+            "exhaustive": {"W": round(pe["watts"], 1), "wall_ms_per_query": round(pe["wall_s_per_call"] * 1e3, 2),
+                           "device_ms_per_query": round(ex_ms, 2), "J_per_query": round(e_e, 2),
+                           "queries": pe["calls"], "span_s": round(pe["span_s"], 2)},
+            "energy_reduction": round(1 - e_r / e_e, 4)}
 
 
 def knn_score_timing(R, torch, tokens, qbank, keep_count, m=6, reps=10) -> dict:
@@ -251,6 +361,10 @@ def main() -> int:
     ap.add_argument("--cpu-sample-layers", type=int, default=16)
     ap.add_argument("--no-exhaustive", action="store_true",
                     help="skip the every-tile, full-budget comparison run")
+    ap.add_argument("--no-energy", action="store_true",
+                    help="skip the energy-per-query comparison (board energy counter)")
+    ap.add_argument("--energy-seconds", type=float, default=4.0,
+                    help="minimum span of energy-counter updates per workload")
     ap.add_argument("--traffic-calibration", action="store_true",
                     help="also run a 1 GiB copy kernel (for HBM counter calibration)")
     args = ap.parse_args()
@@ -403,11 +517,17 @@ def main() -> int:
                                            w.n_v, q.n_keep)
     if not args.no_exhaustive:
         log("exhaustive run (every tile at the full budget) ...")
-        ex = exhaustive_run(R, torch, w, tokens, qbank, sysd, qryd, layers, q.cfg)
+        ex_fn, ex_shape = exhaustive_setup(R, torch, w, tokens, qbank, sysd, qryd, layers, q.cfg)
+        ex = exhaustive_run(ex_fn, ex_shape, w, torch)
         ex["rift_ms_over_exhaustive_ms"] = round(stage_ms_total / ex["ms"], 4)
         ex["latency_reduction"] = round(1 - stage_ms_total / ex["ms"], 4)
         out["exhaustive"] = ex
         log(f"exhaustive: {ex['ms']:.1f} ms")
+        if not args.no_energy:
+            log("energy: idle, Rift and exhaustive loops ...")
+            out["energy"] = energy_run(torch, q.run, ex_fn, stage_ms_total, ex["ms"], args.energy_seconds)
+            log(f"energy: {out['energy']}")
+        del ex_fn
     if not args.no_cpu_baseline:
         tiers = {}
         for L in seq_lens:

@@ -7,13 +7,15 @@
 //   SWIGLU a = silu(h wg^T) * (h wu^T), bf16 out
 //
 // Tiling: a 256x256 output tile per workgroup of 8 waves (2 in M x 4 in N),
-// each wave a 128x64 block of 4x2 v_mfma_f32_32x32x16_bf16 tiles.  K advances
-// 64 per stage through two LDS buffers of 64 KB that LDS DMA (global_load_lds)
-// fills a stage ahead.  Two main loops share that layout: the eight-wave loop
-// (every wave reads its operands for the next 16-deep sub-step while it runs
-// the MFMAs of the current one) and the ping-pong loop (the two waves on a
-// SIMD alternate between a whole stage of MFMAs and the LDS reads of the next
-// stage).  The last tiles of a GEMM can run as 256x128 halves on 4 waves.
+// each wave a 128x64 block of 8x4 v_mfma_f32_16x16x32_bf16 tiles (under the
+// board power limit this instruction sustains more throughput than the
+// 32x32x16 form on the same data).  K advances 64 per stage through two LDS
+// buffers of 64 KB that LDS DMA (global_load_lds) fills a stage ahead.  Two
+// main loops share that layout: the eight-wave loop (every wave reads its
+// operands for the next 32-deep sub-step while it runs the MFMAs of the
+// current one) and the ping-pong loop (the two waves on a SIMD alternate
+// between a whole stage of MFMAs and the LDS reads of the next stage).  The
+// last tiles of a GEMM can run as 256x128 halves on 4 waves.
 //
 // Every output element is one fixed sequence of MFMA accumulations over K, no
 // matter which tile or batch row holds it, so a row's result does not depend on
@@ -143,31 +145,37 @@ constexpr int kStage3 = 2 * BM * BK3;   // elements per stage (A then B)
 __device__ __forceinline__ int swz8(int r) { return ((r >> 1) ^ ((r & 1) << 2)) & 7; }
 
 // ---------------------------------------------------------------------------
-// Wave layout: 2 (M) x 4 (N) waves, each 128 rows x 64 columns, its two
-// 32-column blocks at tile columns c0 and c0 + 64 with
-// c0 = 128 (wn >> 1) + 32 (wn & 1), so the RoPE pairs (j, j + 64) of a head and
-// the gate/up pairs of SwiGLU sit in the same lane.
+// Wave layout: 2 (M) x 4 (N) waves, each 128 rows x 64 columns: eight 16-row
+// blocks mb and four 16-column blocks nb at tile columns
+// c0 + 16 (nb & 1) + 64 (nb >> 1) with c0 = 128 (wn >> 1) + 32 (wn & 1), so the
+// RoPE pairs (j, j + 64) of a head and the gate/up pairs of SwiGLU (blocks nb
+// and nb + 2) sit in the same lane.
+//
+// MFMA operands (lane l = r + 16 q): the A fragment of block mb in 32-deep
+// sub-step s is row 16 mb + r, k = 32 s + 8 q .. + 7, the B fragment of block
+// nb column r of the block, same k; result element v of the block is row
+// 4 q + v, column r.
 __device__ __forceinline__ int w8_c0(int wn) { return 128 * (wn >> 1) + 32 * (wn & 1); }
+__device__ __forceinline__ int w8_col(int wn, int nb) { return w8_c0(wn) + 16 * (nb & 1) + 64 * (nb >> 1); }
 
 // Epilogue.  For the bf16 outputs the stage buffers, free after the main loop,
 // hold the tile: each wave writes its outputs (SiLU(gate)*up, RoPE'd q/k, v)
 // into a row-major tile in LDS, then every thread of the workgroup moves 16
 // contiguous bytes of a row, so global stores are whole row segments.  The
-// residual GEMMs read, add and write float32 straight from the lanes (32
-// consecutive columns per instruction).  acc[m][n][i] is row
-// 8 (i/4) + 4 (lane/32) + (i%4) of the 32x32 block (m, n) of wave (wm, wn),
-// column lane%32; the block's tile columns are c0 + 64 n + lane%32.  A half-tile
-// workgroup (HALF) holds logical tile columns [128 h, 128 h + 128).
+// residual GEMMs read, add and write float32 straight from the lanes (16
+// consecutive columns of 4 rows per instruction).  acc[mb][nb][v] is tile row
+// 128 wm + 16 mb + 4 (lane/16) + v, tile column w8_col(wn, nb) + lane%16.  A
+// half-tile workgroup (HALF) holds logical tile columns [128 h, 128 h + 128).
 constexpr int kStagingBytes = 256 * (256 + 8) * 2;   // largest staging tile (QKV, bf16)
 
 template <int EPI, bool HALF>
-__device__ __forceinline__ void epilogue_staged(const GemmParams& p, f32x16_t (&acc)[4][2], int m0, int bn,
+__device__ __forceinline__ void epilogue_staged(const GemmParams& p, f32x4_t (&acc)[8][4], int m0, int bn,
                                                 int h, int wm, int wn, int lane, const int* pos_lds,
                                                 unsigned char* stage) {
     constexpr int NT = HALF ? 256 : 512;
     const int tid = threadIdx.x;
-    const int col_in = lane & 31;
-    const int row_hi = 4 * (lane >> 5);
+    const int col_in = lane & 15;
+    const int row_hi = 4 * (lane >> 4);
     const int cbase = HALF ? 128 * h : 0;
     __syncthreads();   // every wave is done with the stage buffers
     if constexpr (EPI == EPI_SWIGLU) {
@@ -176,17 +184,19 @@ __device__ __forceinline__ void epilogue_staged(const GemmParams& p, f32x16_t (&
         bf16_t* S = reinterpret_cast<bf16_t*>(stage);
         const int sc = 64 * (wn >> 1) + 32 * (wn & 1) + col_in - (HALF ? 64 * h : 0);
 #pragma unroll
-        for (int m = 0; m < 4; ++m)
+        for (int mb = 0; mb < 8; ++mb)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int r = wm * 128 + m * 32 + 8 * (i >> 2) + row_hi + (i & 3);
-                const float gt = acc[m][0][i];
-                const float up = acc[m][1][i];
-                // silu(g) = g / (1 + e^-g) with the hardware exp2 and reciprocal
-                // (about 1 ulp each; the result is rounded to bf16)
-                const float e = __builtin_amdgcn_exp2f(gt * -1.4426950408889634f);
-                S[r * LD + sc] = f32_to_bf16(gt * __builtin_amdgcn_rcpf(1.0f + e) * up);
-            }
+            for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int r = wm * 128 + mb * 16 + row_hi + v;
+                    const float gt = acc[mb][nb][v];
+                    const float up = acc[mb][nb + 2][v];
+                    // silu(g) = g / (1 + e^-g) with the hardware exp2 and reciprocal
+                    // (about 1 ulp each; the result is rounded to bf16)
+                    const float e = __builtin_amdgcn_exp2f(gt * -1.4426950408889634f);
+                    S[r * LD + sc + 16 * nb] = f32_to_bf16(gt * __builtin_amdgcn_rcpf(1.0f + e) * up);
+                }
         __syncthreads();
         constexpr int VPR = OC / 8;
         bf16_t* out = p.o0 + bn * 128 + (HALF ? 64 * h : 0);
@@ -203,31 +213,37 @@ __device__ __forceinline__ void epilogue_staged(const GemmParams& p, f32x16_t (&
         constexpr int LD = OC + 8;
         bf16_t* S = reinterpret_cast<bf16_t*>(stage);
         const int region = __builtin_amdgcn_readfirstlane((bn * BN) / p.d);
-        const int j = 32 * (wn & 1) + col_in;            // 0..63 within the head
+        const int j = 32 * (wn & 1) + col_in;            // block nb = 0 column within the head (+16 for nb = 1)
         const int sc = 128 * (wn >> 1) + j - cbase;      // staging column of j; j + 64 at sc + 64
 #pragma unroll
-        for (int m = 0; m < 4; ++m) {
+        for (int mb = 0; mb < 8; ++mb) {
             __builtin_amdgcn_sched_barrier(0);
-            const int r0 = wm * 128 + m * 32 + row_hi;
+            const int r0 = wm * 128 + mb * 16 + row_hi;
             if (region == 2) {
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int r = r0 + 8 * (i >> 2) + (i & 3);
-                    S[r * LD + sc] = f32_to_bf16(acc[m][0][i]);
-                    S[r * LD + sc + 64] = f32_to_bf16(acc[m][1][i]);
-                }
+                for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const int r = r0 + v;
+                        S[r * LD + sc + 16 * nb] = f32_to_bf16(acc[mb][nb][v]);
+                        S[r * LD + sc + 16 * nb + 64] = f32_to_bf16(acc[mb][nb + 2][v]);
+                    }
             } else {
-                float2 cs[16];
+                float2 cs[2][4];
 #pragma unroll
-                for (int i = 0; i < 16; ++i) cs[i] = p.rope[(size_t)pos_lds[r0 + 8 * (i >> 2) + (i & 3)] * 64 + j];
+                for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int r = r0 + 8 * (i >> 2) + (i & 3);
-                    const float x1 = acc[m][0][i];
-                    const float x2 = acc[m][1][i];
-                    S[r * LD + sc] = f32_to_bf16(x1 * cs[i].x - x2 * cs[i].y);
-                    S[r * LD + sc + 64] = f32_to_bf16(x2 * cs[i].x + x1 * cs[i].y);
-                }
+                    for (int v = 0; v < 4; ++v) cs[nb][v] = p.rope[(size_t)pos_lds[r0 + v] * 64 + j + 16 * nb];
+#pragma unroll
+                for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const int r = r0 + v;
+                        const float x1 = acc[mb][nb][v];
+                        const float x2 = acc[mb][nb + 2][v];
+                        S[r * LD + sc + 16 * nb] = f32_to_bf16(x1 * cs[nb][v].x - x2 * cs[nb][v].y);
+                        S[r * LD + sc + 16 * nb + 64] = f32_to_bf16(x2 * cs[nb][v].x + x1 * cs[nb][v].y);
+                    }
             }
         }
         __syncthreads();
@@ -244,25 +260,29 @@ __device__ __forceinline__ void epilogue_staged(const GemmParams& p, f32x16_t (&
     } else {   // RESID: x += A B^T in float32, read-modify-write straight from the lanes
         const int c0 = w8_c0(wn);
 #pragma unroll
-        for (int m = 0; m < 4; ++m) {
+        for (int mp = 0; mp < 8; mp += 2) {   // two row blocks at a time
             __builtin_amdgcn_sched_barrier(0);
-            const int r0 = wm * 128 + m * 32 + row_hi;
-            float old[16][2];
+            float old[2][4][4];
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
-                const float* src = p.resid + (size_t)(row < p.M ? row : p.M - 1) * p.N + bn * BN + c0 + col_in;
+            for (int e = 0; e < 2; ++e)
 #pragma unroll
-                for (int n = 0; n < 2; ++n) old[i][n] = src[n * 64];
-            }
+                for (int v = 0; v < 4; ++v) {
+                    const int row = m0 + wm * 128 + (mp + e) * 16 + row_hi + v;
+                    const float* src = p.resid + (size_t)(row < p.M ? row : p.M - 1) * p.N + bn * BN + c0 + col_in;
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int row = m0 + r0 + 8 * (i >> 2) + (i & 3);
-                if (row >= p.M) continue;
-                float* dst = p.resid + (size_t)row * p.N + bn * BN + c0 + col_in;
+                    for (int nb = 0; nb < 4; ++nb) old[e][v][nb] = src[16 * (nb & 1) + 64 * (nb >> 1)];
+                }
 #pragma unroll
-                for (int n = 0; n < 2; ++n) dst[n * 64] = old[i][n] + acc[m][n][i];
-            }
+            for (int e = 0; e < 2; ++e)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int row = m0 + wm * 128 + (mp + e) * 16 + row_hi + v;
+                    if (row >= p.M) continue;
+                    float* dst = p.resid + (size_t)row * p.N + bn * BN + c0 + col_in;
+#pragma unroll
+                    for (int nb = 0; nb < 4; ++nb)
+                        dst[16 * (nb & 1) + 64 * (nb >> 1)] = old[e][v][nb] + acc[mp + e][nb][v];
+                }
         }
         (void)stage;
         (void)cbase;
@@ -270,10 +290,10 @@ __device__ __forceinline__ void epilogue_staged(const GemmParams& p, f32x16_t (&
 }
 
 // Eight-wave main loop (two waves per SIMD, so one wave's LDS or DMA issue
-// stalls are covered by the other's MFMAs).  Within a stage the four 16-deep
-// sub-steps each run 8 MFMAs while the next sub-step's operands are read from
-// LDS.  The barrier sits before sub-step 3: by then stage kt+1 has landed and
-// every wave has read the whole of stage kt, so sub-step 3 also issues the DMA
+// stalls are covered by the other's MFMAs).  Within a stage the two 32-deep
+// sub-steps each run 32 MFMAs while the next sub-step's operands are read from
+// LDS.  The barrier sits before sub-step 1: by then stage kt+1 has landed and
+// every wave has read the whole of stage kt, so sub-step 1 also issues the DMA
 // of stage kt+2 into the buffer stage kt used, a stage before it is needed.
 //
 // HALF: a workgroup of 4 waves computes one half (128 columns, h = 0 or 1) of
@@ -347,32 +367,35 @@ __global__ void __launch_bounds__(HALF ? 256 : 512, 1) gemm_bf16_w8_kernel(GemmP
         }
     }
 
-    f32x16_t acc[4][2];
+    f32x4_t acc[8][4];
 #pragma unroll
-    for (int m = 0; m < 4; ++m)
+    for (int mb = 0; mb < 8; ++mb)
 #pragma unroll
-        for (int n = 0; n < 2; ++n)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) acc[m][n][i] = 0.f;
+        for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
     const int nk = p.K / BK3;
-    const int rd_a = (wm * 128 + (lane & 31)) * BK3;
-    const int rd_b = BM * BK3 + (w8_c0(wn) + (lane & 31)) * BK3;
+    const int rd_a = (wm * 128 + (lane & 15)) * BK3;
+    const int rd_b = BM * BK3 + (w8_c0(wn) + (lane & 15)) * BK3;
     const int key = swz8(lane & 15);
-    const int hsel = lane >> 5;
-    auto swk = [&](int kk) { return ((2 * kk + hsel) ^ key) << 3; };
-    bf16x8_t fa[2][4], fb[2][2];
-    // one LDS read (order a[0], b[0], b[1], a[1..3]) of sub-step kk of buffer buf
-    auto read_one = [&](int slot, int buf, int kk, int q) {
+    const int qsel = lane >> 4;
+    bf16x8_t fa[2][8], fb[2][4];
+    // LDS read q (0..11) of sub-step s of buffer buf, in the order the MFMAs
+    // consume them: a[0], b[0..3], a[1..7]
+    auto read_one = [&](int slot, int buf, int s, int q) {
         const bf16_t* sA = lds + buf * kStage3;
-        const int sw = swk(kk);
-        if (q == 0) fa[slot][0] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw);
-        else if (q <= 2) fb[slot][q - 1] = *reinterpret_cast<const bf16x8_t*>(sA + rd_b + sw + (q - 1) * 64 * BK3);
-        else fa[slot][q - 2] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + (q - 2) * 32 * BK3);
+        const int sw = ((4 * s + qsel) ^ key) << 3;
+        if (q == 0) {
+            fa[slot][0] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw);
+        } else if (q <= 4) {
+            const int nb = q - 1;
+            fb[slot][nb] = *reinterpret_cast<const bf16x8_t*>(sA + rd_b + sw + (16 * (nb & 1) + 64 * (nb >> 1)) * BK3);
+        } else {
+            fa[slot][q - 4] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + (q - 4) * 16 * BK3);
+        }
     };
-    auto mfma_one = [&](int slot, int q) {   // q = 0..7: (m, n) = (q >> 1, q & 1)
-        acc[q >> 1][q & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[slot][q >> 1], fb[slot][q & 1],
-                                                                      acc[q >> 1][q & 1], 0, 0, 0);
+    auto mfma_one = [&](int slot, int i) {   // i = 0..31: (mb, nb) = (i >> 2, i & 3)
+        acc[i >> 2][i & 3] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[slot][i >> 2], fb[slot][i & 3],
+                                                                      acc[i >> 2][i & 3], 0, 0, 0);
     };
 
 #pragma unroll
@@ -384,35 +407,35 @@ __global__ void __launch_bounds__(HALF ? 256 : 512, 1) gemm_bf16_w8_kernel(GemmP
         for (int q = 0; q < NQ; ++q) dma_one(1, 1, q);
     }
 #pragma unroll
-    for (int q = 0; q < 6; ++q) read_one(0, 0, 0, q);
+    for (int q = 0; q < 12; ++q) read_one(0, 0, 0, q);
 
+    // sub-step 0 reads sub-step 1 of the stage; sub-step 1 issues the DMA of
+    // stage kt + 2 and reads sub-step 0 of stage kt + 1
     auto stage = [&](int kt, auto kDma, auto kMore) {
         const int cur = kt & 1;
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int kk = 0; kk < 3; ++kk) {
+        for (int i = 0; i < 32; ++i) {
+            mfma_one(0, i);
+            if ((i & 1) == 0 && (i >> 1) < 12) read_one(1, cur, 1, i >> 1);
             __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                mfma_one(kk & 1, q);
-                if (q < 6) read_one((kk + 1) & 1, cur, kk + 1, q);
-                __builtin_amdgcn_sched_barrier(0);
-            }
         }
         asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
         wg_barrier();
 #pragma unroll
-        for (int m = 0; m < 4; ++m) asm volatile("" : "+v"(fa[1][m]));
+        for (int m = 0; m < 8; ++m) asm volatile("" : "+v"(fa[1][m]));
 #pragma unroll
-        for (int n = 0; n < 2; ++n) asm volatile("" : "+v"(fb[1][n]));
+        for (int n = 0; n < 4; ++n) asm volatile("" : "+v"(fb[1][n]));
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            mfma_one(1, q);
+        for (int i = 0; i < 32; ++i) {
+            mfma_one(1, i);
             if constexpr (decltype(kDma)::value) {
-                dma_one(cur, kt + 2, q);
-                if (q + 8 < NQ) dma_one(cur, kt + 2, q + 8);
+                if ((i & 1) == 1 && (i >> 1) < NQ) dma_one(cur, kt + 2, i >> 1);
             }
-            if constexpr (decltype(kMore)::value) { if (q < 6) read_one(0, cur ^ 1, 0, q); }
+            if constexpr (decltype(kMore)::value) {
+                if ((i & 1) == 0 && (i >> 1) < 12) read_one(0, cur ^ 1, 0, i >> 1);
+            }
             __builtin_amdgcn_sched_barrier(0);
         }
     };
@@ -428,7 +451,7 @@ __global__ void __launch_bounds__(HALF ? 256 : 512, 1) gemm_bf16_w8_kernel(GemmP
 // ---------------------------------------------------------------------------
 // Ping-pong variant.  Same tile, LDS stages, wave sub-tiles and order of
 // accumulation as the eight-wave kernel, but the two waves that share a SIMD
-// take turns: while one issues the 32 MFMAs of a whole 64-deep stage from
+// take turns: while one issues the 64 MFMAs of a whole 64-deep stage from
 // registers, the other reads its operands for the next stage from LDS, and a
 // workgroup barrier separates the turns.  Waves 0-3 (rows 0-127 of the tile)
 // run one turn ahead of waves 4-7 (rows 128-255); the hardware places waves w
@@ -487,30 +510,32 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_pp_kernel(GemmParams p) {
         }
     }
 
-    f32x16_t acc[4][2];
+    f32x4_t acc[8][4];
 #pragma unroll
-    for (int m = 0; m < 4; ++m)
+    for (int mb = 0; mb < 8; ++mb)
 #pragma unroll
-        for (int n = 0; n < 2; ++n)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) acc[m][n][i] = 0.f;
+        for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
     const int nk = p.K / BK3;
-    const int rd_a = (wm * 128 + (lane & 31)) * BK3;
-    const int rd_b = BM * BK3 + (w8_c0(wn) + (lane & 31)) * BK3;
+    const int rd_a = (wm * 128 + (lane & 15)) * BK3;
+    const int rd_b = BM * BK3 + (w8_c0(wn) + (lane & 15)) * BK3;
     const int key = swz8(lane & 15);
-    const int hsel = lane >> 5;
-    bf16x8_t fa[4][4], fb[4][2];   // [k sub-step][m or n]: one whole stage
-    auto read_one = [&](int kt, int r) {   // r = 0..23: sub-step r / 6, operand r % 6
+    const int qsel = lane >> 4;
+    bf16x8_t fa[2][8], fb[2][4];   // [32-deep sub-step][mb or nb]: one whole stage
+    auto read_one = [&](int kt, int r) {   // r = 0..23: sub-step r / 12, operand r % 12
         const bf16_t* sA = lds + (kt & 1) * kStage3;
-        const int kk = r / 6, q = r % 6;
-        const int sw = ((2 * kk + hsel) ^ key) << 3;
-        if (q < 4) fa[kk][q] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + q * 32 * BK3);
-        else fb[kk][q - 4] = *reinterpret_cast<const bf16x8_t*>(sA + rd_b + sw + (q - 4) * 64 * BK3);
+        const int s = r / 12, q = r % 12;
+        const int sw = ((4 * s + qsel) ^ key) << 3;
+        if (q < 8) {
+            fa[s][q] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + q * 16 * BK3);
+        } else {
+            const int nb = q - 8;
+            fb[s][nb] = *reinterpret_cast<const bf16x8_t*>(sA + rd_b + sw + (16 * (nb & 1) + 64 * (nb >> 1)) * BK3);
+        }
     };
-    auto mfma_one = [&](int i) {   // i = 0..31: sub-step i / 8, (m, n) = ((i >> 1) & 3, i & 1)
-        const int kk = i >> 3, m = (i >> 1) & 3, n = i & 1;
-        acc[m][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk][m], fb[kk][n], acc[m][n], 0, 0, 0);
+    auto mfma_one = [&](int i) {   // i = 0..63: sub-step i / 32, (mb, nb) = ((i >> 2) & 7, i & 3)
+        const int s = i >> 5, mb = (i >> 2) & 7, nb = i & 3;
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[s][mb], fb[s][nb], acc[mb][nb], 0, 0, 0);
     };
     auto turn_end = [&]() {
         __builtin_amdgcn_sched_barrier(0);
@@ -530,9 +555,9 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_pp_kernel(GemmParams p) {
     auto mfma_turn = [&](int kt, auto kDma) {
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-        for (int i = 0; i < 32; ++i) {
+        for (int i = 0; i < 64; ++i) {
             mfma_one(i);
-            if constexpr (decltype(kDma)::value) { if ((i & 3) == 3) dma_one(kt + 2, i >> 2); }
+            if constexpr (decltype(kDma)::value) { if ((i & 7) == 7) dma_one(kt + 2, i >> 3); }
             __builtin_amdgcn_sched_barrier(0);
         }
         __builtin_amdgcn_s_setprio(0);
