@@ -42,8 +42,8 @@ GEMM_SRC = os.path.join(ROOT, "paper_2609_29029_amd", "csrc", "gemm_bf16.hip")
 # half the bytes, WRITE_SIZE all of them).  Valid only for the GEMM source it
 # was measured on, identified by its SHA-256; otherwise reported as null.
 TRAFFIC = {"stage": "gate_up_swiglu",
-           "gemm_src_sha256": "863ecebc2fab97f038bda476821128ef760fd2ea81f69a4f86574904fe43acdc",
-           "bytes": 6.9917e9}
+           "gemm_src_sha256": "ad16afa1ec10e20dd691986344eb854b8a153320596be793a9425b9f1e9fa952",
+           "bytes": 7.1492e9}
 
 
 def log(*a):
@@ -163,6 +163,40 @@ def exhaustive_run(run, shape, w, torch) -> dict:
     tflop = sum(fl.values()) * m.n_layers / 1e12
     return {"ms": round(ms, 2), "packed_tokens": T, "prompts": n, "prefill_calls": shape["prefill_calls"],
             "tflop": round(tflop, 1), "frac_bf16_peak": round(tflop / (ms * 1e-3) / PEAK_BF16_TFLOPS, 4)}
+
+
+def mfma_ceiling(torch, seconds_per_form: float = 0.4) -> dict:
+    """bf16 MFMA throughput with nothing but MFMAs on every CU (operands rotating
+    over eight register pairs, as in a GEMM), from libriftcalib.so: the
+    attainable ceiling under the board power limit, reported beside the
+    nominal peak.  Three timed launches per instruction form, median."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_29029_amd", "libriftcalib.so"))
+    lib.rift_calib_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                         ctypes.c_int, ctypes.c_void_p]
+    g = torch.Generator(device="cuda").manual_seed(0x52494654)
+    src = torch.randn(65536, device="cuda", generator=g).to(torch.bfloat16)
+    blocks = torch.cuda.get_device_properties(0).multi_processor_count
+    out = torch.empty(blocks * 512, device="cuda", dtype=torch.float32)
+    stream = torch.cuda.current_stream().cuda_stream
+    per_iter = blocks * 8 * 262144
+    res = {}
+    for form, name in ((0, "v_mfma_f32_16x16x32_bf16"), (1, "v_mfma_f32_32x32x16_bf16")):
+        iters = max(8, int(seconds_per_form * 1.5e15 / per_iter) // 8 * 8)
+        ts = []
+        for rep in range(4):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            rc = lib.rift_calib_mfma_bf16(form, src.data_ptr(), out.data_ptr(), blocks, iters, stream)
+            e1.record()
+            torch.cuda.synchronize()
+            if rc != 0:
+                raise RuntimeError(f"rift_calib_mfma_bf16 returned {rc}")
+            if rep:   # the first launch warms the clocks up
+                ts.append(e0.elapsed_time(e1))
+        tf = per_iter * iters / (statistics.median(ts) * 1e-3) / 1e12
+        res[name] = {"TFLOPs": round(tf, 1), "frac_nominal": round(tf / PEAK_BF16_TFLOPS, 4)}
+    return res
 
 
 class EnergyMeter:
@@ -509,6 +543,11 @@ def main() -> int:
         "hbm": hbm,
     }
     out["packed_tokens_per_s"] = round(T * K / elapsed, 1)
+    ceil = mfma_ceiling(torch)
+    out["mfma_ceiling"] = ceil
+    c16 = ceil["v_mfma_f32_16x16x32_bf16"]["TFLOPs"]
+    out["roofline"]["measured_peak"] = c16
+    out["roofline"]["frac_of_measured_peak"] = round(achieved / c16, 4)
     kn = knn_score_timing(R, torch, tokens, qbank, w.keep_count)
     kn["extra_ms_over_plain_score"] = round(kn["score_ms"] - stage_ms["score"], 4)
     out["knn_smoothing"] = kn

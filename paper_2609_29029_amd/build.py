@@ -1,4 +1,6 @@
-"""Build librift.so (the HIP kernels and the C ABI) for gfx950 with hipcc.
+"""Build librift.so (the HIP kernels and the C ABI) for gfx950 with hipcc, and
+libriftcalib.so, a measurement aid for the benchmark (the MFMA throughput
+ceiling), which nothing on the Rift path loads.
 
 Usage: python -m paper_2609_29029_amd.build   (or build() from Python).
 Every call recompiles; objects go to _build/ next to this file.
@@ -14,10 +16,12 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "librift.so")
+CALIB_OUT = os.path.join(HERE, "libriftcalib.so")
 BUILD = os.path.join(HERE, "_build")
 
 SOURCES = ["score.hip", "knn.hip", "select.hip", "compact.hip", "prefill_misc.hip", "gemm_bf16.hip",
            "attention.hip", "capi.hip"]
+CALIB_SOURCES = ["calib/mfma_ceiling.hip"]
 
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-Wall",
@@ -34,7 +38,7 @@ def hipcc() -> str:
 
 
 def _compile(src: str) -> str:
-    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
+    obj = os.path.join(BUILD, os.path.splitext(src)[0].replace("/", "_") + ".o")
     cmd = [hipcc(), *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
@@ -42,18 +46,24 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = OUT + ".tmp"
+def _link(objs, out: str) -> None:
+    tmp = out + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, OUT)
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    srcs = SOURCES + CALIB_SOURCES
+    with ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        objs = list(ex.map(_compile, srcs))
+    _link(objs[:len(SOURCES)], OUT)
+    _link(objs[len(SOURCES):], CALIB_OUT)
     if verbose:
-        print(f"built {OUT}")
+        print(f"built {OUT} and {CALIB_OUT}")
     return OUT
 
 

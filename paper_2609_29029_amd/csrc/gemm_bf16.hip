@@ -158,6 +158,12 @@ __device__ __forceinline__ int swz8(int r) { return ((r >> 1) ^ ((r & 1) << 2)) 
 __device__ __forceinline__ int w8_c0(int wn) { return 128 * (wn >> 1) + 32 * (wn & 1); }
 __device__ __forceinline__ int w8_col(int wn, int nb) { return w8_c0(wn) + 16 * (nb & 1) + 64 * (nb >> 1); }
 
+// MFMA order inside a 32-deep sub-step: row block mb = i / 4 outer, column
+// block nb inner, in snake order (0 1 2 3, 3 2 1 0, ...) so that consecutive
+// MFMAs change only one operand (fewer input toggles under the power limit).
+// The order of accumulation of any one output is unchanged.
+__device__ __forceinline__ int snake_nb(int i) { return ((i >> 2) & 1) ? 3 - (i & 3) : (i & 3); }
+
 // Epilogue.  For the bf16 outputs the stage buffers, free after the main loop,
 // hold the tile: each wave writes its outputs (SiLU(gate)*up, RoPE'd q/k, v)
 // into a row-major tile in LDS, then every thread of the workgroup moves 16
@@ -393,9 +399,9 @@ __global__ void __launch_bounds__(HALF ? 256 : 512, 1) gemm_bf16_w8_kernel(GemmP
             fa[slot][q - 4] = *reinterpret_cast<const bf16x8_t*>(sA + rd_a + sw + (q - 4) * 16 * BK3);
         }
     };
-    auto mfma_one = [&](int slot, int i) {   // i = 0..31: (mb, nb) = (i >> 2, i & 3)
-        acc[i >> 2][i & 3] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[slot][i >> 2], fb[slot][i & 3],
-                                                                      acc[i >> 2][i & 3], 0, 0, 0);
+    auto mfma_one = [&](int slot, int i) {   // i = 0..31: (mb, nb) = (i >> 2, snake(i))
+        const int mb = i >> 2, nb = snake_nb(i);
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[slot][mb], fb[slot][nb], acc[mb][nb], 0, 0, 0);
     };
 
 #pragma unroll
@@ -533,8 +539,8 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_pp_kernel(GemmParams p) {
             fb[s][nb] = *reinterpret_cast<const bf16x8_t*>(sA + rd_b + sw + (16 * (nb & 1) + 64 * (nb >> 1)) * BK3);
         }
     };
-    auto mfma_one = [&](int i) {   // i = 0..63: sub-step i / 32, (mb, nb) = ((i >> 2) & 7, i & 3)
-        const int s = i >> 5, mb = (i >> 2) & 7, nb = i & 3;
+    auto mfma_one = [&](int i) {   // i = 0..63: sub-step i / 32, (mb, nb) = ((i >> 2) & 7, snake(i))
+        const int s = i >> 5, mb = (i >> 2) & 7, nb = snake_nb(i);
         acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[s][mb], fb[s][nb], acc[mb][nb], 0, 0, 0);
     };
     auto turn_end = [&]() {

@@ -177,3 +177,16 @@ def test_utility_budgets_match_oracle(R):
         R.rift_assign_budgets_utility([0.5], C5, AP, AN, EN, float("inf"), 576)
     b, tot = R.rift_assign_budgets_utility([], C5, AP, AN, EN, 0.1, 576)
     assert b.size == 0 and tot == 0
+
+
+def test_calibration_library_loads_and_rejects_bad_arguments(R):
+    """libriftcalib.so (the benchmark's MFMA-ceiling aid, off the Rift path)
+    loads and validates its arguments on the host; nothing is launched."""
+    L = ctypes.CDLL(os.path.join(ROOT, "paper_2609_29029_amd", "libriftcalib.so"))
+    f = L.rift_calib_mfma_bf16
+    f.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    p = ctypes.c_void_p(16)
+    assert f(2, p, p, 1, 8, None) == -1        # unknown form
+    assert f(0, None, p, 1, 8, None) == -1     # null source
+    assert f(0, p, p, 0, 8, None) == -1        # no workgroups
+    assert f(1, p, p, 1, 12, None) == -1       # iterations not a multiple of 8
