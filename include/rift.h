@@ -194,10 +194,13 @@ RIFT_API rift_status rift_select_tokens(const double* token_key, int32_t n_tiles
  * position_ids [packed_rows] i32 out  0..L-1 within each sequence
  * status       [1] i32 out  0, or RIFT_ERR_SHAPE if a tile id or selected index is
  *              out of range, a budget (sel_offsets step) is outside [0, n_v],
- *              sel_offsets[0] != 0 or T > packed_rows; a bad tile id, budget,
- *              first offset or total stops every row from being written, a bad
- *              selected index only its own row
- * Shape rules: d * sizeof(dt) % 16 == 0; n_sys, n_qry >= 0; 0 <= n_keep <= 65535.
+ *              sel_offsets[0] != 0 or T > packed_rows; a bad first offset or
+ *              total stops every row from being written, a bad tile id or
+ *              budget the rows of that prompt (and of any prompt whose offsets
+ *              reach past sel_offsets[n_keep]), a bad selected index only its
+ *              own row.  sel_idx must hold sel_offsets[n_keep] entries.
+ * Shape rules: d * sizeof(dt) % 16 == 0; n_sys, n_qry >= 0; 0 <= n_keep <= 65535;
+ *              packed_rows <= 2^25 (two waves per packed row).
  */
 RIFT_API rift_status rift_compact(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
                          int32_t d, const int32_t* kept_tiles, const int32_t* sel_offsets,

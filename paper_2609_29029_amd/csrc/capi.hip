@@ -269,7 +269,7 @@ rift_status rift_compact(const void* tokens, rift_dtype dt, int32_t n_tiles, int
     if ((n_sys > 0 && sys_emb == nullptr) || (n_qry > 0 && qry_emb == nullptr)) return RIFT_ERR_NULL;
     if (!dt_valid(dt)) return RIFT_ERR_DTYPE;
     if (n_tiles < 1 || n_v < 1 || d < 1 || n_keep < 0 || n_keep > 65535 || n_sys < 0 || n_qry < 0 ||
-        packed_rows < 0 || ((size_t)d * dt_bytes(dt)) % 16 != 0 || packed_rows > (int64_t)INT32_MAX)
+        packed_rows < 0 || ((size_t)d * dt_bytes(dt)) % 16 != 0 || packed_rows > ((int64_t)1 << 25))
         return RIFT_ERR_SHAPE;
     hipError_t e = launch_compact(tokens, (int)dt_bytes(dt), n_tiles, n_v, d, kept_tiles,
                                   sel_offsets, sel_idx, n_keep, sys_emb, n_sys, qry_emb, n_qry,

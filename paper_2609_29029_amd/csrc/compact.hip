@@ -3,99 +3,159 @@
 //  n_qry query rows]; every retained tile is its own VLM prompt (Sec. 2.3
 // Stage 2, App. B Step 5).
 //
-//   compact_meta  one workgroup: cu_seqlens, checks of offsets, budgets, tile
-//                 ids and capacity, status word.
-//   compact_rows  grid (row group, sequence), one wave per packed row: the
-//                 row's source (system, selected vision or query row) from the
-//                 sequence's offsets, then a coalesced 16-byte-per-lane copy
-//                 with every load of the row in flight before the first store
-//                 (a row of d bf16 is d/512 loads of 1 KB per wave), and the
-//                 row's position id.
+//   compact_rows  two waves per packed row r of [0, packed_rows).  The workgroup
+//                 stages sel_offsets in LDS (searched in place when there are
+//                 more than 4096 prompts) and each wave finds its prompt by
+//                 binary search over the prompt starts rho (n_sys + n_qry) +
+//                 sel_offsets[rho], checks it (first offset, total against the
+//                 capacity, tile id, budget) and copies nothing for a bad one;
+//                 otherwise it finds the row's source (system, selected vision
+//                 or query row) and copies its half of it with a coalesced
+//                 16-byte-per-lane copy, four 1 KB loads in flight before the
+//                 first store (plain loads: streaming hints measured slower),
+//                 and writes the row's position id.
+//                 Workgroup 0 also validates the whole call (every tile id,
+//                 budget and selected index), writes cu_seqlens and writes the
+//                 status word once, with a plain store, so no other launch has
+//                 to clear it first.
 #include "launch.h"
 #include "rift_common.h"
 
 namespace rift {
 
-__global__ void __launch_bounds__(1024)
-compact_meta_kernel(const int* __restrict__ kept, const int* __restrict__ offs, int n_keep,
-                    int n_tiles, int n_v, int fixed, long long cap, int* __restrict__ cu,
-                    int* __restrict__ status) {
-    __shared__ int bad;
-    if (threadIdx.x == 0) bad = 0;
-    __syncthreads();
-    for (int i = threadIdx.x; i <= n_keep; i += blockDim.x) {
-        const long long c = (long long)i * fixed + offs[i];
-        cu[i] = (int)c;
-        if (i < n_keep) {
-            const int t = kept[i];
-            const int b = offs[i + 1] - offs[i];
-            if (t < 0 || t >= n_tiles || b < 0 || b > n_v) atomicOr(&bad, 1);
-        }
-        if (i == 0 && offs[0] != 0) atomicOr(&bad, 1);
-        if (i == n_keep && c > cap) atomicOr(&bad, 1);
+// The whole-call check of workgroup (0, 0): 256 threads, a strided pass over
+// the tile ids and budgets, then (if those hold, so that the number of
+// selected indices is known and within the capacity) over the selected
+// indices; the status word is written once.
+__device__ void compact_validate(const int* __restrict__ kept, const int* __restrict__ offs,
+                                 const int* __restrict__ sel, int n_keep, int n_tiles, int n_v,
+                                 int fixed, long long cap, int* __restrict__ cu, int* __restrict__ status) {
+    __shared__ int bad_shape, bad_sel;
+    const int tid = threadIdx.x;
+    if (tid == 0) {
+        bad_shape = 0;
+        bad_sel = 0;
     }
     __syncthreads();
-    if (threadIdx.x == 0) *status = bad ? (int)RIFT_ERR_SHAPE : 0;
+    const int o_first = offs[0];
+    const int o_last = offs[n_keep];
+    const long long total = (long long)n_keep * fixed + o_last;
+    if (tid == 0) cu[n_keep] = (int)total;
+    for (int i = tid; i < n_keep; i += blockDim.x) cu[i] = (int)((long long)i * fixed + offs[i]);
+    bool bad = o_first != 0 || total > cap;
+    for (int i = tid; i < n_keep; i += blockDim.x) {
+        const int t = kept[i];
+        const int b = offs[i + 1] - offs[i];
+        bad |= t < 0 || t >= n_tiles || b < 0 || b > n_v;
+    }
+    if (bad) atomicOr(&bad_shape, 1);
+    __syncthreads();
+    if (!bad_shape) {
+        bool bs = false;
+        for (int j = tid; j < o_last; j += blockDim.x) {
+            const int tok = sel[j];
+            bs |= tok < 0 || tok >= n_v;
+        }
+        if (bs) atomicOr(&bad_sel, 1);
+    }
+    __syncthreads();
+    if (tid == 0) *status = (bad_shape | bad_sel) ? (int)RIFT_ERR_SHAPE : 0;
 }
 
-__global__ void __launch_bounds__(256)
-compact_rows_kernel(const u32x4_t* __restrict__ tokens, int n_v, int row_vec, int n_tiles,
-                    const int* __restrict__ kept, const int* __restrict__ offs,
-                    const int* __restrict__ sel, const u32x4_t* __restrict__ sys, int n_sys,
-                    const u32x4_t* __restrict__ qry, int n_qry, u32x4_t* __restrict__ packed,
-                    long long cap, int* __restrict__ pos_ids, int* __restrict__ status) {
-    const int rho = blockIdx.y;
-    const int p = blockIdx.x * 4 + (threadIdx.x >> 6);   // position in the sequence
-    const int lane = threadIdx.x & 63;
-    if (*status == (int)RIFT_ERR_SHAPE) return;   // compact_meta rejected the call
-    const int o0 = offs[rho];
-    const int budget = offs[rho + 1] - o0;
-    if (p >= n_sys + budget + n_qry) return;
-    const long long row = (long long)rho * (n_sys + n_qry) + o0 + p;
-    if (row >= cap) return;
+constexpr int kLdsMaxKeep = 4096;
+
+// Half `part` (0 or 1) of packed row r: find its prompt among the offsets `so`
+// (LDS or global), check it and copy that half of the row.
+__device__ __forceinline__ void compact_row(const int* so, long long r, int lane, int part,
+                                            const u32x4_t* __restrict__ tokens, int n_v, int row_vec,
+                                            int n_tiles, const int* __restrict__ kept, int n_keep,
+                                            const int* __restrict__ sel, const u32x4_t* __restrict__ sys,
+                                            int n_sys, const u32x4_t* __restrict__ qry, int n_qry,
+                                            u32x4_t* __restrict__ packed, long long cap,
+                                            int* __restrict__ pos_ids) {
+    const int fixed = n_sys + n_qry;
+    const int o_first = so[0];
+    const int o_last = so[n_keep];
+    const long long total = (long long)n_keep * fixed + o_last;
+    if (o_first != 0 || total > cap || r >= total) return;   // reported by workgroup 0
+    // the last prompt whose start rho * fixed + offs[rho] is <= r (starts do not
+    // decrease when the offsets are valid; the checks below keep every access in
+    // bounds when they are not)
+    int lo = 0, hi = n_keep - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if ((long long)mid * fixed + so[mid] <= r) lo = mid; else hi = mid - 1;
+    }
+    const int rho = lo;
+    const int o0 = so[rho];
+    const int o1 = so[rho + 1];
+    const int budget = o1 - o0;
+    const long long pl = r - ((long long)rho * fixed + o0);
+    // o0 >= 0 and o1 <= o_last keep the reads of sel_idx inside its o_last entries
+    if (budget < 0 || budget > n_v || o0 < 0 || o1 > o_last || pl < 0 || pl >= fixed + budget) return;
+    const int p = (int)pl;
     const u32x4_t* src;
     if (p < n_sys) {
         src = sys + (size_t)p * row_vec;
     } else if (p < n_sys + budget) {
-        const int tok = sel[o0 + (p - n_sys)];
         const int tile = kept[rho];
-        if (tok < 0 || tok >= n_v || tile < 0 || tile >= n_tiles) {
-            if (lane == 0) atomicOr(status, (int)RIFT_ERR_SHAPE);
-            return;
-        }
+        const int tok = sel[o0 + (p - n_sys)];
+        if (tok < 0 || tok >= n_v || tile < 0 || tile >= n_tiles) return;   // reported by workgroup 0
         src = tokens + ((size_t)tile * n_v + tok) * row_vec;
     } else {
         src = qry + (size_t)(p - n_sys - budget) * row_vec;
     }
-    u32x4_t* dst = packed + (size_t)row * row_vec;
-    int v = lane;
-    for (; v + 7 * 64 < row_vec; v += 512) {
-        u32x4_t t[8];
+    u32x4_t* dst = packed + (size_t)r * row_vec;
+    const int half_vec = row_vec / 2;
+    const int vend = part ? row_vec : half_vec;
+    int v = lane + part * half_vec;
+    for (; v + 3 * 64 < vend; v += 256) {
+        u32x4_t t[4];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) t[j] = __builtin_nontemporal_load(src + v + 64 * j);
+        for (int j = 0; j < 4; ++j) t[j] = src[v + 64 * j];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) dst[v + 64 * j] = t[j];
+        for (int j = 0; j < 4; ++j) dst[v + 64 * j] = t[j];
     }
-    for (; v < row_vec; v += 64) dst[v] = src[v];
-    if (lane == 0) pos_ids[row] = p;
+    for (; v < vend; v += 64) dst[v] = src[v];
+    if (lane == 0 && part == 0) pos_ids[r] = p;
+}
+
+__global__ void __launch_bounds__(256)
+compact_rows_kernel(const u32x4_t* __restrict__ tokens, int n_v, int row_vec, int n_tiles,
+                    const int* __restrict__ kept, const int* __restrict__ offs, int n_keep,
+                    const int* __restrict__ sel, const u32x4_t* __restrict__ sys, int n_sys,
+                    const u32x4_t* __restrict__ qry, int n_qry, u32x4_t* __restrict__ packed,
+                    long long cap, int* __restrict__ cu, int* __restrict__ pos_ids,
+                    int* __restrict__ status) {
+    __shared__ int offs_lds[kLdsMaxKeep + 1];
+    if (blockIdx.x == 0)
+        compact_validate(kept, offs, sel, n_keep, n_tiles, n_v, n_sys + n_qry, cap, cu, status);
+    const int lane = threadIdx.x & 63;
+    const long long r = (long long)blockIdx.x * 2 + (threadIdx.x >> 7);   // two rows per workgroup
+    const int part = (threadIdx.x >> 6) & 1;                              // and two waves per row
+    if (n_keep <= kLdsMaxKeep) {
+        for (int i = threadIdx.x; i <= n_keep; i += blockDim.x) offs_lds[i] = offs[i];
+        __syncthreads();
+        compact_row(offs_lds, r, lane, part, tokens, n_v, row_vec, n_tiles, kept, n_keep, sel, sys, n_sys, qry,
+                    n_qry, packed, cap, pos_ids);
+    } else {
+        compact_row(offs, r, lane, part, tokens, n_v, row_vec, n_tiles, kept, n_keep, sel, sys, n_sys, qry, n_qry,
+                    packed, cap, pos_ids);
+    }
 }
 
 hipError_t launch_compact(const void* tokens, int elem_bytes, int n_tiles, int n_v, int d,
                           const int* kept, const int* offs, const int* sel, int n_keep,
                           const void* sys, int n_sys, const void* qry, int n_qry, void* packed,
                           long long cap, int* cu, int* pos_ids, int* status, hipStream_t st) {
-    hipLaunchKernelGGL(compact_meta_kernel, dim3(1), dim3(1024), 0, st, kept, offs, n_keep,
-                       n_tiles, n_v, n_sys + n_qry, cap, cu, status);
     const int row_vec = (int)((size_t)d * elem_bytes / 16);
-    if (cap > 0 && n_keep > 0) {
-        // every sequence has at most n_sys + n_v + n_qry rows (budgets <= n_v)
-        const unsigned gx = (unsigned)((n_sys + n_v + n_qry + 3) / 4);
-        hipLaunchKernelGGL(compact_rows_kernel, dim3(gx, (unsigned)n_keep), dim3(256), 0, st,
-                           static_cast<const u32x4_t*>(tokens), n_v, row_vec, n_tiles, kept, offs,
-                           sel, static_cast<const u32x4_t*>(sys), n_sys,
-                           static_cast<const u32x4_t*>(qry), n_qry, static_cast<u32x4_t*>(packed),
-                           cap, pos_ids, status);
-    }
+    // two waves per row of the packed buffer; at least one workgroup, for the
+    // status word and cu_seqlens
+    const long long g = cap > 0 ? (cap + 1) / 2 : 1;
+    hipLaunchKernelGGL(compact_rows_kernel, dim3((unsigned)g), dim3(256), 0, st,
+                       static_cast<const u32x4_t*>(tokens), n_v, row_vec, n_tiles, kept, offs, n_keep,
+                       sel, static_cast<const u32x4_t*>(sys), n_sys, static_cast<const u32x4_t*>(qry),
+                       n_qry, static_cast<u32x4_t*>(packed), cap, cu, pos_ids, status);
     return hipGetLastError();
 }
 

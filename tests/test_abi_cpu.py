@@ -126,6 +126,9 @@ def test_select_and_compact_validation(R):
     assert c(FAKE, 9, 4, 576, 4096, FAKE, FAKE, FAKE, 2, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 3
     assert c(FAKE, 1, 4, 576, 4, FAKE, FAKE, FAKE, 2, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 2
     assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, -1, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 2
+    # two waves per packed row: at most 2^25 rows
+    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, 2, FAKE, 35, FAKE, 32, FAKE, (1 << 25) + 1, FAKE, FAKE, FAKE,
+             None) == 2
 
 
 def test_prefill_validation_and_workspace(R):

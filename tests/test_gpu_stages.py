@@ -273,6 +273,31 @@ def test_compact_edges(R):
     # a budget (offset step) larger than n_v
     packed, cu, pos, st = run_compact(R, X, "bf16", [0], np.array([0, 21]), np.arange(21) % 20, sysr, qry)
     assert st == 2
+    # offsets that decrease: reported, and no prompt reads past sel_offsets[n_keep] selected indices
+    packed, cu, pos, st = run_compact(R, X, "bf16", [0, 1], np.array([0, 15, 5]), np.arange(5), sysr, qry, rows=40)
+    assert st == 2
+    # a packed buffer longer than the batch: rows past T untouched
+    packed, cu, pos, st = run_compact(R, X, "bf16", kept, offs, sel, sysr, qry, rows=40)
+    r = O.compact(X, kept, offs, sel, sysr, qry)
+    assert st == 0 and np.array_equal(packed[:30], r[0]) and np.all(packed[30:] == 0) and np.all(pos[30:] == -7)
+
+
+def test_compact_many_prompts(R):
+    """More prompts than the kernel stages in LDS (4096): the prompt of each row
+    is then searched in the offsets in global memory."""
+    rng = np.random.default_rng(11)
+    n_tiles, n_v = 5000, 4
+    X = synth.store(rng.standard_normal((n_tiles, n_v, 64)).astype(np.float32), "bf16")
+    sysr = synth.store(rng.standard_normal((1, 64)).astype(np.float32), "bf16")
+    qry = synth.store(rng.standard_normal((2, 64)).astype(np.float32), "bf16")
+    kept = list(rng.permutation(n_tiles)[:4500])
+    budgets = rng.integers(0, n_v + 1, size=len(kept))
+    offs = np.concatenate([[0], np.cumsum(budgets)])
+    sel = np.concatenate([np.sort(rng.permutation(n_v)[:b]) for b in budgets]).astype(np.int64)
+    packed, cu, pos, st = run_compact(R, X, "bf16", kept, offs, sel, sysr, qry)
+    r_packed, r_cu, r_pos = O.compact(X, kept, offs, sel, sysr, qry)
+    assert st == 0
+    assert np.array_equal(packed, r_packed) and np.array_equal(cu, r_cu) and np.array_equal(pos, r_pos)
 
 
 @pytest.mark.slow
