@@ -25,6 +25,13 @@
  *     device status word, and the kernels then write nothing out of bounds.
  *   - Storage types: RIFT_BF16 (bfloat16) or RIFT_F32.  One dtype is shared by
  *     tokens, query bank, system/query embeddings and weights of a call chain.
+ *   - Debug mode (environment variable RIFT_DEBUG=1 when the library is first
+ *     used, or rift_set_debug): rift_score_tiles, rift_select_tokens and
+ *     rift_prefill first scan their floating-point inputs on the device for
+ *     NaN or infinity, wait for the scan (the one place the library
+ *     synchronises its stream) and return RIFT_ERR_NONFINITE, with nothing
+ *     else enqueued, when one is found.  Index bounds are checked on the device
+ *     in every mode (the status words of select and compact).
  */
 #ifndef RIFT_H
 #define RIFT_H
@@ -36,7 +43,7 @@
 extern "C" {
 #endif
 
-#define RIFT_ABI_VERSION 2
+#define RIFT_ABI_VERSION 3
 
 #if defined(__GNUC__) || defined(__clang__)
 #define RIFT_API __attribute__((visibility("default")))
@@ -52,7 +59,8 @@ typedef enum {
     RIFT_ERR_BUDGET = 4,      /* budget, level or tier out of range               */
     RIFT_ERR_WORKSPACE = 5,   /* workspace too small or not 256-byte aligned      */
     RIFT_ERR_HIP = 6,         /* a HIP runtime call or a kernel launch failed     */
-    RIFT_ERR_UNSUPPORTED = 7  /* valid request outside what this build implements */
+    RIFT_ERR_UNSUPPORTED = 7, /* valid request outside what this build implements */
+    RIFT_ERR_NONFINITE = 8    /* a floating-point input holds NaN or infinity     */
 } rift_status;
 
 typedef enum { RIFT_F32 = 0, RIFT_BF16 = 1 } rift_dtype;
@@ -64,6 +72,26 @@ RIFT_API int32_t rift_abi_version(void);
 
 /* Static text for a status code. */
 RIFT_API const char* rift_status_string(rift_status s);
+
+/*
+ * rift_set_debug -- switch the debug mode of the process on (on != 0) or off;
+ * returns the previous setting (1 or 0).  The first use of the library reads
+ * the initial setting from RIFT_DEBUG.  Calls that are already running keep
+ * the mode they started with.
+ */
+RIFT_API int32_t rift_set_debug(int32_t on);
+
+/*
+ * rift_check_finite -- device check that x holds no NaN or infinity, the
+ * check the debug mode runs on the inputs (usable on its own, e.g. on weights
+ * once after loading them).  Asynchronous like every call.
+ * x       [count] dt, any alignment
+ * status  [1] i32 out  0, or RIFT_ERR_NONFINITE
+ * Errors: RIFT_ERR_NULL (status, or x with count > 0), RIFT_ERR_DTYPE,
+ * RIFT_ERR_SHAPE (count < 0).
+ */
+RIFT_API rift_status rift_check_finite(const void* x, rift_dtype dt, int64_t count, int32_t* status,
+                                       rift_stream stream);
 
 /* ------------------------------------------------------------------ Stage 1 */
 

@@ -18,12 +18,13 @@ LIB_PATH = os.path.join(HERE, "librift.so")
 RIFT_OK = 0
 STATUS_NAMES = {0: "RIFT_OK", 1: "RIFT_ERR_NULL", 2: "RIFT_ERR_SHAPE", 3: "RIFT_ERR_DTYPE",
                 4: "RIFT_ERR_BUDGET", 5: "RIFT_ERR_WORKSPACE", 6: "RIFT_ERR_HIP",
-                7: "RIFT_ERR_UNSUPPORTED"}
+                7: "RIFT_ERR_UNSUPPORTED", 8: "RIFT_ERR_NONFINITE"}
 RIFT_F32 = 0
 RIFT_BF16 = 1
 
 # Every symbol include/rift.h declares, in declaration order.
-EXPORTS = ("rift_abi_version", "rift_status_string", "rift_score_workspace_size",
+EXPORTS = ("rift_abi_version", "rift_status_string", "rift_set_debug", "rift_check_finite",
+           "rift_score_workspace_size",
            "rift_score_tiles", "rift_assign_budgets", "rift_assign_budgets_utility",
            "rift_select_tokens", "rift_compact",
            "rift_prefill_workspace_size", "rift_prefill")
@@ -67,6 +68,10 @@ def load() -> ctypes.CDLL:
     L.rift_abi_version.argtypes = []
     L.rift_status_string.restype = ctypes.c_char_p
     L.rift_status_string.argtypes = [I32]
+    L.rift_set_debug.restype = I32
+    L.rift_set_debug.argtypes = [I32]
+    L.rift_check_finite.restype = I32
+    L.rift_check_finite.argtypes = [P, I32, I64, P, P]
     L.rift_score_workspace_size.restype = SZ
     L.rift_score_workspace_size.argtypes = [I32, I32, I32, I32]
     L.rift_score_tiles.restype = I32
@@ -134,6 +139,22 @@ def _need(t, dtype, shape=None, name="tensor"):
         raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
     if not t.is_cuda:
         raise ValueError(f"{name}: must be a device tensor")
+
+
+# ----------------------------------------------------------------------------- checks
+def rift_set_debug(on: bool) -> bool:
+    """Debug mode of the process on or off; returns the previous setting."""
+    return bool(load().rift_set_debug(1 if on else 0))
+
+
+def rift_check_finite(x, status, stream=None) -> None:
+    """status[0] := 0, or RIFT_ERR_NONFINITE if x (bf16 or f32) holds NaN or
+    infinity; enqueued on the stream like every call."""
+    torch = _torch()
+    _need(x, x.dtype, None, "x")
+    _need(status, torch.int32, (1,), "status")
+    _check(load().rift_check_finite(_ptr(x), _dt_code(x), x.numel(), _ptr(status), _stream(stream)),
+           "rift_check_finite")
 
 
 # ----------------------------------------------------------------------------- Stage 1

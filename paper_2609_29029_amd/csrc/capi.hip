@@ -1,7 +1,10 @@
 // C ABI of the Rift hot path: argument validation, workspace carving and
-// kernel launches.  Nothing here allocates device memory or synchronises.
+// kernel launches.  Nothing here allocates device memory; only the debug mode
+// synchronises (to read the result of its input scan).
 #include <math.h>
+#include <stdlib.h>
 
+#include <atomic>
 #include <cmath>
 
 #include <mutex>
@@ -46,8 +49,45 @@ inline bool dt_valid(rift_dtype dt) { return dt == RIFT_BF16 || dt == RIFT_F32; 
 
 inline rift_status hip_status(hipError_t e) { return e == hipSuccess ? RIFT_OK : RIFT_ERR_HIP; }
 
+// debug mode: -1 until first read from RIFT_DEBUG
+std::atomic<int> g_debug{-1};
+
+bool debug_on() {
+    int v = g_debug.load(std::memory_order_relaxed);
+    if (v < 0) {
+        const char* e = getenv("RIFT_DEBUG");
+        const int want = (e != nullptr && e[0] == '1') ? 1 : 0;
+        int expected = -1;
+        g_debug.compare_exchange_strong(expected, want);
+        v = g_debug.load(std::memory_order_relaxed);
+    }
+    return v == 1;
+}
+
+// A floating-point input of a debug-mode check: elements and kind (0 bfloat16,
+// 1 float32, 2 float64).
+struct DebugInput {
+    const void* x;
+    int kind;
+    long long n;
+};
+
+// Scan the inputs into flag (device) and wait for the answer.
+rift_status debug_scan(const DebugInput* in, int count, int* flag, hipStream_t st) {
+    if (launch_nonfinite_clear(flag, st) != hipSuccess) return RIFT_ERR_HIP;
+    for (int i = 0; i < count; ++i)
+        if (launch_nonfinite_scan(in[i].x, in[i].kind, in[i].n, flag, st) != hipSuccess) return RIFT_ERR_HIP;
+    int h = 0;
+    if (hipMemcpyAsync(&h, flag, sizeof(int), hipMemcpyDeviceToHost, st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess)
+        return RIFT_ERR_HIP;
+    return h == (int)RIFT_ERR_NONFINITE ? RIFT_ERR_NONFINITE : RIFT_OK;
+}
+
+inline int dt_kind(rift_dtype dt) { return dt == RIFT_BF16 ? 0 : 1; }
+
 struct PrefillLayout {
-    size_t rope, h, q, k, v, a, gate2, total;
+    size_t rope, h, q, k, v, a, gate2, dbg, total;
 };
 
 PrefillLayout prefill_layout(const rift_model_cfg& c, int64_t T, int64_t P) {
@@ -68,6 +108,8 @@ PrefillLayout prefill_layout(const rift_model_cfg& c, int64_t T, int64_t P) {
     off += align_up((size_t)T * c.ffn * e);
     L.gate2 = off;
     if (c.dt == RIFT_F32) off += align_up((size_t)T * c.ffn * e);
+    L.dbg = off;   // debug mode: flag word of the input scan
+    off += kAlign;
     L.total = off;
     return L;
 }
@@ -106,8 +148,26 @@ const char* rift_status_string(rift_status s) {
         case RIFT_ERR_WORKSPACE: return "workspace too small or not 256-byte aligned";
         case RIFT_ERR_HIP: return "a HIP runtime call or kernel launch failed";
         case RIFT_ERR_UNSUPPORTED: return "valid request outside what this build implements";
+        case RIFT_ERR_NONFINITE: return "a floating-point input holds NaN or infinity";
     }
     return "unknown status";
+}
+
+int32_t rift_set_debug(int32_t on) {
+    const int prev = debug_on() ? 1 : 0;
+    g_debug.store(on != 0 ? 1 : 0, std::memory_order_relaxed);
+    return prev;
+}
+
+rift_status rift_check_finite(const void* x, rift_dtype dt, int64_t count, int32_t* status,
+                              rift_stream stream) {
+    if (status == nullptr || (count > 0 && x == nullptr)) return RIFT_ERR_NULL;
+    if (!dt_valid(dt)) return RIFT_ERR_DTYPE;
+    if (count < 0) return RIFT_ERR_SHAPE;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e = launch_nonfinite_clear(status, st);
+    if (e == hipSuccess) e = launch_nonfinite_scan(x, dt_kind(dt), (long long)count, status, st);
+    return hip_status(e);
 }
 
 namespace {
@@ -115,7 +175,7 @@ namespace {
 // (float64 [n_tiles n_v]), tile embeddings (float32 [n_tiles][d]), their
 // dot products (float64 [n_tiles][n_tiles]) and the smoothed scores.
 struct ScoreLayout {
-    size_t w, inv, emb, gram, smooth, total;
+    size_t w, inv, emb, gram, smooth, dbg, total;
 };
 ScoreLayout score_layout(int32_t n_tiles, int32_t n_v, int32_t d, int32_t knn_m) {
     ScoreLayout L{};
@@ -132,6 +192,8 @@ ScoreLayout score_layout(int32_t n_tiles, int32_t n_v, int32_t d, int32_t knn_m)
         L.smooth = off;
         off += align_up((size_t)n_tiles * sizeof(double));
     }
+    L.dbg = off;   // debug mode: flag word of the input scan
+    off += kAlign;
     L.total = off;
     return L;
 }
@@ -159,6 +221,13 @@ rift_status rift_score_tiles(const void* tokens, rift_dtype dt, int32_t n_tiles,
     if (misaligned(workspace) || ws_bytes < L.total) return RIFT_ERR_WORKSPACE;
     if (init_kernel_attributes() != hipSuccess) return RIFT_ERR_HIP;
     unsigned char* ws = static_cast<unsigned char*>(workspace);
+    if (debug_on()) {
+        const DebugInput in[2] = {{tokens, dt_kind(dt), (long long)n_tiles * n_v * d},
+                                  {query_bank, dt_kind(dt), (long long)(1 + n_bg) * d}};
+        const rift_status ds = debug_scan(in, 2, reinterpret_cast<int*>(ws + L.dbg),
+                                          static_cast<hipStream_t>(stream));
+        if (ds != RIFT_OK) return ds;
+    }
     hipError_t e = launch_score(tokens, dt == RIFT_BF16, n_tiles, n_v, d, query_bank, n_bg,
                                 keep_count, tau, knn_m, token_key, token_sim, tile_score, tile_u,
                                 tile_order, n_keep, reinterpret_cast<float*>(ws + L.w),
@@ -252,6 +321,11 @@ rift_status rift_select_tokens(const double* token_key, int32_t n_tiles, int32_t
     if (n_v < 1 || n_v > 1024 || n_tiles < 1 || (int64_t)n_tiles * n_v > (int64_t)INT32_MAX ||
         n_keep < 0 || n_keep > n_tiles || sel_capacity < 0 || sel_capacity > (int64_t)INT32_MAX)
         return RIFT_ERR_SHAPE;
+    if (debug_on() && n_keep > 0) {   // every key of the scene; the status word holds the flag
+        const DebugInput in[1] = {{token_key, 2, (long long)n_tiles * n_v}};
+        const rift_status ds = debug_scan(in, 1, status, static_cast<hipStream_t>(stream));
+        if (ds != RIFT_OK) return ds;
+    }
     hipError_t e = launch_select(token_key, n_tiles, n_v, kept_tiles, budgets, n_keep, sel_offsets,
                                  sel_idx, sel_capacity, status, static_cast<hipStream_t>(stream));
     return hip_status(e);
@@ -316,6 +390,23 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
 
     hipStream_t st = static_cast<hipStream_t>(stream);
     unsigned char* ws = static_cast<unsigned char*>(workspace);
+    if (debug_on()) {   // the packed input and every weight and gain
+        const int wk = dt_kind(c.dt);
+        const long long dd = (long long)c.d * c.d, df = (long long)c.d * c.ffn;
+        rift_status ds = RIFT_OK;
+        {
+            const DebugInput in[1] = {{x_in, x_dt == RIFT_BF16 ? 0 : 1, (long long)total_tokens * c.d}};
+            ds = debug_scan(in, 1, reinterpret_cast<int*>(ws + L.dbg), st);
+        }
+        for (int l = 0; l < c.n_layers && ds == RIFT_OK; ++l) {
+            const rift_layer_weights& w = layers[l];
+            const DebugInput in[9] = {{w.wq, wk, dd},     {w.wk, wk, dd},     {w.wv, wk, dd},
+                                      {w.wo, wk, dd},     {w.w_gate, wk, df}, {w.w_up, wk, df},
+                                      {w.w_down, wk, df}, {w.g_attn, wk, c.d}, {w.g_ffn, wk, c.d}};
+            ds = debug_scan(in, 9, reinterpret_cast<int*>(ws + L.dbg), st);
+        }
+        if (ds != RIFT_OK) return ds;
+    }
     float2* rope = reinterpret_cast<float2*>(ws + L.rope);
     const int T = total_tokens;
     const int d = c.d;

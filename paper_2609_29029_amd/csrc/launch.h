@@ -18,6 +18,11 @@ hipError_t launch_knn_smooth(const void* tokens, bool bf16, int n_tiles, int n_v
                              const double* inv, float* emb, double* gram, const double* s_raw,
                              int m, double* s_out, hipStream_t st);
 
+// non-finite scan: clear the flag word, then scan buffers into it (kind 0
+// bfloat16, 1 float32, 2 float64; n elements)
+hipError_t launch_nonfinite_clear(int* flag, hipStream_t st);
+hipError_t launch_nonfinite_scan(const void* x, int kind, long long n, int* flag, hipStream_t st);
+
 hipError_t launch_select(const double* token_key, int n_tiles, int n_v, const int* kept,
                          const int* budgets, int n_keep, int* sel_offsets, int* sel_idx,
                          long long cap, int* status, hipStream_t st);

@@ -33,11 +33,11 @@ def declared_symbols():
 def test_library_exports_every_declared_symbol(R):
     L = R.load()
     names = declared_symbols()
-    assert len(names) == 10
+    assert len(names) == 12
     assert tuple(names) == R.EXPORTS
     for n in names:
         assert hasattr(L, n), n
-    assert L.rift_abi_version() == 2
+    assert L.rift_abi_version() == 3
     assert L.rift_status_string(4).decode().startswith("budget")
 
 
@@ -193,3 +193,17 @@ def test_calibration_library_loads_and_rejects_bad_arguments(R):
     assert f(0, None, p, 1, 8, None) == -1     # null source
     assert f(0, p, p, 0, 8, None) == -1        # no workgroups
     assert f(1, p, p, 1, 12, None) == -1       # iterations not a multiple of 8
+
+
+def test_check_finite_validation_and_debug_switch(R):
+    """rift_check_finite rejects bad arguments on the host (nothing launched);
+    rift_set_debug returns the previous setting."""
+    L = R.load()
+    assert L.rift_check_finite(FAKE, 1, 10, None, None) == 1       # no status word
+    assert L.rift_check_finite(None, 1, 10, FAKE, None) == 1       # no input
+    assert L.rift_check_finite(FAKE, 5, 10, FAKE, None) == 3       # unknown dtype
+    assert L.rift_check_finite(FAKE, 0, -1, FAKE, None) == 2       # negative count
+    assert L.rift_status_string(8).decode() == "a floating-point input holds NaN or infinity"
+    prev = L.rift_set_debug(1)
+    assert L.rift_set_debug(0) == 1
+    assert L.rift_set_debug(prev) == 0
