@@ -53,6 +53,19 @@ Readings of points the paper leaves open (numbered as in the design notes):
       largest U, ties to the smaller c.  p_i, the trained predictor's
       probability that the tile holds the object, is out of scope: callers
       pass it (the pipeline passes the tile's normalised score u_i).
+  R14 Optional merge of the remainder into contextual tokens (Sec. 2.3
+      Stage 2: VisionZip keeps the dominant tokens "and merges the remainder";
+      the merge follows VisionZip's published scheme).  A budget c splits into
+      k_c = min(floor(c num / den), n_v - c) contextual and k_d = c - k_c
+      dominant tokens (num/den = 10/64, VisionZip's 54 + 10 at 64 tokens; at
+      the full budget k_c = 0).  The remainder R is the n_v - k_d tokens not
+      selected as dominant, ascending; target j is R[floor(j |R| / k_c)].
+      Every other token of R joins the target j of largest
+      cdot(x_r, x_j) * inv_j (its cosine to the target up to the positive
+      factor 1/|x_r|; inv as for R8), ties to the lower j.  Contextual token j
+      is the float64 sum of its group in ascending index order divided by the
+      group size, rounded to float32 and then to the storage type.  The
+      prompt becomes [system | dominant | contextual (j order) | query].
 """
 from __future__ import annotations
 
@@ -240,17 +253,23 @@ def select_tokens(r: np.ndarray, kept: Sequence[int], budgets: Sequence[int]
 
 
 def compact(x: np.ndarray, kept: Sequence[int], sel_offsets: np.ndarray,
-            sel_idx: np.ndarray, sys: np.ndarray, qry: np.ndarray
+            sel_idx: np.ndarray, sys: np.ndarray, qry: np.ndarray,
+            ctx_rows: np.ndarray = None, ctx_offsets: np.ndarray = None
             ) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
     """Packed varlen batch: sequence rho = [sys | x[kept[rho], sel] | qry]
-    (reading R9), cu_seqlens = prefix sums of lengths, position ids 0..L-1 per
-    sequence.  Works on any element type (it only moves rows)."""
+    (reading R9), or [sys | x[kept[rho], sel] | contextual rows of rho | qry]
+    when contextual rows are given (reading R14); cu_seqlens = prefix sums of
+    lengths, position ids 0..L-1 per sequence.  Works on any element type (it
+    only moves rows)."""
     rows = []
     cu = [0]
     pos = []
     for rho, tile in enumerate(kept):
         sel = sel_idx[sel_offsets[rho]: sel_offsets[rho + 1]]
-        seq = np.concatenate([sys, x[int(tile)][sel], qry], axis=0)
+        parts = [sys, x[int(tile)][sel]]
+        if ctx_rows is not None:
+            parts.append(ctx_rows[ctx_offsets[rho]: ctx_offsets[rho + 1]])
+        seq = np.concatenate(parts + [qry], axis=0)
         rows.append(seq)
         cu.append(cu[-1] + seq.shape[0])
         pos.append(np.arange(seq.shape[0], dtype=np.int32))
@@ -422,3 +441,59 @@ def knn_smooth(s: np.ndarray, cos: np.ndarray, m: int):
         out[i] = acc / (1 + m_eff)
         nbrs.append(js)
     return out, nbrs
+
+
+# ------------------------------------------------- optional contextual merge (R14)
+
+
+def split_budget(c: int, n_v: int, num: int = 10, den: int = 64) -> Tuple[int, int]:
+    """(k_d, k_c): dominant and contextual tokens of a budget c (reading R14):
+    k_c = min(floor(c num / den), n_v - c), k_d = c - k_c."""
+    k_c = min((c * num) // den, n_v - c)
+    return c - k_c, k_c
+
+
+def round_f32_to_bf16(v: np.ndarray) -> np.ndarray:
+    """bfloat16 bit patterns (uint16) of float32 values, round to nearest even
+    on the 16 dropped bits (values here are finite)."""
+    b = np.asarray(v, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    rounded = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
+    return rounded.astype(np.uint16)
+
+
+def merge_context(x: np.ndarray, dominant: Sequence[int], k_c: int):
+    """Contextual tokens of one tile (reading R14).  x: [n_v, d] float64 (the
+    stored token values); dominant: the dominant token indices.  Returns
+    (values [k_c, d] float64 holding float32 values, groups: list of k_c
+    ascending index lists, targets).  Rounding to bfloat16 storage is
+    round_f32_to_bf16 of the values."""
+    n_v = x.shape[0]
+    dom = set(int(t) for t in dominant)
+    R = [t for t in range(n_v) if t not in dom]
+    if k_c == 0:
+        return np.zeros((0, x.shape[1])), [], []
+    if k_c > len(R):
+        raise ValueError("more contextual tokens than remaining tokens")
+    targets = [R[(j * len(R)) // k_c] for j in range(k_c)]
+    inv_t = token_inv_norms(x[targets])
+    groups = [[t] for t in targets]
+    tset = set(targets)
+    for r in R:
+        if r in tset:
+            continue
+        g = cdot(x[targets], x[r])            # one canonical dot per target
+        a = g * inv_t
+        best = 0
+        for j in range(1, k_c):
+            if a[j] > a[best]:
+                best = j
+        groups[best].append(r)
+    vals = np.zeros((k_c, x.shape[1]), dtype=np.float64)
+    for j, grp in enumerate(groups):
+        grp.sort()
+        acc = np.zeros(x.shape[1], dtype=np.float64)
+        for t in grp:
+            acc = acc + x[t]
+        vals[j] = (acc / len(grp)).astype(np.float32).astype(np.float64)
+    return vals, groups, targets
+

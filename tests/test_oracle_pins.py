@@ -493,3 +493,126 @@ def test_utility_budgets_ties_and_order_independence():
     p = np.linspace(0, 1, 101)
     bud = O.utility_budgets(p, C5, AP, AN, EN, 0.1)
     assert np.all(np.diff(bud) >= 0)
+
+
+# ------------------------------------------------------------------ contextual merge (R14)
+
+
+def test_split_budget_visionzip_configurations():
+    # VisionZip's published splits: 54 + 10 at 64 tokens, 108 + 20 at 128, 162 + 30 at 192
+    assert O.split_budget(64, 576) == (54, 10)
+    assert O.split_budget(128, 576) == (108, 20)
+    assert O.split_budget(192, 576) == (162, 30)
+    # nothing left to merge at the full budget; one token left at n_v - 1
+    assert O.split_budget(576, 576) == (576, 0)
+    assert O.split_budget(575, 576) == (574, 1)
+    assert O.split_budget(0, 576) == (0, 0)
+    for c in range(0, 577):
+        kd, kc = O.split_budget(c, 576)
+        assert kd + kc == c and 0 <= kc <= 576 - c
+
+
+def test_round_f32_to_bf16_against_torch_and_hand_cases():
+    torch = pytest.importorskip("torch")
+    # hand cases: 1 + 2^-8 is halfway between 1 and 1 + 2^-7 -> even (1);
+    # 1 + 3 * 2^-9 is above halfway -> 1 + 2^-7; -2.5 is exact
+    hand = np.array([1.0, 1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -9, -2.5, 1.0 + 3 * 2.0 ** -8], np.float32)
+    assert list(O.round_f32_to_bf16(hand)) == [0x3F80, 0x3F80, 0x3F81, 0xC020, 0x3F82]
+    v = np.random.default_rng(0).standard_normal(100_000).astype(np.float32) * 1e3
+    ref = torch.from_numpy(v).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(O.round_f32_to_bf16(v), ref)
+
+
+def _int_tokens(rng, n_v, d, lo=-3, hi=4):
+    return rng.integers(lo, hi, size=(n_v, d)).astype(np.float64)
+
+
+def test_merge_all_targets_and_single_target_closed_forms():
+    rng = np.random.default_rng(4)
+    x = _int_tokens(rng, 20, 64)
+    dom = [0, 3, 7]
+    R = [t for t in range(20) if t not in dom]
+    # as many contextual tokens as remaining tokens: each is its own group
+    vals, groups, targets = O.merge_context(x, dom, len(R))
+    assert targets == R and groups == [[t] for t in R]
+    assert np.array_equal(vals, x[R])
+    # one contextual token: the mean of the whole remainder (exact on small integers / 17)
+    vals, groups, targets = O.merge_context(x, dom, 1)
+    assert targets == [R[0]] and groups == [R]
+    assert np.array_equal(vals[0], (x[R].sum(axis=0) / len(R)).astype(np.float32).astype(np.float64))
+
+
+def test_merge_follows_orthogonal_clusters():
+    d = 32
+    e0, e1 = np.eye(d)[0], np.eye(d)[1]
+    x = np.zeros((12, d))
+    x[0] = e0 + e1
+    x[1] = e0 - e1                       # dominant tokens: not merged
+    for t in range(2, 7):
+        x[t] = (t - 1) * e0              # cluster along e0
+    for t in range(7, 12):
+        x[t] = (t - 6) * 3 * e1          # cluster along e1
+    vals, groups, targets = O.merge_context(x, [0, 1], 2)
+    assert targets == [2, 7]              # R = 2..11, targets R[0] and R[5]
+    assert groups == [[2, 3, 4, 5, 6], [7, 8, 9, 10, 11]]
+    assert np.array_equal(vals[0], 3.0 * e0) and np.array_equal(vals[1], 9.0 * e1)
+
+
+def test_merge_uses_the_cosine_not_the_dot_product():
+    d = 32
+    x = np.zeros((4, d))
+    x[0, 0] = 1.0                        # target 0: short, 0 degrees from the token
+    x[1, :2] = [100.0, 100.0]            # target 1: long, 45 degrees from the token
+    x[2, 0] = 1.0                        # the token: larger dot product with target 1,
+    x[2, 2] = 0.25                       #   larger cosine with target 0
+    x[3, 1] = 1.0
+    # reordered so that the targets R[0] and R[2] are the two candidate rows
+    vals, groups, targets = O.merge_context(x[[0, 2, 1, 3]], [], 2)
+    assert targets == [0, 2]              # rows 0 (short target) and 2 (long target)
+    assert groups[0] == [0, 1]            # the token (row 1) goes to the short target
+
+
+def test_merge_ties_scale_invariance_and_invariants():
+    rng = np.random.default_rng(9)
+    d = 64
+    x = rng.standard_normal((30, d)).astype(np.float32).astype(np.float64)
+    dom = [1, 5, 6, 20]
+    vals, groups, targets = O.merge_context(x, dom, 4)
+    R = [t for t in range(30) if t not in dom]
+    # every remaining token in exactly one group, each target in its own, groups ascending
+    assert sorted(t for g in groups for t in g) == R
+    for g, t in zip(groups, targets):
+        assert t in g and g == sorted(g)
+    # scaling tokens by powers of two changes no assignment (the score scales exactly)
+    xs = x.copy()
+    xs[R[3]] *= 8.0
+    xs[targets[1]] *= 0.25
+    _, groups2, _ = O.merge_context(xs, dom, 4)
+    assert groups2 == groups
+    # brute force with plain normalised dot products agrees when no two cosines are close
+    for j, g in enumerate(groups):
+        for r in g:
+            if r in targets:
+                continue
+            cos = [float(np.dot(x[r], x[t]) / np.linalg.norm(x[t])) for t in targets]
+            best = int(np.argmax(cos))
+            srt = sorted(cos, reverse=True)
+            if srt[0] - srt[1] > 1e-9:
+                assert best == j
+    # two identical targets: every token that prefers them goes to the lower one
+    xt = x.copy()
+    xt[targets[2]] = xt[targets[1]]
+    _, g3, _ = O.merge_context(xt, dom, 4)
+    assert g3[2] == [targets[2]]
+
+
+def test_compact_with_contextual_rows_layout():
+    x = np.arange(3 * 5 * 2, dtype=np.float64).reshape(3, 5, 2)
+    sysr = np.full((2, 2), -1.0)
+    qry = np.full((1, 2), -2.0)
+    ctx = np.array([[100.0, 100.0], [200.0, 200.0], [300.0, 300.0]])
+    packed, cu, pos = O.compact(x, [2, 0], np.array([0, 2, 3]), np.array([1, 4, 0]), sysr, qry,
+                                ctx_rows=ctx, ctx_offsets=np.array([0, 2, 3]))
+    expect = np.concatenate([sysr, x[2][[1, 4]], ctx[0:2], qry, sysr, x[0][[0]], ctx[2:3], qry])
+    assert np.array_equal(packed, expect)
+    assert list(cu) == [0, 7, 12] and list(pos) == list(range(7)) + list(range(5))
