@@ -6,6 +6,9 @@
  *                          (Sec. 2.3 Stage 1, Eq. 1, Listing 1, App. B Step 3)
  *   2. rift_select_tokens  per-tile dominant-token selection under elastic
  *                          budgets (Sec. 2.3 Stage 2)
+ *   (optional) rift_merge_context: the non-selected tokens of each kept
+ *                          tile merged into contextual tokens (VisionZip's
+ *                          "merge the remainder", Sec. 2.3 Stage 2)
  *   3. rift_compact        packing of each retained tile's prompt into one
  *                          varlen batch (each tile is its own VLM call,
  *                          Sec. 2.3 Stage 2 and App. B Step 5)
@@ -43,7 +46,7 @@
 extern "C" {
 #endif
 
-#define RIFT_ABI_VERSION 3
+#define RIFT_ABI_VERSION 4
 
 #if defined(__GNUC__) || defined(__clang__)
 #define RIFT_API __attribute__((visibility("default")))
@@ -212,30 +215,85 @@ RIFT_API rift_status rift_select_tokens(const double* token_key, int32_t n_tiles
                                int64_t sel_capacity, int32_t* status, rift_stream stream);
 
 /*
+ * rift_split_budgets -- [host] split each budget c into dominant and
+ * contextual tokens for rift_merge_context: k_c = min(floor(c num / den),
+ * n_v - c), k_d = c - k_c (num/den = 10/64 gives VisionZip's 54 + 10 at 64
+ * tokens; at the full budget k_c = 0).
+ * budgets [host] [n_keep] in [0, n_v];  dominant, context [host] out [n_keep]
+ * Errors: RIFT_ERR_NULL, RIFT_ERR_SHAPE (n_keep < 0, n_v < 1, num < 0,
+ * den < 1, num > den), RIFT_ERR_BUDGET (a budget out of range).
+ */
+RIFT_API rift_status rift_split_budgets(int32_t n_keep, int32_t n_v, const int32_t* budgets, int32_t num,
+                                        int32_t den, int32_t* dominant, int32_t* context);
+
+/* Workspace bytes of rift_merge_context (256-byte aligned). */
+RIFT_API size_t rift_merge_workspace_size(int32_t n_keep, int32_t n_v);
+
+/*
+ * rift_merge_context -- merge each kept tile's non-selected tokens into
+ * contextual tokens (Sec. 2.3 Stage 2: VisionZip keeps the dominant tokens and
+ * merges the remainder; the scheme is VisionZip's).  For kept tile rho with
+ * dominant tokens sel_idx[sel_offsets[rho] .. sel_offsets[rho + 1]) (from
+ * rift_select_tokens with the dominant budgets) and
+ * k_c = ctx_offsets[rho + 1] - ctx_offsets[rho]: the remainder R is the other
+ * tokens in ascending order; target j is R[floor(j |R| / k_c)]; every other
+ * token of R joins the target j of largest cdot(x_r, x_j) / |x_j| (the cosine
+ * up to 1/|x_r|, with cdot the float64 dot product in the order described for
+ * token_key and |x_j| = sqrt(cdot(x_j, x_j)), a zero token scoring 0), ties to
+ * the lower j; contextual row ctx_offsets[rho] + j is the float64 sum of the
+ * group (target and members) in ascending token order over the group size,
+ * rounded to float32 and then to dt.
+ * tokens       [n_tiles][n_v][d] dt
+ * kept_tiles, sel_offsets, sel_idx   as for rift_compact (the dominant tokens;
+ *              distinct, any order)
+ * ctx_offsets  [n_keep+1] i32       prefix sums of k_c (k_c <= n_v - k_d)
+ * ctx_rows     [ctx_capacity][d] dt out
+ * status       [1] i32 out  0, or RIFT_ERR_SHAPE if an offset, count or tile
+ *              id is out of range, ctx_offsets[n_keep] > ctx_capacity, or a
+ *              dominant index is out of range or repeated (that tile's rows are
+ *              then not written)
+ * workspace    >= rift_merge_workspace_size(n_keep, n_v) bytes, 256-aligned
+ * Shape rules: d % 32 == 0, 32 <= d <= 16384, 1 <= n_v <= 1024,
+ *              0 <= n_keep <= 65535, 0 <= ctx_capacity <= 2^24.
+ */
+RIFT_API rift_status rift_merge_context(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
+                                        int32_t d, const int32_t* kept_tiles, const int32_t* sel_offsets,
+                                        const int32_t* sel_idx, const int32_t* ctx_offsets, int32_t n_keep,
+                                        void* ctx_rows, int64_t ctx_capacity, int32_t* status,
+                                        void* workspace, size_t ws_bytes, rift_stream stream);
+
+/*
  * rift_compact -- pack every kept tile's prompt [n_sys system rows | selected
- * vision rows of the tile, ascending | n_qry query rows] into one varlen batch.
+ * vision rows of the tile, ascending | contextual rows of the tile (optional)
+ * | n_qry query rows] into one varlen batch.
  * tokens   [n_tiles][n_v][d] dt;  sys_emb [n_sys][d] dt;  qry_emb [n_qry][d] dt
  * kept_tiles, sel_offsets, sel_idx as produced for rift_select_tokens
+ * ctx_rows, ctx_offsets   optional (both NULL: none): rows of rift_merge_context
+ *              and their prefix sums [n_keep+1] per kept tile
  * packed       [packed_rows][d] dt out, total rows
- *              T = n_keep*(n_sys+n_qry) + sel_offsets[n_keep] must be <= packed_rows
+ *              T = n_keep*(n_sys+n_qry) + sel_offsets[n_keep] (+ ctx_offsets[n_keep])
+ *              must be <= packed_rows
  * cu_seqlens   [n_keep+1] i32 out  prefix sums of sequence lengths
  * position_ids [packed_rows] i32 out  0..L-1 within each sequence
  * status       [1] i32 out  0, or RIFT_ERR_SHAPE if a tile id or selected index is
- *              out of range, a budget (sel_offsets step) is outside [0, n_v],
- *              sel_offsets[0] != 0 or T > packed_rows; a bad first offset or
- *              total stops every row from being written, a bad tile id or
- *              budget the rows of that prompt (and of any prompt whose offsets
- *              reach past sel_offsets[n_keep]), a bad selected index only its
- *              own row.  sel_idx must hold sel_offsets[n_keep] entries.
+ *              out of range, a budget (sel_offsets step) is outside [0, n_v], a
+ *              ctx_offsets step is negative, a first offset is not 0 or
+ *              T > packed_rows; a bad first offset or total stops every row
+ *              from being written, a bad tile id or budget the rows of that
+ *              prompt (and of any prompt whose offsets reach past the last
+ *              offset), a bad selected index only its own row.  sel_idx must
+ *              hold sel_offsets[n_keep] entries and ctx_rows ctx_offsets[n_keep]
+ *              rows.
  * Shape rules: d * sizeof(dt) % 16 == 0; n_sys, n_qry >= 0; 0 <= n_keep <= 65535;
  *              packed_rows <= 2^25 (two waves per packed row).
  */
 RIFT_API rift_status rift_compact(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
                          int32_t d, const int32_t* kept_tiles, const int32_t* sel_offsets,
-                         const int32_t* sel_idx, int32_t n_keep, const void* sys_emb,
-                         int32_t n_sys, const void* qry_emb, int32_t n_qry, void* packed,
-                         int64_t packed_rows, int32_t* cu_seqlens, int32_t* position_ids,
-                         int32_t* status, rift_stream stream);
+                         const int32_t* sel_idx, int32_t n_keep, const void* ctx_rows,
+                         const int32_t* ctx_offsets, const void* sys_emb, int32_t n_sys,
+                         const void* qry_emb, int32_t n_qry, void* packed, int64_t packed_rows,
+                         int32_t* cu_seqlens, int32_t* position_ids, int32_t* status,
+                         rift_stream stream);
 
 /* ------------------------------------------------------------------ prefill */
 

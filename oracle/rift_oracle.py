@@ -478,16 +478,17 @@ def merge_context(x: np.ndarray, dominant: Sequence[int], k_c: int):
     inv_t = token_inv_norms(x[targets])
     groups = [[t] for t in targets]
     tset = set(targets)
-    for r in R:
-        if r in tset:
-            continue
-        g = cdot(x[targets], x[r])            # one canonical dot per target
-        a = g * inv_t
-        best = 0
-        for j in range(1, k_c):
-            if a[j] > a[best]:
-                best = j
-        groups[best].append(r)
+    others = [r for r in R if r not in tset]
+    xt = x[targets]
+    for i0 in range(0, len(others), 64):       # 64 tokens at a time, every target
+        blk = others[i0:i0 + 64]
+        a = cdot(np.repeat(x[blk][:, None, :], k_c, axis=1), xt[None, :, :]) * inv_t
+        for i, r in enumerate(blk):
+            best = 0                            # largest score, ties to the lower j
+            for j in range(1, k_c):
+                if a[i, j] > a[i, best]:
+                    best = j
+            groups[best].append(r)
     vals = np.zeros((k_c, x.shape[1]), dtype=np.float64)
     for j, grp in enumerate(groups):
         grp.sort()

@@ -26,7 +26,8 @@ RIFT_BF16 = 1
 EXPORTS = ("rift_abi_version", "rift_status_string", "rift_set_debug", "rift_check_finite",
            "rift_score_workspace_size",
            "rift_score_tiles", "rift_assign_budgets", "rift_assign_budgets_utility",
-           "rift_select_tokens", "rift_compact",
+           "rift_select_tokens", "rift_split_budgets", "rift_merge_workspace_size", "rift_merge_context",
+           "rift_compact",
            "rift_prefill_workspace_size", "rift_prefill")
 
 
@@ -82,8 +83,14 @@ def load() -> ctypes.CDLL:
     L.rift_assign_budgets_utility.argtypes = [I32, I32, I32, P, P, P, P, F64, P, P, P]
     L.rift_select_tokens.restype = I32
     L.rift_select_tokens.argtypes = [P, I32, I32, P, P, I32, P, P, I64, P, P]
+    L.rift_split_budgets.restype = I32
+    L.rift_split_budgets.argtypes = [I32, I32, P, I32, I32, P, P]
+    L.rift_merge_workspace_size.restype = SZ
+    L.rift_merge_workspace_size.argtypes = [I32, I32]
+    L.rift_merge_context.restype = I32
+    L.rift_merge_context.argtypes = [P, I32, I32, I32, I32, P, P, P, P, I32, P, I64, P, P, SZ, P]
     L.rift_compact.restype = I32
-    L.rift_compact.argtypes = [P, I32, I32, I32, I32, P, P, P, I32, P, I32, P, I32, P, I64, P, P, P, P]
+    L.rift_compact.argtypes = [P, I32, I32, I32, I32, P, P, P, I32, P, P, P, I32, P, I32, P, I64, P, P, P, P]
     L.rift_prefill_workspace_size.restype = SZ
     L.rift_prefill_workspace_size.argtypes = [ctypes.POINTER(ModelCfg), I32, I32]
     L.rift_prefill.restype = I32
@@ -244,8 +251,44 @@ def rift_select_tokens(token_key, n_tiles: int, n_v: int, kept_tiles, budgets, n
     _check(st, "rift_select_tokens")
 
 
+def rift_split_budgets(budgets, n_v: int, num: int = 10, den: int = 64):
+    """Host-only call: (dominant, context) int32 numpy arrays for budgets."""
+    import numpy as np
+    b = np.ascontiguousarray(budgets, dtype=np.int32)
+    dom = np.zeros(max(1, b.size), dtype=np.int32)
+    ctx = np.zeros(max(1, b.size), dtype=np.int32)
+    st = load().rift_split_budgets(int(b.size), int(n_v), b.ctypes.data if b.size else None, int(num), int(den),
+                                   dom.ctypes.data, ctx.ctypes.data)
+    _check(st, "rift_split_budgets")
+    return dom[:b.size].copy(), ctx[:b.size].copy()
+
+
+def rift_merge_workspace_size(n_keep: int, n_v: int) -> int:
+    return int(load().rift_merge_workspace_size(n_keep, n_v))
+
+
+def rift_merge_context(tokens, kept_tiles, sel_offsets, sel_idx, ctx_offsets, n_keep: int, ctx_rows,
+                       status, workspace, stream=None) -> None:
+    torch = _torch()
+    n_tiles, n_v, d = tokens.shape
+    dt = _dt_code(tokens)
+    _need(tokens, tokens.dtype, name="tokens")
+    _need(ctx_rows, tokens.dtype, (ctx_rows.shape[0], d), "ctx_rows")
+    _need(ctx_offsets, torch.int32, None, "ctx_offsets")
+    _need(status, torch.int32, (1,), "status")
+    _need(workspace, torch.uint8, None, "workspace")
+    if ctx_offsets.numel() < n_keep + 1 or sel_offsets.numel() < n_keep + 1:
+        raise ValueError("ctx_offsets and sel_offsets need n_keep + 1 entries")
+    st = load().rift_merge_context(_ptr(tokens), dt, n_tiles, n_v, d, _ptr(kept_tiles), _ptr(sel_offsets),
+                                   _ptr(sel_idx), _ptr(ctx_offsets), int(n_keep), _ptr(ctx_rows),
+                                   ctx_rows.shape[0], _ptr(status), _ptr(workspace), workspace.numel(),
+                                   _stream(stream))
+    _check(st, "rift_merge_context")
+
+
 def rift_compact(tokens, kept_tiles, sel_offsets, sel_idx, n_keep: int, sys_emb, qry_emb,
-                 packed, cu_seqlens, position_ids, status, stream=None) -> None:
+                 packed, cu_seqlens, position_ids, status, stream=None, ctx_rows=None,
+                 ctx_offsets=None) -> None:
     torch = _torch()
     n_tiles, n_v, d = tokens.shape
     dt = _dt_code(tokens)
@@ -258,8 +301,16 @@ def rift_compact(tokens, kept_tiles, sel_offsets, sel_idx, n_keep: int, sys_emb,
     _need(status, torch.int32, (1,), "status")
     if cu_seqlens.numel() < n_keep + 1 or sel_offsets.numel() < n_keep + 1:
         raise ValueError("cu_seqlens and sel_offsets need n_keep + 1 entries")
+    if (ctx_rows is None) != (ctx_offsets is None):
+        raise ValueError("ctx_rows and ctx_offsets go together")
+    if ctx_rows is not None:
+        _need(ctx_rows, tokens.dtype, (ctx_rows.shape[0], d), "ctx_rows")
+        _need(ctx_offsets, torch.int32, None, "ctx_offsets")
+        if ctx_offsets.numel() < n_keep + 1:
+            raise ValueError("ctx_offsets needs n_keep + 1 entries")
     st = load().rift_compact(_ptr(tokens), dt, n_tiles, n_v, d, _ptr(kept_tiles), _ptr(sel_offsets),
-                             _ptr(sel_idx), int(n_keep), _ptr(sys_emb), sys_emb.shape[0],
+                             _ptr(sel_idx), int(n_keep), _ptr(ctx_rows), _ptr(ctx_offsets),
+                             _ptr(sys_emb), sys_emb.shape[0],
                              _ptr(qry_emb), qry_emb.shape[0], _ptr(packed), packed.shape[0],
                              _ptr(cu_seqlens), _ptr(position_ids), _ptr(status), _stream(stream))
     _check(st, "rift_compact")

@@ -331,25 +331,93 @@ rift_status rift_select_tokens(const double* token_key, int32_t n_tiles, int32_t
     return hip_status(e);
 }
 
+rift_status rift_split_budgets(int32_t n_keep, int32_t n_v, const int32_t* budgets, int32_t num,
+                               int32_t den, int32_t* dominant, int32_t* context) {
+    if (n_keep > 0 && (budgets == nullptr || dominant == nullptr || context == nullptr)) return RIFT_ERR_NULL;
+    if (n_keep < 0 || n_v < 1 || num < 0 || den < 1 || num > den) return RIFT_ERR_SHAPE;
+    for (int i = 0; i < n_keep; ++i)
+        if (budgets[i] < 0 || budgets[i] > n_v) return RIFT_ERR_BUDGET;
+    for (int i = 0; i < n_keep; ++i) {
+        const int64_t c = budgets[i];
+        int64_t kc = c * num / den;
+        if (kc > n_v - c) kc = n_v - c;
+        context[i] = (int32_t)kc;
+        dominant[i] = (int32_t)(c - kc);
+    }
+    return RIFT_OK;
+}
+
+namespace {
+// merge workspace: group of each token, targets, their inverse norms, tile flags
+struct MergeLayout {
+    size_t grp, tgt, inv, ok, total;
+};
+MergeLayout merge_layout(int32_t n_keep, int32_t n_v) {
+    MergeLayout L{};
+    const size_t nk = n_keep > 0 ? (size_t)n_keep : 1;
+    size_t off = 0;
+    L.grp = off;
+    off += align_up(nk * n_v * sizeof(int));
+    L.tgt = off;
+    off += align_up(nk * n_v * sizeof(int));
+    L.inv = off;
+    off += align_up(nk * n_v * sizeof(double));
+    L.ok = off;
+    off += align_up(nk * sizeof(int));
+    L.total = off;
+    return L;
+}
+}  // namespace
+
+size_t rift_merge_workspace_size(int32_t n_keep, int32_t n_v) {
+    if (n_keep < 0 || n_v < 1) return 0;
+    return merge_layout(n_keep, n_v).total;
+}
+
+rift_status rift_merge_context(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
+                               int32_t d, const int32_t* kept_tiles, const int32_t* sel_offsets,
+                               const int32_t* sel_idx, const int32_t* ctx_offsets, int32_t n_keep,
+                               void* ctx_rows, int64_t ctx_capacity, int32_t* status,
+                               void* workspace, size_t ws_bytes, rift_stream stream) {
+    if (sel_offsets == nullptr || ctx_offsets == nullptr || status == nullptr || workspace == nullptr)
+        return RIFT_ERR_NULL;
+    if (n_keep > 0 && (tokens == nullptr || kept_tiles == nullptr || sel_idx == nullptr)) return RIFT_ERR_NULL;
+    if (ctx_capacity > 0 && ctx_rows == nullptr) return RIFT_ERR_NULL;
+    if (!dt_valid(dt)) return RIFT_ERR_DTYPE;
+    if (n_tiles < 1 || n_v < 1 || n_v > 1024 || d < 32 || d > 16384 || d % 32 != 0 || n_keep < 0 ||
+        n_keep > 65535 || ctx_capacity < 0 || ctx_capacity > ((int64_t)1 << 24))
+        return RIFT_ERR_SHAPE;
+    const MergeLayout L = merge_layout(n_keep, n_v);
+    if (misaligned(workspace) || ws_bytes < L.total) return RIFT_ERR_WORKSPACE;
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    hipError_t e = launch_merge(tokens, dt == RIFT_BF16, n_tiles, n_v, d, kept_tiles, sel_offsets, sel_idx,
+                                ctx_offsets, n_keep, ctx_rows, ctx_capacity, status,
+                                reinterpret_cast<int*>(ws + L.grp), reinterpret_cast<int*>(ws + L.tgt),
+                                reinterpret_cast<double*>(ws + L.inv), reinterpret_cast<int*>(ws + L.ok),
+                                static_cast<hipStream_t>(stream));
+    return hip_status(e);
+}
+
 rift_status rift_compact(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
                          int32_t d, const int32_t* kept_tiles, const int32_t* sel_offsets,
-                         const int32_t* sel_idx, int32_t n_keep, const void* sys_emb,
-                         int32_t n_sys, const void* qry_emb, int32_t n_qry, void* packed,
-                         int64_t packed_rows, int32_t* cu_seqlens, int32_t* position_ids,
-                         int32_t* status, rift_stream stream) {
+                         const int32_t* sel_idx, int32_t n_keep, const void* ctx_rows,
+                         const int32_t* ctx_offsets, const void* sys_emb, int32_t n_sys,
+                         const void* qry_emb, int32_t n_qry, void* packed, int64_t packed_rows,
+                         int32_t* cu_seqlens, int32_t* position_ids, int32_t* status,
+                         rift_stream stream) {
     if (sel_offsets == nullptr || cu_seqlens == nullptr || status == nullptr) return RIFT_ERR_NULL;
     if (n_keep > 0 && (tokens == nullptr || kept_tiles == nullptr)) return RIFT_ERR_NULL;
     if (packed_rows > 0 && (packed == nullptr || position_ids == nullptr)) return RIFT_ERR_NULL;
     if ((n_sys > 0 && sys_emb == nullptr) || (n_qry > 0 && qry_emb == nullptr)) return RIFT_ERR_NULL;
+    if ((ctx_rows == nullptr) != (ctx_offsets == nullptr)) return RIFT_ERR_NULL;
     if (!dt_valid(dt)) return RIFT_ERR_DTYPE;
     if (n_tiles < 1 || n_v < 1 || d < 1 || n_keep < 0 || n_keep > 65535 || n_sys < 0 || n_qry < 0 ||
         packed_rows < 0 || ((size_t)d * dt_bytes(dt)) % 16 != 0 || packed_rows > ((int64_t)1 << 25))
         return RIFT_ERR_SHAPE;
     hipError_t e = launch_compact(tokens, (int)dt_bytes(dt), n_tiles, n_v, d, kept_tiles,
-                                  sel_offsets, sel_idx, n_keep, sys_emb, n_sys, qry_emb, n_qry,
-                                  packed, packed_rows, cu_seqlens, position_ids, status,
+                                  sel_offsets, sel_idx, n_keep, ctx_rows, ctx_offsets, sys_emb, n_sys,
+                                  qry_emb, n_qry, packed, packed_rows, cu_seqlens, position_ids, status,
                                   static_cast<hipStream_t>(stream));
-    (void)sel_idx;
     return hip_status(e);
 }
 

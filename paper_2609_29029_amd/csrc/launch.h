@@ -27,10 +27,19 @@ hipError_t launch_select(const double* token_key, int n_tiles, int n_v, const in
                          const int* budgets, int n_keep, int* sel_offsets, int* sel_idx,
                          long long cap, int* status, hipStream_t st);
 
+// ctx / coffs: optional contextual rows and their per-prompt offsets (nullptr: none)
 hipError_t launch_compact(const void* tokens, int elem_bytes, int n_tiles, int n_v, int d,
                           const int* kept, const int* offs, const int* sel, int n_keep,
-                          const void* sys, int n_sys, const void* qry, int n_qry, void* packed,
-                          long long cap, int* cu, int* pos_ids, int* status, hipStream_t st);
+                          const void* ctx, const int* coffs, const void* sys, int n_sys,
+                          const void* qry, int n_qry, void* packed, long long cap, int* cu,
+                          int* pos_ids, int* status, hipStream_t st);
+
+// optional merge of the remainder into contextual tokens; workspace arrays
+// grp, tgt [n_keep][n_v] int, inv [n_keep][n_v] double, ok [n_keep] int
+hipError_t launch_merge(const void* tokens, bool bf16, int n_tiles, int n_v, int d, const int* kept,
+                        const int* offs, const int* sel, const int* coffs, int n_keep, void* ctx_rows,
+                        long long ctx_cap, int* status, int* grp, int* tgt, double* inv, int* ok,
+                        hipStream_t st);
 
 // ---------------------------------------------------------------- prefill pieces
 // RoPE table: tab[p * (hd/2) + j] = (cos, sin)(p * base^(-2j/hd)), p < n_pos.

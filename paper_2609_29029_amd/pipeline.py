@@ -1,5 +1,5 @@
-"""One Rift scene-query on the GPU: score -> budgets -> select -> compact ->
-prefill, enqueued on one stream through the C ABI.  Buffers are allocated once
+"""One Rift scene-query on the GPU: score -> budgets -> select -> (merge) ->
+compact -> prefill, enqueued on one stream through the C ABI.  Buffers are allocated once
 per plan (PyTorch as the allocator) and reused across queries.
 
 In keep-top-K mode with rank-tier budgets the number of kept tiles, the
@@ -7,7 +7,9 @@ budgets and the packed length are known on the host before the query runs, so
 the whole query is enqueued without a device-to-host copy.  Threshold mode
 (keep_count == 0) reads n_keep back once after scoring; the Eq. 2 utility
 policy reads the kept tiles' normalised scores back once (they stand in for the
-object probability p) and assigns budgets on the host.
+object probability p) and assigns budgets on the host.  With `merge`, each
+budget is split into dominant and contextual tokens (VisionZip's merge of the
+remainder); the prompt length stays the budget.
 """
 from __future__ import annotations
 
@@ -37,7 +39,8 @@ class SceneQuery:
     def __init__(self, tokens, qbank, sys_emb, qry_emb, layers: Sequence[dict],
                  shape: PrefillShape, keep_count: int, tau: float, levels: Sequence[int],
                  tier_num: Optional[Sequence[int]], tier_den: int, with_sims: bool = True,
-                 stream=None, knn_m: int = 0, utility: Optional[dict] = None):
+                 stream=None, knn_m: int = 0, utility: Optional[dict] = None,
+                 merge: Optional[Sequence[int]] = None):
         import torch
         self.torch = torch
         self.dev = tokens.device
@@ -50,6 +53,8 @@ class SceneQuery:
         self.knn_m = int(knn_m)
         # utility: dict(levels, alpha_pos, alpha_neg, energy, lam) for the Eq. 2 policy
         self.utility = utility
+        # merge: (num, den) of the contextual share of each budget, or None
+        self.merge = None if merge is None else (int(merge[0]), int(merge[1]))
         n_tiles, n_v, d = tokens.shape
         self.n_tiles, self.n_v, self.d = n_tiles, n_v, d
         nq = qbank.shape[0]
@@ -65,6 +70,7 @@ class SceneQuery:
                                     dtype=torch.uint8, device=dev)
         self.sel_status = torch.empty(1, dtype=i32, device=dev)
         self.cmp_status = torch.empty(1, dtype=i32, device=dev)
+        self.mrg_status = torch.zeros(1, dtype=i32, device=dev)
         self.cfg = R.model_cfg(shape.d, shape.n_heads, shape.head_dim, shape.ffn, shape.n_layers,
                                shape.rms_eps, shape.rope_base,
                                R.RIFT_BF16 if tokens.dtype == torch.bfloat16 else R.RIFT_F32)
@@ -87,13 +93,29 @@ class SceneQuery:
             total = int(budgets.sum())
         self.n_keep = n_keep
         self.budgets_host = budgets
-        self.n_selected = total
+        self.n_selected = total      # vision tokens per query (dominant + contextual)
+        if self.merge is not None:
+            dom, ctx = R.rift_split_budgets(budgets, self.n_v, *self.merge)
+        else:
+            dom, ctx = budgets, np.zeros(len(budgets), dtype=np.int32)
+        self.n_dominant, self.n_context = int(dom.sum()), int(ctx.sum())
         fixed = self.sys.shape[0] + self.qry.shape[0]
         self.total_tokens = n_keep * fixed + total
         self.max_seqlen = fixed + (int(budgets.max()) if n_keep > 0 else 0)
         dev = self.dev
         self.budgets = torch.from_numpy(budgets).to(dev) if n_keep > 0 else \
             torch.zeros(1, dtype=torch.int32, device=dev)
+        # the budgets select works with: the dominant share when merging
+        self.sel_budgets = torch.from_numpy(np.ascontiguousarray(dom, dtype=np.int32)).to(dev) \
+            if n_keep > 0 else torch.zeros(1, dtype=torch.int32, device=dev)
+        if self.merge is not None:
+            coffs = np.concatenate([[0], np.cumsum(ctx)]).astype(np.int32)
+            self.ctx_offsets = torch.from_numpy(coffs).to(dev)
+            self.ctx_rows = torch.empty(max(1, self.n_context), self.d, dtype=self.tokens.dtype, device=dev)
+            mws = max(256, R.rift_merge_workspace_size(n_keep, self.n_v))
+            if mws > getattr(self, "_mws_cap", 0):
+                self.merge_ws = torch.empty(mws, dtype=torch.uint8, device=dev)
+                self._mws_cap = mws
         # buffers grow to the largest plan seen and are reused
         T, P = self.total_tokens, max(1, self.max_seqlen)
         if n_keep + 1 > self._cap[0] or T > self._cap[1] or self._planned_keep is None:
@@ -124,14 +146,24 @@ class SceneQuery:
                            self.n_keep_dev, self.score_ws, self.stream, knn_m=self.knn_m)
 
     def select(self) -> None:
-        R.rift_select_tokens(self.token_key, self.n_tiles, self.n_v, self.tile_order, self.budgets,
-                             self.n_keep, self.sel_offsets, self.sel_idx[:max(1, self.n_selected)],
+        R.rift_select_tokens(self.token_key, self.n_tiles, self.n_v, self.tile_order, self.sel_budgets,
+                             self.n_keep, self.sel_offsets, self.sel_idx[:max(1, self.n_dominant)],
                              self.sel_status, self.stream)
 
+    def merge_context(self) -> None:
+        if self.merge is None:
+            return
+        R.rift_merge_context(self.tokens, self.tile_order, self.sel_offsets, self.sel_idx,
+                             self.ctx_offsets, self.n_keep, self.ctx_rows[:self.n_context],
+                             self.mrg_status, self.merge_ws, self.stream)
+
     def compact(self) -> None:
+        merging = self.merge is not None
         R.rift_compact(self.tokens, self.tile_order, self.sel_offsets, self.sel_idx, self.n_keep,
                        self.sys, self.qry, self.packed, self.cu_seqlens, self.position_ids,
-                       self.cmp_status, self.stream)
+                       self.cmp_status, self.stream,
+                       ctx_rows=self.ctx_rows if merging else None,
+                       ctx_offsets=self.ctx_offsets if merging else None)
 
     def prefill(self, events=None) -> None:
         if self.total_tokens == 0:
@@ -163,9 +195,14 @@ class SceneQuery:
             else:
                 self._plan(int(self.n_keep_dev.item()))
         self.select()
+        self.merge_context()
         self.compact()
         self.prefill()
 
     def check_status(self) -> List[int]:
-        """Device status words of select and compact (synchronises)."""
-        return [int(self.sel_status.item()), int(self.cmp_status.item())]
+        """Device status words of select and compact, and of the merge when
+        it runs (synchronises)."""
+        st = [int(self.sel_status.item()), int(self.cmp_status.item())]
+        if self.merge is not None:
+            st.append(int(self.mrg_status.item()))
+        return st

@@ -33,11 +33,11 @@ def declared_symbols():
 def test_library_exports_every_declared_symbol(R):
     L = R.load()
     names = declared_symbols()
-    assert len(names) == 12
+    assert len(names) == 15
     assert tuple(names) == R.EXPORTS
     for n in names:
         assert hasattr(L, n), n
-    assert L.rift_abi_version() == 3
+    assert L.rift_abi_version() == 4
     assert L.rift_status_string(4).decode().startswith("budget")
 
 
@@ -121,13 +121,13 @@ def test_select_and_compact_validation(R):
     assert L.rift_select_tokens(FAKE, 4, 576, FAKE, FAKE, 2, FAKE, FAKE, 1 << 31, FAKE, None) == 2
     # compact
     c = L.rift_compact
-    assert c(FAKE, 1, 4, 576, 4096, FAKE, None, FAKE, 2, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 1
-    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, 2, None, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 1
-    assert c(FAKE, 9, 4, 576, 4096, FAKE, FAKE, FAKE, 2, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 3
-    assert c(FAKE, 1, 4, 576, 4, FAKE, FAKE, FAKE, 2, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 2
-    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, -1, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 2
+    assert c(FAKE, 1, 4, 576, 4096, FAKE, None, FAKE, 2, None, None, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 1
+    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, 2, None, None, None, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 1
+    assert c(FAKE, 9, 4, 576, 4096, FAKE, FAKE, FAKE, 2, None, None, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 3
+    assert c(FAKE, 1, 4, 576, 4, FAKE, FAKE, FAKE, 2, None, None, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 2
+    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, -1, None, None, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 2
     # two waves per packed row: at most 2^25 rows
-    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, 2, FAKE, 35, FAKE, 32, FAKE, (1 << 25) + 1, FAKE, FAKE, FAKE,
+    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, 2, None, None, FAKE, 35, FAKE, 32, FAKE, (1 << 25) + 1, FAKE, FAKE, FAKE,
              None) == 2
 
 
@@ -207,3 +207,35 @@ def test_check_finite_validation_and_debug_switch(R):
     prev = L.rift_set_debug(1)
     assert L.rift_set_debug(0) == 1
     assert L.rift_set_debug(prev) == 0
+
+
+
+def test_split_budgets_and_merge_validation(R):
+    """rift_split_budgets against the oracle's split; rift_merge_context
+    rejects bad arguments on the host (nothing launched)."""
+    b = [0, 1, 64, 128, 144, 288, 575, 576]
+    dom, ctx = R.rift_split_budgets(b, 576)
+    for c, kd, kc in zip(b, dom, ctx):
+        assert (kd, kc) == O.split_budget(c, 576)
+    dom, ctx = R.rift_split_budgets(b, 576, 0, 1)          # no merge: everything dominant
+    assert list(dom) == b and not ctx.any()
+    L = R.load()
+    arr = (ctypes.c_int32 * 2)(5, 700)
+    out = (ctypes.c_int32 * 2)()
+    assert L.rift_split_budgets(2, 576, arr, 10, 64, out, out) == 4      # 700 > n_v
+    assert L.rift_split_budgets(2, 576, arr, 65, 64, out, out) == 2      # num > den
+    assert L.rift_split_budgets(2, 576, None, 10, 64, out, out) == 1
+    assert R.rift_merge_workspace_size(100, 576) >= 100 * 576 * 16
+    m = L.rift_merge_context
+    ws = R.rift_merge_workspace_size(2, 576)
+    assert m(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, FAKE, 2, FAKE, 10, FAKE, None, ws, None) == 1   # no workspace
+    assert m(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, None, 2, FAKE, 10, FAKE, 4096, ws, None) == 1  # no ctx_offsets
+    assert m(FAKE, 1, 4, 576, 4016, FAKE, FAKE, FAKE, FAKE, 2, FAKE, 10, FAKE, 4096, ws, None) == 2  # d % 32
+    assert m(FAKE, 1, 4, 2000, 4096, FAKE, FAKE, FAKE, FAKE, 2, FAKE, 10, FAKE, 4096, ws, None) == 2  # n_v
+    assert m(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, FAKE, 2, FAKE, 10, FAKE, 4096, ws - 1, None) == 5
+    assert m(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, FAKE, 2, FAKE, 10, FAKE, 4097, ws, None) == 5  # misaligned
+    assert m(FAKE, 7, 4, 576, 4096, FAKE, FAKE, FAKE, FAKE, 2, FAKE, 10, FAKE, 4096, ws, None) == 3
+    # compact: contextual rows and offsets go together
+    c = L.rift_compact
+    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, 2, FAKE, None, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE,
+             FAKE, None) == 1
