@@ -354,6 +354,43 @@ def utility_run(R, torch, w, tokens, qbank, sysd, qryd, layers, q, reps=3) -> di
             "budgets": {int(l): int(c) for l, c in zip(levels, counts)}}
 
 
+def merge_run(R, torch, w, tokens, qbank, sysd, qryd, layers, q, reps=3) -> dict:
+    """The scene-query with each budget split into dominant and contextual
+    tokens (VisionZip's merge of the remainder, 54 + 10 at 64): the same
+    prompt lengths, plus the merge.  Median device time of the merge call and
+    of the whole query over `reps` queries; the merge's float64 work is the
+    canonical dot of every non-target remaining token with every target."""
+    from paper_2609_29029_amd.pipeline import SceneQuery
+    mq = SceneQuery(tokens, qbank, sysd, qryd, layers, q.shape, w.keep_count, w.tau, w.levels,
+                    w.tier_num, w.tier_den, with_sims=True, merge=(10, 64))
+    mq.run()
+    torch.cuda.synchronize()
+    tm, tq = [], []
+    for _ in range(reps):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record()
+        mq.score()
+        mq.select()
+        ev[1].record()
+        mq.merge_context()
+        ev[2].record()
+        mq.compact()
+        mq.prefill()
+        ev[3].record()
+        torch.cuda.synchronize()
+        tm.append(ev[1].elapsed_time(ev[2]))
+        tq.append(ev[0].elapsed_time(ev[3]))
+    assert mq.check_status() == [0, 0, 0]
+    dom, ctx = R.rift_split_budgets(mq.budgets_host, w.n_v)
+    fma = sum(int(w.n_v - kd - kc) * int(kc) * w.model.d for kd, kc in zip(dom, ctx) if kc > 1)
+    ms = statistics.median(tm)
+    return {"ms_per_query": round(statistics.median(tq), 2), "merge_ms": round(ms, 4),
+            "dominant_tokens": int(mq.n_dominant), "contextual_tokens": int(mq.n_context),
+            "retained_vision_tokens": int(mq.n_selected),
+            "fp64_fma": fma, "fp64_TFLOPs": round(2 * fma / (ms * 1e-3) / 1e12, 2),
+            "frac_fp64_vector_peak": round(2 * fma / (ms * 1e-3) / 1e12 / 78.6, 4)}
+
+
 def select_batched(R, torch, token_key, order, budgets, n_tiles, n_v, n_keep, copies=64, reps=10) -> dict:
     """rift_select_tokens over `copies` scene-queries' keys at once (one call),
     for a bandwidth-meaningful number; median of `reps` timed calls."""
@@ -552,6 +589,7 @@ def main() -> int:
     kn["extra_ms_over_plain_score"] = round(kn["score_ms"] - stage_ms["score"], 4)
     out["knn_smoothing"] = kn
     out["utility_policy"] = utility_run(R, torch, w, tokens, qbank, sysd, qryd, layers, q)
+    out["contextual_merge"] = merge_run(R, torch, w, tokens, qbank, sysd, qryd, layers, q)
     out["select_batched"] = select_batched(R, torch, q.token_key, q.tile_order, q.budgets, w.n_tiles,
                                            w.n_v, q.n_keep)
     if not args.no_exhaustive:

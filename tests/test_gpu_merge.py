@@ -142,3 +142,27 @@ def test_scene_query_with_merge_packs_the_oracle_batch(R):
     assert np.array_equal(q.position_ids.cpu().numpy(), r_pos)
     assert np.array_equal(np.diff(r_cu), np.asarray(budgets) + w.n_sys + w.n_qry)
     assert bool(torch.isfinite(q.hidden).all())
+
+
+@pytest.mark.slow
+def test_merge_full_size_sampled(R):
+    """The 400-tile scene: 100 kept tiles (the first 100 ids) at the rank-tier
+    budgets, dominant tokens from the oracle's keys of those tiles; the merge
+    runs on all 100 and the contextual rows of one tile per budget tier are
+    checked bit for bit."""
+    w = synth.get("scene20")
+    sc = synth.make_scene(w)
+    kept = list(range(100))
+    X64 = f64(sc.tokens[:100], w.dtype)
+    w32 = O.query_direction(f64(sc.qbank, w.dtype))
+    r = O.token_keys(X64.reshape(-1, X64.shape[-1]), w32).reshape(100, w.n_v)
+    budgets = O.assign_budgets(100, w.levels, w.tier_num, w.tier_den)
+    split = [O.split_budget(int(c), w.n_v) for c in budgets]
+    kc = [s[1] for s in split]
+    offs, sel = O.select_tokens(r, kept, [s[0] for s in split])
+    got, coffs, st = run_merge(R, sc.tokens, w.dtype, kept, offs, sel, kc)
+    assert st == 0 and got.shape[0] == sum(kc)
+    for rho in (0, 6, 24, 99):   # budgets 576, 288, 144, 64
+        exp = oracle_ctx(sc.tokens, w.dtype, [rho], offs[rho:rho + 2] - offs[rho], sel[offs[rho]:offs[rho + 1]],
+                         [kc[rho]])
+        assert np.array_equal(got[coffs[rho]:coffs[rho + 1]], exp), rho
