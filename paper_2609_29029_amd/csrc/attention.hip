@@ -2,8 +2,11 @@
 // an independent sequence; Sec. 2.3 Stage 2).  Query i of a sequence attends
 // to keys 0..i of the same sequence, scale 1/sqrt(head_dim).
 //
-// bf16, head_dim 128, on MFMA.  One workgroup (4 waves) per (sequence, head,
-// 128-query block); wave w owns queries [32 w, 32 w + 32) of the block.  Keys
+// bf16, head_dim 128, on MFMA.  One workgroup (4 waves) per (sequence, head),
+// looping over the sequence's 128-query blocks (no workgroup is launched for a
+// block past the end of a short prompt; workgroups are numbered sequence by
+// sequence, so prompts packed longest first start first); wave w owns queries
+// [32 w, 32 w + 32) of the block.  Keys
 // and values stream through two LDS buffers 64 at a time, both row-major; the
 // next block's rows are loaded into registers while the current one is used.
 // The wave computes S^T = K Q^T (v_mfma_f32_32x32x16_bf16, M = keys,
@@ -40,19 +43,14 @@ __device__ __forceinline__ v4s_t lds_read_tr16(const bf16_t* p) {
 __global__ void __launch_bounds__(256, 2)
 attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
                  const bf16_t* __restrict__ v, bf16_t* __restrict__ o,
-                 const int* __restrict__ cu, int n_seq, int nqb, int H, float scale_log2) {
+                 const int* __restrict__ cu, int n_seq, int H, float scale_log2) {
     __shared__ __align__(16) bf16_t Ks[2][BKV * KPAD];
     __shared__ __align__(16) bf16_t Vs[2][BKV * VPAD];
 
-    const int bid = blockIdx.x;
-    const int qb = nqb - 1 - (bid % nqb);  // heaviest (last) query blocks first
-    const int rest = bid / nqb;
-    const int seq = rest % n_seq;
-    const int head = rest / n_seq;
+    const int seq = blockIdx.x / H;
+    const int head = blockIdx.x % H;
     const int s0 = cu[seq];
     const int L = cu[seq + 1] - s0;
-    const int q0 = qb * BQ;
-    if (q0 >= L) return;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -62,6 +60,10 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
     const int ld = H * HD;
     const size_t head_off = (size_t)head * HD;
 
+    // query blocks, the longest-running (last) first
+    for (int qb = (L + BQ - 1) / BQ - 1; qb >= 0; --qb) {
+    const int q0 = qb * BQ;
+    __syncthreads();   // the previous block's reads of the K/V buffers are done
     const int qw = q0 + wave * 32;            // first query of this wave
     const int qidx = qw + col;                // this lane's query
     const int q_eff = qidx < L ? qidx : L - 1;
@@ -124,24 +126,38 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
         const int cur = kb_i & 1;
         if (kb_i + 1 < nkv) load_block(kv0 + BKV);
         if (kv0 <= wave_last) {
-            // scores for two 32-key sub-blocks
+            // scores for two 32-key sub-blocks; their MFMA chains interleaved
+            f32x16_t s[2];
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 16; ++i) s[kb][i] = 0.f;
+#pragma unroll
+            for (int kk = 0; kk < 8; ++kk)
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb) {
+                    const bf16x8_t kf =
+                        *reinterpret_cast<const bf16x8_t*>(&Ks[cur][(kb * 32 + col) * KPAD + 8 * h + 16 * kk]);
+                    s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
+                }
+            // raw scores; keys past a query are masked only in blocks that
+            // cross the wave's diagonal.  The running max is kept on the raw
+            // scale (scale_log2 > 0 commutes with max), and p = 2^(s scale - m)
+            // takes one fma and the hardware exp2 (its flush of results below
+            // 2^-126 to zero drops terms far below the row sum's precision).
             float sc[2][16];
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                f32x16_t s;
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) s[i] = 0.f;
-                const bf16_t* krow = &Ks[cur][(kb * 32 + col) * KPAD + 8 * h];
+                for (int i = 0; i < 16; ++i) sc[kb][i] = s[kb][i];
+            if (kv0 + BKV - 1 > qw) {
 #pragma unroll
-                for (int kk = 0; kk < 8; ++kk) {
-                    const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(krow + 16 * kk);
-                    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s, 0, 0, 0);
-                }
+                for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int key = kv0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-                    sc[kb][i] = (key <= q_eff) ? s[i] * scale_log2 : -INFINITY;
-                }
+                    for (int i = 0; i < 16; ++i) {
+                        const int key = kv0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+                        sc[kb][i] = (key <= q_eff) ? sc[kb][i] : -INFINITY;
+                    }
             }
             float bmax = -INFINITY;
 #pragma unroll
@@ -149,24 +165,29 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
 #pragma unroll
                 for (int i = 0; i < 16; ++i) bmax = fmaxf(bmax, sc[kb][i]);
             bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
-            const float m_new = fmaxf(m_run, bmax);
-            const float alpha = exp2f(m_run - m_new);
+            const float m_new = fmaxf(m_run, bmax * scale_log2);
+            const float neg_m = -m_new;
             float rsum = 0.f;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
-                    const float pv = exp2f(sc[kb][i] - m_new);
+                    const float pv = __builtin_amdgcn_exp2f(fmaf(sc[kb][i], scale_log2, neg_m));
                     sc[kb][i] = pv;
                     rsum += pv;
                 }
             rsum += __shfl_xor(rsum, 32);
-            l_run = l_run * alpha + rsum;
+            // rescale the sums only when some query's max moved (exact skip)
+            if (__any(m_new != m_run)) {
+                const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+                l_run *= alpha;
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) oacc[t][i] *= alpha;
+            }
+            l_run += rsum;
             m_run = m_new;
-#pragma unroll
-            for (int t = 0; t < 4; ++t)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) oacc[t][i] *= alpha;
 
             // O^T += V^T P^T.  MFMA step ks of sub-block kb contracts keys
             // 16 ks + 4 h + {0..3} (slots 0..3) and 16 ks + 8 + 4 h + {0..3}
@@ -198,16 +219,18 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
         __syncthreads();
     }
 
-    if (qidx >= L) return;
-    const float inv = 1.0f / l_run;
-    bf16_t* orow = o + (size_t)(s0 + qidx) * ld + head_off;
+    if (qidx < L) {
+        const float inv = 1.0f / l_run;
+        bf16_t* orow = o + (size_t)(s0 + qidx) * ld + head_off;
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+        for (int t = 0; t < 4; ++t)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            const int dcol = t * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-            orow[dcol] = f32_to_bf16(oacc[t][i] * inv);
-        }
+            for (int i = 0; i < 16; ++i) {
+                const int dcol = t * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+                orow[dcol] = f32_to_bf16(oacc[t][i] * inv);
+            }
+    }
+    }   // query blocks
 }
 
 template <int D>
@@ -253,11 +276,10 @@ hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uin
                                  uint16_t* o, const int* cu, int n_seq, int max_seqlen,
                                  int n_heads, hipStream_t st) {
     if (n_seq <= 0 || max_seqlen <= 0) return hipSuccess;
-    const int nqb = (max_seqlen + BQ - 1) / BQ;
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)HD);
-    const long long blocks = (long long)nqb * n_seq * n_heads;
+    const long long blocks = (long long)n_seq * n_heads;
     hipLaunchKernelGGL(attn_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, st, q, k, v, o, cu,
-                       n_seq, nqb, n_heads, scale_log2);
+                       n_seq, n_heads, scale_log2);
     return hipGetLastError();
 }
 
