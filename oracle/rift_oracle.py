@@ -53,6 +53,10 @@ Readings of points the paper leaves open (numbered as in the design notes):
       largest U, ties to the smaller c.  p_i, the trained predictor's
       probability that the tile holds the object, is out of scope: callers
       pass it (the pipeline passes the tile's normalised score u_i).
+  R15 Decode after prefill: each generated token's input embedding is
+      given; token t of a prompt of length L sits at position L + t and
+      attends causally to the prompt and the earlier generated tokens (the
+      decoder layers of R10, no vocabulary projection).
   R14 Optional merge of the remainder into contextual tokens (Sec. 2.3
       Stage 2: VisionZip keeps the dominant tokens "and merges the remainder";
       the merge follows VisionZip's published scheme).  A budget c splits into
@@ -361,6 +365,27 @@ def prefill(packed: np.ndarray, cu_seqlens: np.ndarray, position_ids: np.ndarray
             pos = position_ids[cu_seqlens[i]:cu_seqlens[i + 1]]
             xs[i] = decoder_layer(xs[i], W, n_heads, head_dim, eps, rope_base, pos)
     return xs
+
+
+def decode_outputs(prompt: np.ndarray, new_tokens: np.ndarray,
+                   layers: Sequence[Dict[str, np.ndarray]], n_heads: int, head_dim: int,
+                   eps: float, rope_base: float) -> np.ndarray:
+    """Residual stream after the last layer of each generated token of one
+    prompt: token t (input embedding new_tokens[t], position L + t) attends
+    causally to the prompt and to the tokens before it, so its output is the
+    last row of the decoder stack run on [prompt | new_tokens[:t + 1]] (the
+    prompt rows of that run equal the prompt's own prefill).  prompt: [L, d],
+    new_tokens: [S, d]; returns [S, d]."""
+    prompt = np.asarray(prompt, dtype=np.float64)
+    new_tokens = np.asarray(new_tokens, dtype=np.float64)
+    out = []
+    for t in range(new_tokens.shape[0]):
+        x = np.concatenate([prompt, new_tokens[:t + 1]], axis=0)
+        pos = np.arange(x.shape[0])
+        for W in layers:
+            x = decoder_layer(x, W, n_heads, head_dim, eps, rope_base, pos)
+        out.append(x[-1])
+    return np.stack(out) if out else np.zeros((0, prompt.shape[1]))
 
 
 # ============================================================================ whole query

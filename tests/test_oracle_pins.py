@@ -616,3 +616,42 @@ def test_compact_with_contextual_rows_layout():
     expect = np.concatenate([sysr, x[2][[1, 4]], ctx[0:2], qry, sysr, x[0][[0]], ctx[2:3], qry])
     assert np.array_equal(packed, expect)
     assert list(cu) == [0, 7, 12] and list(pos) == list(range(7)) + list(range(5))
+
+
+# ------------------------------------------------------------------ decode (R15)
+
+
+def _small_layer(rng, d, ffn):
+    W = {k: rng.standard_normal(sh) * 0.1 for k, sh in
+         (("wq", (d, d)), ("wk", (d, d)), ("wv", (d, d)), ("wo", (d, d)),
+          ("w_gate", (ffn, d)), ("w_up", (ffn, d)), ("w_down", (d, ffn)))}
+    W["g_attn"] = np.ones(d)
+    W["g_ffn"] = np.ones(d)
+    return W
+
+
+def test_decode_is_incremental_prefill_and_causal():
+    """Decoding token by token gives what a prefill of the whole extended
+    sequence gives on its last rows (causality: appending tokens changes no
+    earlier row), and the prompt rows of the extended run equal the prompt's
+    own prefill."""
+    rng = np.random.default_rng(17)
+    d, H, hd, ffn = 32, 4, 8, 48
+    layers = [_small_layer(rng, d, ffn) for _ in range(2)]
+    prompt = rng.standard_normal((7, d))
+    new = rng.standard_normal((3, d))
+    out = O.decode_outputs(prompt, new, layers, H, hd, 1e-6, 10000.0)
+    full = np.concatenate([prompt, new])
+    x = full.copy()
+    for W in layers:
+        x = O.decoder_layer(x, W, H, hd, 1e-6, 10000.0, np.arange(10))
+    assert np.allclose(out, x[7:], rtol=0, atol=1e-12)
+    xp = prompt.copy()
+    for W in layers:
+        xp = O.decoder_layer(xp, W, H, hd, 1e-6, 10000.0, np.arange(7))
+    assert np.allclose(x[:7], xp, rtol=0, atol=1e-12)
+    # a changed later token leaves the earlier generated outputs unchanged
+    new2 = new.copy()
+    new2[2] += 1.0
+    out2 = O.decode_outputs(prompt, new2, layers, H, hd, 1e-6, 10000.0)
+    assert np.array_equal(out2[:2], out[:2]) and not np.allclose(out2[2], out[2])
