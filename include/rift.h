@@ -14,7 +14,10 @@
  *                          Sec. 2.3 Stage 2 and App. B Step 5)
  *   4. rift_prefill        LLaMA-7B-shaped decoder prefill of the packed
  *                          prompts (Sec. 2.1; LLaVA-1.5-7B, Sec. 3)
- * plus the host-side budget assignment rift_assign_budgets.
+ * plus the host-side budget assignment rift_assign_budgets, and
+ *   5. rift_decode_step    one generated token per prompt after the prefill,
+ *                          reusing the prefill's key/value cache (the answers
+ *                          are a few words, Sec. 2.2).
  *
  * Conventions shared by every call
  *   - Pointers are DEVICE pointers unless the comment says [host].
@@ -46,7 +49,7 @@
 extern "C" {
 #endif
 
-#define RIFT_ABI_VERSION 4
+#define RIFT_ABI_VERSION 5
 
 #if defined(__GNUC__) || defined(__clang__)
 #define RIFT_API __attribute__((visibility("default")))
@@ -363,6 +366,38 @@ RIFT_API rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_we
                          int32_t max_seqlen, float* hidden_out, void* kv_cache,
                          void* workspace, size_t ws_bytes, void* const* events,
                          rift_stream stream);
+
+/*
+ * rift_decode_workspace_size -- bytes of workspace for rift_decode_step.
+ */
+RIFT_API size_t rift_decode_workspace_size(const rift_model_cfg* cfg, int32_t n_seq, int32_t max_seqlen,
+                                           int32_t max_new);
+
+/*
+ * rift_decode_step -- one generated token per prompt after rift_prefill: the
+ * token `step` of prompt i (input embedding row i of x_new) sits at position
+ * L_i + step, L_i = cu_seqlens[i+1] - cu_seqlens[i], and attends causally to
+ * the prompt's keys and values (kv_cache, as rift_prefill wrote it for these
+ * cu_seqlens) and to those of the prompt's tokens 0..step, which this call and
+ * the earlier steps keep in kv_new.  Same decoder layers as rift_prefill;
+ * bfloat16 models only.  Decode attention keeps scores and probabilities in
+ * float32 (the prefill rounds probabilities to bf16 for its MFMA).
+ * x_new       [n_seq][d] bf16   input embeddings of this step's tokens
+ * cu_seqlens  [n_seq+1] i32     the prefill's prompt offsets
+ * kv_cache    [n_layers][2][total_tokens][d] bf16 (rift_prefill's kv_cache)
+ * kv_new      [n_layers][2][n_seq][max_new][d] bf16: slot `step` is written,
+ *             slots < step are read (caller-owned, kept across steps)
+ * max_seqlen  >= every L_i (positions up to max_seqlen + max_new - 1)
+ * hidden_out  [n_seq][d] f32 out  residual stream of the new tokens after the
+ *             last layer (before any final norm)
+ * Shape rules: 0 <= step < max_new, max_seqlen + max_new <= 16384; the model
+ * rules of rift_prefill.  Errors: RIFT_ERR_UNSUPPORTED for float32 models.
+ */
+RIFT_API rift_status rift_decode_step(const rift_model_cfg* cfg, const rift_layer_weights* layers,
+                                      const void* x_new, const int32_t* cu_seqlens, int32_t n_seq,
+                                      int32_t total_tokens, int32_t max_seqlen, const void* kv_cache,
+                                      void* kv_new, int32_t max_new, int32_t step, float* hidden_out,
+                                      void* workspace, size_t ws_bytes, rift_stream stream);
 
 #ifdef __cplusplus
 }

@@ -28,7 +28,7 @@ EXPORTS = ("rift_abi_version", "rift_status_string", "rift_set_debug", "rift_che
            "rift_score_tiles", "rift_assign_budgets", "rift_assign_budgets_utility",
            "rift_select_tokens", "rift_split_budgets", "rift_merge_workspace_size", "rift_merge_context",
            "rift_compact",
-           "rift_prefill_workspace_size", "rift_prefill")
+           "rift_prefill_workspace_size", "rift_prefill", "rift_decode_workspace_size", "rift_decode_step")
 
 
 class RiftError(RuntimeError):
@@ -93,6 +93,11 @@ def load() -> ctypes.CDLL:
     L.rift_compact.argtypes = [P, I32, I32, I32, I32, P, P, P, I32, P, P, P, I32, P, I32, P, I64, P, P, P, P]
     L.rift_prefill_workspace_size.restype = SZ
     L.rift_prefill_workspace_size.argtypes = [ctypes.POINTER(ModelCfg), I32, I32]
+    L.rift_decode_workspace_size.restype = SZ
+    L.rift_decode_workspace_size.argtypes = [ctypes.POINTER(ModelCfg), I32, I32, I32]
+    L.rift_decode_step.restype = I32
+    L.rift_decode_step.argtypes = [ctypes.POINTER(ModelCfg), ctypes.POINTER(LayerWeights), P, P, I32, I32, I32,
+                                   P, P, I32, I32, P, P, SZ, P]
     L.rift_prefill.restype = I32
     L.rift_prefill.argtypes = [ctypes.POINTER(ModelCfg), ctypes.POINTER(LayerWeights), P, I32, P, P,
                                I32, I32, I32, P, P, P, SZ, P, P]
@@ -362,3 +367,38 @@ def rift_prefill(cfg: ModelCfg, layers: Sequence[dict], x_in, cu_seqlens, positi
                              _ptr(hidden_out), _ptr(kv_cache), _ptr(workspace), workspace.numel(),
                              ev, _stream(stream))
     _check(st, "rift_prefill")
+
+
+# ----------------------------------------------------------------------------- decode
+def rift_decode_workspace_size(cfg: ModelCfg, n_seq: int, max_seqlen: int, max_new: int) -> int:
+    return int(load().rift_decode_workspace_size(ctypes.byref(cfg), int(n_seq), int(max_seqlen), int(max_new)))
+
+
+def rift_decode_step(cfg: ModelCfg, layers: Sequence[dict], x_new, cu_seqlens, total_tokens: int,
+                     max_seqlen: int, kv_cache, kv_new, step: int, hidden_out, workspace,
+                     stream=None) -> None:
+    """One generated token per prompt after rift_prefill (include/rift.h).
+    x_new [n_seq][d] bf16; kv_new [n_layers][2][n_seq][max_new][d] bf16."""
+    torch = _torch()
+    n_seq = x_new.shape[0]
+    if len(layers) != cfg.n_layers:
+        raise ValueError("need one weight set per layer")
+    for w in layers:
+        for n, v in w.items():
+            _need(v, torch.bfloat16, None, n)
+    _need(x_new, torch.bfloat16, (n_seq, cfg.d), "x_new")
+    _need(cu_seqlens, torch.int32, (n_seq + 1,), "cu_seqlens")
+    _need(kv_new, torch.bfloat16, None, "kv_new")
+    if kv_new.dim() != 5 or tuple(kv_new.shape[:3]) != (cfg.n_layers, 2, n_seq) or kv_new.shape[4] != cfg.d:
+        raise ValueError("kv_new must be [n_layers][2][n_seq][max_new][d]")
+    if kv_cache is not None:
+        _need(kv_cache, torch.bfloat16, (cfg.n_layers, 2, int(total_tokens), cfg.d), "kv_cache")
+    _need(hidden_out, torch.float32, (n_seq, cfg.d), "hidden_out")
+    _need(workspace, torch.uint8, None, "workspace")
+    arr = (LayerWeights * max(1, len(layers)))(*[layer_struct(w) for w in layers])
+    st = load().rift_decode_step(ctypes.byref(cfg), arr, _ptr(x_new), _ptr(cu_seqlens), int(n_seq),
+                                 int(total_tokens), int(max_seqlen), _ptr(kv_cache), _ptr(kv_new),
+                                 int(kv_new.shape[3]), int(step), _ptr(hidden_out), _ptr(workspace),
+                                 workspace.numel(), _stream(stream))
+    _check(st, "rift_decode_step")
+

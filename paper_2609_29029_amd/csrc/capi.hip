@@ -594,4 +594,120 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
     return RIFT_OK;
 }
 
+namespace {
+// decode workspace: RoPE table over max_seqlen + max_new positions, the new
+// tokens' positions, h, q, k, v [n_seq][d] and the SwiGLU activation [n_seq][ffn]
+struct DecodeLayout {
+    size_t rope, pos, h, q, k, v, a, total;
+};
+DecodeLayout decode_layout(const rift_model_cfg& c, int64_t n_seq, int64_t n_pos) {
+    DecodeLayout L{};
+    size_t off = 0;
+    L.rope = off;
+    off += align_up((size_t)n_pos * (size_t)(c.head_dim / 2) * sizeof(float2));
+    L.pos = off;
+    off += align_up((size_t)n_seq * sizeof(int));
+    L.h = off;
+    off += align_up((size_t)n_seq * c.d * 2);
+    L.q = off;
+    off += align_up((size_t)n_seq * c.d * 2);
+    L.k = off;
+    off += align_up((size_t)n_seq * c.d * 2);
+    L.v = off;
+    off += align_up((size_t)n_seq * c.d * 2);
+    L.a = off;
+    off += align_up((size_t)n_seq * c.ffn * 2);
+    L.total = off;
+    return L;
+}
+}  // namespace
+
+size_t rift_decode_workspace_size(const rift_model_cfg* cfg, int32_t n_seq, int32_t max_seqlen,
+                                  int32_t max_new) {
+    if (check_cfg(cfg) != RIFT_OK || n_seq < 0 || max_seqlen < 0 || max_new < 1) return 0;
+    return decode_layout(*cfg, n_seq, (int64_t)max_seqlen + max_new).total;
+}
+
+rift_status rift_decode_step(const rift_model_cfg* cfg, const rift_layer_weights* layers, const void* x_new,
+                             const int32_t* cu_seqlens, int32_t n_seq, int32_t total_tokens,
+                             int32_t max_seqlen, const void* kv_cache, void* kv_new, int32_t max_new,
+                             int32_t step, float* hidden_out, void* workspace, size_t ws_bytes,
+                             rift_stream stream) {
+    rift_status cs = check_cfg(cfg);
+    if (cs != RIFT_OK) return cs;
+    const rift_model_cfg c = *cfg;
+    if (c.dt != RIFT_BF16) return RIFT_ERR_UNSUPPORTED;
+    if (n_seq < 0 || total_tokens < 0 || max_seqlen < 0 || max_new < 1 || step < 0 || step >= max_new ||
+        (int64_t)max_seqlen + max_new > 16384 || (int64_t)n_seq * c.ffn >= (1ll << 31) ||
+        (int64_t)total_tokens * c.d >= (1ll << 31))
+        return RIFT_ERR_SHAPE;
+    if (n_seq == 0 || c.n_layers == 0) return RIFT_OK;
+    if (x_new == nullptr || cu_seqlens == nullptr || kv_new == nullptr || hidden_out == nullptr ||
+        workspace == nullptr || layers == nullptr || (total_tokens > 0 && kv_cache == nullptr))
+        return RIFT_ERR_NULL;
+    for (int l = 0; l < c.n_layers; ++l) {
+        const rift_layer_weights& w = layers[l];
+        if (!w.wq || !w.wk || !w.wv || !w.wo || !w.w_gate || !w.w_up || !w.w_down || !w.g_attn ||
+            !w.g_ffn)
+            return RIFT_ERR_NULL;
+    }
+    const int n_pos = max_seqlen + max_new;
+    const DecodeLayout L = decode_layout(c, n_seq, n_pos);
+    if (misaligned(workspace) || ws_bytes < L.total) return RIFT_ERR_WORKSPACE;
+    if (init_kernel_attributes() != hipSuccess) return RIFT_ERR_HIP;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    unsigned char* ws = static_cast<unsigned char*>(workspace);
+    float2* rope = reinterpret_cast<float2*>(ws + L.rope);
+    int* pos = reinterpret_cast<int*>(ws + L.pos);
+    uint16_t* h = reinterpret_cast<uint16_t*>(ws + L.h);
+    uint16_t* qb = reinterpret_cast<uint16_t*>(ws + L.q);
+    uint16_t* kb = reinterpret_cast<uint16_t*>(ws + L.k);
+    uint16_t* vb = reinterpret_cast<uint16_t*>(ws + L.v);
+    uint16_t* a = reinterpret_cast<uint16_t*>(ws + L.a);
+    const int d = c.d;
+    const size_t td = (size_t)total_tokens * d;   // one K or V plane of the prefill cache
+    const size_t nd = (size_t)n_seq * max_new * d;   // one K or V plane of the decode cache
+#define RIFT_TRY(x)                                   \
+    do {                                              \
+        if ((x) != hipSuccess) return RIFT_ERR_HIP;   \
+    } while (0)
+    RIFT_TRY(launch_rope_table(rope, n_pos, c.head_dim, c.rope_base, st));
+    RIFT_TRY(launch_decode_pos(cu_seqlens, n_seq, step, pos, st));
+    for (int l = 0; l < c.n_layers; ++l) {
+        const rift_layer_weights& w = layers[l];
+        const uint16_t* kp = static_cast<const uint16_t*>(kv_cache) + (size_t)(2 * l) * td;
+        const uint16_t* vp = static_cast<const uint16_t*>(kv_cache) + (size_t)(2 * l + 1) * td;
+        uint16_t* kn = static_cast<uint16_t*>(kv_new) + (size_t)(2 * l) * nd;
+        uint16_t* vn = static_cast<uint16_t*>(kv_new) + (size_t)(2 * l + 1) * nd;
+        if (l == 0)
+            RIFT_TRY(launch_rmsnorm(x_new, true, hidden_out, w.g_attn, true, h, true, n_seq, d, c.rms_eps, st));
+        else
+            RIFT_TRY(launch_rmsnorm(hidden_out, false, nullptr, w.g_attn, true, h, true, n_seq, d, c.rms_eps, st));
+        QkvArgs qa{};
+        qa.a = h;
+        qa.wq = static_cast<const uint16_t*>(w.wq);
+        qa.wk = static_cast<const uint16_t*>(w.wk);
+        qa.wv = static_cast<const uint16_t*>(w.wv);
+        qa.q = qb;
+        qa.k = kb;
+        qa.v = vb;
+        qa.rope = rope;
+        qa.pos = pos;
+        qa.n_pos = n_pos;
+        qa.M = n_seq;
+        qa.d = d;
+        RIFT_TRY(launch_gemm_qkv_rope(qa, st));
+        RIFT_TRY(launch_kv_append(kb, vb, kn, vn, n_seq, d, max_new, step, st));
+        RIFT_TRY(launch_decode_attention(qb, kp, vp, kn, vn, cu_seqlens, n_seq, total_tokens, c.n_heads, n_pos,
+                                         max_new, step, h, st));
+        RIFT_TRY(launch_gemm_resid(h, static_cast<const uint16_t*>(w.wo), hidden_out, n_seq, d, d, st));
+        RIFT_TRY(launch_rmsnorm(hidden_out, false, nullptr, w.g_ffn, true, h, true, n_seq, d, c.rms_eps, st));
+        RIFT_TRY(launch_gemm_swiglu(h, static_cast<const uint16_t*>(w.w_gate), static_cast<const uint16_t*>(w.w_up),
+                                    a, n_seq, c.ffn, d, st));
+        RIFT_TRY(launch_gemm_resid(a, static_cast<const uint16_t*>(w.w_down), hidden_out, n_seq, d, c.ffn, st));
+    }
+#undef RIFT_TRY
+    return RIFT_OK;
+}
+
 }  // extern "C"

@@ -80,6 +80,17 @@ hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uin
                                  uint16_t* o, const int* cu, int n_seq, int max_seqlen,
                                  int n_heads, hipStream_t st);
 
+// ---------------------------------------------------------------- decode (bf16)
+// pos[i] = (cu[i+1] - cu[i]) + step
+hipError_t launch_decode_pos(const int* cu, int n_seq, int step, int* pos, hipStream_t st);
+// rows of k, v [n_seq][d] into slot `step` of kc, vc [n_seq][max_new][d]
+hipError_t launch_kv_append(const uint16_t* k, const uint16_t* v, uint16_t* kc, uint16_t* vc, int n_seq, int d,
+                            int max_new, int step, hipStream_t st);
+// one query per prompt over its prefill keys kp/vp [T][H*128] and slots 0..step of kn/vn
+hipError_t launch_decode_attention(const uint16_t* q, const uint16_t* kp, const uint16_t* vp, const uint16_t* kn,
+                                   const uint16_t* vn, const int* cu, int n_seq, int T, int n_heads, int max_keys,
+                                   int max_new, int step, uint16_t* o, hipStream_t st);
+
 // ---------------------------------------------------------------- f32 path
 // C[M][N] = A[M][K] B[N][K]^T (+ C when accumulate)
 hipError_t launch_gemm_f32(const float* a, const float* b, float* c, int M, int N, int K,

@@ -33,11 +33,11 @@ def declared_symbols():
 def test_library_exports_every_declared_symbol(R):
     L = R.load()
     names = declared_symbols()
-    assert len(names) == 15
+    assert len(names) == 17
     assert tuple(names) == R.EXPORTS
     for n in names:
         assert hasattr(L, n), n
-    assert L.rift_abi_version() == 4
+    assert L.rift_abi_version() == 5
     assert L.rift_status_string(4).decode().startswith("budget")
 
 
@@ -239,3 +239,22 @@ def test_split_budgets_and_merge_validation(R):
     c = L.rift_compact
     assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, 2, FAKE, None, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE,
              FAKE, None) == 1
+
+
+
+def test_decode_validation(R):
+    """rift_decode_step rejects bad arguments on the host (nothing launched)."""
+    L = R.load()
+    cfg = R.model_cfg(4096, 32, 128, 11008, 1, 1e-6, 10000.0, R.RIFT_BF16)
+    f32 = R.model_cfg(256, 4, 64, 688, 1, 1e-6, 10000.0, R.RIFT_F32)
+    ws = R.rift_decode_workspace_size(cfg, 4, 643, 8)
+    assert ws > 0 and R.rift_decode_workspace_size(cfg, 4, 643, 0) == 0
+    lw = (R.LayerWeights * 1)(R.LayerWeights(*([FAKE] * 9)))
+    d = L.rift_decode_step
+    assert d(ctypes.byref(f32), lw, FAKE, FAKE, 4, 100, 643, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 7
+    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 643, FAKE, FAKE, 8, 8, FAKE, FAKE, ws, None) == 2  # step
+    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 16380, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 2
+    assert d(ctypes.byref(cfg), lw, None, FAKE, 4, 100, 643, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 1
+    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 643, None, FAKE, 8, 0, FAKE, FAKE, ws, None) == 1
+    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 643, FAKE, FAKE, 8, 0, FAKE, FAKE, ws - 1, None) == 5
+    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 0, 0, 643, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 0  # no prompts
