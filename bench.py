@@ -391,6 +391,41 @@ def merge_run(R, torch, w, tokens, qbank, sysd, qryd, layers, q, reps=3) -> dict
             "frac_fp64_vector_peak": round(2 * fma / (ms * 1e-3) / 1e12 / 78.6, 4)}
 
 
+def decode_run(R, torch, w, q, steps=8) -> dict:
+    """Decode after the scene-query's prefill: the prefill again with its
+    key/value cache kept (every layer's rotated keys and values of all
+    prompts), then `steps` decode steps, one new token per prompt each
+    (synthetic bf16 input embeddings).  A step reads every weight once and
+    every cached key and value once: the HBM-bound work per step."""
+    m = w.model
+    T, n_seq, d = q.total_tokens, q.n_keep, m.d
+    kv = torch.empty(m.n_layers, 2, T, d, dtype=torch.bfloat16, device="cuda")
+    R.rift_prefill(q.cfg, q.layers, q.packed, q.cu_seqlens, q.position_ids, n_seq, q.max_seqlen, q.hidden,
+                   q.prefill_ws, kv_cache=kv)
+    g = torch.Generator(device="cuda").manual_seed(0x52494654)
+    x_new = torch.randn(steps, n_seq, d, device="cuda", generator=g).to(torch.bfloat16)
+    kv_new = torch.empty(m.n_layers, 2, n_seq, steps, d, dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(R.rift_decode_workspace_size(q.cfg, n_seq, q.max_seqlen, steps), dtype=torch.uint8,
+                     device="cuda")
+    out = torch.empty(n_seq, d, dtype=torch.float32, device="cuda")
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    ev[0].record()
+    for t in range(steps):
+        R.rift_decode_step(q.cfg, q.layers, x_new[t], q.cu_seqlens, T, q.max_seqlen, kv, kv_new, t, out, ws)
+        ev[t + 1].record()
+    torch.cuda.synchronize()
+    ms = [ev[t].elapsed_time(ev[t + 1]) for t in range(steps)]
+    weight_bytes = m.n_layers * 2 * (4 * d * d + 3 * d * m.ffn + 2 * d)
+    kv_bytes = m.n_layers * 2 * (T + n_seq * steps / 2) * d * 2
+    med = statistics.median(ms)
+    del kv, kv_new
+    return {"steps": steps, "prompts": n_seq, "ms_per_step": round(med, 3),
+            "tokens_per_s": round(n_seq / (med * 1e-3), 1),
+            "bytes_per_step": round(weight_bytes + kv_bytes), "GBs": round((weight_bytes + kv_bytes) / (med * 1e-3) / 1e9, 1),
+            "frac_hbm": round((weight_bytes + kv_bytes) / (med * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+
+
 def select_batched(R, torch, token_key, order, budgets, n_tiles, n_v, n_keep, copies=64, reps=10) -> dict:
     """rift_select_tokens over `copies` scene-queries' keys at once (one call),
     for a bandwidth-meaningful number; median of `reps` timed calls."""
@@ -590,6 +625,9 @@ def main() -> int:
     out["knn_smoothing"] = kn
     out["utility_policy"] = utility_run(R, torch, w, tokens, qbank, sysd, qryd, layers, q)
     out["contextual_merge"] = merge_run(R, torch, w, tokens, qbank, sysd, qryd, layers, q)
+    if w.dtype == "bf16":
+        out["decode"] = decode_run(R, torch, w, q)
+        log(f"decode: {out['decode']}")
     out["select_batched"] = select_batched(R, torch, q.token_key, q.tile_order, q.budgets, w.n_tiles,
                                            w.n_v, q.n_keep)
     if not args.no_exhaustive:
