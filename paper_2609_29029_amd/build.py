@@ -20,7 +20,7 @@ CALIB_OUT = os.path.join(HERE, "libriftcalib.so")
 BUILD = os.path.join(HERE, "_build")
 
 SOURCES = ["score.hip", "knn.hip", "select.hip", "merge.hip", "compact.hip", "prefill_misc.hip", "gemm_bf16.hip",
-           "attention.hip", "decode.hip", "debug.hip", "capi.hip"]
+           "gemm_skinny.hip", "attention.hip", "decode.hip", "debug.hip", "capi.hip"]
 CALIB_SOURCES = ["calib/mfma_ceiling.hip"]
 
 ARCH = "gfx950"

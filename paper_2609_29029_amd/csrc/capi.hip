@@ -598,8 +598,23 @@ namespace {
 // decode workspace: RoPE table over max_seqlen + max_new positions, the new
 // tokens' positions, h, q, k, v [n_seq][d] and the SwiGLU activation [n_seq][ffn]
 struct DecodeLayout {
-    size_t rope, pos, h, q, k, v, a, total;
+    size_t rope, pos, h, q, k, v, a, part, total;
 };
+// the decode GEMMs split K (float32 partials) when every shape allows it
+bool decode_skinny(const rift_model_cfg& c) {
+    return skinny_supported(3 * c.d, c.d, c.d) && skinny_supported(c.d, c.d, c.d) &&
+           skinny_supported(2 * c.ffn, c.d, c.ffn) && skinny_supported(c.d, c.ffn, c.d) && skinny_norm_supported(c.d);
+}
+size_t decode_part_floats(const rift_model_cfg& c, int64_t n_seq) {
+    if (!decode_skinny(c)) return 0;
+    const int64_t shapes[4][2] = {{3 * (int64_t)c.d, c.d}, {c.d, c.d}, {2 * (int64_t)c.ffn, c.d}, {c.d, c.ffn}};
+    int64_t most = 0;
+    for (const auto& nk : shapes) {
+        const int64_t f = (int64_t)skinny_splits((int)nk[0], (int)nk[1]) * nk[0];
+        most = f > most ? f : most;
+    }
+    return (size_t)(most * n_seq);
+}
 DecodeLayout decode_layout(const rift_model_cfg& c, int64_t n_seq, int64_t n_pos) {
     DecodeLayout L{};
     size_t off = 0;
@@ -617,6 +632,8 @@ DecodeLayout decode_layout(const rift_model_cfg& c, int64_t n_seq, int64_t n_pos
     off += align_up((size_t)n_seq * c.d * 2);
     L.a = off;
     off += align_up((size_t)n_seq * c.ffn * 2);
+    L.part = off;
+    off += align_up(decode_part_floats(c, n_seq) * sizeof(float));
     L.total = off;
     return L;
 }
@@ -673,6 +690,41 @@ rift_status rift_decode_step(const rift_model_cfg* cfg, const rift_layer_weights
     } while (0)
     RIFT_TRY(launch_rope_table(rope, n_pos, c.head_dim, c.rope_base, st));
     RIFT_TRY(launch_decode_pos(cu_seqlens, n_seq, step, pos, st));
+    if (decode_skinny(c)) {
+        // split-K GEMMs; the residual reduce of each layer's last GEMM also
+        // applies the next layer's attention RMSNorm
+        float* part = reinterpret_cast<float*>(ws + L.part);
+        const int F = c.ffn;
+        const int s_qkv = skinny_splits(3 * d, d), s_o = skinny_splits(d, d);
+        const int s_gu = skinny_splits(2 * F, d), s_dn = skinny_splits(d, F);
+        RIFT_TRY(launch_rmsnorm(x_new, true, hidden_out, layers[0].g_attn, true, h, true, n_seq, d, c.rms_eps, st));
+        for (int l = 0; l < c.n_layers; ++l) {
+            const rift_layer_weights& w = layers[l];
+            uint16_t* kn = static_cast<uint16_t*>(kv_new) + (size_t)(2 * l) * nd;
+            uint16_t* vn = static_cast<uint16_t*>(kv_new) + (size_t)(2 * l + 1) * nd;
+            RIFT_TRY(launch_skinny_gemm(h, static_cast<const uint16_t*>(w.wq), static_cast<const uint16_t*>(w.wk),
+                                        static_cast<const uint16_t*>(w.wv), d, n_seq, 3 * d, d, part, st));
+            RIFT_TRY(launch_skinny_qkv(part, s_qkv, n_seq, d, rope, pos, n_pos, qb, kn, vn, max_new, step, st));
+            RIFT_TRY(launch_decode_attention(qb, static_cast<const uint16_t*>(kv_cache) + (size_t)(2 * l) * td,
+                                             static_cast<const uint16_t*>(kv_cache) + (size_t)(2 * l + 1) * td, kn,
+                                             vn, cu_seqlens, n_seq, total_tokens, c.n_heads, n_pos, max_new, step,
+                                             h, st));
+            RIFT_TRY(launch_skinny_gemm(h, static_cast<const uint16_t*>(w.wo), nullptr, nullptr, d, n_seq, d, d,
+                                        part, st));
+            RIFT_TRY(launch_skinny_resid_norm(part, s_o, n_seq, d, hidden_out, static_cast<const uint16_t*>(w.g_ffn),
+                                              h, c.rms_eps, st));
+            RIFT_TRY(launch_skinny_gemm(h, static_cast<const uint16_t*>(w.w_gate),
+                                        static_cast<const uint16_t*>(w.w_up), nullptr, F, n_seq, 2 * F, d, part, st));
+            RIFT_TRY(launch_skinny_swiglu(part, s_gu, n_seq, F, a, st));
+            RIFT_TRY(launch_skinny_gemm(a, static_cast<const uint16_t*>(w.w_down), nullptr, nullptr, d, n_seq, d, F,
+                                        part, st));
+            const bool last = l + 1 == c.n_layers;
+            RIFT_TRY(launch_skinny_resid_norm(part, s_dn, n_seq, d, hidden_out,
+                                              last ? nullptr : static_cast<const uint16_t*>(layers[l + 1].g_attn),
+                                              last ? nullptr : h, c.rms_eps, st));
+        }
+        return RIFT_OK;
+    }
     for (int l = 0; l < c.n_layers; ++l) {
         const rift_layer_weights& w = layers[l];
         const uint16_t* kp = static_cast<const uint16_t*>(kv_cache) + (size_t)(2 * l) * td;

@@ -7,13 +7,14 @@
 //
 //   decode_pos     position of each prompt's new token, L_i + step
 //   kv_append      this step's rotated key and value rows into slot `step`
-//   decode_attn    one workgroup (4 waves) per (prompt, head): the query in
-//                  LDS; scores of every key (one key per lane, four waves
-//                  splitting the keys) in LDS; the max and the sum of
+//   decode_attn    one workgroup (4 waves) per (prompt, head), the 16 lanes
+//                  of each row group reading one key or value row of 256
+//                  bytes whole: scores of every key in LDS (a dot product per
+//                  group, summed over its lanes); the max and the sum of
 //                  2^(s - max) over the workgroup; then the weighted sum of
-//                  the values, each wave a quarter of the keys with every lane
-//                  two of the 128 dimensions, the four partial sums added in
-//                  wave order; output rounded to bfloat16.
+//                  the values, each lane 8 of the 128 dimensions over its
+//                  group's keys, the 16 group sums added in fixed order;
+//                  output rounded to bfloat16.
 #include "launch.h"
 #include "rift_common.h"
 
@@ -40,48 +41,79 @@ __global__ void kv_append_kernel(const u32x4_t* __restrict__ k, const u32x4_t* _
     vc[dst] = v[w];
 }
 
+// Sum over the 16 lanes of each row of the wave, every lane receiving the
+// same sum: pairs, quads (quad_perm), halves (row_half_mirror), rows
+// (row_mirror).  Each step adds two values that every lane of the group sees in
+// one of two orders, so the lanes agree bit for bit.
+__device__ __forceinline__ float row16_sum(float v) {
+    v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xf, 0xf, false));
+    v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4E, 0xf, 0xf, false));
+    v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x141, 0xf, 0xf, false));
+    v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x140, 0xf, 0xf, false));
+    return v;
+}
+
+// Keys are visited in groups of 64: slot s = 4 wave + (lane >> 4) of the 16
+// row groups takes keys j0 + 16 u + s, u < kDecU, and the 16 lanes of a group
+// read one 256-byte row, lane c its bytes 16 c .. 16 c + 15 (dims 8 c .. 8 c + 7).
+constexpr int kDecU = 4;
+
 __global__ void __launch_bounds__(256)
 decode_attn_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ kp, const bf16_t* __restrict__ vp,
                    const bf16_t* __restrict__ kn, const bf16_t* __restrict__ vn, const int* __restrict__ cu,
                    int n_seq, int T, int H, int max_keys, int max_new, int step, float scale_log2,
                    bf16_t* __restrict__ o) {
     extern __shared__ float sc[];   // one score per key
-    __shared__ float qs[DHD];
     __shared__ float red[4];
     __shared__ float part[4][DHD];
     const int seq = blockIdx.x / H;
     const int head = blockIdx.x % H;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int c = lane & 15;
+    const int slot = 4 * wave + (lane >> 4);
     int s0 = cu[seq];
     int L = cu[seq + 1] - s0;
     if (s0 < 0 || L < 0 || s0 + L > T) s0 = L = 0;   // offsets outside the prefill cache: no prompt keys
     // prompt keys, then the generated ones (at most max_keys, the LDS size)
     const int nk = min(L + step + 1, max_keys);
     const int ld = H * DHD;
-    const size_t hoff = (size_t)head * DHD;
-    if (tid < DHD) qs[tid] = bf16_to_f32(q[(size_t)seq * ld + hoff + tid]);
-    __syncthreads();
-    auto key_row = [&](int j, const bf16_t* prompt_base, const bf16_t* new_base) -> const bf16_t* {
-        return j < L ? prompt_base + (size_t)(s0 + j) * ld + hoff
-                     : new_base + ((size_t)seq * max_new + (j - L)) * ld + hoff;
+    const size_t hoff = (size_t)head * DHD + 8 * c;
+    auto row = [&](int j, const bf16_t* prompt_base, const bf16_t* new_base) -> const u32x4_t* {
+        return reinterpret_cast<const u32x4_t*>(
+            j < L ? prompt_base + (size_t)(s0 + j) * ld + hoff
+                  : new_base + ((size_t)seq * max_new + (j - L)) * ld + hoff);
     };
-    // scores, and the running max of this thread's keys
-    float mx = -INFINITY;
-    for (int j = tid; j < nk; j += blockDim.x) {
-        const u32x4_t* kr = reinterpret_cast<const u32x4_t*>(key_row(j, kp, kn));
-        float acc = 0.f;
+    float qf[8];
+    {
+        const u32x4_t qw = *reinterpret_cast<const u32x4_t*>(q + (size_t)seq * ld + hoff);
 #pragma unroll
-        for (int c = 0; c < DHD / 8; ++c) {
-            const u32x4_t w = kr[c];
+        for (int e = 0; e < 4; ++e) {
+            qf[2 * e] = bf16_lo(qw[e]);
+            qf[2 * e + 1] = bf16_hi(qw[e]);
+        }
+    }
+    // scores (base-2 logits), and the running max of this lane's keys
+    float mx = -INFINITY;
+    for (int j0 = 0; j0 < nk; j0 += 16 * kDecU) {
+        u32x4_t kw[kDecU];
+#pragma unroll
+        for (int u = 0; u < kDecU; ++u)
+            kw[u] = __builtin_nontemporal_load(row(min(j0 + 16 * u + slot, nk - 1), kp, kn));
+#pragma unroll
+        for (int u = 0; u < kDecU; ++u) {
+            float acc = 0.f;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                acc = fmaf(bf16_lo(w[e]), qs[8 * c + 2 * e], acc);
-                acc = fmaf(bf16_hi(w[e]), qs[8 * c + 2 * e + 1], acc);
+                acc = fmaf(bf16_lo(kw[u][e]), qf[2 * e], acc);
+                acc = fmaf(bf16_hi(kw[u][e]), qf[2 * e + 1], acc);
+            }
+            const float sl = row16_sum(acc) * scale_log2;
+            const int j = j0 + 16 * u + slot;
+            if (j < nk) {
+                mx = fmaxf(mx, sl);
+                if (c == 0) sc[j] = sl;
             }
         }
-        const float sl = acc * scale_log2;
-        sc[j] = sl;
-        mx = fmaxf(mx, sl);
     }
     for (int s = 32; s >= 1; s >>= 1) mx = fmaxf(mx, __shfl_xor(mx, s));
     if (lane == 0) red[wave] = mx;
@@ -98,20 +130,42 @@ decode_attn_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ kp, 
     if (lane == 0) red[wave] = sum;
     __syncthreads();
     const float inv = 1.0f / ((red[0] + red[1]) + (red[2] + red[3]));
-    // weighted values: wave w takes keys w, w + 4, ...; lane holds dims 2 lane, 2 lane + 1
-    float o0 = 0.f, o1 = 0.f;
-    for (int j = wave; j < nk; j += 4) {
-        const uint32_t w = reinterpret_cast<const uint32_t*>(key_row(j, vp, vn))[lane];
-        const float p = sc[j];
-        o0 = fmaf(p, bf16_lo(w), o0);
-        o1 = fmaf(p, bf16_hi(w), o1);
+    // weighted values over the same key slots; lane c accumulates dims 8 c .. 8 c + 7
+    float acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+    for (int j0 = 0; j0 < nk; j0 += 16 * kDecU) {
+        u32x4_t vw[kDecU];
+#pragma unroll
+        for (int u = 0; u < kDecU; ++u)
+            vw[u] = __builtin_nontemporal_load(row(min(j0 + 16 * u + slot, nk - 1), vp, vn));
+#pragma unroll
+        for (int u = 0; u < kDecU; ++u) {
+            const int j = j0 + 16 * u + slot;
+            if (j < nk) {
+                const float p = sc[j];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    acc[2 * e] = fmaf(p, bf16_lo(vw[u][e]), acc[2 * e]);
+                    acc[2 * e + 1] = fmaf(p, bf16_hi(vw[u][e]), acc[2 * e + 1]);
+                }
+            }
+        }
     }
-    part[wave][2 * lane] = o0;
-    part[wave][2 * lane + 1] = o1;
+    // the four row groups of a wave, then the four waves, in fixed order
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        acc[e] += __shfl_xor(acc[e], 16);
+        acc[e] += __shfl_xor(acc[e], 32);
+    }
+    if (lane < 16) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) part[wave][8 * c + e] = acc[e];
+    }
     __syncthreads();
     if (tid < DHD) {
         const float r = ((part[0][tid] + part[1][tid]) + part[2][tid]) + part[3][tid];
-        o[(size_t)seq * ld + hoff + tid] = f32_to_bf16(r * inv);
+        o[(size_t)seq * ld + (size_t)head * DHD + tid] = f32_to_bf16(r * inv);
     }
 }
 

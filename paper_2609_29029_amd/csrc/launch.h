@@ -91,6 +91,24 @@ hipError_t launch_decode_attention(const uint16_t* q, const uint16_t* kp, const 
                                    const uint16_t* vn, const int* cu, int n_seq, int T, int n_heads, int max_keys,
                                    int max_new, int step, uint16_t* o, hipStream_t st);
 
+// Decode-shaped GEMMs (few rows): K split into S chunks (S from N and K only),
+// float32 partials part[S][M][N] of A [M][K] times the weight regions b0|b1|b2
+// (each [nr][K], N = regions * nr), then reduce kernels that add the partials
+// in chunk order and finish the layer's elementwise work.
+int skinny_splits(int N, int K);
+bool skinny_supported(int N, int K, int nr);
+bool skinny_norm_supported(int d);
+hipError_t launch_skinny_gemm(const uint16_t* a, const uint16_t* b0, const uint16_t* b1, const uint16_t* b2,
+                              int nr, int M, int N, int K, float* part, hipStream_t st);
+// x += sum of partials [S][M][d]; with h, h = bf16(RMSNorm(x) * g)
+hipError_t launch_skinny_resid_norm(const float* part, int S, int M, int d, float* x, const uint16_t* g,
+                                    uint16_t* h, float eps, hipStream_t st);
+// q to q[M][d], k and v to slot `step` of kc, vc [M][max_new][d], RoPE at pos[m]
+hipError_t launch_skinny_qkv(const float* part, int S, int M, int d, const float2* rope, const int* pos, int n_pos,
+                             uint16_t* q, uint16_t* kc, uint16_t* vc, int max_new, int step, hipStream_t st);
+// a[M][F] = silu(gate) * up
+hipError_t launch_skinny_swiglu(const float* part, int S, int M, int F, uint16_t* a, hipStream_t st);
+
 // ---------------------------------------------------------------- f32 path
 // C[M][N] = A[M][K] B[N][K]^T (+ C when accumulate)
 hipError_t launch_gemm_f32(const float* a, const float* b, float* c, int M, int N, int K,
