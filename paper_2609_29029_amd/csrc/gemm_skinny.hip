@@ -184,31 +184,34 @@ skinny_gemm_kernel(SkinnyParams p) {
 }
 
 // x[row] += sum_s part[s][row] (chunk order); then, with h, the RMSNorm of the
-// updated row times g, rounded to bfloat16.  One workgroup per row, thread t
-// holding columns 4 t + 1024 c .. + 3.
-template <int NCH>
-__global__ void __launch_bounds__(256)
+// updated row times g, rounded to bfloat16.  One workgroup of T threads per
+// row, thread t holding columns 4 t + 4 T c .. + 3, c < NCH; every partial of
+// a thread is loaded before the first is added.
+template <int T, int NCH>
+__global__ void __launch_bounds__(T)
 skinny_resid_norm_kernel(const float* __restrict__ part, int S, int M, float* __restrict__ x,
                          const bf16_t* __restrict__ g, bf16_t* __restrict__ h, float eps) {
-    constexpr int d = 1024 * NCH;
-    __shared__ float red[4];
+    constexpr int d = 4 * T * NCH;
+    constexpr int kMaxS = kSkinnyMaxSplit;
+    __shared__ float red[T / 64];
     const int row = blockIdx.x;
     const int tid = threadIdx.x;
     const size_t base = (size_t)row * d + 4 * tid;
+    f32x4_t w[kMaxS][NCH];
+#pragma unroll
+    for (int s = 0; s < kMaxS; ++s)
+        if (s < S)
+#pragma unroll
+            for (int c = 0; c < NCH; ++c)
+                w[s][c] = *reinterpret_cast<const f32x4_t*>(part + (size_t)s * M * d + base + 4 * T * c);
     f32x4_t v[NCH];
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) v[c] = *reinterpret_cast<const f32x4_t*>(part + base + 1024 * c);
-    for (int s = 1; s < S; ++s) {
-        const float* ps = part + (size_t)s * M * d + base;
-        f32x4_t w[NCH];
-#pragma unroll
-        for (int c = 0; c < NCH; ++c) w[c] = *reinterpret_cast<const f32x4_t*>(ps + 1024 * c);
-#pragma unroll
-        for (int c = 0; c < NCH; ++c) v[c] += w[c];
-    }
-#pragma unroll
     for (int c = 0; c < NCH; ++c) {
-        f32x4_t* xp = reinterpret_cast<f32x4_t*>(x + base + 1024 * c);
+        v[c] = w[0][c];
+#pragma unroll
+        for (int s = 1; s < kMaxS; ++s)
+            if (s < S) v[c] += w[s][c];
+        f32x4_t* xp = reinterpret_cast<f32x4_t*>(x + base + 4 * T * c);
         v[c] = *xp + v[c];
         *xp = v[c];
     }
@@ -219,10 +222,13 @@ skinny_resid_norm_kernel(const float* __restrict__ part, int S, int M, float* __
     ss = wave_sum(ss);
     if ((tid & 63) == 0) red[tid >> 6] = ss;
     __syncthreads();
-    const float inv = 1.0f / sqrtf(((red[0] + red[1]) + (red[2] + red[3])) / (float)d + eps);
+    float tot = 0.f;
+#pragma unroll
+    for (int i = 0; i < T / 64; ++i) tot += red[i];
+    const float inv = 1.0f / sqrtf(tot / (float)d + eps);
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
-        const int i = 4 * tid + 1024 * c;
+        const int i = 4 * tid + 4 * T * c;
         const uint2 gw = *reinterpret_cast<const uint2*>(g + i);
         const float y0 = v[c][0] * inv * bf16_lo(gw.x), y1 = v[c][1] * inv * bf16_hi(gw.x);
         const float y2 = v[c][2] * inv * bf16_lo(gw.y), y3 = v[c][3] * inv * bf16_hi(gw.y);
@@ -234,40 +240,54 @@ skinny_resid_norm_kernel(const float* __restrict__ part, int S, int M, float* __
 }
 
 // q | k | v of row m from the partials of [wq | wk | wv] (N = 3 d): thread
-// (m, region, head, j < 64) owns the rotate-half pair (j, j + 64) of its head;
-// q goes to q[m], k and v to slot `step` of prompt m in the decode cache.
+// (m, region, head, j4 < 16) owns columns j = 4 j4 .. + 3 of its head and their
+// rotate-half partners j + 64; q goes to q[m], k and v to slot `step` of
+// prompt m in the decode cache.
 __global__ void __launch_bounds__(256)
 skinny_qkv_kernel(const float* __restrict__ part, int S, int M, int d, const float2* __restrict__ rope,
                   const int* __restrict__ pos, int n_pos, bf16_t* __restrict__ q, bf16_t* __restrict__ kc,
                   bf16_t* __restrict__ vc, int max_new, int step) {
-    const int half = d >> 1;
+    const int per_region = d >> 3;   // (head, j4) pairs
     const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= (long long)M * 3 * half) return;
-    const int m = (int)(idx / (3 * half));
-    const int rem = (int)(idx % (3 * half));
-    const int region = rem / half;
-    const int w = rem % half;
-    const int hc = 128 * (w >> 6) + (w & 63);   // column of j within q, k or v
+    if (idx >= (long long)M * 3 * per_region) return;
+    const int m = (int)(idx / (3 * per_region));
+    const int rem = (int)(idx % (3 * per_region));
+    const int region = rem / per_region;
+    const int w = rem % per_region;
+    const int j = 4 * (w & 15);
+    const int hc = 128 * (w >> 4) + j;   // column of j within q, k or v
     const size_t N = 3 * (size_t)d;
     const float* p0 = part + (size_t)m * N + (size_t)region * d + hc;
-    float x1 = p0[0], x2 = p0[64];
+    f32x4_t x1 = *reinterpret_cast<const f32x4_t*>(p0);
+    f32x4_t x2 = *reinterpret_cast<const f32x4_t*>(p0 + 64);
     for (int s = 1; s < S; ++s) {
         const float* ps = p0 + (size_t)s * M * N;
-        x1 += ps[0];
-        x2 += ps[64];
+        x1 += *reinterpret_cast<const f32x4_t*>(ps);
+        x2 += *reinterpret_cast<const f32x4_t*>(ps + 64);
     }
-    float y1 = x1, y2 = x2;
+    f32x4_t y1 = x1, y2 = x2;
     if (region < 2) {
         int ps = pos[m];
         ps = ps < 0 ? 0 : (ps >= n_pos ? n_pos - 1 : ps);
-        const float2 cs = rope[(size_t)ps * 64 + (w & 63)];
-        y1 = x1 * cs.x - x2 * cs.y;
-        y2 = x2 * cs.x + x1 * cs.y;
+        const f32x4_t* cs = reinterpret_cast<const f32x4_t*>(rope + (size_t)ps * 64 + j);
+        const f32x4_t c01 = cs[0], c23 = cs[1];   // (cos, sin) of j, j+1 and of j+2, j+3
+        const float cv[4] = {c01[0], c01[2], c23[0], c23[2]};
+        const float sv[4] = {c01[1], c01[3], c23[1], c23[3]};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            y1[e] = x1[e] * cv[e] - x2[e] * sv[e];
+            y2[e] = x2[e] * cv[e] + x1[e] * sv[e];
+        }
     }
     bf16_t* dst = region == 0 ? q + (size_t)m * d
                               : (region == 1 ? kc : vc) + ((size_t)m * max_new + step) * d;
-    dst[hc] = f32_to_bf16(y1);
-    dst[hc + 64] = f32_to_bf16(y2);
+    uint2 o1, o2;
+    o1.x = (uint32_t)f32_to_bf16(y1[0]) | ((uint32_t)f32_to_bf16(y1[1]) << 16);
+    o1.y = (uint32_t)f32_to_bf16(y1[2]) | ((uint32_t)f32_to_bf16(y1[3]) << 16);
+    o2.x = (uint32_t)f32_to_bf16(y2[0]) | ((uint32_t)f32_to_bf16(y2[1]) << 16);
+    o2.y = (uint32_t)f32_to_bf16(y2[2]) | ((uint32_t)f32_to_bf16(y2[3]) << 16);
+    *reinterpret_cast<uint2*>(dst + hc) = o1;
+    *reinterpret_cast<uint2*>(dst + hc + 64) = o2;
 }
 
 // a[m][f] = silu(gate) * up from the partials of [wg | wu] (N = 2 F), four
@@ -363,16 +383,18 @@ bool skinny_norm_supported(int d) {
 hipError_t launch_skinny_resid_norm(const float* part, int S, int M, int d, float* x, const uint16_t* g,
                                     uint16_t* h, float eps, hipStream_t st) {
     if (M <= 0) return hipSuccess;
-#define RIFT_SK_NORM(NCH)                                                                                       \
-    if (d == 1024 * NCH) {                                                                                      \
-        hipLaunchKernelGGL(skinny_resid_norm_kernel<NCH>, dim3(M), dim3(256), 0, st, part, S, M, x, g, h, eps); \
-        return hipGetLastError();                                                                               \
+    if (S < 1 || S > kSkinnyMaxSplit) return hipErrorInvalidValue;
+#define RIFT_SK_NORM(T, NCH)                                                                           \
+    if (d == 4 * T * NCH) {                                                                            \
+        hipLaunchKernelGGL((skinny_resid_norm_kernel<T, NCH>), dim3(M), dim3(T), 0, st, part, S, M, x, g, h, \
+                           eps);                                                                       \
+        return hipGetLastError();                                                                      \
     }
-    RIFT_SK_NORM(1)
-    RIFT_SK_NORM(2)
-    RIFT_SK_NORM(4)
-    RIFT_SK_NORM(8)
-    RIFT_SK_NORM(16)
+    RIFT_SK_NORM(256, 1)
+    RIFT_SK_NORM(512, 1)
+    RIFT_SK_NORM(1024, 1)
+    RIFT_SK_NORM(1024, 2)
+    RIFT_SK_NORM(1024, 4)
 #undef RIFT_SK_NORM
     return hipErrorInvalidValue;
 }
@@ -380,7 +402,7 @@ hipError_t launch_skinny_resid_norm(const float* part, int S, int M, int d, floa
 hipError_t launch_skinny_qkv(const float* part, int S, int M, int d, const float2* rope, const int* pos, int n_pos,
                              uint16_t* q, uint16_t* kc, uint16_t* vc, int max_new, int step, hipStream_t st) {
     if (M <= 0) return hipSuccess;
-    const long long n = (long long)M * 3 * (d / 2);
+    const long long n = (long long)M * 3 * (d / 8);
     hipLaunchKernelGGL(skinny_qkv_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part, S, M, d, rope,
                        pos, n_pos, q, kc, vc, max_new, step);
     return hipGetLastError();
