@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define RIFT_ABI_VERSION 5
+#define RIFT_ABI_VERSION 6
 
 #if defined(__GNUC__) || defined(__clang__)
 #define RIFT_API __attribute__((visibility("default")))
@@ -269,15 +269,25 @@ RIFT_API rift_status rift_merge_context(const void* tokens, rift_dtype dt, int32
  * rift_compact -- pack every kept tile's prompt [n_sys system rows | selected
  * vision rows of the tile, ascending | contextual rows of the tile (optional)
  * | n_qry query rows] into one varlen batch.
+ * shared_prefix 0: every prompt holds its own copy of the system rows.
+ *              1: the system rows, identical in every prompt, are written once
+ *              at rows [0, n_sys) as sequence 0 and prompt i holds only its
+ *              rows after them, positions n_sys onwards; rift_prefill and
+ *              rift_decode_step then take n_prefix = n_sys.  Under causal
+ *              attention the prefix's states do not depend on what follows,
+ *              so the prefill's results are those of the unshared layout.
  * tokens   [n_tiles][n_v][d] dt;  sys_emb [n_sys][d] dt;  qry_emb [n_qry][d] dt
  * kept_tiles, sel_offsets, sel_idx as produced for rift_select_tokens
  * ctx_rows, ctx_offsets   optional (both NULL: none): rows of rift_merge_context
  *              and their prefix sums [n_keep+1] per kept tile
  * packed       [packed_rows][d] dt out, total rows
- *              T = n_keep*(n_sys+n_qry) + sel_offsets[n_keep] (+ ctx_offsets[n_keep])
- *              must be <= packed_rows
- * cu_seqlens   [n_keep+1] i32 out  prefix sums of sequence lengths
- * position_ids [packed_rows] i32 out  0..L-1 within each sequence
+ *              T = n_keep*(n_sys+n_qry) + sel_offsets[n_keep] (+ ctx_offsets[n_keep]),
+ *              or with shared_prefix n_sys + n_keep*n_qry + sel_offsets[n_keep]
+ *              (+ ctx_offsets[n_keep]); must be <= packed_rows
+ * cu_seqlens   [n_keep+1] i32 out  prefix sums of sequence lengths ([n_keep+2]
+ *              with shared_prefix: 0, n_sys, then the prompts' ends)
+ * position_ids [packed_rows] i32 out  0..L-1 within each sequence (a prompt
+ *              after a shared prefix: n_sys..n_sys+L-1)
  * status       [1] i32 out  0, or RIFT_ERR_SHAPE if a tile id or selected index is
  *              out of range, a budget (sel_offsets step) is outside [0, n_v], a
  *              ctx_offsets step is negative, a first offset is not 0 or
@@ -288,15 +298,16 @@ RIFT_API rift_status rift_merge_context(const void* tokens, rift_dtype dt, int32
  *              hold sel_offsets[n_keep] entries and ctx_rows ctx_offsets[n_keep]
  *              rows.
  * Shape rules: d * sizeof(dt) % 16 == 0; n_sys, n_qry >= 0; 0 <= n_keep <= 65535;
- *              packed_rows <= 2^25 (two waves per packed row).
+ *              packed_rows <= 2^25 (two waves per packed row); shared_prefix
+ *              0 or 1.
  */
 RIFT_API rift_status rift_compact(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
                          int32_t d, const int32_t* kept_tiles, const int32_t* sel_offsets,
                          const int32_t* sel_idx, int32_t n_keep, const void* ctx_rows,
                          const int32_t* ctx_offsets, const void* sys_emb, int32_t n_sys,
-                         const void* qry_emb, int32_t n_qry, void* packed, int64_t packed_rows,
-                         int32_t* cu_seqlens, int32_t* position_ids, int32_t* status,
-                         rift_stream stream);
+                         const void* qry_emb, int32_t n_qry, int32_t shared_prefix, void* packed,
+                         int64_t packed_rows, int32_t* cu_seqlens, int32_t* position_ids,
+                         int32_t* status, rift_stream stream);
 
 /* ------------------------------------------------------------------ prefill */
 
@@ -346,6 +357,12 @@ RIFT_API size_t rift_prefill_workspace_size(const rift_model_cfg* cfg, int32_t t
  *              total_tokens, every length <= max_seqlen
  * position_ids [total_tokens] i32, each in [0, max_seqlen)  (values outside
  *              are clamped)
+ * n_prefix     0, or the length of a prefix shared by every prompt: sequence 0
+ *              is then rows [0, n_prefix) (cu_seqlens[1] == n_prefix) and each
+ *              other sequence holds only its rows after the prefix (positions
+ *              from n_prefix) and attends to the prefix rows first, exactly as
+ *              if they were packed in front of it (rift_compact with
+ *              shared_prefix); max_seqlen bounds n_prefix + each length.
  * hidden_out   [total_tokens][d] f32 out: residual stream after the last layer
  *              (no final norm, no vocabulary projection)
  * kv_cache     optional out [n_layers][2][total_tokens][d] cfg->dt: per layer
@@ -358,12 +375,14 @@ RIFT_API size_t rift_prefill_workspace_size(const rift_model_cfg* cfg, int32_t t
  *              4 down projection.
  * Implemented: bf16 with head_dim == 128, d % 256 == 0, ffn % 128 == 0;
  *              f32 with head_dim in {64, 128}, d % 64 == 0, ffn % 16 == 0.
- * Shape rules: 1 <= max_seqlen <= 65536, total_tokens >= 0, n_seq >= 0.
+ * Shape rules: 1 <= max_seqlen <= 65536, total_tokens >= 0, n_seq >= 0;
+ *              0 <= n_prefix <= min(total_tokens, max_seqlen), n_seq >= 1 when
+ *              n_prefix > 0.
  */
 RIFT_API rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* layers,
                          const void* x_in, rift_dtype x_dt, const int32_t* cu_seqlens,
                          const int32_t* position_ids, int32_t n_seq, int32_t total_tokens,
-                         int32_t max_seqlen, float* hidden_out, void* kv_cache,
+                         int32_t max_seqlen, int32_t n_prefix, float* hidden_out, void* kv_cache,
                          void* workspace, size_t ws_bytes, void* const* events,
                          rift_stream stream);
 
@@ -383,21 +402,26 @@ RIFT_API size_t rift_decode_workspace_size(const rift_model_cfg* cfg, int32_t n_
  * bfloat16 models only.  Decode attention keeps scores and probabilities in
  * float32 (the prefill rounds probabilities to bf16 for its MFMA).
  * x_new       [n_seq][d] bf16   input embeddings of this step's tokens
- * cu_seqlens  [n_seq+1] i32     the prefill's prompt offsets
+ * cu_seqlens  [n_seq+1] i32     the prefill's prompt offsets ([n_seq+2] with
+ *             n_prefix > 0: the prefill's sequence 0 is the shared prefix and
+ *             prompt i is its sequence i+1; its keys are the n_prefix prefix
+ *             rows, then its own rows, and L_i counts both)
  * kv_cache    [n_layers][2][total_tokens][d] bf16 (rift_prefill's kv_cache)
  * kv_new      [n_layers][2][n_seq][max_new][d] bf16: slot `step` is written,
  *             slots < step are read (caller-owned, kept across steps)
  * max_seqlen  >= every L_i (positions up to max_seqlen + max_new - 1)
  * hidden_out  [n_seq][d] f32 out  residual stream of the new tokens after the
  *             last layer (before any final norm)
- * Shape rules: 0 <= step < max_new, max_seqlen + max_new <= 16384; the model
- * rules of rift_prefill.  Errors: RIFT_ERR_UNSUPPORTED for float32 models.
+ * Shape rules: 0 <= step < max_new, max_seqlen + max_new <= 16384,
+ * 0 <= n_prefix <= min(total_tokens, max_seqlen); the model rules of
+ * rift_prefill.  Errors: RIFT_ERR_UNSUPPORTED for float32 models.
  */
 RIFT_API rift_status rift_decode_step(const rift_model_cfg* cfg, const rift_layer_weights* layers,
                                       const void* x_new, const int32_t* cu_seqlens, int32_t n_seq,
-                                      int32_t total_tokens, int32_t max_seqlen, const void* kv_cache,
-                                      void* kv_new, int32_t max_new, int32_t step, float* hidden_out,
-                                      void* workspace, size_t ws_bytes, rift_stream stream);
+                                      int32_t total_tokens, int32_t max_seqlen, int32_t n_prefix,
+                                      const void* kv_cache, void* kv_new, int32_t max_new, int32_t step,
+                                      float* hidden_out, void* workspace, size_t ws_bytes,
+                                      rift_stream stream);
 
 #ifdef __cplusplus
 }

@@ -90,17 +90,17 @@ def load() -> ctypes.CDLL:
     L.rift_merge_context.restype = I32
     L.rift_merge_context.argtypes = [P, I32, I32, I32, I32, P, P, P, P, I32, P, I64, P, P, SZ, P]
     L.rift_compact.restype = I32
-    L.rift_compact.argtypes = [P, I32, I32, I32, I32, P, P, P, I32, P, P, P, I32, P, I32, P, I64, P, P, P, P]
+    L.rift_compact.argtypes = [P, I32, I32, I32, I32, P, P, P, I32, P, P, P, I32, P, I32, I32, P, I64, P, P, P, P]
     L.rift_prefill_workspace_size.restype = SZ
     L.rift_prefill_workspace_size.argtypes = [ctypes.POINTER(ModelCfg), I32, I32]
     L.rift_decode_workspace_size.restype = SZ
     L.rift_decode_workspace_size.argtypes = [ctypes.POINTER(ModelCfg), I32, I32, I32]
     L.rift_decode_step.restype = I32
     L.rift_decode_step.argtypes = [ctypes.POINTER(ModelCfg), ctypes.POINTER(LayerWeights), P, P, I32, I32, I32,
-                                   P, P, I32, I32, P, P, SZ, P]
+                                   I32, P, P, I32, I32, P, P, SZ, P]
     L.rift_prefill.restype = I32
     L.rift_prefill.argtypes = [ctypes.POINTER(ModelCfg), ctypes.POINTER(LayerWeights), P, I32, P, P,
-                               I32, I32, I32, P, P, P, SZ, P, P]
+                               I32, I32, I32, I32, P, P, P, SZ, P, P]
     _lib = L
     return L
 
@@ -293,7 +293,9 @@ def rift_merge_context(tokens, kept_tiles, sel_offsets, sel_idx, ctx_offsets, n_
 
 def rift_compact(tokens, kept_tiles, sel_offsets, sel_idx, n_keep: int, sys_emb, qry_emb,
                  packed, cu_seqlens, position_ids, status, stream=None, ctx_rows=None,
-                 ctx_offsets=None) -> None:
+                 ctx_offsets=None, shared_prefix: bool = False) -> None:
+    """shared_prefix: the system rows once at the front as sequence 0;
+    cu_seqlens then needs n_keep + 2 entries."""
     torch = _torch()
     n_tiles, n_v, d = tokens.shape
     dt = _dt_code(tokens)
@@ -304,8 +306,8 @@ def rift_compact(tokens, kept_tiles, sel_offsets, sel_idx, n_keep: int, sys_emb,
     _need(cu_seqlens, torch.int32, None, "cu_seqlens")
     _need(position_ids, torch.int32, (packed.shape[0],), "position_ids")
     _need(status, torch.int32, (1,), "status")
-    if cu_seqlens.numel() < n_keep + 1 or sel_offsets.numel() < n_keep + 1:
-        raise ValueError("cu_seqlens and sel_offsets need n_keep + 1 entries")
+    if cu_seqlens.numel() < n_keep + 1 + int(bool(shared_prefix)) or sel_offsets.numel() < n_keep + 1:
+        raise ValueError("cu_seqlens needs n_keep + 1 entries (+ 1 with a shared prefix), sel_offsets n_keep + 1")
     if (ctx_rows is None) != (ctx_offsets is None):
         raise ValueError("ctx_rows and ctx_offsets go together")
     if ctx_rows is not None:
@@ -316,8 +318,9 @@ def rift_compact(tokens, kept_tiles, sel_offsets, sel_idx, n_keep: int, sys_emb,
     st = load().rift_compact(_ptr(tokens), dt, n_tiles, n_v, d, _ptr(kept_tiles), _ptr(sel_offsets),
                              _ptr(sel_idx), int(n_keep), _ptr(ctx_rows), _ptr(ctx_offsets),
                              _ptr(sys_emb), sys_emb.shape[0],
-                             _ptr(qry_emb), qry_emb.shape[0], _ptr(packed), packed.shape[0],
-                             _ptr(cu_seqlens), _ptr(position_ids), _ptr(status), _stream(stream))
+                             _ptr(qry_emb), qry_emb.shape[0], int(bool(shared_prefix)), _ptr(packed),
+                             packed.shape[0], _ptr(cu_seqlens), _ptr(position_ids), _ptr(status),
+                             _stream(stream))
     _check(st, "rift_compact")
 
 
@@ -338,9 +341,10 @@ def layer_struct(w: dict) -> LayerWeights:
 
 def rift_prefill(cfg: ModelCfg, layers: Sequence[dict], x_in, cu_seqlens, position_ids,
                  n_seq: int, max_seqlen: int, hidden_out, workspace, kv_cache=None,
-                 events=None, stream=None) -> None:
+                 events=None, stream=None, n_prefix: int = 0) -> None:
     """events: optional list of 10 * n_layers torch.cuda.Event(enable_timing=True),
-    recorded around each per-layer stage (see include/rift.h)."""
+    recorded around each per-layer stage (see include/rift.h).  n_prefix > 0:
+    sequence 0 is a prefix shared by every other sequence."""
     torch = _torch()
     T = x_in.shape[0]
     if len(layers) != cfg.n_layers:
@@ -363,7 +367,7 @@ def rift_prefill(cfg: ModelCfg, layers: Sequence[dict], x_in, cu_seqlens, positi
                 e.record()
         ev = (ctypes.c_void_p * len(events))(*[int(e.cuda_event) for e in events])
     st = load().rift_prefill(ctypes.byref(cfg), arr, _ptr(x_in), _dt_code(x_in), _ptr(cu_seqlens),
-                             _ptr(position_ids), int(n_seq), int(T), int(max_seqlen),
+                             _ptr(position_ids), int(n_seq), int(T), int(max_seqlen), int(n_prefix),
                              _ptr(hidden_out), _ptr(kv_cache), _ptr(workspace), workspace.numel(),
                              ev, _stream(stream))
     _check(st, "rift_prefill")
@@ -376,9 +380,11 @@ def rift_decode_workspace_size(cfg: ModelCfg, n_seq: int, max_seqlen: int, max_n
 
 def rift_decode_step(cfg: ModelCfg, layers: Sequence[dict], x_new, cu_seqlens, total_tokens: int,
                      max_seqlen: int, kv_cache, kv_new, step: int, hidden_out, workspace,
-                     stream=None) -> None:
+                     stream=None, n_prefix: int = 0) -> None:
     """One generated token per prompt after rift_prefill (include/rift.h).
-    x_new [n_seq][d] bf16; kv_new [n_layers][2][n_seq][max_new][d] bf16."""
+    x_new [n_seq][d] bf16; kv_new [n_layers][2][n_seq][max_new][d] bf16;
+    n_prefix > 0: the prefill's sequence 0 was a shared prefix (cu_seqlens then
+    has n_seq + 2 entries)."""
     torch = _torch()
     n_seq = x_new.shape[0]
     if len(layers) != cfg.n_layers:
@@ -387,7 +393,7 @@ def rift_decode_step(cfg: ModelCfg, layers: Sequence[dict], x_new, cu_seqlens, t
         for n, v in w.items():
             _need(v, torch.bfloat16, None, n)
     _need(x_new, torch.bfloat16, (n_seq, cfg.d), "x_new")
-    _need(cu_seqlens, torch.int32, (n_seq + 1,), "cu_seqlens")
+    _need(cu_seqlens, torch.int32, (n_seq + (2 if n_prefix > 0 else 1),), "cu_seqlens")
     _need(kv_new, torch.bfloat16, None, "kv_new")
     if kv_new.dim() != 5 or tuple(kv_new.shape[:3]) != (cfg.n_layers, 2, n_seq) or kv_new.shape[4] != cfg.d:
         raise ValueError("kv_new must be [n_layers][2][n_seq][max_new][d]")
@@ -397,7 +403,7 @@ def rift_decode_step(cfg: ModelCfg, layers: Sequence[dict], x_new, cu_seqlens, t
     _need(workspace, torch.uint8, None, "workspace")
     arr = (LayerWeights * max(1, len(layers)))(*[layer_struct(w) for w in layers])
     st = load().rift_decode_step(ctypes.byref(cfg), arr, _ptr(x_new), _ptr(cu_seqlens), int(n_seq),
-                                 int(total_tokens), int(max_seqlen), _ptr(kv_cache), _ptr(kv_new),
+                                 int(total_tokens), int(max_seqlen), int(n_prefix), _ptr(kv_cache), _ptr(kv_new),
                                  int(kv_new.shape[3]), int(step), _ptr(hidden_out), _ptr(workspace),
                                  workspace.numel(), _stream(stream))
     _check(st, "rift_decode_step")

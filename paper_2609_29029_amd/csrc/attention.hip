@@ -17,6 +17,13 @@
 // Key blocks start at the sequence start, so a sequence's result does not
 // depend on how it is packed.
 //
+// Shared prefix (n_prefix > 0): sequence 0 is rows [0, n_prefix), a prefix of
+// every other sequence, computed once.  Sequence s > 0 then holds only its own
+// rows; its logical keys are the prefix rows followed by its rows, and its
+// queries sit at logical positions n_prefix onwards.  Key blocks still start
+// at logical key 0, so the result is the same, bit for bit, as with the prefix
+// packed into every sequence.
+//
 // The float32 path (small models) is a plain per-query loop.
 #include "launch.h"
 #include "rift_common.h"
@@ -43,7 +50,7 @@ __device__ __forceinline__ v4s_t lds_read_tr16(const bf16_t* p) {
 __global__ void __launch_bounds__(256, 2)
 attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
                  const bf16_t* __restrict__ v, bf16_t* __restrict__ o,
-                 const int* __restrict__ cu, int n_seq, int H, float scale_log2) {
+                 const int* __restrict__ cu, int n_seq, int H, int n_prefix, float scale_log2) {
     __shared__ __align__(16) bf16_t Ks[2][BKV * KPAD];
     __shared__ __align__(16) bf16_t Vs[2][BKV * VPAD];
 
@@ -51,6 +58,7 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
     const int head = blockIdx.x % H;
     const int s0 = cu[seq];
     const int L = cu[seq + 1] - s0;
+    const int pre = seq > 0 ? n_prefix : 0;   // logical keys before the sequence's own rows
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -84,9 +92,10 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
     float m_run = -INFINITY;
     float l_run = 0.f;
 
-    const int kv_end = (q0 + BQ) < L ? (q0 + BQ) : L;
+    // logical key range of this block and the logical position of the wave's last query
+    const int kv_end = pre + ((q0 + BQ) < L ? (q0 + BQ) : L);
     const int nkv = (kv_end + BKV - 1) / BKV;
-    const int wave_last = (qw + 31) < (L - 1) ? (qw + 31) : (L - 1);
+    const int wave_last = pre + ((qw + 31) < (L - 1) ? (qw + 31) : (L - 1));
 
     // K and V rows of a key block (clamped to the sequence): thread moves
     // 16 bytes of rows rr = (tid + 256 it) / 16 of both, into registers first
@@ -96,8 +105,9 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
         for (int it = 0; it < 4; ++it) {
             const int vec = tid + 256 * it;
             int key = kv0 + (vec >> 4);
-            key = key < L ? key : L - 1;
-            const size_t g = (size_t)(s0 + key) * ld + head_off + (vec & 15) * 8;
+            key = key < pre + L ? key : pre + L - 1;
+            const int row = key < pre ? key : s0 + key - pre;
+            const size_t g = (size_t)row * ld + head_off + (vec & 15) * 8;
             kr[it] = *reinterpret_cast<const u32x4_t*>(k + g);
             vr[it] = *reinterpret_cast<const u32x4_t*>(v + g);
         }
@@ -150,13 +160,13 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) sc[kb][i] = s[kb][i];
-            if (kv0 + BKV - 1 > qw) {
+            if (kv0 + BKV - 1 > pre + qw) {
 #pragma unroll
                 for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                     for (int i = 0; i < 16; ++i) {
                         const int key = kv0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-                        sc[kb][i] = (key <= q_eff) ? sc[kb][i] : -INFINITY;
+                        sc[kb][i] = (key <= pre + q_eff) ? sc[kb][i] : -INFINITY;
                     }
             }
             float bmax = -INFINITY;
@@ -237,11 +247,12 @@ template <int D>
 __global__ void __launch_bounds__(128)
 attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
                 const float* __restrict__ v, float* __restrict__ o, const int* __restrict__ cu,
-                int n_seq, int H, float scale) {
+                int n_seq, int H, int n_prefix, float scale) {
     const int seq = blockIdx.x % n_seq;
     const int head = blockIdx.x / n_seq;
     const int s0 = cu[seq];
     const int L = cu[seq + 1] - s0;
+    const int pre = seq > 0 ? n_prefix : 0;   // shared prefix rows [0, pre) come first
     const int ld = H * D;
     for (int i = threadIdx.x; i < L; i += blockDim.x) {
         const float* qi = q + (size_t)(s0 + i) * ld + head * D;
@@ -249,8 +260,9 @@ attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
 #pragma unroll
         for (int c = 0; c < D; ++c) acc[c] = 0.f;
         float m = -INFINITY, l = 0.f;
-        for (int j = 0; j <= i; ++j) {
-            const float* kj = k + (size_t)(s0 + j) * ld + head * D;
+        for (int jl = 0; jl <= pre + i; ++jl) {
+            const size_t row = jl < pre ? (size_t)jl : (size_t)(s0 + jl - pre);
+            const float* kj = k + row * ld + head * D;
             float s = 0.f;
 #pragma unroll
             for (int c = 0; c < D; ++c) s = fmaf(qi[c], kj[c], s);
@@ -259,7 +271,7 @@ attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
             const float a = expf(m - mn);
             const float p = expf(s - mn);
             l = l * a + p;
-            const float* vj = v + (size_t)(s0 + j) * ld + head * D;
+            const float* vj = v + row * ld + head * D;
 #pragma unroll
             for (int c = 0; c < D; ++c) acc[c] = acc[c] * a + p * vj[c];
             m = mn;
@@ -274,27 +286,27 @@ attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
 
 hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                  uint16_t* o, const int* cu, int n_seq, int max_seqlen,
-                                 int n_heads, hipStream_t st) {
+                                 int n_heads, int n_prefix, hipStream_t st) {
     if (n_seq <= 0 || max_seqlen <= 0) return hipSuccess;
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)HD);
     const long long blocks = (long long)n_seq * n_heads;
     hipLaunchKernelGGL(attn_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, st, q, k, v, o, cu,
-                       n_seq, n_heads, scale_log2);
+                       n_seq, n_heads, n_prefix, scale_log2);
     return hipGetLastError();
 }
 
 hipError_t launch_attention_f32(const float* q, const float* k, const float* v, float* o,
                                 const int* cu, int n_seq, int max_seqlen, int n_heads, int hd,
-                                hipStream_t st) {
+                                int n_prefix, hipStream_t st) {
     if (n_seq <= 0 || max_seqlen <= 0) return hipSuccess;
     const float scale = 1.0f / sqrtf((float)hd);
     const dim3 grid((unsigned)(n_seq * n_heads));
     if (hd == 64)
         hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(128), 0, st, q, k, v, o, cu, n_seq,
-                           n_heads, scale);
+                           n_heads, n_prefix, scale);
     else
         hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(128), 0, st, q, k, v, o, cu, n_seq,
-                           n_heads, scale);
+                           n_heads, n_prefix, scale);
     return hipGetLastError();
 }
 

@@ -402,8 +402,8 @@ rift_status rift_compact(const void* tokens, rift_dtype dt, int32_t n_tiles, int
                          int32_t d, const int32_t* kept_tiles, const int32_t* sel_offsets,
                          const int32_t* sel_idx, int32_t n_keep, const void* ctx_rows,
                          const int32_t* ctx_offsets, const void* sys_emb, int32_t n_sys,
-                         const void* qry_emb, int32_t n_qry, void* packed, int64_t packed_rows,
-                         int32_t* cu_seqlens, int32_t* position_ids, int32_t* status,
+                         const void* qry_emb, int32_t n_qry, int32_t shared_prefix, void* packed,
+                         int64_t packed_rows, int32_t* cu_seqlens, int32_t* position_ids, int32_t* status,
                          rift_stream stream) {
     if (sel_offsets == nullptr || cu_seqlens == nullptr || status == nullptr) return RIFT_ERR_NULL;
     if (n_keep > 0 && (tokens == nullptr || kept_tiles == nullptr)) return RIFT_ERR_NULL;
@@ -412,12 +412,13 @@ rift_status rift_compact(const void* tokens, rift_dtype dt, int32_t n_tiles, int
     if ((ctx_rows == nullptr) != (ctx_offsets == nullptr)) return RIFT_ERR_NULL;
     if (!dt_valid(dt)) return RIFT_ERR_DTYPE;
     if (n_tiles < 1 || n_v < 1 || d < 1 || n_keep < 0 || n_keep > 65535 || n_sys < 0 || n_qry < 0 ||
-        packed_rows < 0 || ((size_t)d * dt_bytes(dt)) % 16 != 0 || packed_rows > ((int64_t)1 << 25))
+        packed_rows < 0 || ((size_t)d * dt_bytes(dt)) % 16 != 0 || packed_rows > ((int64_t)1 << 25) ||
+        (shared_prefix != 0 && shared_prefix != 1))
         return RIFT_ERR_SHAPE;
     hipError_t e = launch_compact(tokens, (int)dt_bytes(dt), n_tiles, n_v, d, kept_tiles,
                                   sel_offsets, sel_idx, n_keep, ctx_rows, ctx_offsets, sys_emb, n_sys,
-                                  qry_emb, n_qry, packed, packed_rows, cu_seqlens, position_ids, status,
-                                  static_cast<hipStream_t>(stream));
+                                  qry_emb, n_qry, shared_prefix != 0, packed, packed_rows, cu_seqlens,
+                                  position_ids, status, static_cast<hipStream_t>(stream));
     return hip_status(e);
 }
 
@@ -430,13 +431,14 @@ size_t rift_prefill_workspace_size(const rift_model_cfg* cfg, int32_t total_toke
 rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* layers,
                          const void* x_in, rift_dtype x_dt, const int32_t* cu_seqlens,
                          const int32_t* position_ids, int32_t n_seq, int32_t total_tokens,
-                         int32_t max_seqlen, float* hidden_out, void* kv_cache, void* workspace,
-                         size_t ws_bytes, void* const* events, rift_stream stream) {
+                         int32_t max_seqlen, int32_t n_prefix, float* hidden_out, void* kv_cache,
+                         void* workspace, size_t ws_bytes, void* const* events, rift_stream stream) {
     rift_status cs = check_cfg(cfg);
     if (cs != RIFT_OK) return cs;
     const rift_model_cfg c = *cfg;
     if (x_dt != c.dt && x_dt != RIFT_F32) return RIFT_ERR_DTYPE;
-    if (total_tokens < 0 || n_seq < 0 || max_seqlen < 1 || max_seqlen > 65536)
+    if (total_tokens < 0 || n_seq < 0 || max_seqlen < 1 || max_seqlen > 65536 || n_prefix < 0 ||
+        n_prefix > total_tokens || n_prefix > max_seqlen || (n_prefix > 0 && n_seq < 1))
         return RIFT_ERR_SHAPE;
     // the bf16 GEMMs address operands with 32-bit byte offsets
     if (c.dt == RIFT_BF16 && (uint64_t)total_tokens * (uint64_t)(c.d > c.ffn ? c.d : c.ffn) >=
@@ -543,7 +545,7 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
             RIFT_TRY(mark(l, 1, 0));
             RIFT_TRY(launch_attention_bf16(static_cast<const uint16_t*>(qb), static_cast<const uint16_t*>(kb),
                                            static_cast<const uint16_t*>(vb), static_cast<uint16_t*>(h),
-                                           cu_seqlens, n_seq, max_seqlen, c.n_heads, st));
+                                           cu_seqlens, n_seq, max_seqlen, c.n_heads, n_prefix, st));
             RIFT_TRY(mark(l, 1, 1));
             RIFT_TRY(mark(l, 2, 0));
             RIFT_TRY(launch_gemm_resid(static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w.wo),
@@ -572,7 +574,7 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
             RIFT_TRY(mark(l, 0, 1));
             RIFT_TRY(mark(l, 1, 0));
             RIFT_TRY(launch_attention_f32(qf, kf, vf, hf, cu_seqlens, n_seq, max_seqlen, c.n_heads,
-                                          c.head_dim, st));
+                                          c.head_dim, n_prefix, st));
             RIFT_TRY(mark(l, 1, 1));
             RIFT_TRY(mark(l, 2, 0));
             RIFT_TRY(launch_gemm_f32(hf, static_cast<const float*>(w.wo), hidden_out, T, d, d, true, st));
@@ -647,8 +649,8 @@ size_t rift_decode_workspace_size(const rift_model_cfg* cfg, int32_t n_seq, int3
 
 rift_status rift_decode_step(const rift_model_cfg* cfg, const rift_layer_weights* layers, const void* x_new,
                              const int32_t* cu_seqlens, int32_t n_seq, int32_t total_tokens,
-                             int32_t max_seqlen, const void* kv_cache, void* kv_new, int32_t max_new,
-                             int32_t step, float* hidden_out, void* workspace, size_t ws_bytes,
+                             int32_t max_seqlen, int32_t n_prefix, const void* kv_cache, void* kv_new,
+                             int32_t max_new, int32_t step, float* hidden_out, void* workspace, size_t ws_bytes,
                              rift_stream stream) {
     rift_status cs = check_cfg(cfg);
     if (cs != RIFT_OK) return cs;
@@ -656,8 +658,11 @@ rift_status rift_decode_step(const rift_model_cfg* cfg, const rift_layer_weights
     if (c.dt != RIFT_BF16) return RIFT_ERR_UNSUPPORTED;
     if (n_seq < 0 || total_tokens < 0 || max_seqlen < 0 || max_new < 1 || step < 0 || step >= max_new ||
         (int64_t)max_seqlen + max_new > 16384 || (int64_t)n_seq * c.ffn >= (1ll << 31) ||
-        (int64_t)total_tokens * c.d >= (1ll << 31))
+        (int64_t)total_tokens * c.d >= (1ll << 31) || n_prefix < 0 || n_prefix > total_tokens ||
+        n_prefix > max_seqlen)
         return RIFT_ERR_SHAPE;
+    // with a shared prefix the prompts are sequences 1..n_seq of the prefill
+    const int32_t* cu_p = cu_seqlens + (n_prefix > 0 ? 1 : 0);
     if (n_seq == 0 || c.n_layers == 0) return RIFT_OK;
     if (x_new == nullptr || cu_seqlens == nullptr || kv_new == nullptr || hidden_out == nullptr ||
         workspace == nullptr || layers == nullptr || (total_tokens > 0 && kv_cache == nullptr))
@@ -689,7 +694,7 @@ rift_status rift_decode_step(const rift_model_cfg* cfg, const rift_layer_weights
         if ((x) != hipSuccess) return RIFT_ERR_HIP;   \
     } while (0)
     RIFT_TRY(launch_rope_table(rope, n_pos, c.head_dim, c.rope_base, st));
-    RIFT_TRY(launch_decode_pos(cu_seqlens, n_seq, step, pos, st));
+    RIFT_TRY(launch_decode_pos(cu_p, n_seq, n_prefix, step, pos, st));
     if (decode_skinny(c)) {
         // split-K GEMMs; the residual reduce of each layer's last GEMM also
         // applies the next layer's attention RMSNorm
@@ -707,8 +712,8 @@ rift_status rift_decode_step(const rift_model_cfg* cfg, const rift_layer_weights
             RIFT_TRY(launch_skinny_qkv(part, s_qkv, n_seq, d, rope, pos, n_pos, qb, kn, vn, max_new, step, st));
             RIFT_TRY(launch_decode_attention(qb, static_cast<const uint16_t*>(kv_cache) + (size_t)(2 * l) * td,
                                              static_cast<const uint16_t*>(kv_cache) + (size_t)(2 * l + 1) * td, kn,
-                                             vn, cu_seqlens, n_seq, total_tokens, c.n_heads, n_pos, max_new, step,
-                                             h, st));
+                                             vn, cu_p, n_seq, total_tokens, n_prefix, c.n_heads, n_pos, max_new,
+                                             step, h, st));
             RIFT_TRY(launch_skinny_gemm(h, static_cast<const uint16_t*>(w.wo), nullptr, nullptr, d, n_seq, d, d,
                                         part, st));
             RIFT_TRY(launch_skinny_resid_norm(part, s_o, n_seq, d, hidden_out, static_cast<const uint16_t*>(w.g_ffn),
@@ -750,8 +755,8 @@ rift_status rift_decode_step(const rift_model_cfg* cfg, const rift_layer_weights
         qa.d = d;
         RIFT_TRY(launch_gemm_qkv_rope(qa, st));
         RIFT_TRY(launch_kv_append(kb, vb, kn, vn, n_seq, d, max_new, step, st));
-        RIFT_TRY(launch_decode_attention(qb, kp, vp, kn, vn, cu_seqlens, n_seq, total_tokens, c.n_heads, n_pos,
-                                         max_new, step, h, st));
+        RIFT_TRY(launch_decode_attention(qb, kp, vp, kn, vn, cu_p, n_seq, total_tokens, n_prefix, c.n_heads,
+                                         n_pos, max_new, step, h, st));
         RIFT_TRY(launch_gemm_resid(h, static_cast<const uint16_t*>(w.wo), hidden_out, n_seq, d, d, st));
         RIFT_TRY(launch_rmsnorm(hidden_out, false, nullptr, w.g_ffn, true, h, true, n_seq, d, c.rms_eps, st));
         RIFT_TRY(launch_gemm_swiglu(h, static_cast<const uint16_t*>(w.w_gate), static_cast<const uint16_t*>(w.w_up),

@@ -1,7 +1,9 @@
 // Decode after prefill: one generated token per prompt and call.  Token
 // `step` of prompt i sits at position L_i + step and attends causally to the
 // prompt's keys and values, kept by the prefill (kv_cache, rotated keys), and
-// to the generated tokens' own, kept in a decode cache slot per step.  The
+// to the generated tokens' own, kept in a decode cache slot per step.  With a
+// shared prefix of P rows (the prefill's sequence 0), a prompt's keys are the
+// P prefix rows followed by its own rows, and L_i counts both.  The
 // decoder layers are those of the prefill (Sec. 2.1; LLaMA-7B shape); the
 // per-token GEMMs run on the prefill's kernels with M = n_seq.
 //
@@ -24,9 +26,12 @@ namespace {
 
 constexpr int DHD = 128;
 
-__global__ void decode_pos_kernel(const int* __restrict__ cu, int n_seq, int step, int* __restrict__ pos) {
+// cu: the prompts' own row offsets (after the shared prefix sequence when
+// n_prefix > 0)
+__global__ void decode_pos_kernel(const int* __restrict__ cu, int n_seq, int n_prefix, int step,
+                                  int* __restrict__ pos) {
     const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n_seq) pos[i] = (cu[i + 1] - cu[i]) + step;
+    if (i < n_seq) pos[i] = n_prefix + (cu[i + 1] - cu[i]) + step;
 }
 
 // 16-byte words of row i of k and v into slot `step` of prompt i
@@ -61,7 +66,7 @@ constexpr int kDecU = 4;
 __global__ void __launch_bounds__(256)
 decode_attn_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ kp, const bf16_t* __restrict__ vp,
                    const bf16_t* __restrict__ kn, const bf16_t* __restrict__ vn, const int* __restrict__ cu,
-                   int n_seq, int T, int H, int max_keys, int max_new, int step, float scale_log2,
+                   int n_seq, int T, int n_prefix, int H, int max_keys, int max_new, int step, float scale_log2,
                    bf16_t* __restrict__ o) {
     extern __shared__ float sc[];   // one score per key
     __shared__ float red[4];
@@ -74,14 +79,17 @@ decode_attn_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ kp, 
     int s0 = cu[seq];
     int L = cu[seq + 1] - s0;
     if (s0 < 0 || L < 0 || s0 + L > T) s0 = L = 0;   // offsets outside the prefill cache: no prompt keys
-    // prompt keys, then the generated ones (at most max_keys, the LDS size)
-    const int nk = min(L + step + 1, max_keys);
+    const int P = n_prefix;                           // shared prefix rows [0, P) of the cache
+    // prefix keys, the prompt's own keys, then the generated ones (at most
+    // max_keys, the LDS size)
+    const int nk = min(P + L + step + 1, max_keys);
     const int ld = H * DHD;
     const size_t hoff = (size_t)head * DHD + 8 * c;
     auto row = [&](int j, const bf16_t* prompt_base, const bf16_t* new_base) -> const u32x4_t* {
         return reinterpret_cast<const u32x4_t*>(
-            j < L ? prompt_base + (size_t)(s0 + j) * ld + hoff
-                  : new_base + ((size_t)seq * max_new + (j - L)) * ld + hoff);
+            j < P ? prompt_base + (size_t)j * ld + hoff
+                  : (j < P + L ? prompt_base + (size_t)(s0 + j - P) * ld + hoff
+                               : new_base + ((size_t)seq * max_new + (j - P - L)) * ld + hoff));
     };
     float qf[8];
     {
@@ -171,8 +179,9 @@ decode_attn_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ kp, 
 
 }  // namespace
 
-hipError_t launch_decode_pos(const int* cu, int n_seq, int step, int* pos, hipStream_t st) {
-    hipLaunchKernelGGL(decode_pos_kernel, dim3((n_seq + 255) / 256), dim3(256), 0, st, cu, n_seq, step, pos);
+hipError_t launch_decode_pos(const int* cu, int n_seq, int n_prefix, int step, int* pos, hipStream_t st) {
+    hipLaunchKernelGGL(decode_pos_kernel, dim3((n_seq + 255) / 256), dim3(256), 0, st, cu, n_seq, n_prefix, step,
+                       pos);
     return hipGetLastError();
 }
 
@@ -187,12 +196,12 @@ hipError_t launch_kv_append(const uint16_t* k, const uint16_t* v, uint16_t* kc, 
 }
 
 hipError_t launch_decode_attention(const uint16_t* q, const uint16_t* kp, const uint16_t* vp, const uint16_t* kn,
-                                   const uint16_t* vn, const int* cu, int n_seq, int T, int n_heads, int max_keys,
-                                   int max_new, int step, uint16_t* o, hipStream_t st) {
+                                   const uint16_t* vn, const int* cu, int n_seq, int T, int n_prefix, int n_heads,
+                                   int max_keys, int max_new, int step, uint16_t* o, hipStream_t st) {
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)DHD);
     hipLaunchKernelGGL(decode_attn_kernel, dim3((unsigned)(n_seq * n_heads)), dim3(256),
-                       (size_t)max_keys * sizeof(float), st, q, kp, vp, kn, vn, cu, n_seq, T, n_heads, max_keys,
-                       max_new, step, scale_log2, o);
+                       (size_t)max_keys * sizeof(float), st, q, kp, vp, kn, vn, cu, n_seq, T, n_prefix, n_heads,
+                       max_keys, max_new, step, scale_log2, o);
     return hipGetLastError();
 }
 

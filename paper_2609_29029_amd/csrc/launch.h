@@ -31,7 +31,7 @@ hipError_t launch_select(const double* token_key, int n_tiles, int n_v, const in
 hipError_t launch_compact(const void* tokens, int elem_bytes, int n_tiles, int n_v, int d,
                           const int* kept, const int* offs, const int* sel, int n_keep,
                           const void* ctx, const int* coffs, const void* sys, int n_sys,
-                          const void* qry, int n_qry, void* packed, long long cap, int* cu,
+                          const void* qry, int n_qry, bool shared, void* packed, long long cap, int* cu,
                           int* pos_ids, int* status, hipStream_t st);
 
 // optional merge of the remainder into contextual tokens; workspace arrays
@@ -78,18 +78,18 @@ hipError_t launch_gemm_swiglu(const uint16_t* a, const uint16_t* wg, const uint1
 // Varlen causal attention, bf16, head_dim 128.  q, k, v, o: [T][H*128].
 hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                  uint16_t* o, const int* cu, int n_seq, int max_seqlen,
-                                 int n_heads, hipStream_t st);
+                                 int n_heads, int n_prefix, hipStream_t st);
 
 // ---------------------------------------------------------------- decode (bf16)
 // pos[i] = (cu[i+1] - cu[i]) + step
-hipError_t launch_decode_pos(const int* cu, int n_seq, int step, int* pos, hipStream_t st);
+hipError_t launch_decode_pos(const int* cu, int n_seq, int n_prefix, int step, int* pos, hipStream_t st);
 // rows of k, v [n_seq][d] into slot `step` of kc, vc [n_seq][max_new][d]
 hipError_t launch_kv_append(const uint16_t* k, const uint16_t* v, uint16_t* kc, uint16_t* vc, int n_seq, int d,
                             int max_new, int step, hipStream_t st);
 // one query per prompt over its prefill keys kp/vp [T][H*128] and slots 0..step of kn/vn
 hipError_t launch_decode_attention(const uint16_t* q, const uint16_t* kp, const uint16_t* vp, const uint16_t* kn,
-                                   const uint16_t* vn, const int* cu, int n_seq, int T, int n_heads, int max_keys,
-                                   int max_new, int step, uint16_t* o, hipStream_t st);
+                                   const uint16_t* vn, const int* cu, int n_seq, int T, int n_prefix, int n_heads,
+                                   int max_keys, int max_new, int step, uint16_t* o, hipStream_t st);
 
 // Decode-shaped GEMMs (few rows): K split into S chunks (S from N and K only),
 // float32 partials part[S][M][N] of A [M][K] times the weight regions b0|b1|b2
@@ -121,7 +121,7 @@ hipError_t launch_swiglu_f32(const float* g, const float* u, float* a, long long
                              hipStream_t st);
 hipError_t launch_attention_f32(const float* q, const float* k, const float* v, float* o,
                                 const int* cu, int n_seq, int max_seqlen, int n_heads, int hd,
-                                hipStream_t st);
+                                int n_prefix, hipStream_t st);
 // elementwise widening copy of a [rows][d] matrix into f32
 hipError_t launch_to_f32(const void* x, bool x_bf16, float* out, long long n, hipStream_t st);
 // copy f32 -> storage type (for KV-cache output of the f32 path / bf16 keys)

@@ -9,7 +9,9 @@ the whole query is enqueued without a device-to-host copy.  Threshold mode
 policy reads the kept tiles' normalised scores back once (they stand in for the
 object probability p) and assigns budgets on the host.  With `merge`, each
 budget is split into dominant and contextual tokens (VisionZip's merge of the
-remainder); the prompt length stays the budget.
+remainder); the prompt length stays the budget.  With `shared_prefix` the
+system rows, the same at the head of every prompt, are packed and prefilled
+once as sequence 0; the prompts' results are unchanged (causal attention).
 """
 from __future__ import annotations
 
@@ -40,7 +42,7 @@ class SceneQuery:
                  shape: PrefillShape, keep_count: int, tau: float, levels: Sequence[int],
                  tier_num: Optional[Sequence[int]], tier_den: int, with_sims: bool = True,
                  stream=None, knn_m: int = 0, utility: Optional[dict] = None,
-                 merge: Optional[Sequence[int]] = None):
+                 merge: Optional[Sequence[int]] = None, shared_prefix: bool = False):
         import torch
         self.torch = torch
         self.dev = tokens.device
@@ -55,6 +57,8 @@ class SceneQuery:
         self.utility = utility
         # merge: (num, den) of the contextual share of each budget, or None
         self.merge = None if merge is None else (int(merge[0]), int(merge[1]))
+        self.shared = bool(shared_prefix)
+        self.n_prefix = sys_emb.shape[0] if self.shared else 0
         n_tiles, n_v, d = tokens.shape
         self.n_tiles, self.n_v, self.d = n_tiles, n_v, d
         nq = qbank.shape[0]
@@ -100,8 +104,11 @@ class SceneQuery:
             dom, ctx = budgets, np.zeros(len(budgets), dtype=np.int32)
         self.n_dominant, self.n_context = int(dom.sum()), int(ctx.sum())
         fixed = self.sys.shape[0] + self.qry.shape[0]
-        self.total_tokens = n_keep * fixed + total
         self.max_seqlen = fixed + (int(budgets.max()) if n_keep > 0 else 0)
+        if self.shared:
+            self.total_tokens = self.n_prefix + n_keep * self.qry.shape[0] + total
+        else:
+            self.total_tokens = n_keep * fixed + total
         dev = self.dev
         self.budgets = torch.from_numpy(budgets).to(dev) if n_keep > 0 else \
             torch.zeros(1, dtype=torch.int32, device=dev)
@@ -118,8 +125,8 @@ class SceneQuery:
                 self._mws_cap = mws
         # buffers grow to the largest plan seen and are reused
         T, P = self.total_tokens, max(1, self.max_seqlen)
-        if n_keep + 1 > self._cap[0] or T > self._cap[1] or self._planned_keep is None:
-            cap_keep = max(n_keep + 1, self._cap[0])
+        if n_keep + 2 > self._cap[0] or T > self._cap[1] or self._planned_keep is None:
+            cap_keep = max(n_keep + 2, self._cap[0])
             cap_T = max(T, self._cap[1], 1)
             self.sel_offsets_all = torch.empty(cap_keep, dtype=torch.int32, device=dev)
             self.cu_seqlens_all = torch.empty(cap_keep, dtype=torch.int32, device=dev)
@@ -130,7 +137,8 @@ class SceneQuery:
             self._cap = (cap_keep, cap_T)
             self._ws_cap = 0
         self.sel_offsets = self.sel_offsets_all[:n_keep + 1]
-        self.cu_seqlens = self.cu_seqlens_all[:n_keep + 1]
+        self.cu_seqlens = self.cu_seqlens_all[:n_keep + (2 if self.shared else 1)]
+        self.n_seq = n_keep + (1 if self.shared else 0)   # sequences of the prefill
         self.packed = self.packed_all[:T]
         self.position_ids = self.position_all[:T]
         self.hidden = self.hidden_all[:T]
@@ -163,14 +171,14 @@ class SceneQuery:
                        self.sys, self.qry, self.packed, self.cu_seqlens, self.position_ids,
                        self.cmp_status, self.stream,
                        ctx_rows=self.ctx_rows if merging else None,
-                       ctx_offsets=self.ctx_offsets if merging else None)
+                       ctx_offsets=self.ctx_offsets if merging else None, shared_prefix=self.shared)
 
     def prefill(self, events=None) -> None:
         if self.total_tokens == 0:
             return
         R.rift_prefill(self.cfg, self.layers, self.packed, self.cu_seqlens, self.position_ids,
-                       self.n_keep, max(1, self.max_seqlen), self.hidden, self.prefill_ws,
-                       events=events, stream=self.stream)
+                       self.n_seq, max(1, self.max_seqlen), self.hidden, self.prefill_ws,
+                       events=events, stream=self.stream, n_prefix=self.n_prefix)
 
     def plan_utility(self) -> None:
         """Eq. 2 budgets for the kept tiles, with each tile's normalised score u

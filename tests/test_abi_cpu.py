@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol(R):
     assert tuple(names) == R.EXPORTS
     for n in names:
         assert hasattr(L, n), n
-    assert L.rift_abi_version() == 5
+    assert L.rift_abi_version() == 6
     assert L.rift_status_string(4).decode().startswith("budget")
 
 
@@ -121,13 +121,16 @@ def test_select_and_compact_validation(R):
     assert L.rift_select_tokens(FAKE, 4, 576, FAKE, FAKE, 2, FAKE, FAKE, 1 << 31, FAKE, None) == 2
     # compact
     c = L.rift_compact
-    assert c(FAKE, 1, 4, 576, 4096, FAKE, None, FAKE, 2, None, None, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 1
-    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, 2, None, None, None, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 1
-    assert c(FAKE, 9, 4, 576, 4096, FAKE, FAKE, FAKE, 2, None, None, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 3
-    assert c(FAKE, 1, 4, 576, 4, FAKE, FAKE, FAKE, 2, None, None, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 2
-    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, -1, None, None, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE, FAKE, None) == 2
+    assert c(FAKE, 1, 4, 576, 4096, FAKE, None, FAKE, 2, None, None, FAKE, 35, FAKE, 32, 0, FAKE, 100, FAKE, FAKE, FAKE, None) == 1
+    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, 2, None, None, None, 35, FAKE, 32, 0, FAKE, 100, FAKE, FAKE, FAKE, None) == 1
+    assert c(FAKE, 9, 4, 576, 4096, FAKE, FAKE, FAKE, 2, None, None, FAKE, 35, FAKE, 32, 0, FAKE, 100, FAKE, FAKE, FAKE, None) == 3
+    assert c(FAKE, 1, 4, 576, 4, FAKE, FAKE, FAKE, 2, None, None, FAKE, 35, FAKE, 32, 0, FAKE, 100, FAKE, FAKE, FAKE, None) == 2
+    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, -1, None, None, FAKE, 35, FAKE, 32, 0, FAKE, 100, FAKE, FAKE, FAKE, None) == 2
     # two waves per packed row: at most 2^25 rows
-    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, 2, None, None, FAKE, 35, FAKE, 32, FAKE, (1 << 25) + 1, FAKE, FAKE, FAKE,
+    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, 2, None, None, FAKE, 35, FAKE, 32, 0, FAKE, (1 << 25) + 1, FAKE, FAKE, FAKE,
+             None) == 2
+    # shared_prefix is 0 or 1
+    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, 2, None, None, FAKE, 35, FAKE, 32, 2, FAKE, 100, FAKE, FAKE, FAKE,
              None) == 2
 
 
@@ -140,14 +143,17 @@ def test_prefill_validation_and_workspace(R):
     assert expect <= ws <= expect + 8 * 256
     lw = (R.LayerWeights * 1)(R.LayerWeights(*([FAKE] * 9)))
 
-    def call(c, T=10, n_seq=1, max_len=10, x=FAKE, x_dt=1, wsb=1 << 40):
-        return L.rift_prefill(ctypes.byref(c), lw, x, x_dt, FAKE, FAKE, n_seq, T, max_len, FAKE, None,
+    def call(c, T=10, n_seq=1, max_len=10, x=FAKE, x_dt=1, wsb=1 << 40, n_prefix=0):
+        return L.rift_prefill(ctypes.byref(c), lw, x, x_dt, FAKE, FAKE, n_seq, T, max_len, n_prefix, FAKE, None,
                               0x10000, wsb, None, None)
     assert call(cfg, T=0) == 0                              # nothing to do
     assert call(cfg, x=None) == 1
     assert call(cfg, x_dt=5) == 3
     assert call(cfg, max_len=0) == 2 and call(cfg, n_seq=-1) == 2
     assert call(cfg, wsb=100) == 5
+    # a shared prefix: within the batch and max_seqlen, with at least one sequence
+    assert call(cfg, n_prefix=-1) == 2 and call(cfg, n_prefix=11) == 2
+    assert call(cfg, T=20, max_len=10, n_prefix=11) == 2 and call(cfg, n_seq=0, n_prefix=3) == 2
     for bad in (R.model_cfg(4096, 64, 64, 11008, 1, 1e-6, 1e4, R.RIFT_BF16),    # bf16 needs head_dim 128
                 R.model_cfg(4160, 32, 130, 11008, 1, 1e-6, 1e4, R.RIFT_BF16),
                 R.model_cfg(256, 4, 64, 690, 1, 1e-6, 1e4, R.RIFT_F32)):        # ffn % 16
@@ -237,7 +243,7 @@ def test_split_budgets_and_merge_validation(R):
     assert m(FAKE, 7, 4, 576, 4096, FAKE, FAKE, FAKE, FAKE, 2, FAKE, 10, FAKE, 4096, ws, None) == 3
     # compact: contextual rows and offsets go together
     c = L.rift_compact
-    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, 2, FAKE, None, FAKE, 35, FAKE, 32, FAKE, 100, FAKE, FAKE,
+    assert c(FAKE, 1, 4, 576, 4096, FAKE, FAKE, FAKE, 2, FAKE, None, FAKE, 35, FAKE, 32, 0, FAKE, 100, FAKE, FAKE,
              FAKE, None) == 1
 
 
@@ -251,10 +257,13 @@ def test_decode_validation(R):
     assert ws > 0 and R.rift_decode_workspace_size(cfg, 4, 643, 0) == 0
     lw = (R.LayerWeights * 1)(R.LayerWeights(*([FAKE] * 9)))
     d = L.rift_decode_step
-    assert d(ctypes.byref(f32), lw, FAKE, FAKE, 4, 100, 643, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 7
-    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 643, FAKE, FAKE, 8, 8, FAKE, FAKE, ws, None) == 2  # step
-    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 16380, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 2
-    assert d(ctypes.byref(cfg), lw, None, FAKE, 4, 100, 643, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 1
-    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 643, None, FAKE, 8, 0, FAKE, FAKE, ws, None) == 1
-    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 643, FAKE, FAKE, 8, 0, FAKE, FAKE, ws - 1, None) == 5
-    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 0, 0, 643, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 0  # no prompts
+    assert d(ctypes.byref(f32), lw, FAKE, FAKE, 4, 100, 643, 0, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 7
+    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 643, 0, FAKE, FAKE, 8, 8, FAKE, FAKE, ws, None) == 2  # step
+    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 16380, 0, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 2
+    assert d(ctypes.byref(cfg), lw, None, FAKE, 4, 100, 643, 0, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 1
+    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 643, 0, None, FAKE, 8, 0, FAKE, FAKE, ws, None) == 1
+    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 643, 0, FAKE, FAKE, 8, 0, FAKE, FAKE, ws - 1, None) == 5
+    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 0, 0, 643, 0, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 0  # no prompts
+    # shared prefix longer than the prefill batch, or negative
+    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 643, 101, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 2
+    assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 643, -1, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 2

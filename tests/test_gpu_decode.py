@@ -182,3 +182,55 @@ def test_decode_two_row_tiles(R):
     R.rift_decode_step(cfg, [W], upload(new[0, 129:130], "bf16"), cu1, L, L, kv, kvn, 0, out, dws)
     torch.cuda.synchronize()
     assert np.array_equal(out.cpu().numpy()[0].astype(np.float64), got[0, 129])
+
+
+def test_decode_after_shared_prefix_matches_unshared(R):
+    """Decode after a prefill whose system rows were shared (n_prefix) gives
+    the same outputs, bit for bit, as after the per-prompt packing: the prompt's
+    keys are the prefix rows then its own, in the same order."""
+    torch = torch_mod()
+    w = synth.get("one_tile")
+    m = w.model
+    rng = np.random.default_rng(21)
+    store = lambda a: synth.store(a.astype(np.float32), "bf16")
+    P, own = 6, [4, 11, 1]
+    prefix = store(rng.standard_normal((P, m.d)))
+    rows = [store(rng.standard_normal((L, m.d))) for L in own]
+    steps = 2
+    new = store(rng.standard_normal((steps, len(own), m.d)))
+    W = upload_layer(synth.make_layer(w, 0), "bf16")
+    cfg = R.model_cfg(m.d, m.n_heads, m.head_dim, m.ffn, 1, m.rms_eps, m.rope_base, R.RIFT_BF16)
+    Lmax = P + max(own)
+
+    def run(shared):
+        if shared:
+            x = np.concatenate([prefix] + rows)
+            cu = np.concatenate([[0, P], P + np.cumsum(own)])
+            pos = np.concatenate([np.arange(P)] + [P + np.arange(L) for L in own])
+            n_seq = len(own) + 1
+        else:
+            x = np.concatenate([np.concatenate([prefix, r]) for r in rows])
+            cu = np.concatenate([[0], np.cumsum([P + L for L in own])])
+            pos = np.concatenate([np.arange(P + L) for L in own])
+            n_seq = len(own)
+        T = x.shape[0]
+        cu_d = torch.tensor(cu, dtype=torch.int32, device="cuda")
+        ws = torch.empty(R.rift_prefill_workspace_size(cfg, T, Lmax), dtype=torch.uint8, device="cuda")
+        kv = torch.empty(1, 2, T, m.d, dtype=torch.bfloat16, device="cuda")
+        hid = torch.empty(T, m.d, dtype=torch.float32, device="cuda")
+        R.rift_prefill(cfg, [W], upload(x, "bf16"), cu_d, torch.tensor(pos, dtype=torch.int32, device="cuda"),
+                       n_seq, Lmax, hid, ws, kv_cache=kv, n_prefix=P if shared else 0)
+        kvn = torch.empty(1, 2, len(own), steps, m.d, dtype=torch.bfloat16, device="cuda")
+        dws = torch.empty(R.rift_decode_workspace_size(cfg, len(own), Lmax, steps), dtype=torch.uint8,
+                          device="cuda")
+        outs = []
+        for t in range(steps):
+            out = torch.empty(len(own), m.d, dtype=torch.float32, device="cuda")
+            R.rift_decode_step(cfg, [W], upload(new[t], "bf16"), cu_d, T, Lmax, kv, kvn, t, out, dws,
+                               n_prefix=P if shared else 0)
+            outs.append(out)
+        torch.cuda.synchronize()
+        return np.stack([o.cpu().numpy() for o in outs])
+
+    a, b = run(False), run(True)
+    assert np.array_equal(a, b)

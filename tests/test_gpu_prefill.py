@@ -24,11 +24,11 @@ def R():
     return R
 
 
-def make_query(w, sc, layers_dev, with_sims=True):
+def make_query(w, sc, layers_dev, with_sims=True, shared_prefix=False):
     from paper_2609_29029_amd.pipeline import SceneQuery
     return SceneQuery(upload(sc.tokens, w.dtype), upload(sc.qbank, w.dtype), upload(sc.sys, w.dtype),
                       upload(sc.qry, w.dtype), layers_dev, plan_shape(w), w.keep_count, w.tau,
-                      w.levels, w.tier_num, w.tier_den, with_sims=with_sims)
+                      w.levels, w.tier_num, w.tier_den, with_sims=with_sims, shared_prefix=shared_prefix)
 
 
 def oracle_packed(w, sc):
@@ -267,3 +267,44 @@ def test_prefill_small_and_ragged_batches(R, lens):
         for i in range(len(lens)):
             alone = run(x[cu[i]:cu[i + 1]], np.array([0, lens[i]], dtype=np.int32), np.arange(lens[i], dtype=np.int32))
             assert np.array_equal(alone, hid[cu[i]:cu[i + 1]])
+
+
+@pytest.mark.parametrize("name", ["tiny", "scene8"])
+def test_shared_prefix_prefill_matches_unshared(R, name):
+    """The system rows prefilled once as a shared prefix give every prompt the
+    same hidden states and key/value cache rows, bit for bit, as packing them
+    into every prompt (two layers; the attention's key blocks start at the
+    same logical key)."""
+    torch = torch_mod()
+    w = synth.get(name)
+    sc = synth.make_scene(w)
+    Wd = upload_layer(synth.make_layer(w, 0), w.dtype)
+    n_sys = sc.sys.shape[0]
+    qa = make_query(w, sc, [Wd], shared_prefix=False)
+    qb = make_query(w, sc, [Wd], shared_prefix=True)
+    qa.run()
+    qb.run()
+    torch.cuda.synchronize()
+    assert qa.check_status() == [0, 0] and qb.check_status() == [0, 0]
+    assert qb.total_tokens == qa.total_tokens - (qa.n_keep - 1) * n_sys
+    cfg2 = R.model_cfg(w.model.d, w.model.n_heads, w.model.head_dim, w.model.ffn, 2, w.model.rms_eps,
+                       w.model.rope_base, qa.cfg.dt)
+    outs = []
+    for q in (qa, qb):
+        T = q.total_tokens
+        ws = torch.empty(R.rift_prefill_workspace_size(cfg2, T, q.max_seqlen), dtype=torch.uint8, device="cuda")
+        kv = torch.empty(2, 2, T, w.model.d, dtype=q.packed.dtype, device="cuda")
+        hid = torch.empty(T, w.model.d, dtype=torch.float32, device="cuda")
+        R.rift_prefill(cfg2, [Wd, Wd], q.packed, q.cu_seqlens, q.position_ids, q.n_seq, q.max_seqlen, hid, ws,
+                       kv_cache=kv, n_prefix=q.n_prefix)
+        torch.cuda.synchronize()
+        outs.append((hid.cpu().numpy(), kv.float().cpu().numpy(), q.cu_seqlens.cpu().numpy()))
+    (ha, ka, cua), (hb, kb, cub) = outs
+    assert cub[1] == n_sys and len(cub) == len(cua) + 1
+    for i in range(qa.n_keep):
+        a0, a1 = int(cua[i]), int(cua[i + 1])
+        b0, b1 = int(cub[i + 1]), int(cub[i + 2])
+        assert np.array_equal(ha[a0:a0 + n_sys], hb[:n_sys]), i
+        assert np.array_equal(ha[a0 + n_sys:a1], hb[b0:b1]), i
+        assert np.array_equal(ka[:, :, a0:a0 + n_sys], kb[:, :, :n_sys]), i
+        assert np.array_equal(ka[:, :, a0 + n_sys:a1], kb[:, :, b0:b1]), i

@@ -218,23 +218,40 @@ def test_select_empty(R):
 
 
 # ----------------------------------------------------------------------------- compact
-def run_compact(R, X, dtype, kept, offs, sel, sysr, qry, rows=None):
+def run_compact(R, X, dtype, kept, offs, sel, sysr, qry, rows=None, shared=False):
     torch = torch_mod()
     n_keep = len(kept)
-    T = n_keep * (sysr.shape[0] + qry.shape[0]) + int(offs[-1])
+    if shared:
+        T = sysr.shape[0] + n_keep * qry.shape[0] + int(offs[-1])
+    else:
+        T = n_keep * (sysr.shape[0] + qry.shape[0]) + int(offs[-1])
     rows = T if rows is None else rows
     Xd = upload(X, dtype)
     packed = torch.zeros(rows, X.shape[-1], dtype=Xd.dtype, device="cuda")
-    cu = torch.full((n_keep + 1,), -7, dtype=torch.int32, device="cuda")
+    cu = torch.full((n_keep + (2 if shared else 1),), -7, dtype=torch.int32, device="cuda")
     pos = torch.full((rows,), -7, dtype=torch.int32, device="cuda")
     st = torch.full((1,), -7, dtype=torch.int32, device="cuda")
     kept_d = torch.tensor(list(kept) or [0], dtype=torch.int32, device="cuda")
     offs_d = torch.tensor(list(offs), dtype=torch.int32, device="cuda")
     sel_d = torch.tensor(list(sel) or [0], dtype=torch.int32, device="cuda")
     R.rift_compact(Xd, kept_d, offs_d, sel_d, n_keep, upload(sysr, dtype), upload(qry, dtype),
-                   packed, cu, pos, st)
+                   packed, cu, pos, st, shared_prefix=shared)
     torch.cuda.synchronize()
     return download_stored(packed, dtype), cu.cpu().numpy(), pos.cpu().numpy(), int(st.item())
+
+
+def shared_layout(r_packed, r_cu, r_pos, n_sys):
+    """The oracle's per-prompt layout rearranged as a shared prefix: the first
+    prompt's n_sys system rows once, then every prompt's rows after them."""
+    rows = [r_packed[:n_sys]]
+    pos = [np.arange(n_sys)]
+    cu = [0, n_sys]
+    for i in range(len(r_cu) - 1):
+        a, b = int(r_cu[i]) + n_sys, int(r_cu[i + 1])
+        rows.append(r_packed[a:b])
+        pos.append(r_pos[a:b])
+        cu.append(cu[-1] + b - a)
+    return np.concatenate(rows), np.array(cu), np.concatenate(pos)
 
 
 @pytest.mark.parametrize("name", ["tiny", "scene8"])
@@ -311,3 +328,41 @@ def test_score_knn_smoothing_full_size(R):
                     sims=False, knn_m=6)
     ref = O.scene_query_stage1(X64, Q64, w.keep_count, w.tau, knn_m=6)
     check_stage1(got, ref, X64, Q64, sims=False)
+
+
+@pytest.mark.parametrize("name", ["tiny", "scene8"])
+def test_compact_shared_prefix(R, name):
+    """Shared-prefix layout: the system rows once at the front (sequence 0),
+    each prompt's own rows after them at positions n_sys onwards; bit for bit
+    the oracle's packing rearranged."""
+    w = synth.get(name)
+    sc = synth.make_scene(w)
+    ref = oracle_stage1(sc, w.keep_count, w.tau)
+    kept = list(ref["order"][: ref["n_keep"]])
+    budgets = O.assign_budgets(len(kept), w.levels, w.tier_num, w.tier_den)
+    offs, sel = O.select_tokens(ref["r"], kept, budgets)
+    packed, cu, pos, st = run_compact(R, sc.tokens, w.dtype, kept, offs, sel, sc.sys, sc.qry, shared=True)
+    e_packed, e_cu, e_pos = shared_layout(*O.compact(sc.tokens, kept, offs, sel, sc.sys, sc.qry), sc.sys.shape[0])
+    assert st == 0
+    assert np.array_equal(packed, e_packed) and np.array_equal(cu, e_cu) and np.array_equal(pos, e_pos)
+
+
+def test_compact_shared_prefix_edges(R):
+    rng = np.random.default_rng(4)
+    X = synth.store(rng.standard_normal((4, 20, 64)).astype(np.float32), "bf16")
+    sysr = synth.store(rng.standard_normal((3, 64)).astype(np.float32), "bf16")
+    qry = synth.store(rng.standard_normal((2, 64)).astype(np.float32), "bf16")
+    kept, offs, sel = [3, 1], np.array([0, 0, 20]), np.arange(20)
+    packed, cu, pos, st = run_compact(R, X, "bf16", kept, offs, sel, sysr, qry, shared=True)
+    e = shared_layout(*O.compact(X, kept, offs, sel, sysr, qry), 3)
+    assert st == 0 and np.array_equal(packed, e[0]) and np.array_equal(cu, e[1]) and np.array_equal(pos, e[2])
+    # nothing kept: the prefix alone
+    packed, cu, pos, st = run_compact(R, X, "bf16", [], np.array([0]), np.zeros(0, int), sysr, qry, shared=True)
+    assert st == 0 and list(cu) == [0, 3] and np.array_equal(packed, sysr) and list(pos) == [0, 1, 2]
+    # capacity too small
+    packed, cu, pos, st = run_compact(R, X, "bf16", kept, offs, sel, sysr, qry, rows=10, shared=True)
+    assert st == 2
+    # no system rows: an empty prefix sequence
+    packed, cu, pos, st = run_compact(R, X, "bf16", kept, offs, sel, sysr[:0], qry, shared=True)
+    e = O.compact(X, kept, offs, sel, sysr[:0], qry)
+    assert st == 0 and np.array_equal(packed, e[0]) and list(cu) == [0] + list(e[1]) and np.array_equal(pos, e[2])
