@@ -35,24 +35,30 @@ KERNEL_NAMES = {"qkv_rope": "QKV+RoPE GEMM (gemm_bf16_pp_kernel<0> + half-tile t
                 "down_proj": "down projection + residual (gemm_bf16_w8_kernel<1> + half-tile tail)"}
 GEMM_SRC = os.path.join(ROOT, "paper_2609_29029_amd", "csrc", "gemm_bf16.hip")
 
-# HBM traffic of one gate/up+SwiGLU launch at the 400-tile workload (whole tiles
-# and the half-tile tail together), from two rocprofv3 --pmc runs of this
+# HBM traffic of one gate/up+SwiGLU launch at the 400-tile workload with the shared
+# system prefix (T = 18,739 packed rows), from two rocprofv3 --pmc runs of this
 # script with --traffic-calibration (FETCH_SIZE, then WRITE_SIZE), each scaled
 # by what the counter reads for the 1 GiB calibration copy (FETCH_SIZE reads
 # half the bytes, WRITE_SIZE all of them).  Valid only for the GEMM source it
 # was measured on, identified by its SHA-256; otherwise reported as null.
 TRAFFIC = {"stage": "gate_up_swiglu",
            "gemm_src_sha256": "ad16afa1ec10e20dd691986344eb854b8a153320596be793a9425b9f1e9fa952",
-           "bytes": 7.1492e9}
+           "packed_tokens": 18739,
+           "bytes": 6.5730e9}
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def stage_flops(T: int, d: int, ffn: int, seq_lens) -> dict:
-    """Algorithmic flops of one launch of each prefill stage (one layer)."""
-    attn = sum(2 * 2 * d * L * (L + 1) // 2 for L in seq_lens)  # QK^T and PV over the causal triangle
+def stage_flops(T: int, d: int, ffn: int, seq_lens, n_prefix: int = 0) -> dict:
+    """Algorithmic flops of one launch of each prefill stage (one layer) over
+    T packed rows.  seq_lens are the prompts' whole lengths; with a shared
+    prefix of n_prefix rows its causal triangle is computed once, and each
+    prompt's own queries attend to the prefix and to their own earlier rows."""
+    P = n_prefix
+    attn = sum(2 * 2 * d * (L * (L + 1) // 2 - P * (P + 1) // 2) for L in seq_lens)
+    attn += 2 * 2 * d * P * (P + 1) // 2   # QK^T and PV over the causal triangles
     return {"qkv_rope": 2 * T * d * 3 * d, "attention": attn, "out_proj": 2 * T * d * d,
             "gate_up_swiglu": 2 * T * d * 2 * ffn, "down_proj": 2 * T * ffn * d}
 
@@ -100,20 +106,23 @@ def cpu_baseline(w, sc, seq_lens_by_tier, n_tiles_sample: int, n_layers_sample: 
                        f"thread, BLAS on {blas_threads}")}
 
 
-def exhaustive_setup(R, torch, w, tokens, qbank, sysd, qryd, layers, cfg, chunk: int = 50):
+def exhaustive_setup(R, torch, w, tokens, qbank, sysd, qryd, layers, cfg, chunk: int = 50,
+                     shared: bool = True):
     """Every tile kept at the full budget n_v: the no-pruning baseline the
     paper compares against.  Same kernels; the prefill runs as consecutive
     calls of `chunk` prompts each (all prompts have the same length), since one
-    call is limited to T * max(d, ffn) < 2^31.  Returns a function that enqueues
-    one whole exhaustive query on the current stream and returns its status
-    words, and the query's shape."""
+    call is limited to T * max(d, ffn) < 2^31.  With `shared`, as in the Rift
+    query, each call's prompts share their system rows (packed once per call).
+    Returns a function that enqueues one whole exhaustive query on the current
+    stream and returns its status words, and the query's shape."""
     n, nv, d = tokens.shape
     dev = tokens.device
     f64, f32, i32 = torch.float64, torch.float32, torch.int32
     nq = qbank.shape[0]
     fixed = sysd.shape[0] + qryd.shape[0]
+    P = sysd.shape[0] if shared else 0
     L = nv + fixed
-    T = n * L
+    Lown = L - P                      # packed rows of a prompt after a shared prefix
     key = torch.empty(n * nv, dtype=f64, device=dev)
     sim = torch.empty(n * nv, nq, dtype=f32, device=dev)
     score = torch.empty(n, dtype=f64, device=dev)
@@ -125,26 +134,31 @@ def exhaustive_setup(R, torch, w, tokens, qbank, sysd, qryd, layers, cfg, chunk:
     offs = torch.empty(n + 1, dtype=i32, device=dev)
     sel = torch.empty(n * nv, dtype=i32, device=dev)
     st1 = torch.empty(1, dtype=i32, device=dev)
-    packed = torch.empty(T, d, dtype=tokens.dtype, device=dev)
-    cu = torch.empty(n + 1, dtype=i32, device=dev)
-    pos = torch.empty(T, dtype=i32, device=dev)
-    st2 = torch.empty(1, dtype=i32, device=dev)
     chunks = [(c, min(n, c + chunk)) for c in range(0, n, chunk)]
-    cu_c = {m: torch.arange(0, m + 1, dtype=i32, device=dev) * L for m in {b - a for a, b in chunks}}
-    ws = torch.empty(R.rift_prefill_workspace_size(cfg, chunk * L, L), dtype=torch.uint8, device=dev)
-    hid = torch.empty(chunk * L, d, dtype=f32, device=dev)
+    # one packed batch per prefill call: [system rows once | prompts' own rows]
+    Tc = {m: P + m * Lown for m in {b - a for a, b in chunks}}
+    T = sum(P + (b - a) * Lown for a, b in chunks)
+    packed = torch.empty(max(Tc.values()), d, dtype=tokens.dtype, device=dev)
+    cu = torch.empty(chunk + 2, dtype=i32, device=dev)
+    pos = torch.empty(max(Tc.values()), dtype=i32, device=dev)
+    offs_c = torch.arange(0, chunk + 1, dtype=i32, device=dev) * nv   # every budget is n_v
+    st2 = torch.empty(len(chunks), dtype=i32, device=dev)
+    ws = torch.empty(R.rift_prefill_workspace_size(cfg, max(Tc.values()), L), dtype=torch.uint8, device=dev)
+    hid = torch.empty(max(Tc.values()), d, dtype=f32, device=dev)
 
     def run():
         R.rift_score_tiles(tokens, qbank, n, 0.0, key, sim, score, u, order, nkeep, sws)
         R.rift_select_tokens(key, n, nv, order, budgets, n, offs, sel, st1)
-        R.rift_compact(tokens, order, offs, sel, n, sysd, qryd, packed, cu, pos, st2)
-        for a, b in chunks:
+        for c, (a, b) in enumerate(chunks):
             m = b - a
-            R.rift_prefill(cfg, layers, packed[a * L:b * L], cu_c[m], pos[a * L:b * L], m, L,
-                           hid[:m * L], ws)
+            ncu = m + (2 if shared else 1)
+            R.rift_compact(tokens, order[a:b], offs_c[:m + 1], sel[a * nv:b * nv], m, sysd, qryd,
+                           packed[:Tc[m]], cu[:ncu], pos[:Tc[m]], st2[c:c + 1], shared_prefix=shared)
+            R.rift_prefill(cfg, layers, packed[:Tc[m]], cu[:ncu], pos[:Tc[m]], ncu - 1, L, hid[:Tc[m]], ws,
+                           n_prefix=P)
         return st1, st2
 
-    return run, {"packed_tokens": T, "prompts": n, "prefill_calls": len(chunks), "seq_len": L}
+    return run, {"packed_tokens": T, "prompts": n, "prefill_calls": len(chunks), "seq_len": L, "n_prefix": P}
 
 
 def exhaustive_run(run, shape, w, torch) -> dict:
@@ -155,11 +169,17 @@ def exhaustive_run(run, shape, w, torch) -> dict:
     st1, st2 = run()
     e1.record()
     torch.cuda.synchronize()
-    assert int(st1.item()) == 0 and int(st2.item()) == 0
+    assert int(st1.item()) == 0 and int(st2.abs().max().item()) == 0
     ms = e0.elapsed_time(e1)
     m = w.model
     T, L, n = shape["packed_tokens"], shape["seq_len"], shape["prompts"]
-    fl = stage_flops(T, m.d, m.ffn, [L] * n)
+    P = shape["n_prefix"]
+    per = -(-n // shape["prefill_calls"])
+    fl = {k: 0 for k in STAGES}
+    for a in range(0, n, per):   # each call's own shared prefix
+        mc = min(n, a + per) - a
+        for k, v in stage_flops(P + mc * (L - P), m.d, m.ffn, [L] * mc, P).items():
+            fl[k] += v
     tflop = sum(fl.values()) * m.n_layers / 1e12
     return {"ms": round(ms, 2), "packed_tokens": T, "prompts": n, "prefill_calls": shape["prefill_calls"],
             "tflop": round(tflop, 1), "frac_bf16_peak": round(tflop / (ms * 1e-3) / PEAK_BF16_TFLOPS, 4)}
@@ -339,7 +359,7 @@ def utility_run(R, torch, w, tokens, qbank, sysd, qryd, layers, q, reps=3) -> di
     query including that synchronisation."""
     from paper_2609_29029_amd.pipeline import SceneQuery
     uq = SceneQuery(tokens, qbank, sysd, qryd, layers, q.shape, w.keep_count, w.tau, w.levels,
-                    w.tier_num, w.tier_den, with_sims=True, utility=UTILITY)
+                    w.tier_num, w.tier_den, with_sims=True, utility=UTILITY, shared_prefix=q.shared)
     uq.run()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -362,7 +382,7 @@ def merge_run(R, torch, w, tokens, qbank, sysd, qryd, layers, q, reps=3) -> dict
     canonical dot of every non-target remaining token with every target."""
     from paper_2609_29029_amd.pipeline import SceneQuery
     mq = SceneQuery(tokens, qbank, sysd, qryd, layers, q.shape, w.keep_count, w.tau, w.levels,
-                    w.tier_num, w.tier_den, with_sims=True, merge=(10, 64))
+                    w.tier_num, w.tier_den, with_sims=True, merge=(10, 64), shared_prefix=q.shared)
     mq.run()
     torch.cuda.synchronize()
     tm, tq = [], []
@@ -400,8 +420,8 @@ def decode_run(R, torch, w, q, steps=8) -> dict:
     m = w.model
     T, n_seq, d = q.total_tokens, q.n_keep, m.d
     kv = torch.empty(m.n_layers, 2, T, d, dtype=torch.bfloat16, device="cuda")
-    R.rift_prefill(q.cfg, q.layers, q.packed, q.cu_seqlens, q.position_ids, n_seq, q.max_seqlen, q.hidden,
-                   q.prefill_ws, kv_cache=kv)
+    R.rift_prefill(q.cfg, q.layers, q.packed, q.cu_seqlens, q.position_ids, q.n_seq, q.max_seqlen, q.hidden,
+                   q.prefill_ws, kv_cache=kv, n_prefix=q.n_prefix)
     g = torch.Generator(device="cuda").manual_seed(0x52494654)
     x_new = torch.randn(steps, n_seq, d, device="cuda", generator=g).to(torch.bfloat16)
     kv_new = torch.empty(m.n_layers, 2, n_seq, steps, d, dtype=torch.bfloat16, device="cuda")
@@ -412,12 +432,14 @@ def decode_run(R, torch, w, q, steps=8) -> dict:
     torch.cuda.synchronize()
     ev[0].record()
     for t in range(steps):
-        R.rift_decode_step(q.cfg, q.layers, x_new[t], q.cu_seqlens, T, q.max_seqlen, kv, kv_new, t, out, ws)
+        R.rift_decode_step(q.cfg, q.layers, x_new[t], q.cu_seqlens, T, q.max_seqlen, kv, kv_new, t, out, ws,
+                           n_prefix=q.n_prefix)
         ev[t + 1].record()
     torch.cuda.synchronize()
     ms = [ev[t].elapsed_time(ev[t + 1]) for t in range(steps)]
     weight_bytes = m.n_layers * 2 * (4 * d * d + 3 * d * m.ffn + 2 * d)
-    kv_bytes = m.n_layers * 2 * (T + n_seq * steps / 2) * d * 2
+    keys = T + (n_seq - 1) * q.n_prefix if q.n_prefix > 0 else T   # every prompt reads the shared rows too
+    kv_bytes = m.n_layers * 2 * (keys + n_seq * steps / 2) * d * 2
     med = statistics.median(ms)
     del kv, kv_new
     return {"steps": steps, "prompts": n_seq, "ms_per_step": round(med, 3),
@@ -463,6 +485,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="scene20_l32")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-shared-prefix", action="store_true",
+                    help="pack the system rows into every prompt instead of prefilling them once")
     ap.add_argument("--cpu-sample-tiles", type=int, default=128)
     ap.add_argument("--cpu-sample-layers", type=int, default=16)
     ap.add_argument("--no-exhaustive", action="store_true",
@@ -509,9 +533,10 @@ def main() -> int:
     torch.cuda.synchronize()
     log(f"setup {time.perf_counter() - t_setup:.1f} s")
 
+    shared = not args.no_shared_prefix
     q = SceneQuery(tokens, qbank, sysd, qryd, layers,
                    PrefillShape(m.d, m.n_heads, m.head_dim, m.ffn, m.n_layers, m.rms_eps, m.rope_base),
-                   w.keep_count, w.tau, w.levels, w.tier_num, w.tier_den, with_sims=True)
+                   w.keep_count, w.tau, w.levels, w.tier_num, w.tier_den, with_sims=True, shared_prefix=shared)
     T, n_ret = q.total_tokens, q.n_selected
     budgets = [int(b) for b in q.budgets_host]
     seq_lens = [w.n_sys + b + w.n_qry for b in budgets]
@@ -574,7 +599,7 @@ def main() -> int:
         ds = [lay[s][10 * l + 2 * g].elapsed_time(lay[s][10 * l + 2 * g + 1])
               for s in range(K) for l in range(m.n_layers)]
         per_launch[name] = sum(ds) / len(ds)
-    fl = stage_flops(T, m.d, m.ffn, seq_lens)
+    fl = stage_flops(T, m.d, m.ffn, seq_lens, q.n_prefix)
     stage_roof = {n: {"ms": round(per_launch[n], 4),
                       "tflops": round(fl[n] / (per_launch[n] * 1e-3) / 1e12, 1),
                       "frac_bf16_peak": round(fl[n] / (per_launch[n] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
@@ -584,14 +609,14 @@ def main() -> int:
     with open(GEMM_SRC, "rb") as f:
         src_sha = hashlib.sha256(f.read()).hexdigest()
     traffic = (TRAFFIC["bytes"] if dom == TRAFFIC["stage"] and src_sha == TRAFFIC["gemm_src_sha256"]
-               and w.name == "scene20_l32" else None)
+               and w.name == "scene20_l32" and T == TRAFFIC["packed_tokens"] else None)
     achieved = fl[dom] / (per_launch[dom] * 1e-3) / 1e12
     prefill_flops = sum(fl.values()) * m.n_layers
     # HBM-bound stages: algorithmic bytes
     e = 2 if w.dtype == "bf16" else 4
     score_bytes = w.n_tiles * w.n_v * m.d * e + w.n_tiles * w.n_v * (8 + 4 * (1 + w.n_bg))
-    compact_bytes = n_ret * m.d * e * 2 + q.n_keep * (w.n_sys + w.n_qry) * m.d * e + \
-        (w.n_sys + w.n_qry) * m.d * e
+    # vision rows read and written, system/query rows written (read once)
+    compact_bytes = n_ret * m.d * e * 2 + (T - n_ret) * m.d * e + (w.n_sys + w.n_qry) * m.d * e
     hbm = {"score_GBs": round(score_bytes / (stage_ms["score"] * 1e-3) / 1e9, 1),
            "score_frac": round(score_bytes / (stage_ms["score"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
            "compact_GBs": round(compact_bytes / (stage_ms["compact"] * 1e-3) / 1e9, 1),
@@ -605,7 +630,8 @@ def main() -> int:
                                f"{w.keep_count}, budgets {list(w.levels)} by score rank, "
                                f"{m.n_layers}-layer LLaMA-7B-shaped varlen prefill",
                    "retained_vision_tokens": n_ret, "packed_tokens": T, "sequences": q.n_keep,
-                   "max_seqlen": q.max_seqlen, "prefill_tflop": round(prefill_flops / 1e12, 2)},
+                   "max_seqlen": q.max_seqlen, "prefill_tflop": round(prefill_flops / 1e12, 2),
+                   "shared_prefix_rows": q.n_prefix},
         "roofline": {"bound": "mfma", "kernel": KERNEL_NAMES[dom], "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic},
@@ -615,6 +641,23 @@ def main() -> int:
         "hbm": hbm,
     }
     out["packed_tokens_per_s"] = round(T * K / elapsed, 1)
+    if shared:
+        # the same query with the system rows packed into every prompt
+        uq = SceneQuery(tokens, qbank, sysd, qryd, layers, q.shape, w.keep_count, w.tau, w.levels,
+                        w.tier_num, w.tier_den, with_sims=True, shared_prefix=False)
+        uq.run()
+        torch.cuda.synchronize()
+        t_u = time.perf_counter()
+        for _ in range(3):
+            uq.run()
+        torch.cuda.synchronize()
+        ms_u = (time.perf_counter() - t_u) * 1e3 / 3
+        assert uq.check_status() == [0, 0]
+        out["unshared_prefix"] = {"ms_per_step": round(ms_u, 3), "tokens_per_s": round(n_ret / (ms_u * 1e-3), 1),
+                                  "packed_tokens": uq.total_tokens,
+                                  "speedup_of_sharing": round(ms_u / ms_step, 4)}
+        log(f"unshared prefix: {out['unshared_prefix']}")
+        del uq
     ceil = mfma_ceiling(torch)
     out["mfma_ceiling"] = ceil
     c16 = ceil["v_mfma_f32_16x16x32_bf16"]["TFLOPs"]
@@ -632,7 +675,7 @@ def main() -> int:
                                            w.n_v, q.n_keep)
     if not args.no_exhaustive:
         log("exhaustive run (every tile at the full budget) ...")
-        ex_fn, ex_shape = exhaustive_setup(R, torch, w, tokens, qbank, sysd, qryd, layers, q.cfg)
+        ex_fn, ex_shape = exhaustive_setup(R, torch, w, tokens, qbank, sysd, qryd, layers, q.cfg, shared=shared)
         ex = exhaustive_run(ex_fn, ex_shape, w, torch)
         ex["rift_ms_over_exhaustive_ms"] = round(stage_ms_total / ex["ms"], 4)
         ex["latency_reduction"] = round(1 - stage_ms_total / ex["ms"], 4)
