@@ -655,3 +655,29 @@ def test_decode_is_incremental_prefill_and_causal():
     new2[2] += 1.0
     out2 = O.decode_outputs(prompt, new2, layers, H, hd, 1e-6, 10000.0)
     assert np.array_equal(out2[:2], out[:2]) and not np.allclose(out2[2], out[2])
+
+
+def test_causal_prefix_states_do_not_depend_on_later_rows():
+    """The reading behind the shared system prefix: under causal attention the
+    states of a sequence's first P rows, after every layer, are those of the P
+    rows alone, whatever follows them (prompts that differ after a common
+    prefix agree on it to rounding)."""
+    rng = np.random.default_rng(7)
+    d, H, hd, F = 64, 4, 16, 96
+    mk = lambda *s: rng.standard_normal(s) * 0.2
+    layers = [dict(wq=mk(d, d), wk=mk(d, d), wv=mk(d, d), wo=mk(d, d), w_gate=mk(F, d), w_up=mk(F, d),
+                   w_down=mk(d, F), g_attn=1 + mk(d), g_ffn=1 + mk(d)) for _ in range(2)]
+    P = 5
+    prefix = rng.standard_normal((P, d))
+    tails = [rng.standard_normal((n, d)) for n in (0, 3, 9)]
+    outs = []
+    for tail in tails:
+        x = np.concatenate([prefix, tail])
+        cu = np.array([0, len(x)])
+        outs.append(O.prefill(x, cu, np.arange(len(x)), layers, H, hd, 1e-6, 10000.0)[0])
+    for o in outs[1:]:
+        assert np.allclose(o[:P], outs[0], rtol=1e-12, atol=1e-12)
+    # and a change inside the prefix does change what follows
+    x2 = np.concatenate([prefix + np.eye(P, d) * 0.5, tails[2]])
+    o2 = O.prefill(x2, np.array([0, len(x2)]), np.arange(len(x2)), layers, H, hd, 1e-6, 10000.0)[0]
+    assert not np.allclose(o2[P:], outs[2][P:], rtol=1e-6, atol=1e-6)
