@@ -57,3 +57,17 @@ def plan_shape(w: synth.Workload):
     from paper_2609_29029_amd.pipeline import PrefillShape
     m = w.model
     return PrefillShape(m.d, m.n_heads, m.head_dim, m.ffn, m.n_layers, m.rms_eps, m.rope_base)
+
+
+def shared_layout(r_packed, r_cu, r_pos, n_sys):
+    """The oracle's per-prompt layout rearranged as a shared prefix: the first
+    prompt's n_sys system rows once, then every prompt's rows after them."""
+    rows = [r_packed[:n_sys]]
+    pos = [np.arange(n_sys)]
+    cu = [0, n_sys]
+    for i in range(len(r_cu) - 1):
+        a, b = int(r_cu[i]) + n_sys, int(r_cu[i + 1])
+        rows.append(r_packed[a:b])
+        pos.append(r_pos[a:b])
+        cu.append(cu[-1] + b - a)
+    return np.concatenate(rows), np.array(cu), np.concatenate(pos)

@@ -7,7 +7,7 @@ import pytest
 
 import synth
 from oracle import rift_oracle as O
-from tests.rift_testlib import download_stored, f64, oracle_stage1, torch_mod, upload
+from tests.rift_testlib import shared_layout, download_stored, f64, oracle_stage1, torch_mod, upload
 
 pytestmark = pytest.mark.gpu
 
@@ -166,3 +166,38 @@ def test_merge_full_size_sampled(R):
         exp = oracle_ctx(sc.tokens, w.dtype, [rho], offs[rho:rho + 2] - offs[rho], sel[offs[rho]:offs[rho + 1]],
                          [kc[rho]])
         assert np.array_equal(got[coffs[rho]:coffs[rho + 1]], exp), rho
+
+
+def test_scene_query_with_merge_and_shared_prefix(R):
+    """The merge with the system rows shared: the packed batch is the oracle's
+    rearranged (prefix once, then each prompt's dominant, contextual and query
+    rows), and the hidden states equal those of the per-prompt packing bit for
+    bit."""
+    torch = torch_mod()
+    from paper_2609_29029_amd.pipeline import PrefillShape, SceneQuery
+    w = synth.get("scene8")
+    sc = synth.make_scene(w)
+    m = w.model
+    up = lambda a: upload(a, w.dtype)
+    layers = [{k: up(v) for k, v in synth.make_layer(w, 0).items()}]
+    qs = []
+    for shared in (False, True):
+        q = SceneQuery(up(sc.tokens), up(sc.qbank), up(sc.sys), up(sc.qry), layers,
+                       PrefillShape(m.d, m.n_heads, m.head_dim, m.ffn, 1, m.rms_eps, m.rope_base),
+                       w.keep_count, w.tau, w.levels, w.tier_num, w.tier_den, merge=(10, 64), shared_prefix=shared)
+        q.run()
+        torch.cuda.synchronize()
+        assert q.check_status() == [0, 0, 0]
+        qs.append(q)
+    qa, qb = qs
+    n_sys = sc.sys.shape[0]
+    pa, cua, posa = download_stored(qa.packed, w.dtype), qa.cu_seqlens.cpu().numpy(), qa.position_ids.cpu().numpy()
+    e_packed, e_cu, e_pos = shared_layout(pa, cua, posa, n_sys)
+    assert np.array_equal(download_stored(qb.packed, w.dtype), e_packed)
+    assert np.array_equal(qb.cu_seqlens.cpu().numpy(), e_cu) and np.array_equal(qb.position_ids.cpu().numpy(), e_pos)
+    ha, hb = qa.hidden.cpu().numpy(), qb.hidden.cpu().numpy()
+    cub = qb.cu_seqlens.cpu().numpy()
+    for i in range(qa.n_keep):
+        a0, a1 = int(cua[i]), int(cua[i + 1])
+        assert np.array_equal(ha[a0:a0 + n_sys], hb[:n_sys]), i
+        assert np.array_equal(ha[a0 + n_sys:a1], hb[int(cub[i + 1]):int(cub[i + 2])]), i

@@ -6,7 +6,7 @@ import pytest
 
 import synth
 from oracle import rift_oracle as O
-from tests.rift_testlib import f64, oracle_stage1, torch_mod, upload, download_stored
+from tests.rift_testlib import shared_layout, f64, oracle_stage1, torch_mod, upload, download_stored
 
 pytestmark = pytest.mark.gpu
 
@@ -240,18 +240,6 @@ def run_compact(R, X, dtype, kept, offs, sel, sysr, qry, rows=None, shared=False
     return download_stored(packed, dtype), cu.cpu().numpy(), pos.cpu().numpy(), int(st.item())
 
 
-def shared_layout(r_packed, r_cu, r_pos, n_sys):
-    """The oracle's per-prompt layout rearranged as a shared prefix: the first
-    prompt's n_sys system rows once, then every prompt's rows after them."""
-    rows = [r_packed[:n_sys]]
-    pos = [np.arange(n_sys)]
-    cu = [0, n_sys]
-    for i in range(len(r_cu) - 1):
-        a, b = int(r_cu[i]) + n_sys, int(r_cu[i + 1])
-        rows.append(r_packed[a:b])
-        pos.append(r_pos[a:b])
-        cu.append(cu[-1] + b - a)
-    return np.concatenate(rows), np.array(cu), np.concatenate(pos)
 
 
 @pytest.mark.parametrize("name", ["tiny", "scene8"])
