@@ -287,9 +287,11 @@ def test_compact_edges(R):
     assert st == 0 and np.array_equal(packed[:30], r[0]) and np.all(packed[30:] == 0) and np.all(pos[30:] == -7)
 
 
-def test_compact_many_prompts(R):
+@pytest.mark.parametrize("shared", [False, True])
+def test_compact_many_prompts(R, shared):
     """More prompts than the kernel stages in LDS (4096): the prompt of each row
-    is then searched in the offsets in global memory."""
+    is then searched in the offsets in global memory (per-prompt and shared
+    system rows)."""
     rng = np.random.default_rng(11)
     n_tiles, n_v = 5000, 4
     X = synth.store(rng.standard_normal((n_tiles, n_v, 64)).astype(np.float32), "bf16")
@@ -299,8 +301,10 @@ def test_compact_many_prompts(R):
     budgets = rng.integers(0, n_v + 1, size=len(kept))
     offs = np.concatenate([[0], np.cumsum(budgets)])
     sel = np.concatenate([np.sort(rng.permutation(n_v)[:b]) for b in budgets]).astype(np.int64)
-    packed, cu, pos, st = run_compact(R, X, "bf16", kept, offs, sel, sysr, qry)
+    packed, cu, pos, st = run_compact(R, X, "bf16", kept, offs, sel, sysr, qry, shared=shared)
     r_packed, r_cu, r_pos = O.compact(X, kept, offs, sel, sysr, qry)
+    if shared:
+        r_packed, r_cu, r_pos = shared_layout(r_packed, r_cu, r_pos, sysr.shape[0])
     assert st == 0
     assert np.array_equal(packed, r_packed) and np.array_equal(cu, r_cu) and np.array_equal(pos, r_pos)
 
