@@ -28,11 +28,12 @@ METRIC = "retained vision tokens prefilled/sec + ms per 400-tile scene query, 1 
 PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 STAGES = ("qkv_rope", "attention", "out_proj", "gate_up_swiglu", "down_proj")
-KERNEL_NAMES = {"qkv_rope": "QKV+RoPE GEMM (gemm_bf16_pp_kernel<0> + half-tile tail)",
+# (each GEMM adds a half-tile tail launch when its last round over the CUs is at most half full)
+KERNEL_NAMES = {"qkv_rope": "QKV+RoPE GEMM (gemm_bf16_pp_kernel<0>)",
                 "attention": "varlen causal attention (attn_bf16_kernel)",
-                "out_proj": "output projection + residual (gemm_bf16_w8_kernel<1> + half-tile tail)",
-                "gate_up_swiglu": "gate/up+SwiGLU GEMM (gemm_bf16_pp_kernel<2> + half-tile tail)",
-                "down_proj": "down projection + residual (gemm_bf16_w8_kernel<1> + half-tile tail)"}
+                "out_proj": "output projection + residual (gemm_bf16_w8_kernel<1>)",
+                "gate_up_swiglu": "gate/up+SwiGLU GEMM (gemm_bf16_pp_kernel<2>)",
+                "down_proj": "down projection + residual (gemm_bf16_w8_kernel<1>)"}
 GEMM_SRC = os.path.join(ROOT, "paper_2609_29029_amd", "csrc", "gemm_bf16.hip")
 
 # HBM traffic of one gate/up+SwiGLU launch at the 400-tile workload with the shared
