@@ -193,9 +193,9 @@ def test_decode_after_shared_prefix_matches_unshared(R):
     m = w.model
     rng = np.random.default_rng(21)
     store = lambda a: synth.store(a.astype(np.float32), "bf16")
-    P, own = 6, [4, 11, 1]
+    P, own = 6, [4, 11, 0, 1]   # a prompt with no rows after the prefix too
     prefix = store(rng.standard_normal((P, m.d)))
-    rows = [store(rng.standard_normal((L, m.d))) for L in own]
+    rows = [store(rng.standard_normal((L, m.d))).reshape(L, m.d) for L in own]
     steps = 2
     new = store(rng.standard_normal((steps, len(own), m.d)))
     W = upload_layer(synth.make_layer(w, 0), "bf16")
