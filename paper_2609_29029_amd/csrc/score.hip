@@ -1,17 +1,19 @@
 // Stage 1 of Rift (Sec. 2.3, Eq. 1; Listing 1; App. B Step 3) on gfx950.
 //
 //   prep_w       w = t - (1/M) sum_j B_j in float64, rounded to float32.
-//   score_tiles  one workgroup per tile of up to 10 waves, a wave per 64-token
-//                group (every 10th group beyond 640 tokens); each token row is
-//                read a whole 128-byte line at a time, a line ahead of its use.
-//                A single pass over the tile's tokens computes, per token,
+//   score_tiles  one wave per 32 tokens of a tile (token sets of all tiles
+//                dealt out four to a workgroup, so the work spreads evenly over
+//                the CUs whatever the tile count).  bf16 rows are read 512
+//                contiguous bytes at a time into a per-wave LDS buffer, the next
+//                chunk in flight while the current one is computed.  One pass
+//                over the tokens computes, per token,
 //                  * the float64 ranking key r = (x.w)/|x| on the VALUs, in the
 //                    fixed granule order (8-wide granules, granule g into
 //                    accumulator g mod 4, then (a0+a2)+(a1+a3));
 //                  * the cosines to t and every B_j with bf16 (or f32) MFMA,
-//                    the query-versus-token relevance GEMM;
-//                then pools the tile score s_i = mean r through LDS (64 strided
-//                partial sums, halving tree, divide by n_v).
+//                    the query-versus-token relevance GEMM.
+//   tile_pool    one wave per tile: s_i = mean r (64 strided partial sums in
+//                token order, halving tree, divide by n_v).
 //   rank_tiles   one workgroup: bitonic sort of (s desc, id asc), min-max
 //                normalisation u, retention by top-K or u >= tau.
 //
@@ -44,17 +46,20 @@ __global__ void prep_w_kernel(const void* __restrict__ qbank, int is_bf16, int d
     w32[i] = (float)w;
 }
 
+constexpr int kScoreWaves = 4;          // waves per workgroup
+constexpr int kScoreTok = 32;           // tokens per wave: two 16-token MFMA column blocks
+constexpr int kChunkSteps = 8;          // k-steps (32 elements each) per staged chunk: 512 bytes of a bf16 row
+constexpr int kStageBytes = kScoreTok * kChunkSteps * 64;   // one wave's LDS staging buffer (16 KB)
+
 template <bool kBf16>
-__global__ void __launch_bounds__(640)
-score_tiles_kernel(const void* __restrict__ tokens, int n_v, int d,
+__global__ void __launch_bounds__(64 * kScoreWaves)
+score_tiles_kernel(const void* __restrict__ tokens, int n_tiles, int n_v, int d,
                    const void* __restrict__ qbank, int nq, const float* __restrict__ w32,
                    double* __restrict__ token_key, float* __restrict__ token_sim,
-                   double* __restrict__ tile_score, double* __restrict__ inv_out) {
+                   double* __restrict__ inv_out) {
     extern __shared__ __align__(16) unsigned char smem[];
     float* w_lds = reinterpret_cast<float*>(smem);
-    double* r_lds = reinterpret_cast<double*>(smem + (size_t)d * sizeof(float));
 
-    const int tile = blockIdx.x;
     const int wave = threadIdx.x >> 6;
     const int lane = threadIdx.x & 63;
     const int r = lane & 15;
@@ -63,77 +68,118 @@ score_tiles_kernel(const void* __restrict__ tokens, int n_v, int d,
     for (int i = threadIdx.x; i < d; i += blockDim.x) w_lds[i] = w32[i];
     __syncthreads();
 
-    const int n_groups = (n_v + 63) >> 6;       // 64 tokens per group
-    const int n_waves = blockDim.x >> 6;
-    for (int grp = wave; grp < n_groups; grp += n_waves) {
-    int tok[4];
-    size_t row_off[4];
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-        tok[b] = grp * 64 + b * 16 + r;
-        int t_clamped = tok[b] < n_v ? tok[b] : n_v - 1;
-        row_off[b] = ((size_t)tile * n_v + t_clamped) * (size_t)d;
-    }
+    const int n_sets = (n_v + kScoreTok - 1) / kScoreTok;
+    const long long gw = (long long)blockIdx.x * kScoreWaves + wave;   // this wave's token set of all tiles
+    if (gw >= (long long)n_tiles * n_sets) return;
+    const int tile = (int)(gw / n_sets);
+    const int t0 = (int)(gw % n_sets) * kScoreTok;
+    const size_t tile_row0 = (size_t)tile * n_v;
     const size_t q_off = (size_t)(r < nq ? r : nq - 1) * d;
     const int steps = d / 32;
 
-    double n2[4] = {0.0, 0.0, 0.0, 0.0};
-    double g[4] = {0.0, 0.0, 0.0, 0.0};
-    f32x4_t acc[4];
-#pragma unroll
-    for (int b = 0; b < 4; ++b) acc[b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    double n2[2] = {0.0, 0.0};
+    double g[2] = {0.0, 0.0};
+    f32x4_t acc[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
 
     if constexpr (kBf16) {
-        const bf16_t* X = static_cast<const bf16_t*>(tokens);
+        // The wave's 32 token rows are read 512 bytes at a time: load i covers
+        // rows 2i and 2i + 1 (lanes 0-31 and 32-63), 16 bytes a lane, so each
+        // request is two contiguous 512-byte pieces.  The pieces go through a
+        // 16 KB LDS buffer (row lt at lt * 512, 16-byte unit j stored at unit
+        // j ^ (lt & 15)) and are read back in the MFMA B layout: for k-step s,
+        // lane (r, q) takes unit 4 s + q of row 16 b + r, which the swizzle
+        // spreads over distinct banks.  The next chunk's loads are in flight
+        // while the current one is computed.
+        const unsigned char* Xt = static_cast<const unsigned char*>(tokens) + tile_row0 * (size_t)d * 2;
         const bf16_t* Q = static_cast<const bf16_t*>(qbank);
-        // ring of four register sets.  Two consecutive steps cover the two
-        // halves of each token row's 128-byte lines, so their loads are issued
-        // together, a line ahead: at even s, the loads of steps s + 2, s + 3.
-        u32x4_t xs[4][4], qs[4];
-        auto load = [&](int st, int slot) {
-            const int k = st * 32 + q * 8;
+        unsigned char* stage = smem + (size_t)d * sizeof(float) + (size_t)wave * kStageBytes;
+        const unsigned row_bytes = (unsigned)d * 2;
+        const int unit = lane & 31;
+        unsigned src_row[16];   // byte offset of each loaded row in the tile (n_v * 2 d < 2^31)
 #pragma unroll
-            for (int b = 0; b < 4; ++b) xs[slot][b] = *reinterpret_cast<const u32x4_t*>(X + row_off[b] + k);
-            qs[slot] = *reinterpret_cast<const u32x4_t*>(Q + q_off + k);
+        for (int i = 0; i < 16; ++i) {
+            const int lt = 2 * i + (lane >> 5);
+            src_row[i] = (unsigned)(t0 + lt < n_v ? t0 + lt : n_v - 1) * row_bytes;
+        }
+        const int n_chunks = (steps + kChunkSteps - 1) / kChunkSteps;
+        u32x4_t P[16], Qc[kChunkSteps];
+        // Issued after the query loads of the chunk being computed, so the
+        // waits on those (the counter drains in order) leave these in flight.
+        auto issue = [&](int c) __attribute__((always_inline)) {
+            unsigned off = (unsigned)c * 512 + (unsigned)unit * 16;
+            off = off < row_bytes - 16 ? off : row_bytes - 16;   // past the row end in a partial last chunk
+#pragma unroll
+            for (int i = 0; i < 16; ++i) P[i] = *reinterpret_cast<const u32x4_t*>(Xt + src_row[i] + off);
         };
+        auto load_q = [&](int c) __attribute__((always_inline)) {
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-            if (j < steps) load(j, j);
-        for (int s0 = 0; s0 < steps; s0 += 4) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int s = s0 + j;
-                if (s >= steps) break;
-                if ((j & 1) == 0) {
-                    if (s + 2 < steps) load(s + 2, (j + 2) & 3);
-                    if (s + 3 < steps) load(s + 3, (j + 3) & 3);
-                }
-                const int k = s * 32 + q * 8;
-                const f32x4_t w0 = *reinterpret_cast<const f32x4_t*>(w_lds + k);
-                const f32x4_t w1 = *reinterpret_cast<const f32x4_t*>(w_lds + k + 4);
-                const double wd[8] = {(double)w0[0], (double)w0[1], (double)w0[2], (double)w0[3],
-                                      (double)w1[0], (double)w1[1], (double)w1[2], (double)w1[3]};
-                const bf16x8_t qa = __builtin_bit_cast(bf16x8_t, qs[j]);
-#pragma unroll
-                for (int b = 0; b < 4; ++b) {
-                    const u32x4_t x = xs[j][b];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const double x0 = (double)bf16_lo(x[e]);
-                        const double x1 = (double)bf16_hi(x[e]);
-                        n2[b] = fma(x0, x0, n2[b]);
-                        g[b] = fma(x0, wd[2 * e], g[b]);
-                        n2[b] = fma(x1, x1, n2[b]);
-                        g[b] = fma(x1, wd[2 * e + 1], g[b]);
-                    }
-                    acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, __builtin_bit_cast(bf16x8_t, x),
-                                                                     acc[b], 0, 0, 0);
-                }
+            for (int s = 0; s < kChunkSteps; ++s) {
+                int st = c * kChunkSteps + s;
+                st = st < steps ? st : steps - 1;
+                Qc[s] = *reinterpret_cast<const u32x4_t*>(Q + q_off + st * 32 + q * 8);
             }
+        };
+        auto stage_write = [&]() __attribute__((always_inline)) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int lt = 2 * i + (lane >> 5);
+                *reinterpret_cast<u32x4_t*>(stage + lt * 512 + ((unit ^ (lt & 15)) << 4)) = P[i];
+            }
+            __builtin_amdgcn_wave_barrier();
+        };
+        auto step = [&](int st, int s) __attribute__((always_inline)) {   // global k-step st, slot s of the chunk
+            const int k = st * 32 + q * 8;
+            const f32x4_t w0 = *reinterpret_cast<const f32x4_t*>(w_lds + k);
+            const f32x4_t w1 = *reinterpret_cast<const f32x4_t*>(w_lds + k + 4);
+            const double wd[8] = {(double)w0[0], (double)w0[1], (double)w0[2], (double)w0[3],
+                                  (double)w1[0], (double)w1[1], (double)w1[2], (double)w1[3]};
+            const bf16x8_t qa = __builtin_bit_cast(bf16x8_t, Qc[s]);
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+                const u32x4_t x =
+                    *reinterpret_cast<const u32x4_t*>(stage + (16 * b + r) * 512 + (((4 * s + q) ^ r) << 4));
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const double x0 = (double)bf16_lo(x[e]);
+                    const double x1 = (double)bf16_hi(x[e]);
+                    n2[b] = fma(x0, x0, n2[b]);
+                    g[b] = fma(x0, wd[2 * e], g[b]);
+                    n2[b] = fma(x1, x1, n2[b]);
+                    g[b] = fma(x1, wd[2 * e + 1], g[b]);
+                }
+                acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, __builtin_bit_cast(bf16x8_t, x), acc[b], 0, 0, 0);
+            }
+        };
+        auto full_chunk = [&](int c) __attribute__((always_inline)) {
+#pragma unroll
+            for (int s = 0; s < kChunkSteps; ++s) step(c * kChunkSteps + s, s);
+            __builtin_amdgcn_wave_barrier();   // reads done before the buffer is refilled
+        };
+        issue(0);
+        for (int c = 0; c + 1 < n_chunks; ++c) {
+            stage_write();
+            load_q(c);
+            issue(c + 1);
+            full_chunk(c);
+        }
+        stage_write();
+        load_q(n_chunks - 1);
+        const int last = n_chunks - 1;
+        const int tail = steps - last * kChunkSteps;
+        if (tail == kChunkSteps) {
+            full_chunk(last);
+        } else {
+            for (int s = 0; s < tail; ++s) step(last * kChunkSteps + s, s);
         }
     } else {
         const float* X = static_cast<const float*>(tokens);
         const float* Q = static_cast<const float*>(qbank);
+        size_t row_off[2];
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const int t = t0 + 16 * b + r < n_v ? t0 + 16 * b + r : n_v - 1;
+            row_off[b] = (tile_row0 + t) * (size_t)d;
+        }
         for (int s = 0; s < steps; ++s) {
             const int k = s * 32 + q * 8;
             const f32x4_t w0 = *reinterpret_cast<const f32x4_t*>(w_lds + k);
@@ -143,7 +189,7 @@ score_tiles_kernel(const void* __restrict__ tokens, int n_v, int d,
             const f32x4_t qa1 = *reinterpret_cast<const f32x4_t*>(Q + q_off + k + 4);
             const float qa[8] = {qa0[0], qa0[1], qa0[2], qa0[3], qa1[0], qa1[1], qa1[2], qa1[3]};
 #pragma unroll
-            for (int b = 0; b < 4; ++b) {
+            for (int b = 0; b < 2; ++b) {
                 const f32x4_t x0 = *reinterpret_cast<const f32x4_t*>(X + row_off[b] + k);
                 const f32x4_t x1 = *reinterpret_cast<const f32x4_t*>(X + row_off[b] + k + 4);
                 const float xv[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
@@ -161,24 +207,23 @@ score_tiles_kernel(const void* __restrict__ tokens, int n_v, int d,
     // Fold the four granule accumulators of each token: lanes r, r+16, r+32,
     // r+48 hold a0..a3.  xor 32 pairs a0 with a2 and a1 with a3; xor 16 then
     // adds the two pair sums.  Every lane of the token ends with the same value.
-    const size_t key_base = (size_t)tile * n_v;
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
+    for (int b = 0; b < 2; ++b) {
+        const int tok = t0 + 16 * b + r;
         double nn = n2[b] + __shfl_xor(n2[b], 32);
         nn = nn + __shfl_xor(nn, 16);
         double gg = g[b] + __shfl_xor(g[b], 32);
         gg = gg + __shfl_xor(gg, 16);
         double key = (nn == 0.0) ? 0.0 : gg / sqrt(nn);
         key = key + 0.0;  // -0 -> +0
-        const bool valid = tok[b] < n_v;
+        const bool valid = tok < n_v;
         if (valid && q == 0) {
-            token_key[key_base + tok[b]] = key;
-            r_lds[tok[b]] = key;
-            if (inv_out != nullptr) inv_out[key_base + tok[b]] = (nn == 0.0) ? 0.0 : 1.0 / sqrt(nn);
+            token_key[tile_row0 + tok] = key;
+            if (inv_out != nullptr) inv_out[tile_row0 + tok] = (nn == 0.0) ? 0.0 : 1.0 / sqrt(nn);
         }
         if (token_sim != nullptr && valid) {
             const float inv = (nn > 0.0) ? (float)(1.0 / sqrt(nn)) : 0.0f;
-            float* dst = token_sim + (key_base + tok[b]) * (size_t)nq;
+            float* dst = token_sim + (tile_row0 + tok) * (size_t)nq;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const int m = 4 * q + v;
@@ -186,20 +231,24 @@ score_tiles_kernel(const void* __restrict__ tokens, int n_v, int d,
             }
         }
     }
-    }   // token groups
-    __syncthreads();
+}
 
-    // Tile score: 64 strided partial sums of r, halving tree, divide by n_v.
-    if (wave == 0) {
-        double p = 0.0;
-        for (int i = lane; i < n_v; i += 64) p = p + r_lds[i];
+// Tile score: 64 strided partial sums of the tile's keys (token order), a
+// halving tree, divided by n_v.  One wave per tile, four tiles per workgroup.
+__global__ void __launch_bounds__(256)
+tile_pool_kernel(const double* __restrict__ token_key, int n_tiles, int n_v, double* __restrict__ tile_score) {
+    const int tile = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (tile >= n_tiles) return;
+    const double* k = token_key + (size_t)tile * n_v;
+    double p = 0.0;
+    for (int i = lane; i < n_v; i += 64) p = p + k[i];
 #pragma unroll
-        for (int s = 32; s >= 1; s >>= 1) {
-            const double o = __shfl_down(p, s);
-            p = p + o;
-        }
-        if (lane == 0) tile_score[tile] = p / (double)n_v;
+    for (int s = 32; s >= 1; s >>= 1) {
+        const double o = __shfl_down(p, s);
+        p = p + o;
     }
+    if (lane == 0) tile_score[tile] = p / (double)n_v;
 }
 
 // a precedes b: larger score first, then lower tile id.
@@ -265,17 +314,19 @@ hipError_t launch_score(const void* tokens, bool bf16, int n_tiles, int n_v, int
                         double* gram, double* s_smooth, hipStream_t st) {
     hipLaunchKernelGGL(prep_w_kernel, dim3((d + 255) / 256), dim3(256), 0, st, qbank, bf16 ? 1 : 0,
                        d, n_bg, w32);
-    const int groups = (n_v + 63) / 64;
-    const int waves = groups < 10 ? groups : 10;   // a wave takes every 10th group beyond 640 tokens
-    const size_t lds = (size_t)d * sizeof(float) + (size_t)groups * 64 * sizeof(double);
+    const long long sets = (long long)n_tiles * ((n_v + kScoreTok - 1) / kScoreTok);
+    const unsigned wgs = (unsigned)((sets + kScoreWaves - 1) / kScoreWaves);
+    const size_t lds = (size_t)d * sizeof(float) + (bf16 ? (size_t)kScoreWaves * kStageBytes : 0);
     double* inv_out = knn_m > 0 ? inv : nullptr;
     if (bf16) {
-        hipLaunchKernelGGL(score_tiles_kernel<true>, dim3(n_tiles), dim3(waves * 64), lds, st,
-                           tokens, n_v, d, qbank, 1 + n_bg, w32, token_key, token_sim, tile_score, inv_out);
+        hipLaunchKernelGGL(score_tiles_kernel<true>, dim3(wgs), dim3(64 * kScoreWaves), lds, st,
+                           tokens, n_tiles, n_v, d, qbank, 1 + n_bg, w32, token_key, token_sim, inv_out);
     } else {
-        hipLaunchKernelGGL(score_tiles_kernel<false>, dim3(n_tiles), dim3(waves * 64), lds, st,
-                           tokens, n_v, d, qbank, 1 + n_bg, w32, token_key, token_sim, tile_score, inv_out);
+        hipLaunchKernelGGL(score_tiles_kernel<false>, dim3(wgs), dim3(64 * kScoreWaves), lds, st,
+                           tokens, n_tiles, n_v, d, qbank, 1 + n_bg, w32, token_key, token_sim, inv_out);
     }
+    hipLaunchKernelGGL(tile_pool_kernel, dim3((unsigned)((n_tiles + 3) / 4)), dim3(256), 0, st, token_key, n_tiles,
+                       n_v, tile_score);
     const double* s_rank = tile_score;
     double* s_copy = nullptr;
     if (knn_m > 0) {
@@ -294,7 +345,7 @@ hipError_t launch_score(const void* tokens, bool bf16, int n_tiles, int n_v, int
 
 namespace rift {
 hipError_t score_init_attributes() {
-    const int bytes = 16384 * (int)sizeof(float) + 1024 * (int)sizeof(double);
+    const int bytes = 16384 * (int)sizeof(float) + kScoreWaves * kStageBytes;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&score_tiles_kernel<true>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
     if (e != hipSuccess) return e;
