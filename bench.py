@@ -45,7 +45,7 @@ GEMM_SRC = os.path.join(ROOT, "paper_2609_29029_amd", "csrc", "gemm_bf16.hip")
 TRAFFIC = {"stage": "gate_up_swiglu",
            "gemm_src_sha256": "ad16afa1ec10e20dd691986344eb854b8a153320596be793a9425b9f1e9fa952",
            "packed_tokens": 18739,
-           "bytes": 6.5730e9}
+           "bytes": 7.1092e9}
 
 
 def log(*a):
