@@ -105,11 +105,12 @@ score_tiles_kernel(const void* __restrict__ tokens, int n_tiles, int n_v, int d,
         u32x4_t P[16], Qc[kChunkSteps];
         // Issued after the query loads of the chunk being computed, so the
         // waits on those (the counter drains in order) leave these in flight.
+        // Nontemporal: each token row is read exactly once.
         auto issue = [&](int c) __attribute__((always_inline)) {
             unsigned off = (unsigned)c * 512 + (unsigned)unit * 16;
             off = off < row_bytes - 16 ? off : row_bytes - 16;   // past the row end in a partial last chunk
 #pragma unroll
-            for (int i = 0; i < 16; ++i) P[i] = *reinterpret_cast<const u32x4_t*>(Xt + src_row[i] + off);
+            for (int i = 0; i < 16; ++i) P[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(Xt + src_row[i] + off));
         };
         auto load_q = [&](int c) __attribute__((always_inline)) {
 #pragma unroll
