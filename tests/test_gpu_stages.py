@@ -122,6 +122,7 @@ def test_score_threshold_mode(R):
     ("bf16", 3, 45, 800, 2),     # three whole 256-element row chunks and a 1-step tail
     ("bf16", 2, 33, 4064, 1),    # fifteen whole chunks and a 7-step tail, one token past a 32-token set
     ("f32", 2, 33, 800, 2),      # the float32 path on the same ragged shapes
+    ("bf16", 4096, 4, 32, 0),    # the maximum tile count (one sort of 4096 keys), minimum d
 ])
 def test_score_edge_shapes(R, dtype, n_tiles, n_v, d, n_bg):
     rng = np.random.default_rng(n_tiles * 1000 + n_v)
