@@ -64,47 +64,82 @@ def stage_flops(T: int, d: int, ffn: int, seq_lens, n_prefix: int = 0) -> dict:
             "gate_up_swiglu": 2 * T * d * 2 * ffn, "down_proj": 2 * T * ffn * d}
 
 
-def cpu_baseline(w, sc, seq_lens_by_tier, n_tiles_sample: int, n_layers_sample: int) -> dict:
-    """The oracle as it stands, on a bounded sample of the same workload:
-    Stage 1 and selection on `n_tiles_sample` tiles, and `n_layers_sample`
-    decoder layers on one prompt of each budget tier; extrapolated to the whole
-    query (every layer costs the same)."""
+def _cpu_keys_worker(args):
+    """One worker of the CPU baseline: the oracle's per-token keys of a slice
+    of tiles (stored values in, float64 keys out)."""
+    tiles, dtype, qbank = args
     import synth
     from oracle import rift_oracle as O
+    return O.token_keys(synth.to_f64(tiles, dtype), O.query_direction(synth.to_f64(qbank, dtype)))
+
+
+def cpu_baseline(w, sc, seq_lens_by_tier, n_layers_sample: int) -> dict:
+    """The oracle as it stands on the host cores.  Every core in the process's
+    affinity set is used, capped at the host share of one GPU (16): BLAS and
+    OpenMP pools are set to that count, and the per-token keys of Stage 1 (the
+    oracle's cost there) are spread over that many worker processes, a slice
+    of tiles each.  Stage 1 (all tiles), selection and compaction run on the
+    whole query; the prefill runs `n_layers_sample` decoder layers on one
+    prompt of each budget tier and is extrapolated to every prompt and layer
+    (every layer costs the same)."""
+    import multiprocessing as mp
+    from concurrent.futures import ProcessPoolExecutor
+    import synth
+    from oracle import rift_oracle as O
+    cores = max(1, min(len(os.sched_getaffinity(0)), 16))
     try:
-        from threadpoolctl import threadpool_info
-        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()
-                            if i.get("user_api") == "blas"] or [1])
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=cores)
     except Exception:  # pragma: no cover
-        blas_threads = 1
+        limiter = None
     m = w.model
-    X = synth.to_f64(sc.tokens[:n_tiles_sample], w.dtype)
-    Q = synth.to_f64(sc.qbank, w.dtype)
+    times = {}
+    # Stage 1: keys in parallel over tile slices (fresh interpreters: the
+    # parent has initialised the GPU, the workers never touch it), then the
+    # oracle's pooling, normalisation and ranking on the gathered keys
     t0 = time.perf_counter()
-    st = O.scene_query_stage1(X, Q, min(w.keep_count, n_tiles_sample), w.tau)
-    kept = list(st["order"][: st["n_keep"]])
-    O.select_tokens(st["r"], kept, [w.levels[0]] * len(kept))
-    t_stage1 = (time.perf_counter() - t0) * (w.n_tiles / n_tiles_sample)
+    bounds = np.linspace(0, w.n_tiles, cores + 1).astype(int)
+    jobs = [(sc.tokens[a:b], w.dtype, sc.qbank) for a, b in zip(bounds[:-1], bounds[1:]) if b > a]
+    with ProcessPoolExecutor(max_workers=len(jobs), mp_context=mp.get_context("spawn")) as ex:
+        r = np.concatenate(list(ex.map(_cpu_keys_worker, jobs)))
+    s = O.tile_scores(r)
+    u = O.normalise(s)
+    order, n_keep = O.rank_and_keep(s, u, w.keep_count, w.tau)
+    times["stage1_s"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    kept = list(order[:n_keep])
+    budgets = O.assign_budgets(len(kept), w.levels, w.tier_num, w.tier_den)
+    offs, sel = O.select_tokens(r, kept, budgets)
+    times["select_s"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    O.compact(sc.tokens, kept, offs, sel, sc.sys, sc.qry)
+    times["compact_s"] = time.perf_counter() - t0
     W = {k: synth.to_f64(v, w.dtype) for k, v in synth.make_layer(w, 0).items()}
     rng = np.random.default_rng(0)
     t_prefill = 0.0
     n_ls = max(1, min(n_layers_sample, m.n_layers))
+    measured = 0.0
     for L, count in seq_lens_by_tier:
         x = rng.standard_normal((L, m.d))
         t0 = time.perf_counter()
         for _ in range(n_ls):
             x = O.decoder_layer(x, W, m.n_heads, m.head_dim, m.rms_eps, m.rope_base, np.arange(L))
-        t_prefill += (time.perf_counter() - t0) * count * m.n_layers / n_ls
-    total = t_stage1 + t_prefill
-    retained = sum(L - w.n_sys - w.n_qry for L, c in seq_lens_by_tier for _ in range(c))
-    return {"value": retained / total, "unit": "tokens/s", "cores": int(blas_threads),
-            "kind": "oracle",
-            "sample": (f"float64 NumPy oracle: Stage 1 + selection on {n_tiles_sample} of "
-                       f"{w.n_tiles} tiles, {n_ls} decoder layers on one prompt per budget tier "
-                       f"(lengths {[L for L, _ in seq_lens_by_tier]}); extrapolated to "
-                       f"{w.n_tiles} tiles and {sum(c for _, c in seq_lens_by_tier)} prompts x "
-                       f"{m.n_layers} layers = {total:.1f} s per query; Stage 1 runs on one "
-                       f"thread, BLAS on {blas_threads}")}
+        dt = time.perf_counter() - t0
+        measured += dt
+        t_prefill += dt * count * m.n_layers / n_ls
+    times["prefill_s"] = t_prefill
+    if limiter is not None:
+        limiter.restore_original_limits()
+    total = sum(times.values())
+    retained = int(sum(budgets))
+    return {"value": retained / total, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "stage_s": {k: round(v, 2) for k, v in times.items()},
+            "sample": (f"float64 NumPy oracle on {cores} cores: Stage 1 on all {w.n_tiles} tiles "
+                       f"({len(jobs)} worker processes over tile slices), selection and compaction of "
+                       f"the whole query, measured; prefill measured as {n_ls} decoder layers on one "
+                       f"prompt per budget tier (lengths {[L for L, _ in seq_lens_by_tier]}, "
+                       f"{measured:.1f} s) and extrapolated to {sum(c for _, c in seq_lens_by_tier)} "
+                       f"prompts x {m.n_layers} layers; {total:.1f} s per query")}
 
 
 def exhaustive_setup(R, torch, w, tokens, qbank, sysd, qryd, layers, cfg, chunk: int = 50,
@@ -479,6 +514,73 @@ def select_batched(R, torch, token_key, order, budgets, n_tiles, n_v, n_keep, co
             "frac_hbm": round(nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
 
 
+def _kernel_label(name: str) -> str:
+    """Short kernel name for a rocprofv3 row: namespaces and argument lists
+    dropped, template arguments kept."""
+    import re
+    k = name.replace("void ", "").replace("rift::(anonymous namespace)::", "").replace("rift::", "")
+    m = re.match(r"[\w:]+(<[^>]*>)?", k)
+    return m.group(0) if m else k[:60]
+
+
+def counter_report(paths) -> str:
+    """Summarise rocprofv3 --pmc CSV files (one pass per file: the hardware
+    collects a few counters per run) as a markdown table per kernel.
+    Derived figures:
+      clock     GRBM_GUI_ACTIVE / 8 XCDs over the dispatch's duration
+      MFMA busy SQ_VALU_MFMA_BUSY_CYCLES over (clock cycles x 1,024 SIMDs)
+      SQ busy   SQ_BUSY_CYCLES over (clock cycles x 32 shader engines)
+      HBM-side bytes  FETCH_SIZE and WRITE_SIZE (KiB) scaled by what the same
+                counters read for the 1 GiB calibration copy (torch.neg over
+                2^28 floats: 1 GiB read, 1 GiB written)."""
+    import csv
+    import glob
+    files = []
+    for p in paths:
+        files += sorted(glob.glob(os.path.join(p, "**", "*counter_collection.csv"), recursive=True)) \
+            if os.path.isdir(p) else [p]
+    # per kernel: counter -> list of per-dispatch values; dispatch durations
+    vals: dict = {}
+    durs: dict = {}
+    for f in files:
+        seen = set()
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                k = _kernel_label(r["Kernel_Name"])
+                vals.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+                key = (f, r["Dispatch_Id"])
+                if key not in seen:
+                    seen.add(key)
+                    durs.setdefault(k, []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    calib = {c: statistics.mean(v) for k, d in vals.items() if "neg" in k for c, v in d.items()}
+    f_scale = (1 << 30) / (calib["FETCH_SIZE"] * 1024) if calib.get("FETCH_SIZE") else None
+    w_scale = (1 << 30) / (calib["WRITE_SIZE"] * 1024) if calib.get("WRITE_SIZE") else None
+    lines = ["| kernel | dispatches | mean us | clock GHz | MFMA busy | SQ busy | fetch GB | write GB | HBM-side GB/s | frac of 8 TB/s |",
+             "|---|---|---|---|---|---|---|---|---|---|"]
+    for k in sorted(vals):
+        if "neg" in k:
+            continue
+        d = {c: statistics.mean(v) for c, v in vals[k].items()}
+        us = statistics.mean(durs[k]) / 1e3
+        clk = d["GRBM_GUI_ACTIVE"] / 8 / (us * 1e3) if "GRBM_GUI_ACTIVE" in d else None
+        cyc = d["GRBM_GUI_ACTIVE"] / 8 if "GRBM_GUI_ACTIVE" in d else None
+        busy = d["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * 1024) if cyc and "SQ_VALU_MFMA_BUSY_CYCLES" in d else None
+        sqb = d["SQ_BUSY_CYCLES"] / (cyc * 32) if cyc and "SQ_BUSY_CYCLES" in d else None
+        fgb = d["FETCH_SIZE"] * 1024 * f_scale / 1e9 if f_scale and "FETCH_SIZE" in d else None
+        wgb = d["WRITE_SIZE"] * 1024 * w_scale / 1e9 if w_scale and "WRITE_SIZE" in d else None
+        gbs = ((fgb or 0) + (wgb or 0)) / (us * 1e-6) if (fgb is not None or wgb is not None) else None
+
+        def fmt(x, nd):
+            return "" if x is None else f"{x:.{nd}f}"
+        lines.append(f"| `{k}` | {len(durs[k])} | {us:.1f} | {fmt(clk, 3)} | {fmt(busy and busy * 100, 1)}{'%' if busy else ''} | "
+                     f"{fmt(sqb, 2)} | {fmt(fgb, 4)} | {fmt(wgb, 4)} | {fmt(gbs, 0)} | {fmt(gbs and gbs / PEAK_HBM_GBS, 3)} |")
+    if f_scale or w_scale:
+        lines.append("")
+        lines.append(f"Calibration copy (1 GiB read, 1 GiB written): FETCH_SIZE x {f_scale or 0:.3f}, "
+                     f"WRITE_SIZE x {w_scale or 0:.3f}.")
+    return "\n".join(lines)
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -488,7 +590,6 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-shared-prefix", action="store_true",
                     help="pack the system rows into every prompt instead of prefilling them once")
-    ap.add_argument("--cpu-sample-tiles", type=int, default=128)
     ap.add_argument("--cpu-sample-layers", type=int, default=16)
     ap.add_argument("--no-exhaustive", action="store_true",
                     help="skip the every-tile, full-budget comparison run")
@@ -498,7 +599,14 @@ def main() -> int:
                     help="minimum span of energy-counter updates per workload")
     ap.add_argument("--traffic-calibration", action="store_true",
                     help="also run a 1 GiB copy kernel (for HBM counter calibration)")
+    ap.add_argument("--core-only", action="store_true",
+                    help="time the scene-query and the batched select only (for counter runs)")
+    ap.add_argument("--counter-report", nargs="+", metavar="CSV_OR_DIR",
+                    help="print a per-kernel summary of rocprofv3 --pmc CSV output and exit (no GPU)")
     args = ap.parse_args()
+    if args.counter_report:
+        print(counter_report(args.counter_report))
+        return 0
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the Rift path here is a single-GPU build "
               "(no collectives); run it with --gpus 1", file=sys.stderr)
@@ -605,6 +713,13 @@ def main() -> int:
                       "tflops": round(fl[n] / (per_launch[n] * 1e-3) / 1e12, 1),
                       "frac_bf16_peak": round(fl[n] / (per_launch[n] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
                   for n in STAGES}
+    # At these prompt lengths attention is bound by HBM, not by the MFMA: it
+    # reads q, k and v and writes o once per layer (4 T d storage elements).
+    attn_bytes = 4 * T * m.d * (2 if w.dtype == "bf16" else 4)
+    stage_roof["attention"].update(
+        {"bound": "hbm", "hbm_bytes": attn_bytes,
+         "GBs": round(attn_bytes / (per_launch["attention"] * 1e-3) / 1e9, 1),
+         "frac_hbm": round(attn_bytes / (per_launch["attention"] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)})
     dom = max(STAGES, key=lambda n: per_launch[n])
     import hashlib
     with open(GEMM_SRC, "rb") as f:
@@ -642,6 +757,11 @@ def main() -> int:
         "hbm": hbm,
     }
     out["packed_tokens_per_s"] = round(T * K / elapsed, 1)
+    if args.core_only:
+        out["select_batched"] = select_batched(R, torch, q.token_key, q.tile_order, q.budgets, w.n_tiles,
+                                               w.n_v, q.n_keep)
+        print(json.dumps(out), flush=True)
+        return 0
     if shared:
         # the same query with the system rows packed into every prompt
         uq = SceneQuery(tokens, qbank, sysd, qryd, layers, q.shape, w.keep_count, w.tau, w.levels,
@@ -692,8 +812,7 @@ def main() -> int:
         for L in seq_lens:
             tiers[L] = tiers.get(L, 0) + 1
         t_cpu = time.perf_counter()
-        out["cpu_baseline"] = cpu_baseline(w, sc, sorted(tiers.items(), reverse=True),
-                                           args.cpu_sample_tiles, args.cpu_sample_layers)
+        out["cpu_baseline"] = cpu_baseline(w, sc, sorted(tiers.items(), reverse=True), args.cpu_sample_layers)
         log(f"cpu baseline {time.perf_counter() - t_cpu:.1f} s")
     print(json.dumps(out), flush=True)
     return 0

@@ -8,7 +8,7 @@
  *                          budgets (Sec. 2.3 Stage 2)
  *   (optional) rift_merge_context: the non-selected tokens of each kept
  *                          tile merged into contextual tokens (VisionZip's
- *                          "merge the remainder", Sec. 2.3 Stage 2)
+ *                          merge of the remaining tokens, Sec. 2.3 Stage 2)
  *   3. rift_compact        packing of each retained tile's prompt into one
  *                          varlen batch (each tile is its own VLM call,
  *                          Sec. 2.3 Stage 2 and App. B Step 5)
@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define RIFT_ABI_VERSION 6
+#define RIFT_ABI_VERSION 7
 
 #if defined(__GNUC__) || defined(__clang__)
 #define RIFT_API __attribute__((visibility("default")))
@@ -65,8 +65,8 @@ typedef enum {
     RIFT_ERR_BUDGET = 4,      /* budget, level or tier out of range               */
     RIFT_ERR_WORKSPACE = 5,   /* workspace too small or not 256-byte aligned      */
     RIFT_ERR_HIP = 6,         /* a HIP runtime call or a kernel launch failed     */
-    RIFT_ERR_UNSUPPORTED = 7, /* valid request outside what this build implements */
-    RIFT_ERR_NONFINITE = 8    /* a floating-point input holds NaN or infinity     */
+    RIFT_ERR_NONFINITE = 7,   /* a floating-point input holds NaN or infinity     */
+    RIFT_ERR_UNSUPPORTED = 8  /* valid request outside what this build implements */
 } rift_status;
 
 typedef enum { RIFT_F32 = 0, RIFT_BF16 = 1 } rift_dtype;
@@ -118,9 +118,10 @@ RIFT_API size_t rift_score_workspace_size(int32_t n_tiles, int32_t n_v, int32_t 
  *             == 0: keep every tile with u >= tau (tau is compared in float64)
  * knn_m       0: no smoothing.  > 0: before normalisation each tile score is
  *             averaged with the scores of its knn_m most visually similar tiles
- *             (Listing 1's note "smoothed with its 6 most similar tiles";
- *             App. B Step 3).  The tile embedding is the float32-rounded sum of
- *             its unit tokens, accumulated over tokens in ascending order with
+ *             (the optional smoothing of Listing 1's note and App. B Step 3,
+ *             which the paper runs with six neighbours).  The tile embedding
+ *             is the float32-rounded sum of its unit tokens, accumulated over
+ *             tokens in ascending order with
  *             each product and sum rounded on its own; similarity is the cosine
  *             of the canonical dot products; neighbours are the knn_m (at most
  *             n_tiles - 1) largest over the other tiles, ties to the lower id;

@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(HERE, "librift.so")
 RIFT_OK = 0
 STATUS_NAMES = {0: "RIFT_OK", 1: "RIFT_ERR_NULL", 2: "RIFT_ERR_SHAPE", 3: "RIFT_ERR_DTYPE",
                 4: "RIFT_ERR_BUDGET", 5: "RIFT_ERR_WORKSPACE", 6: "RIFT_ERR_HIP",
-                7: "RIFT_ERR_UNSUPPORTED", 8: "RIFT_ERR_NONFINITE"}
+                7: "RIFT_ERR_NONFINITE", 8: "RIFT_ERR_UNSUPPORTED"}
 RIFT_F32 = 0
 RIFT_BF16 = 1
 

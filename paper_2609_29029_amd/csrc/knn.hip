@@ -109,24 +109,31 @@ tile_gram_kernel(const float* __restrict__ emb, int n, int d, double* __restrict
 __global__ void __launch_bounds__(64)
 knn_smooth_kernel(const double* __restrict__ G, int n, const double* __restrict__ s_raw, int m,
                   double* __restrict__ s_out) {
-    extern __shared__ double cosL[];   // [n]
+    extern __shared__ double cosL[];   // [n] cosines, then [n] taken flags
+    unsigned char* taken = reinterpret_cast<unsigned char*>(cosL + n);
     const int i = blockIdx.x;
     const int lane = threadIdx.x;
     const double gii = G[(size_t)i * n + i];
     for (int j = lane; j < n; j += 64) {
         const double den = sqrt(gii * G[(size_t)j * n + j]);
         const double c = (den == 0.0) ? 0.0 : G[(size_t)i * n + j] / den;
-        cosL[j] = (j == i) ? -INFINITY : c;
+        // A NaN cosine (only from a non-finite input) ranks below every other
+        // candidate; it stays a candidate, so every round picks some tile.
+        cosL[j] = (c == c) ? c : -INFINITY;
+        taken[j] = (j == i) ? 1 : 0;
     }
     __syncthreads();
     const int m_eff = m < n - 1 ? m : n - 1;
     double acc = s_raw[i];
     for (int r = 0; r < m_eff; ++r) {
+        // arg-max over the tiles not yet taken: (cosine desc, id asc).  At least
+        // n - 1 - r >= 1 tiles are left, and any of them beats the start value
+        // (a -inf cosine ties -inf and has the lower id), so bj ends in [0, n).
         double bv = -INFINITY;
         int bj = 0x7fffffff;
         for (int j = lane; j < n; j += 64) {
             const double v = cosL[j];
-            if (v > bv || (v == bv && j < bj)) {
+            if (!taken[j] && (v > bv || (v == bv && j < bj))) {
                 bv = v;
                 bj = j;
             }
@@ -141,7 +148,7 @@ knn_smooth_kernel(const double* __restrict__ G, int n, const double* __restrict_
             }
         }
         __syncthreads();
-        if ((bj & 63) == lane) cosL[bj] = -INFINITY;   // taken
+        if ((bj & 63) == lane) taken[bj] = 1;
         __syncthreads();
         acc = acc + s_raw[bj];
     }
@@ -160,7 +167,7 @@ hipError_t launch_knn_smooth(const void* tokens, bool bf16, int n_tiles, int n_v
         hipLaunchKernelGGL(pool_embed_kernel<false>, pgrid, dim3(64), 0, st, tokens, n_v, d, inv, emb);
     const dim3 ggrid((n_tiles + 15) / 16, (n_tiles + 15) / 16);
     hipLaunchKernelGGL(tile_gram_kernel, ggrid, dim3(256), 0, st, emb, n_tiles, d, gram);
-    hipLaunchKernelGGL(knn_smooth_kernel, dim3(n_tiles), dim3(64), (size_t)n_tiles * sizeof(double), st,
+    hipLaunchKernelGGL(knn_smooth_kernel, dim3(n_tiles), dim3(64), (size_t)n_tiles * (sizeof(double) + 1), st,
                        gram, n_tiles, s_raw, m, s_out);
     return hipGetLastError();
 }

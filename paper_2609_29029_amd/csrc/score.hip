@@ -266,8 +266,11 @@ rank_tiles_kernel(const double* __restrict__ s, int n, int keep_count, double ta
     __shared__ int kept;
     int N = 1;
     while (N < n) N <<= 1;
+    // A NaN score (only from a non-finite input) sorts as -inf: it ties the
+    // pads and precedes them by id, so the first n entries are real tile ids.
     for (int i = threadIdx.x; i < N; i += blockDim.x) {
-        key[i] = i < n ? s[i] : -INFINITY;
+        const double si = i < n ? s[i] : -INFINITY;
+        key[i] = (si == si) ? si : -INFINITY;
         id[i] = i;
         if (s_copy != nullptr && i < n) s_copy[i] = s[i];
     }
@@ -300,7 +303,7 @@ rank_tiles_kernel(const double* __restrict__ s, int n, int keep_count, double ta
     for (int p = threadIdx.x; p < n; p += blockDim.x) {
         const double u = (smax == smin) ? 1.0 : (key[p] - smin) / range;
         order[p] = id[p];
-        if (id[p] < n) u_out[id[p]] = (float)u;  // only a NaN score could sort a pad this early
+        u_out[id[p]] = (float)u;
         local += (u >= tau) ? 1 : 0;
     }
     if (keep_count == 0 && local) atomicAdd(&kept, local);

@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol(R):
     assert tuple(names) == R.EXPORTS
     for n in names:
         assert hasattr(L, n), n
-    assert L.rift_abi_version() == 6
+    assert L.rift_abi_version() == 7
     assert L.rift_status_string(4).decode().startswith("budget")
 
 
@@ -157,7 +157,7 @@ def test_prefill_validation_and_workspace(R):
     for bad in (R.model_cfg(4096, 64, 64, 11008, 1, 1e-6, 1e4, R.RIFT_BF16),    # bf16 needs head_dim 128
                 R.model_cfg(4160, 32, 130, 11008, 1, 1e-6, 1e4, R.RIFT_BF16),
                 R.model_cfg(256, 4, 64, 690, 1, 1e-6, 1e4, R.RIFT_F32)):        # ffn % 16
-        assert call(bad) == 7
+        assert call(bad) == 8   # RIFT_ERR_UNSUPPORTED
     assert call(R.model_cfg(4096, 31, 128, 11008, 1, 1e-6, 1e4, R.RIFT_BF16)) == 2
     assert call(R.model_cfg(4096, 32, 128, 11008, 1, 1e-6, 1e4, 9)) == 3
     assert R.rift_prefill_workspace_size(R.model_cfg(4096, 64, 64, 11008, 1, 1e-6, 1e4, R.RIFT_BF16), 10, 10) == 0
@@ -209,7 +209,7 @@ def test_check_finite_validation_and_debug_switch(R):
     assert L.rift_check_finite(None, 1, 10, FAKE, None) == 1       # no input
     assert L.rift_check_finite(FAKE, 5, 10, FAKE, None) == 3       # unknown dtype
     assert L.rift_check_finite(FAKE, 0, -1, FAKE, None) == 2       # negative count
-    assert L.rift_status_string(8).decode() == "a floating-point input holds NaN or infinity"
+    assert L.rift_status_string(7).decode() == "a floating-point input holds NaN or infinity"
     prev = L.rift_set_debug(1)
     assert L.rift_set_debug(0) == 1
     assert L.rift_set_debug(prev) == 0
@@ -257,7 +257,7 @@ def test_decode_validation(R):
     assert ws > 0 and R.rift_decode_workspace_size(cfg, 4, 643, 0) == 0
     lw = (R.LayerWeights * 1)(R.LayerWeights(*([FAKE] * 9)))
     d = L.rift_decode_step
-    assert d(ctypes.byref(f32), lw, FAKE, FAKE, 4, 100, 643, 0, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 7
+    assert d(ctypes.byref(f32), lw, FAKE, FAKE, 4, 100, 643, 0, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 8
     assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 643, 0, FAKE, FAKE, 8, 8, FAKE, FAKE, ws, None) == 2  # step
     assert d(ctypes.byref(cfg), lw, FAKE, FAKE, 4, 100, 16380, 0, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 2
     assert d(ctypes.byref(cfg), lw, None, FAKE, 4, 100, 643, 0, FAKE, FAKE, 8, 0, FAKE, FAKE, ws, None) == 1

@@ -10,7 +10,7 @@ from tests.rift_testlib import torch_mod, upload, upload_layer
 
 pytestmark = pytest.mark.gpu
 
-NONFINITE = 8
+NONFINITE = 7
 
 
 @pytest.fixture(scope="module")
@@ -99,6 +99,39 @@ def test_debug_mode_score(R, debug):
     R.rift_set_debug(False)
     st, key = score_call(R, bad, qbank)
     assert st == 0
+
+
+def test_nonfinite_token_with_smoothing_keeps_indices_in_range(R):
+    """Debug mode off, six-neighbour smoothing, one infinite token: that
+    tile's embedding, similarities and score are NaN.  The neighbour search
+    still picks a tile in range every round (a NaN similarity ranks last), and
+    the NaN score sorts behind every finite one, so the order stays a
+    permutation of the tile ids with the bad tile last."""
+    torch = torch_mod()
+    prev = R.rift_set_debug(False)
+    try:
+        w = synth.get("scene8")
+        sc = synth.make_scene(w)
+        tokens, qbank = upload(sc.tokens, w.dtype), upload(sc.qbank, w.dtype)
+        bad_tile = 5
+        tokens[bad_tile, 100, 7] = float("inf")
+        n_tiles, n_v, d = tokens.shape
+        key = torch.empty(n_tiles * n_v, dtype=torch.float64, device="cuda")
+        score = torch.empty(n_tiles, dtype=torch.float64, device="cuda")
+        u = torch.empty(n_tiles, dtype=torch.float32, device="cuda")
+        order = torch.empty(n_tiles, dtype=torch.int32, device="cuda")
+        nk = torch.empty(1, dtype=torch.int32, device="cuda")
+        ws = torch.empty(R.rift_score_workspace_size(n_tiles, n_v, d, 6), dtype=torch.uint8, device="cuda")
+        R.rift_score_tiles(tokens, qbank, 16, 0.0, key, None, score, u, order, nk, ws, knn_m=6)
+        torch.cuda.synchronize()
+        o = order.cpu().numpy()
+        s = score.cpu().numpy()
+        assert sorted(o.tolist()) == list(range(n_tiles))
+        assert o[-1] == bad_tile and int(nk.item()) == 16
+        assert not np.isfinite(s[bad_tile])
+        assert np.isfinite(np.delete(s, bad_tile)).all()
+    finally:
+        R.rift_set_debug(prev)
 
 
 def test_debug_mode_select(R, debug):

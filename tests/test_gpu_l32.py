@@ -5,88 +5,192 @@ teacher-forced: the oracle runs layer l on the GPU's own input to layer l, for
 sampled layers and prompts, and each must stay within 2e-2 (rowwise max
 relative error).  The 32-layer call must equal the chain of 32 one-layer calls
 bit for bit, and the end-to-end error against a float64 32-layer run is
-reported."""
+reported.
+
+Both packings are covered: one prompt per kept tile with its own system rows,
+and the shared system prefix (the system rows prefilled once as sequence 0,
+every prompt attending to them first), which is the layout the benchmark
+times.  The shared packing must give every prompt the same 32-layer hidden
+states as the per-prompt packing, bit for bit."""
 import numpy as np
 import pytest
 
 import synth
 from oracle import rift_oracle as O
-from tests.rift_testlib import (f64, oracle_layer_weights, oracle_stage1, rowwise_rel_err,
-                                torch_mod, upload, upload_layer, download_stored)
+from tests.rift_testlib import (f64, oracle_layer_weights, oracle_stage1, plan_shape, rowwise_rel_err,
+                                torch_mod, upload, upload_layer)
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 CHECK_LAYERS = (0, 1, 15, 31)
 
 
-def test_scene20_l32_per_layer_teacher_forced():
+@pytest.fixture(scope="module")
+def l32():
+    """The scene, its oracle packing and the 32 layers on the device (host
+    copies of the checked layers only)."""
     import paper_2609_29029_amd as R
     torch = torch_mod()
     assert torch.cuda.is_available()
     R.load()
     w = synth.get("scene20_l32")
-    m = w.model
     sc = synth.make_scene(w)
+    print("scene20_l32: oracle Stage 1 on 400 tiles ...", flush=True)
     ref = oracle_stage1(sc, w.keep_count, w.tau)
     kept = list(ref["order"][: ref["n_keep"]])
     budgets = O.assign_budgets(len(kept), w.levels, w.tier_num, w.tier_den)
     offs, sel = O.select_tokens(ref["r"], kept, budgets)
     packed, cu, pos = O.compact(sc.tokens, kept, offs, sel, sc.sys, sc.qry)
-    T, d = packed.shape
-    L = int(np.diff(cu).max())
-    lens = np.diff(cu)
-    # shortest, longest, and the last prompt (its rows sit in the last, partial GEMM tiles)
-    seqs = sorted({int(np.argmin(lens)), int(np.argmax(lens)), len(lens) - 1})
-
     host_layers = {}
     dev_layers = []
-    for l in range(m.n_layers):
+    for l in range(w.model.n_layers):
         W = synth.make_layer(w, l)
         if l in CHECK_LAYERS:
             host_layers[l] = W
         dev_layers.append(upload_layer(W, w.dtype))
         del W
+        if l % 8 == 7:
+            print(f"scene20_l32: {l + 1}/{w.model.n_layers} layers on the device", flush=True)
+    yield dict(R=R, w=w, sc=sc, kept=kept, packed=packed, cu=cu, pos=pos, host_layers=host_layers,
+               dev_layers=dev_layers)
+    del dev_layers
+    torch.cuda.empty_cache()
 
-    cfg1 = R.model_cfg(m.d, m.n_heads, m.head_dim, m.ffn, 1, m.rms_eps, m.rope_base, R.RIFT_BF16)
-    cfg32 = R.model_cfg(m.d, m.n_heads, m.head_dim, m.ffn, m.n_layers, m.rms_eps, m.rope_base, R.RIFT_BF16)
-    ws = torch.empty(R.rift_prefill_workspace_size(cfg32, T, L), dtype=torch.uint8, device="cuda")
+
+def _cfg(R, m, n_layers):
+    return R.model_cfg(m.d, m.n_heads, m.head_dim, m.ffn, n_layers, m.rms_eps, m.rope_base, R.RIFT_BF16)
+
+
+def _chain_teacher_forced(R, L32, packed, cu, pos, n_seq, n_prefix, max_len, seq_rows, check_layers, label):
+    """Run the 32 layers as 32 one-layer calls; at each checked layer compare
+    the chosen prompts' outputs with the oracle layer applied to the GPU's own
+    input rows.  seq_rows(i) gives the packed row indices of prompt i in the
+    order the oracle sees them (with a shared prefix: the prefix rows, then the
+    prompt's own).  Returns the chain's output."""
+    torch = torch_mod()
+    w = L32["w"]
+    m = w.model
+    T, d = packed.shape
     x = upload(packed, w.dtype)
+    cfg1 = _cfg(R, m, 1)
+    ws = torch.empty(R.rift_prefill_workspace_size(_cfg(R, m, m.n_layers), T, max_len), dtype=torch.uint8,
+                     device="cuda")
     cu_d, pos_d = torch.from_numpy(cu).cuda(), torch.from_numpy(pos).cuda()
-
-    # layer-by-layer chain; keep the inputs of the checked layers
+    lens = np.array([len(seq_rows(i)) for i in range(n_seq - (1 if n_prefix else 0))])
+    # shortest, longest, and the last prompt (its rows sit in the last, partial GEMM tiles)
+    seqs = sorted({int(np.argmin(lens)), int(np.argmax(lens)), len(lens) - 1})
     cur = torch.empty(T, d, dtype=torch.float32, device="cuda")
-    inputs = {0: f64(packed, w.dtype)}
+    layer_in = None
     for l in range(m.n_layers):
-        R.rift_prefill(cfg1, [dev_layers[l]], x if l == 0 else cur, cu_d, pos_d, len(kept), L, cur, ws)
-        if l + 1 in CHECK_LAYERS:
+        if l in check_layers:
             torch.cuda.synchronize()
-            inputs[l + 1] = cur.cpu().numpy().astype(np.float64)
-        if l in CHECK_LAYERS:
+            layer_in = f64(packed, w.dtype) if l == 0 else cur.cpu().numpy().astype(np.float64)
+        R.rift_prefill(cfg1, [L32["dev_layers"][l]], x if l == 0 else cur, cu_d, pos_d, n_seq, max_len, cur, ws,
+                       n_prefix=n_prefix)
+        if l in check_layers:
             torch.cuda.synchronize()
             out = cur.cpu().numpy().astype(np.float64)
-            Wo = oracle_layer_weights(host_layers[l], w.dtype)
+            Wo = oracle_layer_weights(L32["host_layers"][l], w.dtype)
             for i in seqs:
-                s0, s1 = cu[i], cu[i + 1]
-                y = O.decoder_layer(inputs[l][s0:s1], Wo, m.n_heads, m.head_dim, m.rms_eps, m.rope_base, pos[s0:s1])
-                err = rowwise_rel_err(out[s0:s1], y)
-                print(f"layer {l} seq {i} (L={s1 - s0}): teacher-forced rel err {err:.3e}")
-                assert err <= 2e-2, (l, i, err)
-    chain = cur.clone()
+                rows = seq_rows(i)
+                y = O.decoder_layer(layer_in[rows], Wo, m.n_heads, m.head_dim, m.rms_eps, m.rope_base, pos[rows])
+                err = rowwise_rel_err(out[rows], y)
+                print(f"[{label}] layer {l} prompt {i} (L={len(rows)}): teacher-forced rel err {err:.3e}")
+                assert err <= 2e-2, (label, l, i, err)
+    return cur
+
+
+def test_scene20_l32_per_layer_teacher_forced(l32):
+    """Per-prompt packing: every checked layer within 2e-2 teacher-forced;
+    the 32-layer call equals the chain of one-layer calls bit for bit."""
+    torch = torch_mod()
+    R, w = l32["R"], l32["w"]
+    m = w.model
+    packed, cu, pos = l32["packed"], l32["cu"], l32["pos"]
+    T, d = packed.shape
+    L = int(np.diff(cu).max())
+    n_seq = len(cu) - 1
+    x = upload(packed, w.dtype)
+    chain = _chain_teacher_forced(R, l32, packed, cu, pos, n_seq, 0, L,
+                                  lambda i: np.arange(cu[i], cu[i + 1]), CHECK_LAYERS, "per-prompt")
 
     # the 32-layer call equals the chain bit for bit
     full = torch.empty(T, d, dtype=torch.float32, device="cuda")
-    R.rift_prefill(cfg32, dev_layers, x, cu_d, pos_d, len(kept), L, full, ws)
+    ws = torch.empty(R.rift_prefill_workspace_size(_cfg(R, m, m.n_layers), T, L), dtype=torch.uint8, device="cuda")
+    R.rift_prefill(_cfg(R, m, m.n_layers), l32["dev_layers"], x, torch.from_numpy(cu).cuda(),
+                   torch.from_numpy(pos).cuda(), n_seq, L, full, ws)
     torch.cuda.synchronize()
     assert torch.equal(full, chain)
 
     # end-to-end against float64, reported (bf16 storage compounds over 32 layers)
-    i = seqs[0]
+    lens = np.diff(cu)
+    i = int(np.argmin(lens))
     s0, s1 = cu[i], cu[i + 1]
     xs = f64(packed[s0:s1], w.dtype)
     for l in range(m.n_layers):
-        Wl = host_layers.get(l)
+        Wl = l32["host_layers"].get(l)
         Wo = oracle_layer_weights(Wl if Wl is not None else synth.make_layer(w, l), w.dtype)
         xs = O.decoder_layer(xs, Wo, m.n_heads, m.head_dim, m.rms_eps, m.rope_base, pos[s0:s1])
     e2e = rowwise_rel_err(full.cpu().numpy()[s0:s1].astype(np.float64), xs)
-    print(f"end-to-end 32-layer rel err on seq {i} (L={s1 - s0}): {e2e:.3e} (reported, not gated)")
+    print(f"end-to-end 32-layer rel err on prompt {i} (L={s1 - s0}): {e2e:.3e} (reported, not gated)")
     assert np.isfinite(e2e)
+
+
+def test_scene20_l32_shared_prefix_is_the_benched_query(l32):
+    """The benchmark's configuration: the whole scene-query (score, select,
+    compact with the shared system prefix, 32-layer prefill) through
+    SceneQuery.  Its packing equals the oracle's per-prompt packing rearranged
+    around one prefix; every prompt's 32-layer hidden states, and the prefix
+    rows, equal those of the per-prompt packing bit for bit; and the shared
+    layout passes the teacher-forced per-layer gate at layers 0 and 31 on the
+    shortest, longest and last prompts."""
+    from paper_2609_29029_amd.pipeline import SceneQuery
+    from tests.rift_testlib import download_stored, shared_layout
+    torch = torch_mod()
+    R, w, sc = l32["R"], l32["w"], l32["sc"]
+    m = w.model
+    n_sys = sc.sys.shape[0]
+    dev = dict(tokens=upload(sc.tokens, w.dtype), qbank=upload(sc.qbank, w.dtype), sys=upload(sc.sys, w.dtype),
+               qry=upload(sc.qry, w.dtype))
+
+    def query(shared):
+        q = SceneQuery(dev["tokens"], dev["qbank"], dev["sys"], dev["qry"], l32["dev_layers"], plan_shape(w),
+                       w.keep_count, w.tau, w.levels, w.tier_num, w.tier_den, with_sims=False,
+                       shared_prefix=shared)
+        q.run()
+        torch.cuda.synchronize()
+        assert q.check_status() == [0, 0]
+        return q
+
+    qb = query(True)
+    # stages 1-3 of the benched query against the oracle
+    s_packed, s_cu, s_pos = shared_layout(l32["packed"], l32["cu"], l32["pos"], n_sys)
+    s_cu, s_pos = s_cu.astype(np.int32), s_pos.astype(np.int32)
+    assert np.array_equal(qb.tile_order.cpu().numpy()[: len(l32["kept"])], np.array(l32["kept"]))
+    assert np.array_equal(download_stored(qb.packed, w.dtype), s_packed)
+    assert np.array_equal(qb.cu_seqlens.cpu().numpy(), s_cu)
+    assert np.array_equal(qb.position_ids.cpu().numpy(), s_pos)
+    hb = qb.hidden.cpu().numpy()
+    del qb
+    torch.cuda.empty_cache()
+    qa = query(False)
+    ha = qa.hidden.cpu().numpy()
+    cua = qa.cu_seqlens.cpu().numpy()
+    del qa
+    torch.cuda.empty_cache()
+
+    # every prompt's rows and the prefix rows equal the per-prompt packing bit for bit
+    for i in range(len(cua) - 1):
+        a0, a1 = int(cua[i]), int(cua[i + 1])
+        b0, b1 = int(s_cu[i + 1]), int(s_cu[i + 2])
+        assert np.array_equal(ha[a0:a0 + n_sys], hb[:n_sys]), i
+        assert np.array_equal(ha[a0 + n_sys:a1], hb[b0:b1]), i
+
+    # teacher-forced per layer on the shared layout: prompt i is the prefix rows
+    # followed by its own rows
+    L = int(n_sys + np.diff(s_cu)[1:].max())
+    chain = _chain_teacher_forced(
+        R, l32, s_packed, s_cu, s_pos, len(s_cu) - 1, n_sys, L,
+        lambda i: np.concatenate([np.arange(n_sys), np.arange(s_cu[i + 1], s_cu[i + 2])]), (0, 31), "shared")
+    # the query's 32-layer call equals the chain of one-layer calls
+    assert np.array_equal(chain.cpu().numpy(), hb)

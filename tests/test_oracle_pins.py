@@ -131,6 +131,69 @@ def test_token_key_scale_invariance_and_zero():
     assert np.all(z == 0.0) and not np.any(np.signbit(z))
 
 
+# ----------------------------------------------------------------------------- token cosines
+def test_token_sims_hand_cases():
+    """Cosines of Eq. 1's terms (the relevance GEMM's output), worked by hand
+    with t = e0 and B_1 = e1: a token along e0 of any length is [1, 0]; along
+    e0 + e1 it is [1/sqrt2, 1/sqrt2]; along -e1 it is [0, -1]; an all-zero token
+    is [0, 0].  Dividing by |q| instead of |x|, or dropping the 1/|x|, fails the
+    first row (3 instead of 1)."""
+    d = 32
+    e = np.eye(d)
+    qb = np.stack([e[0], e[1]])
+    x = np.stack([3.0 * e[0], e[0] + e[1], -0.25 * e[1], np.zeros(d)])
+    got = O.token_sims(x, qb)
+    h = 1.0 / math.sqrt(2.0)
+    want = np.array([[1.0, 0.0], [h, h], [0.0, -1.0], [0.0, 0.0]])
+    assert got.shape == (4, 2)
+    assert np.allclose(got, want, rtol=0, atol=1e-15)
+    assert got[3, 0] == 0.0 and got[3, 1] == 0.0
+
+
+def test_token_sims_against_fsum_cosines():
+    """Every element against the correctly rounded dot product over the
+    correctly rounded norm, on bfloat16-valued tokens and unit query-bank rows
+    rounded to bfloat16 (the stored values of the scenes): the two differ only
+    by the rounding of the matrix product and the norm (a few ulps of a value
+    below 1).  A transposed or mis-indexed operand gives differences of order
+    0.1."""
+    rng = np.random.default_rng(19)
+    d, m = 256, 15
+    rb = lambda a: synth.bf16_to_f32(synth.round_bf16(a.astype(np.float32))).astype(np.float64)
+    qb = rb(np.stack([_unit(rng.standard_normal(d)) for _ in range(1 + m)]))
+    x = rb(rng.standard_normal((24, d)))
+    x[5] += 16.0 * qb[0]         # a planted, strongly aligned token (cosine near 0.7)
+    x = rb(x)
+    got = O.token_sims(x, qb)
+    assert got.shape == (24, 1 + m)
+    for i in range(x.shape[0]):
+        nrm = math.sqrt(math.fsum(x[i] * x[i]))
+        for j in range(1 + m):
+            ref = math.fsum(x[i] * qb[j]) / nrm
+            assert abs(got[i, j] - ref) <= 1e-15, (i, j, got[i, j], ref)
+    assert got[5, 0] > 0.5 > float(np.abs(np.delete(got[:, 0], 5)).max())
+
+
+def test_token_sims_scale_invariance_and_eq1_margin():
+    """Scaling a token by a power of two leaves its cosines bitwise unchanged
+    (every product, the norm and the quotient scale exactly).  The Eq. 1 margin
+    cos(x, t) - mean_j cos(x, B_j) built from these cosines matches the ranking
+    key, which is computed by a different route (one dot product with
+    w = t - mean_j B_j rounded to float32) -- to within that rounding."""
+    rng = np.random.default_rng(20)
+    d, m = 256, 15
+    rb = lambda a: synth.bf16_to_f32(synth.round_bf16(a.astype(np.float32))).astype(np.float64)
+    qb = rb(np.stack([_unit(rng.standard_normal(d)) for _ in range(1 + m)]))
+    x = rb(rng.standard_normal((16, d)))
+    s = O.token_sims(x, qb)
+    for k in (-4, 3, 9):
+        assert np.array_equal(O.token_sims(x * 2.0 ** k, qb), s)
+    margin = s[:, 0] - s[:, 1:].mean(axis=1)
+    r = O.token_keys(x, O.query_direction(qb))
+    assert np.abs(margin - r).max() < 1e-6
+    assert np.abs(margin).max() > 1e-2   # the check is not vacuous
+
+
 # ----------------------------------------------------------------------------- tile scores, u, rank
 def test_tile_score_is_eq1_with_mean_unit_embedding():
     """s_i = V_i.t - mean_j V_i.B_j with V_i the mean of unit tokens (reading R1),
