@@ -157,6 +157,33 @@ RIFT_API rift_status rift_score_tiles(const void* tokens, rift_dtype dt, int32_t
                              float* tile_u, int32_t* tile_order, int32_t* n_keep,
                              void* workspace, size_t ws_bytes, rift_stream stream);
 
+/*
+ * rift_score_tiles_noalloc -- rift_score_tiles without a workspace argument,
+ * for callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops that forbid allocation).  Same arguments, outputs,
+ * shape rules and errors as rift_score_tiles; the workspace is a static
+ * device array of RIFT_SCORE_SCRATCH_BYTES that the library holds on each GPU
+ * it runs on until the process ends.  The call runs on the current device;
+ * `stream` must belong to it.  Nothing is allocated (no hipMalloc, no
+ * allocating library routine).
+ * Limit: calls whose rift_score_workspace_size(n_tiles, n_v, d, knn_m)
+ * exceeds RIFT_SCORE_SCRATCH_BYTES return RIFT_ERR_WORKSPACE and enqueue
+ * nothing (every call without smoothing fits; with smoothing, e.g. 400 tiles
+ * x 576 tokens at d = 4096 needs about 9.7 MB).
+ * Every call on a GPU shares that GPU's array: calls that overlap in time on
+ * one GPU (different streams or threads, or another host thread's call that
+ * has not finished) race on it and must be ordered by the caller.  Nothing in
+ * the array needs to start at zero: every word a call reads, the same call
+ * writes first.
+ */
+#define RIFT_SCORE_SCRATCH_BYTES (16u << 20)
+RIFT_API rift_status rift_score_tiles_noalloc(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
+                                              int32_t d, const void* query_bank, int32_t n_bg,
+                                              int32_t keep_count, double tau, int32_t knn_m,
+                                              double* token_key, float* token_sim, double* tile_score,
+                                              float* tile_u, int32_t* tile_order, int32_t* n_keep,
+                                              rift_stream stream);
+
 /* ------------------------------------------------------------------ Stage 2 */
 
 /*

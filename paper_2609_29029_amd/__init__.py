@@ -6,5 +6,6 @@ from ._lib import (EXPORTS, LIB_PATH, RIFT_BF16, RIFT_F32, LayerWeights, ModelCf
                    rift_assign_budgets_utility, rift_check_finite, rift_compact, rift_decode_step,
                    rift_decode_workspace_size,
                    rift_merge_context, rift_merge_workspace_size, rift_prefill,
-                   rift_prefill_workspace_size, rift_score_tiles, rift_score_workspace_size,
+                   rift_prefill_workspace_size, rift_score_tiles, rift_score_tiles_noalloc,
+                   rift_score_workspace_size,
                    rift_select_tokens, rift_set_debug, rift_split_budgets)

@@ -25,7 +25,7 @@ RIFT_BF16 = 1
 # Every symbol include/rift.h declares, in declaration order.
 EXPORTS = ("rift_abi_version", "rift_status_string", "rift_set_debug", "rift_check_finite",
            "rift_score_workspace_size",
-           "rift_score_tiles", "rift_assign_budgets", "rift_assign_budgets_utility",
+           "rift_score_tiles", "rift_score_tiles_noalloc", "rift_assign_budgets", "rift_assign_budgets_utility",
            "rift_select_tokens", "rift_split_budgets", "rift_merge_workspace_size", "rift_merge_context",
            "rift_compact",
            "rift_prefill_workspace_size", "rift_prefill", "rift_decode_workspace_size", "rift_decode_step")
@@ -77,6 +77,8 @@ def load() -> ctypes.CDLL:
     L.rift_score_workspace_size.argtypes = [I32, I32, I32, I32]
     L.rift_score_tiles.restype = I32
     L.rift_score_tiles.argtypes = [P, I32, I32, I32, I32, P, I32, I32, F64, I32, P, P, P, P, P, P, P, SZ, P]
+    L.rift_score_tiles_noalloc.restype = I32
+    L.rift_score_tiles_noalloc.argtypes = [P, I32, I32, I32, I32, P, I32, I32, F64, I32, P, P, P, P, P, P, P]
     L.rift_assign_budgets.restype = I32
     L.rift_assign_budgets.argtypes = [I32, I32, P, I32, P, I32, P, P]
     L.rift_assign_budgets_utility.restype = I32
@@ -196,6 +198,29 @@ def rift_score_tiles(tokens, query_bank, keep_count: int, tau: float, token_key,
                                  _ptr(tile_score), _ptr(tile_u), _ptr(tile_order), _ptr(n_keep),
                                  _ptr(workspace), workspace.numel(), _stream(stream))
     _check(st, "rift_score_tiles")
+
+
+def rift_score_tiles_noalloc(tokens, query_bank, keep_count: int, tau: float, token_key, token_sim,
+                             tile_score, tile_u, tile_order, n_keep, stream=None, knn_m: int = 0) -> None:
+    """rift_score_tiles on the library's static scratch (no workspace)."""
+    torch = _torch()
+    n_tiles, n_v, d = tokens.shape
+    nq = query_bank.shape[0]
+    dt = _dt_code(tokens)
+    _need(tokens, tokens.dtype, name="tokens")
+    _need(query_bank, tokens.dtype, (nq, d), "query_bank")
+    _need(token_key, torch.float64, (n_tiles * n_v,), "token_key")
+    if token_sim is not None:
+        _need(token_sim, torch.float32, (n_tiles * n_v, nq), "token_sim")
+    _need(tile_score, torch.float64, (n_tiles,), "tile_score")
+    _need(tile_u, torch.float32, (n_tiles,), "tile_u")
+    _need(tile_order, torch.int32, (n_tiles,), "tile_order")
+    _need(n_keep, torch.int32, (1,), "n_keep")
+    st = load().rift_score_tiles_noalloc(_ptr(tokens), dt, n_tiles, n_v, d, _ptr(query_bank), nq - 1,
+                                         int(keep_count), float(tau), int(knn_m), _ptr(token_key),
+                                         _ptr(token_sim), _ptr(tile_score), _ptr(tile_u), _ptr(tile_order),
+                                         _ptr(n_keep), _stream(stream))
+    _check(st, "rift_score_tiles_noalloc")
 
 
 # ----------------------------------------------------------------------------- Stage 2

@@ -204,37 +204,106 @@ size_t rift_score_workspace_size(int32_t n_tiles, int32_t n_v, int32_t d, int32_
     return score_layout(n_tiles, n_v, d, knn_m).total;
 }
 
-rift_status rift_score_tiles(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
-                             int32_t d, const void* query_bank, int32_t n_bg, int32_t keep_count,
-                             double tau, int32_t knn_m, double* token_key, float* token_sim,
-                             double* tile_score, float* tile_u, int32_t* tile_order, int32_t* n_keep,
-                             void* workspace, size_t ws_bytes, rift_stream stream) {
+}  // extern "C"
+
+namespace {
+
+// Argument checks of rift_score_tiles that do not involve the workspace.
+rift_status score_check(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v, int32_t d,
+                        const void* query_bank, int32_t n_bg, int32_t keep_count, double tau, int32_t knn_m,
+                        const double* token_key, const double* tile_score, const float* tile_u,
+                        const int32_t* tile_order, const int32_t* n_keep) {
     if (tokens == nullptr || query_bank == nullptr || token_key == nullptr ||
-        tile_score == nullptr || tile_u == nullptr || tile_order == nullptr || n_keep == nullptr ||
-        workspace == nullptr)
+        tile_score == nullptr || tile_u == nullptr || tile_order == nullptr || n_keep == nullptr)
         return RIFT_ERR_NULL;
     if (!dt_valid(dt)) return RIFT_ERR_DTYPE;
     if (n_tiles < 1 || n_tiles > 4096 || n_v < 1 || n_v > 1024 || d < 32 || d > 16384 ||
         d % 32 != 0 || n_bg < 0 || n_bg > 15 || keep_count < 0 || isnan(tau) || knn_m < 0)
         return RIFT_ERR_SHAPE;
-    const ScoreLayout L = score_layout(n_tiles, n_v, d, knn_m);
-    if (misaligned(workspace) || ws_bytes < L.total) return RIFT_ERR_WORKSPACE;
+    return RIFT_OK;
+}
+
+// Enqueue the scoring of a validated call on a workspace laid out by
+// score_layout (device memory of at least L.total bytes, 256-byte aligned).
+rift_status score_enqueue(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v, int32_t d,
+                          const void* query_bank, int32_t n_bg, int32_t keep_count, double tau, int32_t knn_m,
+                          double* token_key, float* token_sim, double* tile_score, float* tile_u,
+                          int32_t* tile_order, int32_t* n_keep, unsigned char* ws, const ScoreLayout& L,
+                          hipStream_t st) {
     if (init_kernel_attributes() != hipSuccess) return RIFT_ERR_HIP;
-    unsigned char* ws = static_cast<unsigned char*>(workspace);
     if (debug_on()) {
         const DebugInput in[2] = {{tokens, dt_kind(dt), (long long)n_tiles * n_v * d},
                                   {query_bank, dt_kind(dt), (long long)(1 + n_bg) * d}};
-        const rift_status ds = debug_scan(in, 2, reinterpret_cast<int*>(ws + L.dbg),
-                                          static_cast<hipStream_t>(stream));
+        const rift_status ds = debug_scan(in, 2, reinterpret_cast<int*>(ws + L.dbg), st);
         if (ds != RIFT_OK) return ds;
     }
     hipError_t e = launch_score(tokens, dt == RIFT_BF16, n_tiles, n_v, d, query_bank, n_bg,
                                 keep_count, tau, knn_m, token_key, token_sim, tile_score, tile_u,
                                 tile_order, n_keep, reinterpret_cast<float*>(ws + L.w),
                                 reinterpret_cast<double*>(ws + L.inv), reinterpret_cast<float*>(ws + L.emb),
-                                reinterpret_cast<double*>(ws + L.gram), reinterpret_cast<double*>(ws + L.smooth),
-                                static_cast<hipStream_t>(stream));
+                                reinterpret_cast<double*>(ws + L.gram), reinterpret_cast<double*>(ws + L.smooth), st);
     return hip_status(e);
+}
+
+// Scratch of rift_score_tiles_noalloc: one copy per GPU, resident until the
+// process ends.  In host code `scratch` only names the symbol; its device
+// address on each GPU comes from hipGetSymbolAddress with that GPU current.
+constexpr size_t kScoreScratchBytes = (size_t)RIFT_SCORE_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+__device__ __align__(256) unsigned char scratch[kScoreScratchBytes];
+std::mutex g_scratch_mu;
+unsigned char* g_scratch_ptr[kMaxDevices] = {};
+
+// The current GPU's address of `scratch`, looked up once per device.
+rift_status scratch_address(unsigned char** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return RIFT_ERR_HIP;
+    if (dev < 0 || dev >= kMaxDevices) return RIFT_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return RIFT_ERR_HIP;
+        g_scratch_ptr[dev] = static_cast<unsigned char*>(p);
+    }
+    *out = g_scratch_ptr[dev];
+    return RIFT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rift_status rift_score_tiles(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
+                             int32_t d, const void* query_bank, int32_t n_bg, int32_t keep_count,
+                             double tau, int32_t knn_m, double* token_key, float* token_sim,
+                             double* tile_score, float* tile_u, int32_t* tile_order, int32_t* n_keep,
+                             void* workspace, size_t ws_bytes, rift_stream stream) {
+    rift_status c = score_check(tokens, dt, n_tiles, n_v, d, query_bank, n_bg, keep_count, tau, knn_m, token_key,
+                                tile_score, tile_u, tile_order, n_keep);
+    if (c != RIFT_OK) return c;
+    if (workspace == nullptr) return RIFT_ERR_NULL;
+    const ScoreLayout L = score_layout(n_tiles, n_v, d, knn_m);
+    if (misaligned(workspace) || ws_bytes < L.total) return RIFT_ERR_WORKSPACE;
+    return score_enqueue(tokens, dt, n_tiles, n_v, d, query_bank, n_bg, keep_count, tau, knn_m, token_key,
+                         token_sim, tile_score, tile_u, tile_order, n_keep, static_cast<unsigned char*>(workspace),
+                         L, static_cast<hipStream_t>(stream));
+}
+
+rift_status rift_score_tiles_noalloc(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v,
+                                     int32_t d, const void* query_bank, int32_t n_bg, int32_t keep_count,
+                                     double tau, int32_t knn_m, double* token_key, float* token_sim,
+                                     double* tile_score, float* tile_u, int32_t* tile_order, int32_t* n_keep,
+                                     rift_stream stream) {
+    rift_status c = score_check(tokens, dt, n_tiles, n_v, d, query_bank, n_bg, keep_count, tau, knn_m, token_key,
+                                tile_score, tile_u, tile_order, n_keep);
+    if (c != RIFT_OK) return c;
+    const ScoreLayout L = score_layout(n_tiles, n_v, d, knn_m);
+    if (L.total > kScoreScratchBytes) return RIFT_ERR_WORKSPACE;
+    unsigned char* ws = nullptr;
+    c = scratch_address(&ws);
+    if (c != RIFT_OK) return c;
+    return score_enqueue(tokens, dt, n_tiles, n_v, d, query_bank, n_bg, keep_count, tau, knn_m, token_key,
+                         token_sim, tile_score, tile_u, tile_order, n_keep, ws, L, static_cast<hipStream_t>(stream));
 }
 
 rift_status rift_assign_budgets(int32_t n_keep, int32_t n_v, const int32_t* levels,

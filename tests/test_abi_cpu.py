@@ -33,7 +33,7 @@ def declared_symbols():
 def test_library_exports_every_declared_symbol(R):
     L = R.load()
     names = declared_symbols()
-    assert len(names) == 17
+    assert len(names) == 18
     assert tuple(names) == R.EXPORTS
     for n in names:
         assert hasattr(L, n), n
@@ -106,6 +106,33 @@ def test_score_validation(R):
     assert need >= 256 * 4 + 4 * 576 * 8 + 4 * 256 * 4 + 4 * 4 * 8 + 4 * 8
     assert call(knn=6, wsb=need - 1) == 5
     assert R.rift_score_workspace_size(4, 576, 4096, -1) == 0
+
+
+def test_score_noalloc_validation_and_scratch_limit(R):
+    """The workspace-free scoring call validates like rift_score_tiles and
+    rejects, before any device work, a call whose workspace would exceed the
+    static scratch (16 MiB)."""
+    L = R.load()
+    args = dict(tokens=FAKE, dt=1, n_tiles=4, n_v=576, d=256, qb=FAKE, n_bg=15, keep=2, tau=0.37, knn=0,
+                key=FAKE, sim=None, s=FAKE, u=FAKE, order=FAKE, nk=FAKE)
+
+    def call(**over):
+        a = dict(args, **over)
+        return L.rift_score_tiles_noalloc(a["tokens"], a["dt"], a["n_tiles"], a["n_v"], a["d"], a["qb"],
+                                          a["n_bg"], a["keep"], a["tau"], a["knn"], a["key"], a["sim"], a["s"],
+                                          a["u"], a["order"], a["nk"], None)
+    assert call(tokens=None) == 1 and call(order=None) == 1
+    assert call(dt=7) == 3
+    for bad in (dict(n_tiles=0), dict(n_tiles=4097), dict(n_v=1025), dict(d=48), dict(n_bg=16),
+                dict(keep=-1), dict(tau=float("nan")), dict(knn=-1)):
+        assert call(**bad) == 2, bad
+    limit = 16 << 20
+    # 4096 tiles of 1024 tokens with smoothing need far more than the scratch
+    assert R.rift_score_workspace_size(4096, 1024, 4096, 6) > limit
+    assert call(n_tiles=4096, n_v=1024, d=4096, knn=6) == 5
+    # the largest scene without smoothing, and 400 x 576 x 4096 with it, fit
+    assert R.rift_score_workspace_size(4096, 1024, 16384, 0) <= limit
+    assert R.rift_score_workspace_size(400, 576, 4096, 6) <= limit
 
 
 def test_select_and_compact_validation(R):
