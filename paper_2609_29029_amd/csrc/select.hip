@@ -2,93 +2,37 @@
 // budget of dominant tokens, ranked by the per-token margin, ties to the lower
 // token index, emitted in ascending index order.
 //
-//   select_offsets  one workgroup: validates budgets and tile ids, writes the
-//                   exclusive prefix sums sel_offsets (each thread sums a
-//                   contiguous run, then one scan over the threads) and the
-//                   status word.
-//   select_topk     one wave per kept tile, keys in registers: a radix select
-//                   (8-bit digits from the top, histogram in the wave's own
-//                   LDS slice; it stops once the bin that holds the
-//                   budget-th key is taken whole) finds the budget-th pair in
-//                   (descending key, ascending index) order, then ballot
-//                   prefix counts write the chosen indices in ascending order.
+// One launch.  A workgroup of W waves handles W consecutive kept tiles, one
+// wave per tile:
+//   1. the wave issues the loads of its tile's keys (tile id clamped so every
+//      read is in bounds whatever the ids hold);
+//   2. meanwhile the workgroup reads every budget and tile id of the call:
+//      the call is valid only if all of them are in range and the total fits
+//      (then every workgroup reaches the same verdict), and the sum of the
+//      budgets before its first tile is its base offset;
+//   3. each wave finds the budget-th key of its tile, (key desc, index asc),
+//      by deciding the order-preserving key bits one at a time from the
+//      highest bit in which its keys differ: per bit, a ballot per element
+//      counts the candidates with a 0 there; the side that holds the
+//      budget-th key stays candidate, and when that is the 1 side every
+//      0-side candidate is taken.  The search ends once the candidates left
+//      are exactly the ones still needed (on distinct keys after about
+//      log2(n_v) + 2 bits), else after bit 0 with equal keys, of which the
+//      lowest indices are taken.  Candidate and taken sets are wave-wide bit
+//      masks (lane l, element e = token 64 e + l), so the search is a few
+//      vector compares and scalar mask operations per bit, with no shared
+//      memory traffic;
+//   4. the taken tokens are written in ascending index order (ballot prefix
+//      counts).
+// Workgroup 0 writes the status word; the workgroup of the last tile writes
+// the total offset.
 #include "launch.h"
 #include "rift_common.h"
 
 namespace rift {
 
-constexpr int kOffBatch = 8;
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
 
-__global__ void __launch_bounds__(1024)
-select_offsets_kernel(const int* __restrict__ kept, const int* __restrict__ budgets, int n_keep,
-                      int n_tiles, int n_v, long long cap, int* __restrict__ offs,
-                      int* __restrict__ status) {
-    __shared__ int bad;
-    __shared__ long long wave_sum[16];
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    if (tid == 0) bad = 0;
-    __syncthreads();
-    // thread t owns budgets [t per, (t + 1) per): validate and sum them, in
-    // batches of kOffBatch whose loads are all issued before the first is used
-    const int per = (n_keep + 1023) / 1024;
-    const int i0 = tid * per;
-    const int i1 = min(i0 + per, n_keep);
-    long long mine = 0;
-    bool bad_mine = false;
-    for (int j0 = i0; j0 < i1; j0 += kOffBatch) {
-        int bv[kOffBatch], tv[kOffBatch];
-#pragma unroll
-        for (int j = 0; j < kOffBatch; ++j) {
-            const int i = min(j0 + j, i1 - 1);
-            bv[j] = budgets[i];
-            tv[j] = kept[i];
-        }
-#pragma unroll
-        for (int j = 0; j < kOffBatch; ++j) {
-            if (j0 + j >= i1) break;
-            const int b = bv[j], t = tv[j];
-            bad_mine |= b < 0 || b > n_v || t < 0 || t >= n_tiles;
-            mine += b < 0 ? 0 : (b > n_v ? n_v : b);
-        }
-    }
-    if (bad_mine) atomicOr(&bad, 1);
-    // exclusive scan over threads: within the wave, then across the 16 waves
-    long long incl = mine;
-#pragma unroll
-    for (int s = 1; s < 64; s <<= 1) {
-        const long long o = __shfl_up(incl, s);
-        if (lane >= s) incl += o;
-    }
-    if (lane == 63) wave_sum[wave] = incl;
-    __syncthreads();
-    long long base = 0, total = 0;
-    for (int w = 0; w < 16; ++w) {
-        if (w < wave) base += wave_sum[w];
-        total += wave_sum[w];
-    }
-    if (tid == 0 && total > cap) bad = 1;
-    __syncthreads();
-    if (bad) {
-        for (int i = tid; i <= n_keep; i += blockDim.x) offs[i] = 0;
-    } else {
-        long long run = base + incl - mine;
-        for (int j0 = i0; j0 < i1; j0 += kOffBatch) {
-            int bv[kOffBatch];
-#pragma unroll
-            for (int j = 0; j < kOffBatch; ++j) bv[j] = budgets[min(j0 + j, i1 - 1)];
-#pragma unroll
-            for (int j = 0; j < kOffBatch; ++j) {
-                if (j0 + j >= i1) break;
-                offs[j0 + j] = (int)run;
-                run += bv[j];   // validated above: 0 <= bv[j] <= n_v
-            }
-        }
-        if (tid == 0) offs[n_keep] = (int)total;
-    }
-    if (tid == 0) *status = bad ? (int)RIFT_ERR_BUDGET : 0;
-}
 
 // Order-preserving map of a key to an unsigned integer, descending: a larger
 // key gives a smaller value.  -0 is first made +0 so that the two compare equal,
@@ -98,7 +42,6 @@ __device__ __forceinline__ uint64_t desc_bits(double x) {
     const uint64_t asc = (b >> 63) ? ~b : (b | 0x8000000000000000ull);
     return ~asc;
 }
-
 
 // Inclusive prefix sum over the 64 lanes of a wave with DPP moves: shifts by
 // 1, 2, 4 and 8 inside each row of 16 lanes (lanes shifted in from outside
@@ -114,116 +57,366 @@ __device__ __forceinline__ unsigned wave_incl_scan(unsigned v) {
     return v;
 }
 
-// NE: keys per lane the kernel is built for (n_v <= 64 NE); 9 covers a 24 x 24
-// token tile, 16 the largest n_v (1024).
-template <int NE>
-__global__ void __launch_bounds__(256)
-select_topk_kernel(const double* __restrict__ token_key, int n_v, int n_keep,
-                   const int* __restrict__ kept, const int* __restrict__ offs,
-                   const int* __restrict__ status, int* __restrict__ sel_idx) {
-    __shared__ unsigned hist_all[4][256];
-    const int wave = threadIdx.x >> 6;
-    const int lane = threadIdx.x & 63;
-    const int rho = blockIdx.x * 4 + wave;
-    if (rho >= n_keep) return;
-    // the status word, this tile's offsets and its id are loaded together
-    const int bad = *status;
-    const int off = offs[rho];
-    const int off_end = offs[rho + 1];
-    const int tile = kept[rho];
-    if (bad != 0) return;
-    const int budget = off_end - off;
-    if (budget <= 0) return;
-    if (budget >= n_v) {
-        for (int i = lane; i < n_v; i += 64) sel_idx[off + i] = i;
-        return;
+// Sum over the wave (every lane gets it).
+__device__ __forceinline__ int wave_sum(int v) {
+    return __builtin_amdgcn_readlane((int)wave_incl_scan((unsigned)v), 63);
+}
+
+// Minimum and maximum over the wave, by the same DPP steps (lanes shifted in
+// from outside contribute the identity), read from lane 63.
+__device__ __forceinline__ float wave_min(float v) {
+    const int inf = __builtin_bit_cast(int, INFINITY);
+    v = fminf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(inf, __builtin_bit_cast(int, v), 0x111, 0xf, 0xf, false)));
+    v = fminf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(inf, __builtin_bit_cast(int, v), 0x112, 0xf, 0xf, false)));
+    v = fminf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(inf, __builtin_bit_cast(int, v), 0x114, 0xf, 0xf, false)));
+    v = fminf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(inf, __builtin_bit_cast(int, v), 0x118, 0xf, 0xf, false)));
+    v = fminf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(inf, __builtin_bit_cast(int, v), 0x142, 0xa, 0xf, false)));
+    v = fminf(v, __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(inf, __builtin_bit_cast(int, v), 0x143, 0xc, 0xf, false)));
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
+}
+__device__ __forceinline__ float wave_max(float v) { return -wave_min(-v); }
+
+// NE: keys per lane the kernel is built for (n_v <= 64 NE); W: waves (kept
+// tiles) per workgroup.
+template <int NE, int W>
+__global__ void __launch_bounds__(64 * W)
+select_kernel(const double* __restrict__ token_key, int n_tiles, int n_v, int n_keep,
+              const int* __restrict__ kept, const int* __restrict__ budgets, int cap,
+              int* __restrict__ offs, int* __restrict__ sel_idx, int* __restrict__ status) {
+    __shared__ int red_before[W], red_total[W], red_bad[W];
+    __shared__ __align__(16) unsigned hist_all[W][256];
+    const int tid = threadIdx.x;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wave: keeps the masks scalar
+    const int lane = tid & 63;
+    const int first = blockIdx.x * W;
+    const int rho = first + wave;
+    const bool has_tile = rho < n_keep;
+
+    // 1. the loads, longest first: this wave's tile id; the first round of
+    //    every budget and id of the call (16 bytes at a time when both arrays
+    //    allow it); this wave's keys (tile id clamped: every read is in bounds
+    //    whatever the ids hold); the budgets of this workgroup's tiles up to
+    //    this wave's (uniform, through the scalar cache)
+    int tile = has_tile ? kept[rho] : 0;
+    const bool vec = ((reinterpret_cast<uintptr_t>(budgets) | reinterpret_cast<uintptr_t>(kept)) & 15u) == 0;
+    constexpr int kV = 4;                       // 16-byte vectors per thread per round
+    constexpr int kRound = kV * 64 * W;         // vectors per round
+    const int n4 = vec ? n_keep >> 2 : 0;       // whole vectors; the rest one by one
+    i32x4_t bv[kV], tv[kV];
+    if (n4 > 0) {
+#pragma unroll
+        for (int j = 0; j < kV; ++j) {
+            const int v = min(tid + j * 64 * W, n4 - 1);
+            bv[j] = reinterpret_cast<const i32x4_t*>(budgets)[v];
+            tv[j] = reinterpret_cast<const i32x4_t*>(kept)[v];
+        }
     }
-    unsigned* hist = hist_all[wave];
-    const double* kt = token_key + (size_t)tile * n_v;
-    const int ne = (n_v + 63) >> 6;   // elements per lane; element e of lane l is index 64 e + l
-    // every load in bounds (index clamped to the last key), none behind a branch,
-    // so the wave waits for its keys once
+    tile = tile < 0 ? 0 : (tile >= n_tiles ? n_tiles - 1 : tile);
+    const char* kb = reinterpret_cast<const char*>(token_key + (size_t)tile * n_v);
     double raw[NE];
 #pragma unroll
-    for (int e = 0; e < NE; ++e) raw[e] = kt[min(64 * e + lane, n_v - 1)];
-    uint64_t u[NE];
+    for (int e = 0; e < NE; ++e) {
+        const unsigned i = min((unsigned)(64 * e + lane), (unsigned)(n_v - 1));
+        raw[e] = *reinterpret_cast<const double*>(kb + i * 8u);
+    }
+    int off = 0, budget = 0;
 #pragma unroll
-    for (int e = 0; e < NE; ++e)
-        u[e] = (64 * e + lane < n_v) ? desc_bits(raw[e]) : ~0ull;   // padding sorts last
-    // the budget-th smallest value T of u over the valid elements, digit by digit
-    uint64_t prefix = 0, mask = 0;
+    for (int w = 0; w < W; ++w) {
+        const int bw = first + w < n_keep ? budgets[first + w] : 0;
+        off += w < wave ? bw : 0;
+        budget = w == wave ? bw : budget;
+    }
+
+    // 2. validity, base offset and total of the call: the largest budget and
+    //    id as unsigned values (a negative one is huge), the sums
+    unsigned bmax = 0u, tmax = 0u, total = 0u, before = 0u;
+    auto acc4 = [&](int v, const i32x4_t& b4, const i32x4_t& t4) __attribute__((always_inline)) {
+        bmax = max(bmax, max(max((unsigned)b4[0], (unsigned)b4[1]), max((unsigned)b4[2], (unsigned)b4[3])));
+        tmax = max(tmax, max(max((unsigned)t4[0], (unsigned)t4[1]), max((unsigned)t4[2], (unsigned)t4[3])));
+        const unsigned s = (unsigned)b4[0] + (unsigned)b4[1] + (unsigned)b4[2] + (unsigned)b4[3];
+        total += s;
+        if (4 * v + 3 < first) {
+            before += s;
+        } else if (4 * v < first) {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) before += 4 * v + c < first ? (unsigned)b4[c] : 0u;
+        }
+    };
+#pragma unroll
+    for (int j = 0; j < kV; ++j)
+        if (tid + j * 64 * W < n4) acc4(tid + j * 64 * W, bv[j], tv[j]);
+    for (int v0 = tid + kRound; v0 < n4; v0 += kRound) {   // calls of more than one round
+#pragma unroll
+        for (int j = 0; j < kV; ++j) {
+            const int v = min(v0 + j * 64 * W, n4 - 1);
+            bv[j] = reinterpret_cast<const i32x4_t*>(budgets)[v];
+            tv[j] = reinterpret_cast<const i32x4_t*>(kept)[v];
+        }
+#pragma unroll
+        for (int j = 0; j < kV; ++j)
+            if (v0 + j * 64 * W < n4) acc4(v0 + j * 64 * W, bv[j], tv[j]);
+    }
+    for (int i = 4 * n4 + tid; i < n_keep; i += 64 * W) {
+        const unsigned bi = (unsigned)budgets[i];
+        bmax = max(bmax, bi);
+        tmax = max(tmax, (unsigned)kept[i]);
+        total += bi;
+        before += i < first ? bi : 0u;
+    }
+    before = wave_sum((int)before);
+    total = wave_sum((int)total);
+    const bool any_bad = __ballot(bmax > (unsigned)n_v || tmax >= (unsigned)n_tiles) != 0ull;
+    if (lane == 0) {
+        red_before[wave] = (int)before;
+        red_total[wave] = (int)total;
+        red_bad[wave] = any_bad;
+    }
+    // only shared memory is waited for at the barrier, so the keys stay in flight
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    before = 0u;
+    total = 0u;
+    int badw = 0;
+#pragma unroll
+    for (int w = 0; w < W; ++w) {
+        before += (unsigned)red_before[w];
+        total += (unsigned)red_total[w];
+        badw |= red_bad[w];
+    }
+    // valid budgets and ids keep every sum within n_tiles * n_v <= INT32_MAX
+    if (badw == 0 && total > (unsigned)cap) badw = 1;
+    badw = __builtin_amdgcn_readfirstlane(badw);
+    if (blockIdx.x == 0 && tid == 0) {
+        *status = badw ? (int)RIFT_ERR_BUDGET : 0;
+        if (n_keep == 0) offs[0] = 0;
+    }
+    off = __builtin_amdgcn_readfirstlane((int)before + off);
+    if (has_tile && lane == 0) {
+        offs[rho] = badw ? 0 : off;
+        if (rho == n_keep - 1) offs[n_keep] = badw ? 0 : (int)total;
+    }
+    if (badw || !has_tile) return;
+    budget = __builtin_amdgcn_readfirstlane(budget);
+    if (budget <= 0) return;
+    int* out = sel_idx + off;
+    if (budget >= n_v) {
+        for (int i = lane; i < n_v; i += 64) out[i] = i;
+        return;
+    }
+
+    // 3. which tokens to take.  First, when the keys are finite as float32
+    // and not all equal, one histogram pass over 256 value buckets of their
+    // float32 range: bucket = trunc((max - f) * (256 / (max - min))), clamped
+    // to 255, with f the key rounded to float32.  Each step (the rounding to
+    // float32, the subtraction, the product with a positive factor, the
+    // truncation) is monotone, so every key of a lower bucket is strictly
+    // larger than every key of a higher one.  The buckets before the one that
+    // holds the budget-th key are taken whole; that bucket's keys, usually a
+    // handful, are the candidates for the rest.
+    unsigned* hist = hist_all[wave];
+    uint64_t cand[NE], take[NE];
     int k = budget;
-    for (int shift = 56; shift >= 0; shift -= 8) {
+    int ncand = n_v;
+    bool fin = true;
+    float fmn = INFINITY, fmx = -INFINITY;
+    float f[NE];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) hist[4 * lane + j] = 0;
+    for (int e = 0; e < NE; ++e) {
+        const int base = 64 * e;
+        cand[e] = base >= n_v ? 0ull : (base + 64 <= n_v ? ~0ull : ((1ull << (n_v - base)) - 1ull));
+        take[e] = 0ull;
+        f[e] = (float)raw[e];
+        if (base + lane < n_v) {
+            fin = fin && (f[e] - f[e] == 0.0f);   // false for NaN, infinities and float32 overflow
+            fmn = fminf(fmn, f[e]);
+            fmx = fmaxf(fmx, f[e]);
+        }
+    }
+    fmn = wave_min(fmn);
+    fmx = wave_max(fmx);
+    const bool all_finite = __ballot(!fin) == 0ull;
+    const float range = __fsub_rn(fmx, fmn);
+    const float scale = 256.0f / range;
+    if (all_finite && range > 0.0f && range - range == 0.0f && scale - scale == 0.0f) {
+        int bkt[NE];
+        *reinterpret_cast<u32x4_t*>(hist + 4 * lane) = u32x4_t{0u, 0u, 0u, 0u};
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
         for (int e = 0; e < NE; ++e) {
-            const int i = 64 * e + lane;
-            if (e < ne && i < n_v && (u[e] & mask) == prefix)
-                atomicAdd(&hist[(unsigned)(u[e] >> shift) & 255u], 1u);
+            const int t = (int)__fmul_rn(__fsub_rn(fmx, f[e]), scale);
+            bkt[e] = t < 255 ? t : 255;
+            if (64 * e + lane < n_v) atomicAdd(&hist[bkt[e]], 1u);
         }
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        unsigned c[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) c[j] = hist[4 * lane + j];
+        const u32x4_t c = *reinterpret_cast<const u32x4_t*>(hist + 4 * lane);
         const unsigned mine = c[0] + c[1] + c[2] + c[3];
-        unsigned before = wave_incl_scan(mine) - mine;   // count in bins < 4 lane
+        unsigned bsum = wave_incl_scan(mine) - mine;   // keys in buckets < 4 lane
         int hit = -1;
-        unsigned hit_before = 0;
+        unsigned hit_before = 0, hit_count = 0;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            if (hit < 0 && before < (unsigned)k && (unsigned)k <= before + c[j]) {
+            if (hit < 0 && bsum < (unsigned)k && (unsigned)k <= bsum + c[j]) {
                 hit = 4 * lane + j;
-                hit_before = before;
+                hit_before = bsum;
+                hit_count = c[j];
             }
-            before += c[j];
+            bsum += c[j];
         }
-        unsigned hit_count = 0;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            if (hit == 4 * lane + j) hit_count = c[j];
-        const uint64_t hits = __ballot(hit >= 0);
-        const int src = __builtin_ctzll(hits);   // exactly one lane holds the digit
-        const int digit = __builtin_amdgcn_readlane(hit, src);
+        const int src = __builtin_ctzll(__ballot(hit >= 0));   // exactly one lane holds the bucket
+        const int B = __builtin_amdgcn_readlane(hit, src);
         k -= (int)__builtin_amdgcn_readlane(hit_before, src);
-        prefix |= (uint64_t)digit << shift;
-        mask |= 255ull << shift;
-        // every candidate left in the bin is taken: the digits below no longer matter
-        if ((int)__builtin_amdgcn_readlane(hit_count, src) == k) break;
+        ncand = (int)__builtin_amdgcn_readlane(hit_count, src);
+#pragma unroll
+        for (int e = 0; e < NE; ++e) {
+            take[e] = __ballot(bkt[e] < B) & cand[e];
+            cand[e] = __ballot(bkt[e] == B) & cand[e];
+        }
     }
-    // take every u whose masked value is below the prefix, and the first k (by
-    // index) of those equal to it; write ascending
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    int eq_seen = 0, written = 0;
+    if (ncand != k && ncand <= 64 && all_finite) {
+        // Rank each candidate among the candidates by (key desc, index asc)
+        // with plain float64 comparisons (-0 and +0 compare equal); take the
+        // first k.  The histogram's slice of shared memory holds them.
+        double* cx = reinterpret_cast<double*>(hist);
+        int* ci = reinterpret_cast<int*>(hist + 128);
+        int* chosen = reinterpret_cast<int*>(hist + 192);
+        int slot0 = 0;
+        int slot[NE];
+#pragma unroll
+        for (int e = 0; e < NE; ++e) {
+            slot[e] = slot0 + __popcll(cand[e] & below);
+            if ((cand[e] >> lane) & 1ull) {
+                cx[slot[e]] = raw[e];
+                ci[slot[e]] = 64 * e + lane;
+            }
+            slot0 += __popcll(cand[e]);
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        if (lane < ncand) {
+            const double mx = cx[lane];
+            const int mi = ci[lane];
+            int r = 0;
+            for (int j = 0; j < ncand; ++j) {
+                const double xj = cx[j];
+                const int ij = ci[j];
+                r += (xj > mx || (xj == mx && ij < mi)) ? 1 : 0;
+            }
+            chosen[lane] = r < k ? 1 : 0;
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+        for (int e = 0; e < NE; ++e) {
+            const bool mine_c = (cand[e] >> lane) & 1ull;
+            take[e] |= __ballot(mine_c && chosen[mine_c ? slot[e] : 0] != 0);
+            cand[e] = 0ull;
+        }
+        k = 0;
+    } else if (ncand != k) {
+        // Many candidates (wide ties, non-finite or extreme keys): decide the
+        // order-preserving key bits one at a time from the highest bit in
+        // which the candidates differ.  Per bit, a ballot per element counts
+        // the candidates with a 0 there; the side holding the k-th stays
+        // candidate, and when that is the 1 side the 0 side is taken.  It ends
+        // once exactly k candidates remain, else after bit 0 with equal keys.
+        uint32_t hi[NE], lo[NE];
+        uint32_t ah = ~0u, al = ~0u, oh = 0u, ol = 0u;
+#pragma unroll
+        for (int e = 0; e < NE; ++e) {
+            const uint64_t u = desc_bits(raw[e]);
+            hi[e] = (uint32_t)(u >> 32);
+            lo[e] = (uint32_t)u;
+            if ((cand[e] >> lane) & 1ull) {
+                ah &= hi[e];
+                al &= lo[e];
+                oh |= hi[e];
+                ol |= lo[e];
+            }
+        }
+#pragma unroll
+        for (int s = 32; s >= 1; s >>= 1) {
+            ah &= __shfl_xor(ah, s);
+            al &= __shfl_xor(al, s);
+            oh |= __shfl_xor(oh, s);
+            ol |= __shfl_xor(ol, s);
+        }
+        const uint32_t dh = __builtin_amdgcn_readfirstlane(ah ^ oh);
+        const uint32_t dl = __builtin_amdgcn_readfirstlane(al ^ ol);
+        auto decide = [&](const uint32_t (&word)[NE], int b) __attribute__((always_inline)) {
+            uint64_t zero[NE];
+            int c0 = 0;
+#pragma unroll
+            for (int e = 0; e < NE; ++e) {
+                zero[e] = __ballot(((word[e] >> b) & 1u) == 0u) & cand[e];
+                c0 += __popcll(zero[e]);
+            }
+            if (k <= c0) {
+#pragma unroll
+                for (int e = 0; e < NE; ++e) cand[e] = zero[e];
+                ncand = c0;
+            } else {
+                k -= c0;
+                ncand -= c0;
+#pragma unroll
+                for (int e = 0; e < NE; ++e) {
+                    take[e] |= zero[e];
+                    cand[e] &= ~zero[e];
+                }
+            }
+        };
+        if ((dh | dl) != 0u) {
+            int b = dh != 0u ? 63 - __builtin_clz(dh) : 31 - __builtin_clz(dl);
+            for (; b >= 32 && ncand != k; --b) decide(hi, b - 32);
+            for (; b >= 0 && ncand != k; --b) decide(lo, b);
+        }
+    }
+    // the candidates left: all of them when exactly k remain, else (equal
+    // keys) the k of lowest index
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
-        if (e >= ne) break;
-        const int i = 64 * e + lane;
-        const bool valid = i < n_v;
-        const uint64_t um = u[e] & mask;
-        const bool eq = valid && um == prefix;
-        const uint64_t eqm = __ballot(eq);
-        const bool take = valid && (um < prefix || (eq && eq_seen + __popcll(eqm & below) < k));
-        eq_seen += __popcll(eqm);
-        const uint64_t tm = __ballot(take);
-        if (take) sel_idx[off + written + __popcll(tm & below)] = i;
-        written += __popcll(tm);
+        uint64_t c = cand[e];
+        const int pc = __popcll(c);
+        if (pc <= k) {
+            take[e] |= c;
+            k -= pc;
+        } else {
+            while (k > 0) {
+                const uint64_t low = c & (~c + 1ull);
+                take[e] |= low;
+                c ^= low;
+                --k;
+            }
+        }
+    }
+
+    // 4. ascending index order: element e before e + 1, lane order within
+    int written = 0;
+#pragma unroll
+    for (int e = 0; e < NE; ++e) {
+        const uint64_t t = take[e];
+        if ((t >> lane) & 1ull) out[written + __popcll(t & below)] = 64 * e + lane;
+        written += __popcll(t);
     }
 }
 
 hipError_t launch_select(const double* token_key, int n_tiles, int n_v, const int* kept,
                          const int* budgets, int n_keep, int* sel_offsets, int* sel_idx,
                          long long cap, int* status, hipStream_t st) {
-    hipLaunchKernelGGL(select_offsets_kernel, dim3(1), dim3(1024), 0, st, kept, budgets, n_keep,
-                       n_tiles, n_v, cap, sel_offsets, status);
-    if (n_keep > 0)
-        if (n_v <= 64 * 9)
-            hipLaunchKernelGGL(select_topk_kernel<9>, dim3((n_keep + 3) / 4), dim3(256), 0, st, token_key,
-                               n_v, n_keep, kept, sel_offsets, status, sel_idx);
-        else
-            hipLaunchKernelGGL(select_topk_kernel<16>, dim3((n_keep + 3) / 4), dim3(256), 0, st, token_key,
-                               n_v, n_keep, kept, sel_offsets, status, sel_idx);
+    // Every workgroup reads all budgets: few tiles per workgroup spread a
+    // query's tiles over the CUs; more amortise those reads in large calls
+    // (eight waves: 16 left some CUs with twice the work of others).
+    const int c = (int)(cap < 0x7fffffffLL ? cap : 0x7fffffffLL);
+    auto go = [&](auto kernel, int W) {
+        const unsigned wgs = (unsigned)((n_keep + W - 1) / W);
+        hipLaunchKernelGGL(kernel, dim3(wgs > 0 ? wgs : 1u), dim3(64 * W), 0, st, token_key, n_tiles, n_v, n_keep,
+                           kept, budgets, c, sel_offsets, sel_idx, status);
+    };
+    const bool small = n_keep <= 4 * 256;
+    if (n_v <= 64 * 9) {
+        if (small) go(select_kernel<9, 4>, 4);
+        else go(select_kernel<9, 8>, 8);
+    } else {
+        if (small) go(select_kernel<16, 4>, 4);
+        else go(select_kernel<16, 8>, 8);
+    }
     return hipGetLastError();
 }
 

@@ -206,6 +206,48 @@ def test_select_ragged_sizes(R, n_v):
     assert st == 0 and np.array_equal(offs, r_offs) and np.array_equal(sel, r_sel)
 
 
+@pytest.mark.parametrize("case", ["dup_in_bucket", "crowded_bucket", "infinities", "two_values", "tiny_range"])
+def test_select_narrowing_cases(R, case):
+    """Inputs aimed at each way the kernel narrows the candidates: repeated
+    values inside the bucket of the budget-th key (ranked by index), one value
+    bucket holding most keys (the bit-by-bit fallback), infinite keys (no
+    value buckets), two distinct values, and keys a few ulps apart."""
+    rng = np.random.default_rng(hash(case) % 2**32)
+    n_tiles, n_v = 8, 576
+    if case == "dup_in_bucket":
+        base = rng.standard_normal((n_tiles, n_v)) * 0.02
+        keys = np.where(rng.random((n_tiles, n_v)) < 0.5, np.round(base, 3), base)
+    elif case == "crowded_bucket":
+        keys = 1.0 + rng.standard_normal((n_tiles, n_v)) * 1e-9
+        keys[:, ::97] = rng.standard_normal((n_tiles, 6)) * 100.0
+    elif case == "infinities":
+        keys = rng.standard_normal((n_tiles, n_v))
+        keys[:, 3] = np.inf
+        keys[:, 7::50] = -np.inf
+    elif case == "two_values":
+        keys = rng.choice([0.25, -0.75], size=(n_tiles, n_v))
+    else:
+        keys = 0.5 + rng.integers(-4, 5, size=(n_tiles, n_v)) * 2.0 ** -52
+    kept = list(range(n_tiles))
+    budgets = [64, 144, 288, 1, 575, 300, 2, 500]
+    offs, sel, st = run_select(R, keys, kept, budgets)
+    r_offs, r_sel = O.select_tokens(keys, kept, budgets)
+    assert st == 0 and np.array_equal(offs, r_offs) and np.array_equal(sel, r_sel)
+
+
+def test_select_many_tiles(R):
+    """More kept tiles than one pass of a workgroup's budget loads (8,192):
+    every workgroup's base offset and the whole selection against the oracle."""
+    rng = np.random.default_rng(21)
+    n_tiles, n_v = 9500, 40
+    keys = rng.integers(-20, 21, size=(n_tiles, n_v)).astype(np.float64) * 0.125
+    kept = list(rng.permutation(n_tiles)[:9000])
+    budgets = list(rng.integers(0, n_v + 1, size=9000))
+    offs, sel, st = run_select(R, keys, kept, budgets)
+    r_offs, r_sel = O.select_tokens(keys, kept, budgets)
+    assert st == 0 and np.array_equal(offs, r_offs) and np.array_equal(sel, r_sel)
+
+
 def test_select_rejects_bad_budgets(R):
     keys = np.zeros((2, 10))
     for budgets, kept in (([11, 1], [0, 1]), ([-1, 1], [0, 1]), ([1, 1], [0, 2])):
