@@ -171,17 +171,21 @@ rift_status rift_check_finite(const void* x, rift_dtype dt, int64_t count, int32
 }
 
 namespace {
-// score workspace: w (float32 [d]); with smoothing, then inverse token norms
-// (float64 [n_tiles n_v]), tile embeddings (float32 [n_tiles][d]), their
-// dot products (float64 [n_tiles][n_tiles]) and the smoothed scores.
+// score workspace: w (float32 [d]), the per-tile arrival counters and the
+// pooled-tile counter (int32 [n_tiles + 1], cleared by the call itself); with
+// smoothing, then inverse token norms (float64 [n_tiles n_v]), tile
+// embeddings (float32 [n_tiles][d]), their dot products (float64
+// [n_tiles][n_tiles]) and the smoothed scores.
 struct ScoreLayout {
-    size_t w, inv, emb, gram, smooth, dbg, total;
+    size_t w, cnt, inv, emb, gram, smooth, dbg, total;
 };
 ScoreLayout score_layout(int32_t n_tiles, int32_t n_v, int32_t d, int32_t knn_m) {
     ScoreLayout L{};
     size_t off = 0;
     L.w = off;
     off += align_up((size_t)d * sizeof(float));
+    L.cnt = off;
+    off += align_up((size_t)(n_tiles + 1) * sizeof(int));
     if (knn_m > 0) {
         L.inv = off;
         off += align_up((size_t)n_tiles * n_v * sizeof(double));
@@ -240,7 +244,7 @@ rift_status score_enqueue(const void* tokens, rift_dtype dt, int32_t n_tiles, in
     hipError_t e = launch_score(tokens, dt == RIFT_BF16, n_tiles, n_v, d, query_bank, n_bg,
                                 keep_count, tau, knn_m, token_key, token_sim, tile_score, tile_u,
                                 tile_order, n_keep, reinterpret_cast<float*>(ws + L.w),
-                                reinterpret_cast<double*>(ws + L.inv), reinterpret_cast<float*>(ws + L.emb),
+                                reinterpret_cast<int*>(ws + L.cnt), reinterpret_cast<double*>(ws + L.inv), reinterpret_cast<float*>(ws + L.emb),
                                 reinterpret_cast<double*>(ws + L.gram), reinterpret_cast<double*>(ws + L.smooth), st);
     return hip_status(e);
 }

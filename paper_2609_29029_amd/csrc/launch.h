@@ -11,7 +11,7 @@ namespace rift {
 hipError_t launch_score(const void* tokens, bool bf16, int n_tiles, int n_v, int d,
                         const void* qbank, int n_bg, int keep_count, double tau, int knn_m,
                         double* token_key, float* token_sim, double* tile_score, float* tile_u,
-                        int* tile_order, int* n_keep, float* w32, double* inv, float* emb,
+                        int* tile_order, int* n_keep, float* w32, int* arrivals, double* inv, float* emb,
                         double* gram, double* s_smooth, hipStream_t st);
 // optional score smoothing over each tile's knn_m most similar tiles
 hipError_t launch_knn_smooth(const void* tokens, bool bf16, int n_tiles, int n_v, int d,

@@ -123,6 +123,8 @@ def test_score_threshold_mode(R):
     ("bf16", 2, 33, 4064, 1),    # fifteen whole chunks and a 7-step tail, one token past a 32-token set
     ("f32", 2, 33, 800, 2),      # the float32 path on the same ragged shapes
     ("bf16", 4096, 4, 32, 0),    # the maximum tile count (one sort of 4096 keys), minimum d
+    ("bf16", 1024, 8, 32, 1),    # the most tiles ranked by counting
+    ("bf16", 1025, 40, 64, 2),   # the fewest ranked by sorting; workgroups straddle tiles
 ])
 def test_score_edge_shapes(R, dtype, n_tiles, n_v, d, n_bg):
     rng = np.random.default_rng(n_tiles * 1000 + n_v)
@@ -136,6 +138,24 @@ def test_score_edge_shapes(R, dtype, n_tiles, n_v, d, n_bg):
     ref = O.scene_query_stage1(X64, Q64, 2, 0.37)
     check_stage1(got, ref, X64, Q64)
     assert got["token_key"].reshape(n_tiles, n_v)[0, 3] == 0.0
+
+
+@pytest.mark.parametrize("n_tiles", [300, 1500])
+def test_score_threshold_mode_many_tiles(R, n_tiles):
+    """Retention by u >= tau over scenes ranked by counting (300 tiles) and
+    by sorting (1,500 tiles): order, u and the kept count against the
+    oracle."""
+    rng = np.random.default_rng(n_tiles)
+    x32 = rng.standard_normal((n_tiles, 20, 64)).astype(np.float32)
+    q = rng.standard_normal((3, 64))
+    q = (q / np.linalg.norm(q, axis=1, keepdims=True)).astype(np.float32)
+    x32[7] += 4.0 * q[0]             # a relevant tile (cosine near 0.45), so u spreads over [0, 1]
+    X, Q = synth.store(x32, "bf16"), synth.store(q, "bf16")
+    got = run_score(R, upload(X, "bf16"), upload(Q, "bf16"), 0, 0.37)
+    X64, Q64 = f64(X, "bf16"), f64(Q, "bf16")
+    ref = O.scene_query_stage1(X64, Q64, 0, 0.37)
+    check_stage1(got, ref, X64, Q64)
+    assert got["tile_order"][0] == 7 and int(got["n_keep"][0]) == ref["n_keep"] >= 1
 
 
 def test_score_equal_tiles(R):
