@@ -2,13 +2,19 @@
 // an independent sequence; Sec. 2.3 Stage 2).  Query i of a sequence attends
 // to keys 0..i of the same sequence, scale 1/sqrt(head_dim).
 //
-// bf16, head_dim 128, on MFMA.  One workgroup (4 waves) per (sequence, head),
-// looping over the sequence's 128-query blocks (no workgroup is launched for a
-// block past the end of a short prompt; workgroups are numbered sequence by
-// sequence, so prompts packed longest first start first); wave w owns queries
-// [32 w, 32 w + 32) of the block.  Keys
-// and values stream through two LDS buffers 64 at a time, both row-major; the
-// next block's rows are loaded into registers while the current one is used.
+// bf16, head_dim 128, on MFMA.  One workgroup of W = 4 waves per (sequence,
+// head), looping over the sequence's 128-query blocks, the last
+// (longest-running) first; wave w owns queries [32 w, 32 w + 32) of the block
+// (workgroups are numbered sequence by sequence, so prompts packed longest
+// first start first).  Keys and values stream 64 at a time through a ring of
+// S = 2 LDS stages that LDS DMA fills a block ahead, one barrier per block,
+// and two workgroups share a CU.  Tile rows are 256 bytes, unpadded; the
+// 16-byte chunks of row r sit at chunk ^ (r & 15) for keys and chunk ^
+// 4 (r & 3) for values, which keeps both the key-row reads and the
+// transposing value reads free of bank conflicts.  (The kernel also runs
+// with W = 8, two query blocks sharing each key/value tile, and with deeper
+// rings; on the 400-tile query those were slower: one workgroup a CU leaves
+// the SIMDs half idle on prompts of a single query block.)
 // The wave computes S^T = K Q^T (v_mfma_f32_32x32x16_bf16, M = keys,
 // N = queries), so each lane holds one query's scores in registers; the online
 // softmax runs in float32 (running max and sum per query); the unnormalised
@@ -35,24 +41,46 @@ namespace {
 constexpr int HD = 128;
 constexpr int BQ = 128;
 constexpr int BKV = 64;
-constexpr int KPAD = HD + 8;    // K tile row stride (elements): 272 B, b128 reads of 32 rows 2-way
-constexpr int VPAD = HD + 32;   // V tile row stride (elements): 320 B, transposing reads 2-way
+constexpr int kRowBytes = HD * 2;               // one key or value row
+constexpr int kTileBytes = BKV * kRowBytes;     // 16 KB
+constexpr int kStageBytes = 2 * kTileBytes;     // keys, then values
 
 typedef short v4s_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
 
 // ds_read_b64_tr_b16: lane i of each 16-lane group g gets, in component j, the
 // 16-bit element at (address passed by lane 16 g + 4 j + i / 4) + i % 4.
-__device__ __forceinline__ v4s_t lds_read_tr16(const bf16_t* p) {
+__device__ __forceinline__ v4s_t lds_read_tr16(const void* p) {
     return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t*)(p));
 }
 
-__global__ void __launch_bounds__(256, 2)
+// LDS DMA of 16 bytes per lane from a per-lane global address into
+// LDS[m0 + 16 lane] (m0 wave-uniform).
+__device__ __forceinline__ void dma16v(const void* gaddr, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :: "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(gaddr) : "memory", "m0");
+}
+
+// wait until at most n of this wave's vector memory operations are outstanding
+__device__ __forceinline__ void wait_vm(int n) {
+    switch (n) {
+        case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+        case 4: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+        case 8: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+        case 16: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
+        default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    }
+}
+
+// W waves (W / 4 query blocks per pass), S ring stages.
+template <int W, int S>
+__global__ void __launch_bounds__(64 * W, W == 8 ? 1 : 2)
 attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
                  const bf16_t* __restrict__ v, bf16_t* __restrict__ o,
                  const int* __restrict__ cu, int n_seq, int H, int n_prefix, float scale_log2) {
-    __shared__ __align__(16) bf16_t Ks[2][BKV * KPAD];
-    __shared__ __align__(16) bf16_t Vs[2][BKV * VPAD];
+    constexpr int G = W / 4;                 // query blocks per pass
+    constexpr int NDMA = 32 / W;             // DMA instructions per wave per key block
+    __shared__ __align__(16) unsigned char ring[S * kStageBytes];
 
     const int seq = blockIdx.x / H;
     const int head = blockIdx.x % H;
@@ -62,185 +90,203 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int grp = wave >> 2;                // with W = 8: 0 the upper block of a pass, 1 the lower
+    const int wq = wave & 3;                  // wave within its block
     const int h = lane >> 5;
     const int col = lane & 31;
     const int ld = H * HD;
     const size_t head_off = (size_t)head * HD;
+    const uint32_t ring0 = (uint32_t)(uintptr_t)ring;
 
-    // query blocks, the longest-running (last) first
-    for (int qb = (L + BQ - 1) / BQ - 1; qb >= 0; --qb) {
-    const int q0 = qb * BQ;
-    __syncthreads();   // the previous block's reads of the K/V buffers are done
-    const int qw = q0 + wave * 32;            // first query of this wave
-    const int qidx = qw + col;                // this lane's query
-    const int q_eff = qidx < L ? qidx : L - 1;
-
-    // Q^T B-operand fragments: lane holds Q[query][16 kk + 8 h .. + 8]
-    bf16x8_t qf[8];
-    {
-        const bf16_t* qrow = q + (size_t)(s0 + q_eff) * ld + head_off + 8 * h;
+    // DMA of logical key block `blk` into stage blk % 4: 32 instructions of
+    // four 256-byte rows each (0..15 keys, 16..31 values); wave w issues
+    // 4 w .. 4 w + 3 (waves 0-3 keys, 4-7 values).  Lane l moves chunk
+    // position l % 16 of row 4 jj + l / 16, i.e. global chunk position ^ swz.
+    const bool dma_v = wave >= W / 2;
+    const bf16_t* dma_src = dma_v ? v : k;
+    const int dma_row_lo = lane >> 4;
+    auto dma_block = [&](int blk) {
+        const uint32_t sb = ring0 + (uint32_t)(blk % S) * kStageBytes + (dma_v ? kTileBytes : 0);
 #pragma unroll
-        for (int kk = 0; kk < 8; ++kk) qf[kk] = *reinterpret_cast<const bf16x8_t*>(qrow + 16 * kk);
-    }
-
-    f32x16_t oacc[4];
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) oacc[t][i] = 0.f;
-    float m_run = -INFINITY;
-    float l_run = 0.f;
-
-    // logical key range of this block and the logical position of the wave's last query
-    const int kv_end = pre + ((q0 + BQ) < L ? (q0 + BQ) : L);
-    const int nkv = (kv_end + BKV - 1) / BKV;
-    const int wave_last = pre + ((qw + 31) < (L - 1) ? (qw + 31) : (L - 1));
-
-    // K and V rows of a key block (clamped to the sequence): thread moves
-    // 16 bytes of rows rr = (tid + 256 it) / 16 of both, into registers first
-    u32x4_t kr[4], vr[4];
-    auto load_block = [&](int kv0) {
-#pragma unroll
-        for (int it = 0; it < 4; ++it) {
-            const int vec = tid + 256 * it;
-            int key = kv0 + (vec >> 4);
+        for (int i = 0; i < NDMA; ++i) {
+            const int jj = NDMA * (wave % (W / 2)) + i;
+            const int row = 4 * jj + dma_row_lo;
+            int key = blk * BKV + row;
             key = key < pre + L ? key : pre + L - 1;
-            const int row = key < pre ? key : s0 + key - pre;
-            const size_t g = (size_t)row * ld + head_off + (vec & 15) * 8;
-            kr[it] = *reinterpret_cast<const u32x4_t*>(k + g);
-            vr[it] = *reinterpret_cast<const u32x4_t*>(v + g);
-        }
-    };
-    auto store_block = [&](int buf) {
-#pragma unroll
-        for (int it = 0; it < 4; ++it) {
-            const int vec = tid + 256 * it;
-            const int rr = vec >> 4;
-            const int cc = (vec & 15) * 8;
-            *reinterpret_cast<u32x4_t*>(&Ks[buf][rr * KPAD + cc]) = kr[it];
-            *reinterpret_cast<u32x4_t*>(&Vs[buf][rr * VPAD + cc]) = vr[it];
+            const int grow = key < pre ? key : s0 + key - pre;
+            const int swz = dma_v ? 4 * (row & 3) : (row & 15);
+            const int c = (lane & 15) ^ swz;
+            dma16v(dma_src + (size_t)grow * ld + head_off + c * 8, sb + (uint32_t)jj * 1024u);
         }
     };
 
-    // transposing-read addresses of this lane as a source lane: group g,
-    // component j, quad u -> key 4 (g >> 1) + j (+ 8), dims 16 (g & 1) + 4 u
+    // per-lane byte offsets of the operand reads within a stage
+    //   keys: row kb*32 + col, chunk 2 kk + h at (2 kk + h) ^ (col & 15)
+    //   values (transposing): source lane (tg, tj, tu) passes key row
+    //   4 (tg >> 1) + tj (+ 16 ks + 32 kb, + 8 for the upper half) and
+    //   dimensions 16 (tg & 1) + 4 tu + 32 t: chunk (2 (tg & 1) + tu / 2) | 4 t
+    //   at chunk ^ 4 tj, byte 8 (tu & 1) within it
     const int tg = lane >> 4, tj = (lane >> 2) & 3, tu = lane & 3;
-    const int v_off = (4 * (tg >> 1) + tj) * VPAD + 16 * (tg & 1) + 4 * tu;
+    const int k_row_off = col * kRowBytes;
+    const int v_off = (4 * (tg >> 1) + tj) * kRowBytes + (2 * (tg & 1) + (tu >> 1)) * 16 + 8 * (tu & 1);
 
-    load_block(0);
-    store_block(0);
-    __syncthreads();
-    for (int kb_i = 0; kb_i < nkv; ++kb_i) {
-        const int kv0 = kb_i * BKV;
-        const int cur = kb_i & 1;
-        if (kb_i + 1 < nkv) load_block(kv0 + BKV);
-        if (kv0 <= wave_last) {
-            // scores for two 32-key sub-blocks; their MFMA chains interleaved
-            f32x16_t s[2];
+    const int nqb = (L + BQ - 1) / BQ;
+    for (int pr = 0; G * pr < nqb; ++pr) {
+        const int qb_hi = nqb - 1 - G * pr;
+        const int qb = qb_hi - grp;               // -1: the lower half has no block
+        const int q0 = qb >= 0 ? qb * BQ : 0;
+        const int qw = q0 + wq * 32;              // first query of this wave
+        const int qidx = qw + col;                // this lane's query
+        const int q_eff = qidx < L ? qidx : L - 1;
+        // logical position of the wave's last query, -1 when it has none
+        const int wave_last = (qb >= 0 && qw < L) ? pre + ((qw + 31) < (L - 1) ? (qw + 31) : (L - 1)) : -1;
+
+        asm volatile("s_barrier" ::: "memory");   // every wave is done with the ring
+        // Q^T B-operand fragments: lane holds Q[query][16 kk + 8 h .. + 8]
+        bf16x8_t qf[8];
+        {
+            const bf16_t* qrow = q + (size_t)(s0 + q_eff) * ld + head_off + 8 * h;
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
+            for (int kk = 0; kk < 8; ++kk) qf[kk] = *reinterpret_cast<const bf16x8_t*>(qrow + 16 * kk);
+        }
+
+        f32x16_t oacc[4];
 #pragma unroll
-                for (int i = 0; i < 16; ++i) s[kb][i] = 0.f;
+        for (int t = 0; t < 4; ++t)
 #pragma unroll
-            for (int kk = 0; kk < 8; ++kk)
+            for (int i = 0; i < 16; ++i) oacc[t][i] = 0.f;
+        float m_run = -INFINITY;
+        float l_run = 0.f;
+
+        // key blocks of the pair: up to the end of the upper query block
+        const int kv_end = pre + ((qb_hi + 1) * BQ < L ? (qb_hi + 1) * BQ : L);
+        const int nkv = (kv_end + BKV - 1) / BKV;
+        const int pro = nkv < S - 1 ? nkv : S - 1;
+        for (int b = 0; b < pro; ++b) dma_block(b);
+        // The compiler waits for the Q loads here, once per pair (with them,
+        // for the ring's first blocks, issued just after); in the loop it then
+        // has no load of its own outstanding, and the explicit waits below
+        // keep up to two blocks in flight.
 #pragma unroll
-                for (int kb = 0; kb < 2; ++kb) {
-                    const bf16x8_t kf =
-                        *reinterpret_cast<const bf16x8_t*>(&Ks[cur][(kb * 32 + col) * KPAD + 8 * h + 16 * kk]);
-                    s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
+        for (int kk = 0; kk < 8; ++kk) asm volatile("" : "+v"(qf[kk]));
+
+        for (int b = 0; b < nkv; ++b) {
+            // block b has landed (the Q loads, issued earlier, too) once at
+            // most the DMA of blocks b+1, b+2 is outstanding; after the barrier
+            // every wave's share has, and every wave is done with block b-1
+            const int later = (nkv - 1 < b + S - 2 ? nkv - 1 : b + S - 2) - b;
+            wait_vm(NDMA * later);
+            asm volatile("s_barrier" ::: "memory");
+            if (b + S - 1 < nkv) dma_block(b + S - 1);    // into the stage block b-1 used
+
+            const int kv0 = b * BKV;
+            if (kv0 <= wave_last) {
+                const unsigned char* Kb = ring + (b % S) * kStageBytes;
+                const unsigned char* Vb = Kb + kTileBytes;
+                // scores for two 32-key sub-blocks; their MFMA chains interleaved
+                f32x16_t s[2];
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) s[kb][i] = 0.f;
+#pragma unroll
+                for (int kk = 0; kk < 8; ++kk)
+#pragma unroll
+                    for (int kb = 0; kb < 2; ++kb) {
+                        const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(
+                            Kb + kb * 32 * kRowBytes + k_row_off + (((2 * kk + h) ^ (col & 15)) << 4));
+                        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
+                    }
+                // raw scores; keys past a query are masked only in blocks that
+                // cross the wave's diagonal.  The running max is kept on the raw
+                // scale (scale_log2 > 0 commutes with max), and p = 2^(s scale - m)
+                // takes one fma and the hardware exp2 (its flush of results below
+                // 2^-126 to zero drops terms far below the row sum's precision).
+                float sc[2][16];
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) sc[kb][i] = s[kb][i];
+                if (kv0 + BKV - 1 > pre + qw) {
+#pragma unroll
+                    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) {
+                            const int key = kv0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+                            sc[kb][i] = (key <= pre + q_eff) ? sc[kb][i] : -INFINITY;
+                        }
                 }
-            // raw scores; keys past a query are masked only in blocks that
-            // cross the wave's diagonal.  The running max is kept on the raw
-            // scale (scale_log2 > 0 commutes with max), and p = 2^(s scale - m)
-            // takes one fma and the hardware exp2 (its flush of results below
-            // 2^-126 to zero drops terms far below the row sum's precision).
-            float sc[2][16];
+                float bmax = -INFINITY;
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
+                for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) sc[kb][i] = s[kb][i];
-            if (kv0 + BKV - 1 > pre + qw) {
+                    for (int i = 0; i < 16; ++i) bmax = fmaxf(bmax, sc[kb][i]);
+                bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
+                const float m_new = fmaxf(m_run, bmax * scale_log2);
+                const float neg_m = -m_new;
+                float rsum = 0.f;
 #pragma unroll
                 for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                     for (int i = 0; i < 16; ++i) {
-                        const int key = kv0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-                        sc[kb][i] = (key <= pre + q_eff) ? sc[kb][i] : -INFINITY;
+                        const float pv = __builtin_amdgcn_exp2f(fmaf(sc[kb][i], scale_log2, neg_m));
+                        sc[kb][i] = pv;
+                        rsum += pv;
+                    }
+                rsum += __shfl_xor(rsum, 32);
+                // rescale the sums only when some query's max moved (exact skip)
+                if (__any(m_new != m_run)) {
+                    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+                    l_run *= alpha;
+#pragma unroll
+                    for (int t = 0; t < 4; ++t)
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) oacc[t][i] *= alpha;
+                }
+                l_run += rsum;
+                m_run = m_new;
+
+                // O^T += V^T P^T.  MFMA step ks of sub-block kb contracts keys
+                // 16 ks + 4 h + {0..3} (slots 0..3) and 16 ks + 8 + 4 h + {0..3}
+                // (slots 4..7) of lane half h: the P values this lane holds, and
+                // two transposing reads of the value tile give the same keys.
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int ks = 0; ks < 2; ++ks) {
+                        bf16x8_t pf;
+#pragma unroll
+                        for (int jj = 0; jj < 8; ++jj) pf[jj] = (__bf16)sc[kb][8 * ks + jj];
+                        const unsigned char* vb = Vb + (kb * 32 + 16 * ks) * kRowBytes + v_off;
+#pragma unroll
+                        for (int t = 0; t < 4; ++t) {
+                            const int tsw = ((t ^ tj) << 6);   // chunk group t moved by the row's swizzle
+                            const v4s_t lo = lds_read_tr16(vb + tsw);
+                            const v4s_t hi = lds_read_tr16(vb + tsw + 8 * kRowBytes);
+                            const u32x4_t vv = {__builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 0, 1)),
+                                                __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 2, 3)),
+                                                __builtin_bit_cast(uint32_t, __builtin_shufflevector(hi, hi, 0, 1)),
+                                                __builtin_bit_cast(uint32_t, __builtin_shufflevector(hi, hi, 2, 3))};
+                            oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vv),
+                                                                              pf, oacc[t], 0, 0, 0);
+                        }
                     }
             }
-            float bmax = -INFINITY;
+        }
+
+        if (qb >= 0 && qidx < L) {
+            const float inv = 1.0f / l_run;
+            bf16_t* orow = o + (size_t)(s0 + qidx) * ld + head_off;
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) bmax = fmaxf(bmax, sc[kb][i]);
-            bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
-            const float m_new = fmaxf(m_run, bmax * scale_log2);
-            const float neg_m = -m_new;
-            float rsum = 0.f;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
+            for (int t = 0; t < 4; ++t)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
-                    const float pv = __builtin_amdgcn_exp2f(fmaf(sc[kb][i], scale_log2, neg_m));
-                    sc[kb][i] = pv;
-                    rsum += pv;
-                }
-            rsum += __shfl_xor(rsum, 32);
-            // rescale the sums only when some query's max moved (exact skip)
-            if (__any(m_new != m_run)) {
-                const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-                l_run *= alpha;
-#pragma unroll
-                for (int t = 0; t < 4; ++t)
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) oacc[t][i] *= alpha;
-            }
-            l_run += rsum;
-            m_run = m_new;
-
-            // O^T += V^T P^T.  MFMA step ks of sub-block kb contracts keys
-            // 16 ks + 4 h + {0..3} (slots 0..3) and 16 ks + 8 + 4 h + {0..3}
-            // (slots 4..7) of lane half h: the P values this lane holds, and two
-            // transposing reads of the row-major V tile give the same keys.
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-                    bf16x8_t pf;
-#pragma unroll
-                    for (int jj = 0; jj < 8; ++jj) pf[jj] = (__bf16)sc[kb][8 * ks + jj];
-                    const bf16_t* vb = &Vs[cur][(kb * 32 + 16 * ks) * VPAD + v_off];
-#pragma unroll
-                    for (int t = 0; t < 4; ++t) {
-                        const v4s_t lo = lds_read_tr16(vb + 32 * t);
-                        const v4s_t hi = lds_read_tr16(vb + 32 * t + 8 * VPAD);
-                        const u32x4_t vv = {__builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 0, 1)),
-                                            __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 2, 3)),
-                                            __builtin_bit_cast(uint32_t, __builtin_shufflevector(hi, hi, 0, 1)),
-                                            __builtin_bit_cast(uint32_t, __builtin_shufflevector(hi, hi, 2, 3))};
-                        oacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vv),
-                                                                          pf, oacc[t], 0, 0, 0);
-                    }
+                    const int dcol = t * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+                    orow[dcol] = f32_to_bf16(oacc[t][i] * inv);
                 }
         }
-        // the other buffer was last read before the previous barrier
-        if (kb_i + 1 < nkv) store_block(cur ^ 1);
-        __syncthreads();
-    }
-
-    if (qidx < L) {
-        const float inv = 1.0f / l_run;
-        bf16_t* orow = o + (size_t)(s0 + qidx) * ld + head_off;
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int dcol = t * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-                orow[dcol] = f32_to_bf16(oacc[t][i] * inv);
-            }
-    }
-    }   // query blocks
+    }   // query block pairs
 }
 
 template <int D>
@@ -290,8 +336,8 @@ hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uin
     if (n_seq <= 0 || max_seqlen <= 0) return hipSuccess;
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)HD);
     const long long blocks = (long long)n_seq * n_heads;
-    hipLaunchKernelGGL(attn_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, st, q, k, v, o, cu,
-                       n_seq, n_heads, n_prefix, scale_log2);
+    hipLaunchKernelGGL((attn_bf16_kernel<4, 2>), dim3((unsigned)blocks), dim3(256), 0, st, q, k, v, o, cu, n_seq,
+                       n_heads, n_prefix, scale_log2);
     return hipGetLastError();
 }
 
