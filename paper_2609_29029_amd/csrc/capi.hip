@@ -3,6 +3,7 @@
 // synchronises (to read the result of its input scan).
 #include <math.h>
 #include <stdlib.h>
+#include <string.h>
 
 #include <atomic>
 #include <cmath>
@@ -45,7 +46,19 @@ inline bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) &
 
 inline size_t dt_bytes(rift_dtype dt) { return dt == RIFT_BF16 ? 2 : 4; }
 
-inline bool dt_valid(rift_dtype dt) { return dt == RIFT_BF16 || dt == RIFT_F32; }
+// A caller may pass any integer as an enum: its first inspection reads the
+// bits (loading an enum outside its range would be undefined behaviour).
+template <typename E>
+inline int enum_bits(const E& e) {
+    int v = 0;
+    memcpy(&v, &e, sizeof v);
+    return v;
+}
+
+inline bool dt_valid(const rift_dtype& dt) {
+    const int v = enum_bits(dt);
+    return v == (int)RIFT_BF16 || v == (int)RIFT_F32;
+}
 
 inline rift_status hip_status(hipError_t e) { return e == hipSuccess ? RIFT_OK : RIFT_ERR_HIP; }
 
@@ -139,7 +152,7 @@ extern "C" {
 int32_t rift_abi_version(void) { return RIFT_ABI_VERSION; }
 
 const char* rift_status_string(rift_status s) {
-    switch (s) {
+    switch (enum_bits(s)) {
         case RIFT_OK: return "ok";
         case RIFT_ERR_NULL: return "a required pointer is NULL";
         case RIFT_ERR_SHAPE: return "a size breaks the shape rules of the call";
@@ -213,7 +226,7 @@ size_t rift_score_workspace_size(int32_t n_tiles, int32_t n_v, int32_t d, int32_
 namespace {
 
 // Argument checks of rift_score_tiles that do not involve the workspace.
-rift_status score_check(const void* tokens, rift_dtype dt, int32_t n_tiles, int32_t n_v, int32_t d,
+rift_status score_check(const void* tokens, const rift_dtype& dt, int32_t n_tiles, int32_t n_v, int32_t d,
                         const void* query_bank, int32_t n_bg, int32_t keep_count, double tau, int32_t knn_m,
                         const double* token_key, const double* tile_score, const float* tile_u,
                         const int32_t* tile_order, const int32_t* n_keep) {
@@ -509,7 +522,7 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
     rift_status cs = check_cfg(cfg);
     if (cs != RIFT_OK) return cs;
     const rift_model_cfg c = *cfg;
-    if (x_dt != c.dt && x_dt != RIFT_F32) return RIFT_ERR_DTYPE;
+    if (!dt_valid(x_dt) || (x_dt != c.dt && x_dt != RIFT_F32)) return RIFT_ERR_DTYPE;
     if (total_tokens < 0 || n_seq < 0 || max_seqlen < 1 || max_seqlen > 65536 || n_prefix < 0 ||
         n_prefix > total_tokens || n_prefix > max_seqlen || (n_prefix > 0 && n_seq < 1))
         return RIFT_ERR_SHAPE;
