@@ -40,12 +40,13 @@ GEMM_SRC = os.path.join(ROOT, "paper_2609_29029_amd", "csrc", "gemm_bf16.hip")
 # system prefix (T = 18,739 packed rows), from two rocprofv3 --pmc runs of this
 # script with --traffic-calibration (FETCH_SIZE, then WRITE_SIZE), each scaled
 # by what the counter reads for the 1 GiB calibration copy (FETCH_SIZE reads
-# half the bytes, WRITE_SIZE all of them).  Valid only for the GEMM source it
-# was measured on, identified by its SHA-256; otherwise reported as null.
+# half the bytes, WRITE_SIZE all of them): 6.2033 GB fetched + 0.4126 GB written
+# (profiles/scene20_l32_counters.md).  Valid only for the GEMM source it was
+# measured on, identified by its SHA-256; otherwise reported as null.
 TRAFFIC = {"stage": "gate_up_swiglu",
            "gemm_src_sha256": "ad16afa1ec10e20dd691986344eb854b8a153320596be793a9425b9f1e9fa952",
            "packed_tokens": 18739,
-           "bytes": 7.1092e9}
+           "bytes": 6.6159e9}
 
 
 def log(*a):
@@ -523,61 +524,110 @@ def _kernel_label(name: str) -> str:
     return m.group(0) if m else k[:60]
 
 
+def trace_report(paths) -> str:
+    """Per-kernel durations from rocprofv3 --kernel-trace CSV files: calls,
+    total and average microseconds and share of the kernel time, launches of
+    one kernel with different grids apart."""
+    import csv
+    import glob
+    files = []
+    for p in paths:
+        files += sorted(glob.glob(os.path.join(p, "**", "*kernel_trace.csv"), recursive=True)) \
+            if os.path.isdir(p) else [p]
+    durs: dict = {}
+    for f in files:
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                k = (_kernel_label(r["Kernel_Name"]), int(r.get("Grid_Size_X", 0) or 0))
+                if k[0].startswith(("at::", "__amd")):
+                    continue   # torch's and the runtime's own kernels (input copies, fills)
+                durs.setdefault(k, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    grids: dict = {}
+    for lab, g in durs:
+        grids.setdefault(lab, set()).add(g)
+    total = sum(sum(v) for v in durs.values())
+    lines = ["| kernel | calls | total us | average us | % |", "|---|---|---|---|---|"]
+    for k, v in sorted(durs.items(), key=lambda kv: -sum(kv[1])):
+        nm = f"`{k[0]}`" + (f" (grid {k[1]})" if len(grids[k[0]]) > 1 else "")
+        lines.append(f"| {nm} | {len(v)} | {sum(v):.0f} | {sum(v) / len(v):.1f} | {100 * sum(v) / total:.2f} |")
+    return "\n".join(lines)
+
+
 def counter_report(paths) -> str:
     """Summarise rocprofv3 --pmc CSV files (one pass per file: the hardware
-    collects a few counters per run) as a markdown table per kernel.
-    Derived figures:
+    collects a few counters per run) as markdown tables per kernel; launches of
+    one kernel with different grids are listed apart.  Derived figures:
       clock     GRBM_GUI_ACTIVE / 8 XCDs over the dispatch's duration
       MFMA busy SQ_VALU_MFMA_BUSY_CYCLES over (clock cycles x 1,024 SIMDs)
       SQ busy   SQ_BUSY_CYCLES over (clock cycles x 32 shader engines)
       HBM-side bytes  FETCH_SIZE and WRITE_SIZE (KiB) scaled by what the same
                 counters read for the 1 GiB calibration copy (torch.neg over
-                2^28 floats: 1 GiB read, 1 GiB written)."""
+                2^28 floats: 1 GiB read, 1 GiB written)
+      waiting   SQ_WAIT_ANY over SQ_WAVE_CYCLES (share of wave time stalled)
+      LDS       SQ_LDS_BANK_CONFLICT over SQ_LDS_IDX_ACTIVE."""
     import csv
     import glob
     files = []
     for p in paths:
         files += sorted(glob.glob(os.path.join(p, "**", "*counter_collection.csv"), recursive=True)) \
             if os.path.isdir(p) else [p]
-    # per kernel: counter -> list of per-dispatch values; dispatch durations
     vals: dict = {}
     durs: dict = {}
+    grids: dict = {}
     for f in files:
         seen = set()
         with open(f) as fh:
             for r in csv.DictReader(fh):
-                k = _kernel_label(r["Kernel_Name"])
+                k = (_kernel_label(r["Kernel_Name"]), int(r.get("Grid_Size", 0) or 0))
                 vals.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
                 key = (f, r["Dispatch_Id"])
                 if key not in seen:
                     seen.add(key)
                     durs.setdefault(k, []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
-    calib = {c: statistics.mean(v) for k, d in vals.items() if "neg" in k for c, v in d.items()}
+    for lab, g in vals:
+        grids.setdefault(lab, set()).add(g)
+
+    def name(k):
+        return f"`{k[0]}`" + (f" (grid {k[1]})" if len(grids[k[0]]) > 1 else "")
+    calib = {c: statistics.mean(v) for k, d in vals.items() if "neg" in k[0] for c, v in d.items()}
     f_scale = (1 << 30) / (calib["FETCH_SIZE"] * 1024) if calib.get("FETCH_SIZE") else None
     w_scale = (1 << 30) / (calib["WRITE_SIZE"] * 1024) if calib.get("WRITE_SIZE") else None
+
+    def fmt(x, nd):
+        return "" if x is None else f"{x:.{nd}f}"
     lines = ["| kernel | dispatches | mean us | clock GHz | MFMA busy | SQ busy | fetch GB | write GB | HBM-side GB/s | frac of 8 TB/s |",
              "|---|---|---|---|---|---|---|---|---|---|"]
+    stall = ["| kernel | waiting / wave time | VALU instr / wave | SALU instr / wave | LDS instr / wave | LDS bank conflicts / active |",
+             "|---|---|---|---|---|---|"]
     for k in sorted(vals):
-        if "neg" in k:
+        if "neg" in k[0] or k[0].startswith("__amd") or k[0].startswith("at::"):
             continue
         d = {c: statistics.mean(v) for c, v in vals[k].items()}
         us = statistics.mean(durs[k]) / 1e3
-        clk = d["GRBM_GUI_ACTIVE"] / 8 / (us * 1e3) if "GRBM_GUI_ACTIVE" in d else None
         cyc = d["GRBM_GUI_ACTIVE"] / 8 if "GRBM_GUI_ACTIVE" in d else None
+        clk = cyc / (us * 1e3) if cyc else None
         busy = d["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * 1024) if cyc and "SQ_VALU_MFMA_BUSY_CYCLES" in d else None
         sqb = d["SQ_BUSY_CYCLES"] / (cyc * 32) if cyc and "SQ_BUSY_CYCLES" in d else None
         fgb = d["FETCH_SIZE"] * 1024 * f_scale / 1e9 if f_scale and "FETCH_SIZE" in d else None
         wgb = d["WRITE_SIZE"] * 1024 * w_scale / 1e9 if w_scale and "WRITE_SIZE" in d else None
         gbs = ((fgb or 0) + (wgb or 0)) / (us * 1e-6) if (fgb is not None or wgb is not None) else None
-
-        def fmt(x, nd):
-            return "" if x is None else f"{x:.{nd}f}"
-        lines.append(f"| `{k}` | {len(durs[k])} | {us:.1f} | {fmt(clk, 3)} | {fmt(busy and busy * 100, 1)}{'%' if busy else ''} | "
-                     f"{fmt(sqb, 2)} | {fmt(fgb, 4)} | {fmt(wgb, 4)} | {fmt(gbs, 0)} | {fmt(gbs and gbs / PEAK_HBM_GBS, 3)} |")
+        lines.append(f"| {name(k)} | {len(durs[k])} | {us:.1f} | {fmt(clk, 3)} | "
+                     f"{'' if busy is None else f'{busy * 100:.1f}%'} | {fmt(sqb, 2)} | {fmt(fgb, 4)} | {fmt(wgb, 4)} | "
+                     f"{fmt(gbs, 0)} | {fmt(gbs and gbs / PEAK_HBM_GBS, 3)} |")
+        if "SQ_WAVE_CYCLES" in d or "SQ_INSTS_LDS" in d:
+            waves = d.get("SQ_WAVES")
+            wait = d["SQ_WAIT_ANY"] / d["SQ_WAVE_CYCLES"] if "SQ_WAIT_ANY" in d and d.get("SQ_WAVE_CYCLES") else None
+            per = (lambda c: d[c] / waves if waves and c in d else None)
+            conf = (d["SQ_LDS_BANK_CONFLICT"] / d["SQ_LDS_IDX_ACTIVE"]
+                    if d.get("SQ_LDS_IDX_ACTIVE") and "SQ_LDS_BANK_CONFLICT" in d else None)
+            stall.append(f"| {name(k)} | {'' if wait is None else f'{wait * 100:.1f}%'} | {fmt(per('SQ_INSTS_VALU'), 0)} | "
+                         f"{fmt(per('SQ_INSTS_SALU'), 0)} | {fmt(per('SQ_INSTS_LDS'), 0)} | {fmt(conf, 4)} |")
     if f_scale or w_scale:
         lines.append("")
         lines.append(f"Calibration copy (1 GiB read, 1 GiB written): FETCH_SIZE x {f_scale or 0:.3f}, "
                      f"WRITE_SIZE x {w_scale or 0:.3f}.")
+    if len(stall) > 2:
+        lines += ["", *stall]
     return "\n".join(lines)
 
 
@@ -603,9 +653,14 @@ def main() -> int:
                     help="time the scene-query and the batched select only (for counter runs)")
     ap.add_argument("--counter-report", nargs="+", metavar="CSV_OR_DIR",
                     help="print a per-kernel summary of rocprofv3 --pmc CSV output and exit (no GPU)")
+    ap.add_argument("--trace-report", nargs="+", metavar="CSV_OR_DIR",
+                    help="print a per-kernel summary of rocprofv3 --kernel-trace CSV output and exit (no GPU)")
     args = ap.parse_args()
     if args.counter_report:
         print(counter_report(args.counter_report))
+        return 0
+    if args.trace_report:
+        print(trace_report(args.trace_report))
         return 0
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the Rift path here is a single-GPU build "
@@ -760,6 +815,8 @@ def main() -> int:
     if args.core_only:
         out["select_batched"] = select_batched(R, torch, q.token_key, q.tile_order, q.budgets, w.n_tiles,
                                                w.n_v, q.n_keep)
+        out["select_batched_512"] = select_batched(R, torch, q.token_key, q.tile_order, q.budgets, w.n_tiles,
+                                                   w.n_v, q.n_keep, copies=512, reps=3)
         print(json.dumps(out), flush=True)
         return 0
     if shared:
@@ -794,6 +851,10 @@ def main() -> int:
         log(f"decode: {out['decode']}")
     out["select_batched"] = select_batched(R, torch, q.token_key, q.tile_order, q.budgets, w.n_tiles,
                                            w.n_v, q.n_keep)
+    # many rounds of tiles over the CUs: the streaming rate, without the
+    # one-round latency of the 64-query call
+    out["select_batched_512"] = select_batched(R, torch, q.token_key, q.tile_order, q.budgets, w.n_tiles,
+                                               w.n_v, q.n_keep, copies=512)
     if not args.no_exhaustive:
         log("exhaustive run (every tile at the full budget) ...")
         ex_fn, ex_shape = exhaustive_setup(R, torch, w, tokens, qbank, sysd, qryd, layers, q.cfg, shared=shared)
