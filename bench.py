@@ -226,25 +226,33 @@ def mfma_ceiling(torch, seconds_per_form: float = 0.4) -> dict:
     """bf16 MFMA throughput with nothing but MFMAs on every CU (operands rotating
     over eight register pairs, as in a GEMM), from libriftcalib.so: the
     attainable ceiling under the board power limit, reported beside the
-    nominal peak.  Three timed launches per instruction form, median."""
+    nominal peak.  Also with all-zero operands (which draw far less power, so
+    the clock stays near its maximum): two waves per SIMD, the instruction's
+    own rate, and one wave per SIMD, the rate at which a lone wave can issue
+    (the ping-pong GEMM loop has one MFMA wave per SIMD at a time).  Three
+    timed launches per case, median."""
     import ctypes
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_29029_amd", "libriftcalib.so"))
     lib.rift_calib_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
                                          ctypes.c_int, ctypes.c_void_p]
     g = torch.Generator(device="cuda").manual_seed(0x52494654)
     src = torch.randn(65536, device="cuda", generator=g).to(torch.bfloat16)
+    zero = torch.zeros(65536, device="cuda", dtype=torch.bfloat16)
     blocks = torch.cuda.get_device_properties(0).multi_processor_count
     out = torch.empty(blocks * 512, device="cuda", dtype=torch.float32)
     stream = torch.cuda.current_stream().cuda_stream
-    per_iter = blocks * 8 * 262144
     res = {}
-    for form, name in ((0, "v_mfma_f32_16x16x32_bf16"), (1, "v_mfma_f32_32x32x16_bf16")):
+    cases = ((0, src, "v_mfma_f32_16x16x32_bf16"), (1, src, "v_mfma_f32_32x32x16_bf16"),
+             (0, zero, "v_mfma_f32_16x16x32_bf16 zero operands"),
+             (2, zero, "v_mfma_f32_16x16x32_bf16 zero operands, one wave per SIMD"))
+    for form, operands, name in cases:
+        per_iter = blocks * (4 if form == 2 else 8) * 262144
         iters = max(8, int(seconds_per_form * 1.5e15 / per_iter) // 8 * 8)
         ts = []
         for rep in range(4):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record()
-            rc = lib.rift_calib_mfma_bf16(form, src.data_ptr(), out.data_ptr(), blocks, iters, stream)
+            rc = lib.rift_calib_mfma_bf16(form, operands.data_ptr(), out.data_ptr(), blocks, iters, stream)
             e1.record()
             torch.cuda.synchronize()
             if rc != 0:
@@ -353,6 +361,37 @@ def energy_run(torch, rift_query, ex_run, rift_ms, ex_ms, min_seconds: float) ->
                            "device_ms_per_query": round(ex_ms, 2), "J_per_query": round(e_e, 2),
                            "queries": pe["calls"], "span_s": round(pe["span_s"], 2)},
             "energy_reduction": round(1 - e_r / e_e, 4)}
+
+
+def gemm_operand_split(R, torch, q, reps=3) -> dict:
+    """One prefill layer at the query's packed shape (shared prefix), per stage:
+    once with the query's packed input and first layer's weights, once with the
+    input and every weight matrix zero (norm gains one).  The kernels and shapes
+    are the same; zero operands barely toggle the matrix cores, so the board
+    stays below its power limit and the clock near its maximum, and the ratio of
+    the two times is what the power limit costs each GEMM.  Runs alternate;
+    median of `reps` per case."""
+    sh = q.shape
+    cfg = R.model_cfg(sh.d, sh.n_heads, sh.head_dim, sh.ffn, 1, sh.rms_eps, sh.rope_base, R.RIFT_BF16)
+    L0 = q.layers[0]
+    zl = {k: (torch.ones_like(v) if k.startswith("g_") else torch.zeros_like(v)) for k, v in L0.items()}
+    T = q.total_tokens
+    x_rand = q.packed
+    x_zero = torch.zeros_like(x_rand)
+    hid = torch.empty(T, sh.d, dtype=torch.float32, device=x_rand.device)
+    ws = torch.empty(R.rift_prefill_workspace_size(cfg, T, q.max_seqlen), dtype=torch.uint8, device=x_rand.device)
+    times = {"query_operands": {k: [] for k in STAGES}, "zero_operands": {k: [] for k in STAGES}}
+    for _ in range(reps):
+        for name, layer, x in (("query_operands", L0, x_rand), ("zero_operands", zl, x_zero)):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(10)]
+            R.rift_prefill(cfg, [layer], x, q.cu_seqlens, q.position_ids, q.n_seq, q.max_seqlen, hid, ws,
+                           events=ev, n_prefix=q.n_prefix)
+            torch.cuda.synchronize()
+            for i, k in enumerate(STAGES):
+                times[name][k].append(ev[2 * i].elapsed_time(ev[2 * i + 1]))
+    out = {name: {k: round(statistics.median(v), 4) for k, v in d.items()} for name, d in times.items()}
+    out["zero_over_query_time"] = {k: round(out["zero_operands"][k] / out["query_operands"][k], 4) for k in STAGES}
+    return out
 
 
 def knn_score_timing(R, torch, tokens, qbank, keep_count, m=6, reps=10) -> dict:
@@ -841,6 +880,9 @@ def main() -> int:
     c16 = ceil["v_mfma_f32_16x16x32_bf16"]["TFLOPs"]
     out["roofline"]["measured_peak"] = c16
     out["roofline"]["frac_of_measured_peak"] = round(achieved / c16, 4)
+    if w.dtype == "bf16":
+        out["gemm_operand_split"] = gemm_operand_split(R, torch, q)
+        log(f"gemm operand split: {out['gemm_operand_split']['zero_over_query_time']}")
     kn = knn_score_timing(R, torch, tokens, qbank, w.keep_count)
     kn["extra_ms_over_plain_score"] = round(kn["score_ms"] - stage_ms["score"], 4)
     out["knn_smoothing"] = kn

@@ -222,7 +222,8 @@ def test_calibration_library_loads_and_rejects_bad_arguments(R):
     f = L.rift_calib_mfma_bf16
     f.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
     p = ctypes.c_void_p(16)
-    assert f(2, p, p, 1, 8, None) == -1        # unknown form
+    assert f(3, p, p, 1, 8, None) == -1        # unknown form
+    assert f(-1, p, p, 1, 8, None) == -1
     assert f(0, None, p, 1, 8, None) == -1     # null source
     assert f(0, p, p, 0, 8, None) == -1        # no workgroups
     assert f(1, p, p, 1, 12, None) == -1       # iterations not a multiple of 8
