@@ -40,13 +40,13 @@ GEMM_SRC = os.path.join(ROOT, "paper_2609_29029_amd", "csrc", "gemm_bf16.hip")
 # system prefix (T = 18,739 packed rows), from two rocprofv3 --pmc runs of this
 # script with --traffic-calibration (FETCH_SIZE, then WRITE_SIZE), each scaled
 # by what the counter reads for the 1 GiB calibration copy (FETCH_SIZE reads
-# half the bytes, WRITE_SIZE all of them): 6.2033 GB fetched + 0.4126 GB written
+# half the bytes, WRITE_SIZE all of them): 5.2470 GB fetched + 0.4126 GB written
 # (profiles/scene20_l32_counters.md).  Valid only for the GEMM source it was
 # measured on, identified by its SHA-256; otherwise reported as null.
 TRAFFIC = {"stage": "gate_up_swiglu",
-           "gemm_src_sha256": "ad16afa1ec10e20dd691986344eb854b8a153320596be793a9425b9f1e9fa952",
+           "gemm_src_sha256": "dd9c199ed184925964da38eb57b53d4dff2942d2ee756b8521214171f2513aa7",
            "packed_tokens": 18739,
-           "bytes": 6.6159e9}
+           "bytes": 5.6596e9}
 
 
 def log(*a):

@@ -21,9 +21,13 @@
 // matter which tile or batch row holds it, so a row's result does not depend on
 // what else is packed with it.
 //
-// Tile order: the hardware hands workgroup b to XCD b mod 8; each XCD gets a
-// contiguous range of tile ids, and tile ids walk 8 M-tiles per N-tile, so the
-// workgroups resident on one XCD share A and B panels in that XCD's L2.
+// Tile order: tile ids walk 8 M-tiles per N-tile.  The hardware hands
+// workgroup b to XCD b mod 8, and one workgroup fits a CU, so the 256
+// workgroups of a round run together: in each round every XCD takes 32
+// consecutive tile ids (8 M-tiles x 4 N-tiles, sharing A and B panels in its
+// L2) of the same block of 256, so all XCDs stream the same 8 A panels at the
+// same time, and the A panels of one M-group plus all of B stay in the
+// memory-side cache while the group's rounds walk N.
 #include <type_traits>
 
 #include "launch.h"
@@ -68,6 +72,15 @@ __device__ __forceinline__ int xcd_remap(int bid, int count) {
     const int base = count >> 3;
     const int extra = count & 7;
     return xcd * base + (xcd < extra ? xcd : extra) + slot;
+}
+
+// Workgroup bid of a launch of `count` whole tiles -> tile id: within each
+// block of 256 workgroups, XCD bid mod 8 takes ids 32 (bid mod 8) + [0, 32) of
+// the block; the last partial block is spread over the XCDs by xcd_remap.
+__device__ __forceinline__ int round_remap(int bid, int count) {
+    const int full = count & ~255;
+    if (bid >= full) return full + xcd_remap(bid - full, count - full);
+    return (bid & ~255) + (bid & 7) * 32 + ((bid >> 3) & 31);
 }
 
 // Tile t of the grouped order: 8 M-tiles per N-tile, so tiles with nearby t
@@ -316,7 +329,7 @@ __global__ void __launch_bounds__(HALF ? 256 : 512, 1) gemm_bf16_w8_kernel(GemmP
         h = i & 1;
         group_coords(p.n_full + (i >> 1), p.num_m, p.num_n, bm, bn);
     } else {
-        group_coords(xcd_remap(blockIdx.x, p.n_full), p.num_m, p.num_n, bm, bn);
+        group_coords(round_remap(blockIdx.x, p.n_full), p.num_m, p.num_n, bm, bn);
     }
     const int m0 = bm * BM;
 
@@ -476,7 +489,7 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_pp_kernel(GemmParams p) {
     __shared__ __align__(16) bf16_t lds[kStagingBytes / 2];   // two stages, then the epilogue tile
     __shared__ int pos_lds[BM];   // QKV: clamped position of each tile row
     int bm, bn;
-    group_coords(xcd_remap(blockIdx.x, p.n_full), p.num_m, p.num_n, bm, bn);
+    group_coords(round_remap(blockIdx.x, p.n_full), p.num_m, p.num_n, bm, bn);
     const int m0 = bm * BM;
 
     const int tid = threadIdx.x;
