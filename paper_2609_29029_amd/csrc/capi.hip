@@ -624,8 +624,13 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
             qa.n_pos = max_seqlen;
             qa.M = T;
             qa.d = d;
+            // Tile walk directions: each GEMM starts with the rows its input's
+            // producer wrote last (norms and attention write rows in ascending
+            // order), so its first A panels come from the memory-side cache:
+            // QKV, out and gate/up walk backwards, down (after the backward
+            // gate/up) forwards.  Results do not depend on the order.
             RIFT_TRY(mark(l, 0, 0));
-            RIFT_TRY(launch_gemm_qkv_rope(qa, st));
+            RIFT_TRY(launch_gemm_qkv_rope(qa, st, true));
             RIFT_TRY(mark(l, 0, 1));
             // attention output reuses the h buffer (h is consumed by the QKV GEMM)
             RIFT_TRY(mark(l, 1, 0));
@@ -635,16 +640,17 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
             RIFT_TRY(mark(l, 1, 1));
             RIFT_TRY(mark(l, 2, 0));
             RIFT_TRY(launch_gemm_resid(static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w.wo),
-                                       hidden_out, T, d, d, st));
+                                       hidden_out, T, d, d, st, true));
             RIFT_TRY(mark(l, 2, 1));
             RIFT_TRY(launch_rmsnorm(hidden_out, false, nullptr, w.g_ffn, true, h, true, T, d, c.rms_eps, st));
             uint16_t* a = reinterpret_cast<uint16_t*>(ws + L.a);
             RIFT_TRY(mark(l, 3, 0));
             RIFT_TRY(launch_gemm_swiglu(static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w.w_gate),
-                                        static_cast<const uint16_t*>(w.w_up), a, T, c.ffn, d, st));
+                                        static_cast<const uint16_t*>(w.w_up), a, T, c.ffn, d, st, true));
             RIFT_TRY(mark(l, 3, 1));
             RIFT_TRY(mark(l, 4, 0));
-            RIFT_TRY(launch_gemm_resid(a, static_cast<const uint16_t*>(w.w_down), hidden_out, T, d, c.ffn, st));
+            RIFT_TRY(launch_gemm_resid(a, static_cast<const uint16_t*>(w.w_down), hidden_out, T, d, c.ffn, st,
+                                       false));
             RIFT_TRY(mark(l, 4, 1));
         } else {
             float* hf = static_cast<float*>(h);

@@ -27,7 +27,8 @@
 // consecutive tile ids (8 M-tiles x 4 N-tiles, sharing A and B panels in its
 // L2) of the same block of 256, so all XCDs stream the same 8 A panels at the
 // same time, and the A panels of one M-group plus all of B stay in the
-// memory-side cache while the group's rounds walk N.
+// memory-side cache while the group's rounds walk N.  With `reverse` a launch
+// walks the same order from its last whole tile to its first.
 #include <type_traits>
 
 #include "launch.h"
@@ -61,6 +62,7 @@ struct GemmParams {
     int num_m, num_n;   // 256x256 output tiles
     int n_full;         // tiles 0 .. n_full-1 (grouped order) run as whole tiles,
                         // the rest as two 256x128 halves each
+    int reverse;        // walk the whole tiles from the last to the first
 };
 
 // Workgroup bid of a launch of `count` workgroups -> its index in that launch,
@@ -329,7 +331,9 @@ __global__ void __launch_bounds__(HALF ? 256 : 512, 1) gemm_bf16_w8_kernel(GemmP
         h = i & 1;
         group_coords(p.n_full + (i >> 1), p.num_m, p.num_n, bm, bn);
     } else {
-        group_coords(round_remap(blockIdx.x, p.n_full), p.num_m, p.num_n, bm, bn);
+        int t = round_remap(blockIdx.x, p.n_full);
+        if (p.reverse) t = p.n_full - 1 - t;
+        group_coords(t, p.num_m, p.num_n, bm, bn);
     }
     const int m0 = bm * BM;
 
@@ -489,7 +493,11 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_pp_kernel(GemmParams p) {
     __shared__ __align__(16) bf16_t lds[kStagingBytes / 2];   // two stages, then the epilogue tile
     __shared__ int pos_lds[BM];   // QKV: clamped position of each tile row
     int bm, bn;
-    group_coords(round_remap(blockIdx.x, p.n_full), p.num_m, p.num_n, bm, bn);
+    {
+        int t = round_remap(blockIdx.x, p.n_full);
+        if (p.reverse) t = p.n_full - 1 - t;
+        group_coords(t, p.num_m, p.num_n, bm, bn);
+    }
     const int m0 = bm * BM;
 
     const int tid = threadIdx.x;
@@ -672,7 +680,7 @@ hipError_t launch_gemm(GemmParams p, int num_n, hipStream_t st) {
 
 }  // namespace
 
-hipError_t launch_gemm_qkv_rope(const QkvArgs& a, hipStream_t st) {
+hipError_t launch_gemm_qkv_rope(const QkvArgs& a, hipStream_t st, bool reverse) {
     GemmParams p{};
     p.a = a.a;
     p.b0 = a.wq;
@@ -688,11 +696,12 @@ hipError_t launch_gemm_qkv_rope(const QkvArgs& a, hipStream_t st) {
     p.rope = a.rope;
     p.pos = a.pos;
     p.n_pos = a.n_pos;
+    p.reverse = reverse ? 1 : 0;
     return launch_gemm<EPI_QKV>(p, p.N / BN, st);
 }
 
 hipError_t launch_gemm_resid(const uint16_t* a, const uint16_t* b, float* resid, int M, int N,
-                             int K, hipStream_t st) {
+                             int K, hipStream_t st, bool reverse) {
     GemmParams p{};
     p.a = a;
     p.b0 = b;
@@ -700,11 +709,12 @@ hipError_t launch_gemm_resid(const uint16_t* a, const uint16_t* b, float* resid,
     p.N = N;
     p.K = K;
     p.resid = resid;
+    p.reverse = reverse ? 1 : 0;
     return launch_gemm<EPI_RESID>(p, N / BN, st);
 }
 
 hipError_t launch_gemm_swiglu(const uint16_t* a, const uint16_t* wg, const uint16_t* wu,
-                              uint16_t* out, int M, int F, int K, hipStream_t st) {
+                              uint16_t* out, int M, int F, int K, hipStream_t st, bool reverse) {
     GemmParams p{};
     p.a = a;
     p.b0 = wg;
@@ -714,6 +724,7 @@ hipError_t launch_gemm_swiglu(const uint16_t* a, const uint16_t* wg, const uint1
     p.K = K;
     p.d = F;
     p.o0 = out;
+    p.reverse = reverse ? 1 : 0;
     return launch_gemm<EPI_SWIGLU>(p, F / 128, st);
 }
 

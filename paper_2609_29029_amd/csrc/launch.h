@@ -65,15 +65,19 @@ struct QkvArgs {
     int n_pos;
     int M, d;
 };
-hipError_t launch_gemm_qkv_rope(const QkvArgs& a, hipStream_t st);
+// The GEMMs walk their output tiles from the first row block to the last, or
+// with `reverse` from the last to the first.  The order changes no result; it
+// decides which rows of A a GEMM reads first, and the rows its producer wrote
+// last are still in the memory-side cache.
+hipError_t launch_gemm_qkv_rope(const QkvArgs& a, hipStream_t st, bool reverse = false);
 
 // resid[M][N] += A[M][K] B[N][K]^T  (attention output and FFN down projections)
 hipError_t launch_gemm_resid(const uint16_t* a, const uint16_t* b, float* resid, int M, int N,
-                             int K, hipStream_t st);
+                             int K, hipStream_t st, bool reverse = false);
 
 // out[M][F] = silu(A Wg^T) * (A Wu^T), A [M][K], Wg, Wu [F][K]
 hipError_t launch_gemm_swiglu(const uint16_t* a, const uint16_t* wg, const uint16_t* wu,
-                              uint16_t* out, int M, int F, int K, hipStream_t st);
+                              uint16_t* out, int M, int F, int K, hipStream_t st, bool reverse = false);
 
 // Varlen causal attention, bf16, head_dim 128.  q, k, v, o: [T][H*128].
 hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
