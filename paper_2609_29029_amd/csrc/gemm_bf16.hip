@@ -485,9 +485,10 @@ __global__ void __launch_bounds__(HALF ? 256 : 512, 1) gemm_bf16_w8_kernel(GemmP
 //   group 0: t = 2j   reads stage j          t = 2j+1  MFMAs of stage j
 //   group 1: t = 2j+1 reads stage j          t = 2j+2  MFMAs of stage j
 // Stage j sits in buffer j mod 2 and is last read in turn 2j+1, so the LDS
-// DMA of stage j+2 is issued in turn 2j+2 (group 0 while reading stage j+1,
-// group 1 between its MFMAs of stage j) and every wave waits for its own DMA
-// at the end of turn 2j+3, before group 0 reads stage j+2.
+// DMA of stage j+2 is issued in turn 2j+2, all of it by group 0 while it reads
+// stage j+1 (wave w moves its own rows and those of wave w + 4): the MFMA turns
+// issue nothing but MFMAs, and the read turns have time to spare.  Group 0
+// waits for that DMA at the end of turn 2j+3, before it reads stage j+2.
 template <int EPI>
 __global__ void __launch_bounds__(512, 1) gemm_bf16_pp_kernel(GemmParams p) {
     __shared__ __align__(16) bf16_t lds[kStagingBytes / 2];   // two stages, then the epilogue tile
@@ -526,6 +527,22 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_pp_kernel(GemmParams p) {
         const size_t ko = (size_t)kt * BK3;
         if (q < 4) dma16s(p.a + ko, aoff[q], sb + q * 1024u);
         else dma16s(bbase[q - 4] + ko, boff[q - 4], sb + BM * BK3 * 2 + (q - 4) * 1024u);
+    };
+    // the share of wave w + 4 (rows + 128), issued by wave w of group 0; the B
+    // row of tile row r + 128 is that of r plus 128 (64 for SWIGLU), same matrix
+    const uint32_t bdelta = (uint32_t)(EPI == EPI_SWIGLU ? 64 : 128) * (uint32_t)p.K * 2u;
+    auto dma_partner = [&](int kt, int q) {
+        const uint32_t sb = ring_wave + 4u * 4096u + (uint32_t)(kt & 1) * (kStage3 * 2);
+        const size_t ko = (size_t)kt * BK3;
+        if (q < 4) {
+            const int row = 8 * (4 * (wave + 4) + q) + (lane >> 3);
+            const int c = (lane & 7) ^ swz8(row);
+            int ar = m0 + row;
+            ar = ar < p.M ? ar : p.M - 1;
+            dma16s(p.a + ko, ((uint32_t)ar * (uint32_t)p.K + (uint32_t)c * 8u) * 2u, sb + q * 1024u);
+        } else {
+            dma16s(bbase[q - 4] + ko, boff[q - 4] + bdelta, sb + BM * BK3 * 2 + (q - 4) * 1024u);
+        }
     };
 
     if constexpr (EPI == EPI_QKV) {
@@ -569,22 +586,25 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_pp_kernel(GemmParams p) {
         wg_barrier();
         __builtin_amdgcn_sched_barrier(0);
     };
-    // reads of stage kt; with kDma, this wave's share of the DMA of stage kt + 1
+    // reads of stage kt; with kDma (group 0 only), the DMA of stage kt + 1 for
+    // this wave's rows and for those of wave + 4
     auto read_turn = [&](int kt, auto kDma) {
 #pragma unroll
         for (int r = 0; r < 24; ++r) {
             read_one(kt, r);
-            if constexpr (decltype(kDma)::value) { if (r % 3 == 2) dma_one(kt + 1, r / 3); }
+            if constexpr (decltype(kDma)::value) {
+                if (r % 3 == 2) dma_one(kt + 1, r / 3);
+                if (r % 3 == 0) dma_partner(kt + 1, r / 3);
+            }
         }
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     };
-    // MFMAs of stage kt; with kDma, this wave's share of the DMA of stage kt + 2
-    auto mfma_turn = [&](int kt, auto kDma) {
+    // MFMAs of stage kt
+    auto mfma_turn = [&]() {
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int i = 0; i < 64; ++i) {
             mfma_one(i);
-            if constexpr (decltype(kDma)::value) { if ((i & 7) == 7) dma_one(kt + 2, i >> 3); }
             __builtin_amdgcn_sched_barrier(0);
         }
         __builtin_amdgcn_s_setprio(0);
@@ -609,7 +629,7 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_pp_kernel(GemmParams p) {
         auto step = [&](int kt, auto kDma) {
             read_turn(kt, kDma);
             turn_end();
-            mfma_turn(kt, F_{});
+            mfma_turn();
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             turn_end();
         };
@@ -619,22 +639,14 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_pp_kernel(GemmParams p) {
         if (kt < nk) step(kt, F_{});
     } else {
         turn_end();
-        auto step = [&](int kt, auto kDma) {
+        for (int kt = 0; kt < nk; ++kt) {
             read_turn(kt, F_{});
+            // only the prologue's DMA of stage 1 can still be in flight here
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             turn_end();
-            mfma_turn(kt, kDma);
-        };
-        int kt = 0;
-        for (; kt + 2 < nk; ++kt) {
-            step(kt, T_{});
-            turn_end();
+            mfma_turn();
+            if (kt + 1 < nk) turn_end();
         }
-        if (kt + 1 < nk) {
-            step(kt++, F_{});
-            turn_end();
-        }
-        step(kt, F_{});
     }
     epilogue_staged<EPI, false>(p, acc, m0, bn, 0, wm, wn, lane, pos_lds, reinterpret_cast<unsigned char*>(lds));
 }
