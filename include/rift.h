@@ -401,8 +401,9 @@ RIFT_API size_t rift_prefill_workspace_size(const rift_model_cfg* cfg, int32_t t
  *              after stage g of layer l -- g = 0 QKV projection (+RoPE),
  *              1 attention, 2 output projection, 3 gate/up projection (+SwiGLU),
  *              4 down projection.
- * Implemented: bf16 with head_dim == 128, d % 256 == 0, ffn % 128 == 0;
- *              f32 with head_dim in {64, 128}, d % 64 == 0, ffn % 16 == 0.
+ * Implemented: bf16 with head_dim in {64, 128}, d % 256 == 0, ffn % 128 == 0;
+ *              f32 with head_dim in {64, 128}, d % 64 == 0, ffn % 16 == 0;
+ *              anything else returns RIFT_ERR_UNSUPPORTED.
  * Shape rules: 1 <= max_seqlen <= 65536, total_tokens >= 0, n_seq >= 0;
  *              0 <= n_prefix <= min(total_tokens, max_seqlen), n_seq >= 1 when
  *              n_prefix > 0.

@@ -2,7 +2,7 @@
 // an independent sequence; Sec. 2.3 Stage 2).  Query i of a sequence attends
 // to keys 0..i of the same sequence, scale 1/sqrt(head_dim).
 //
-// bf16, head_dim 128, on MFMA.  One workgroup of W = 4 waves per (sequence,
+// bf16, head_dim 128 or 64, on MFMA.  One workgroup of W = 4 waves per (sequence,
 // head), looping over the sequence's 128-query blocks, the last
 // (longest-running) first; wave w owns queries [32 w, 32 w + 32) of the block
 // (workgroups are numbered sequence by sequence, so prompts packed longest
@@ -38,10 +38,10 @@ namespace rift {
 
 namespace {
 
-constexpr int HD = 128;
+constexpr int kLdsDims = 128;                   // dimensions of an LDS key or value row
 constexpr int BQ = 128;
 constexpr int BKV = 64;
-constexpr int kRowBytes = HD * 2;               // one key or value row
+constexpr int kRowBytes = kLdsDims * 2;         // one key or value row
 constexpr int kTileBytes = BKV * kRowBytes;     // 16 KB
 constexpr int kStageBytes = 2 * kTileBytes;     // keys, then values
 
@@ -72,8 +72,11 @@ __device__ __forceinline__ void wait_vm(int n) {
     }
 }
 
-// W waves (W / 4 query blocks per pass), S ring stages.
-template <int W, int S>
+// W waves (W / 4 query blocks per pass), S ring stages, head dim HD (128 or
+// 64).  With HD = 64 the tiles keep their 256-byte rows: the DMA fills only
+// the head's 8 chunks of each row, and the score and output MFMAs stop at the
+// head's dimensions (the other chunks are never read).
+template <int W, int S, int HD>
 __global__ void __launch_bounds__(64 * W, W == 8 ? 1 : 2)
 attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
                  const bf16_t* __restrict__ v, bf16_t* __restrict__ o,
@@ -117,7 +120,8 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
             const int grow = key < pre ? key : s0 + key - pre;
             const int swz = dma_v ? 4 * (row & 3) : (row & 15);
             const int c = (lane & 15) ^ swz;
-            dma16v(dma_src + (size_t)grow * ld + head_off + c * 8, sb + (uint32_t)jj * 1024u);
+            if (HD == kLdsDims || c < HD / 8)
+                dma16v(dma_src + (size_t)grow * ld + head_off + c * 8, sb + (uint32_t)jj * 1024u);
         }
     };
 
@@ -144,16 +148,18 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
 
         asm volatile("s_barrier" ::: "memory");   // every wave is done with the ring
         // Q^T B-operand fragments: lane holds Q[query][16 kk + 8 h .. + 8]
-        bf16x8_t qf[8];
+        constexpr int NKK = HD / 16;             // 16-dimension steps of the score MFMAs
+        constexpr int NT = HD / 32;              // 32-dimension output blocks
+        bf16x8_t qf[NKK];
         {
             const bf16_t* qrow = q + (size_t)(s0 + q_eff) * ld + head_off + 8 * h;
 #pragma unroll
-            for (int kk = 0; kk < 8; ++kk) qf[kk] = *reinterpret_cast<const bf16x8_t*>(qrow + 16 * kk);
+            for (int kk = 0; kk < NKK; ++kk) qf[kk] = *reinterpret_cast<const bf16x8_t*>(qrow + 16 * kk);
         }
 
-        f32x16_t oacc[4];
+        f32x16_t oacc[NT];
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
+        for (int t = 0; t < NT; ++t)
 #pragma unroll
             for (int i = 0; i < 16; ++i) oacc[t][i] = 0.f;
         float m_run = -INFINITY;
@@ -169,7 +175,7 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
         // has no load of its own outstanding, and the explicit waits below
         // keep up to two blocks in flight.
 #pragma unroll
-        for (int kk = 0; kk < 8; ++kk) asm volatile("" : "+v"(qf[kk]));
+        for (int kk = 0; kk < NKK; ++kk) asm volatile("" : "+v"(qf[kk]));
 
         for (int b = 0; b < nkv; ++b) {
             // block b has landed (the Q loads, issued earlier, too) once at
@@ -191,7 +197,7 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
 #pragma unroll
                     for (int i = 0; i < 16; ++i) s[kb][i] = 0.f;
 #pragma unroll
-                for (int kk = 0; kk < 8; ++kk)
+                for (int kk = 0; kk < NKK; ++kk)
 #pragma unroll
                     for (int kb = 0; kb < 2; ++kb) {
                         const bf16x8_t kf = *reinterpret_cast<const bf16x8_t*>(
@@ -240,7 +246,7 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
                     const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
                     l_run *= alpha;
 #pragma unroll
-                    for (int t = 0; t < 4; ++t)
+                    for (int t = 0; t < NT; ++t)
 #pragma unroll
                         for (int i = 0; i < 16; ++i) oacc[t][i] *= alpha;
                 }
@@ -260,7 +266,7 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
                         for (int jj = 0; jj < 8; ++jj) pf[jj] = (__bf16)sc[kb][8 * ks + jj];
                         const unsigned char* vb = Vb + (kb * 32 + 16 * ks) * kRowBytes + v_off;
 #pragma unroll
-                        for (int t = 0; t < 4; ++t) {
+                        for (int t = 0; t < NT; ++t) {
                             const int tsw = ((t ^ tj) << 6);   // chunk group t moved by the row's swizzle
                             const v4s_t lo = lds_read_tr16(vb + tsw);
                             const v4s_t hi = lds_read_tr16(vb + tsw + 8 * kRowBytes);
@@ -279,7 +285,7 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
             const float inv = 1.0f / l_run;
             bf16_t* orow = o + (size_t)(s0 + qidx) * ld + head_off;
 #pragma unroll
-            for (int t = 0; t < 4; ++t)
+            for (int t = 0; t < NT; ++t)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
                     const int dcol = t * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
@@ -332,12 +338,17 @@ attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
 
 hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                  uint16_t* o, const int* cu, int n_seq, int max_seqlen,
-                                 int n_heads, int n_prefix, hipStream_t st) {
+                                 int n_heads, int hd, int n_prefix, hipStream_t st) {
     if (n_seq <= 0 || max_seqlen <= 0) return hipSuccess;
-    const float scale_log2 = 1.4426950408889634f / sqrtf((float)HD);
+    if (hd != 64 && hd != 128) return hipErrorInvalidValue;
+    const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
     const long long blocks = (long long)n_seq * n_heads;
-    hipLaunchKernelGGL((attn_bf16_kernel<4, 2>), dim3((unsigned)blocks), dim3(256), 0, st, q, k, v, o, cu, n_seq,
-                       n_heads, n_prefix, scale_log2);
+    if (hd == 128)
+        hipLaunchKernelGGL((attn_bf16_kernel<4, 2, 128>), dim3((unsigned)blocks), dim3(256), 0, st, q, k, v, o, cu,
+                           n_seq, n_heads, n_prefix, scale_log2);
+    else
+        hipLaunchKernelGGL((attn_bf16_kernel<4, 2, 64>), dim3((unsigned)blocks), dim3(256), 0, st, q, k, v, o, cu,
+                           n_seq, n_heads, n_prefix, scale_log2);
     return hipGetLastError();
 }
 

@@ -135,7 +135,7 @@ rift_status check_cfg(const rift_model_cfg* cfg) {
         return RIFT_ERR_SHAPE;
     if (!(cfg->rms_eps >= 0.0f) || !(cfg->rope_base > 0.0f)) return RIFT_ERR_SHAPE;
     if (cfg->dt == RIFT_BF16) {
-        if (cfg->head_dim != 128 || cfg->d % 256 != 0 || cfg->ffn % 128 != 0)
+        if ((cfg->head_dim != 64 && cfg->head_dim != 128) || cfg->d % 256 != 0 || cfg->ffn % 128 != 0)
             return RIFT_ERR_UNSUPPORTED;
         if ((uint64_t)cfg->d * cfg->ffn >= (1ull << 31)) return RIFT_ERR_UNSUPPORTED;
     } else {
@@ -624,6 +624,7 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
             qa.n_pos = max_seqlen;
             qa.M = T;
             qa.d = d;
+            qa.hd = c.head_dim;
             // Tile walk directions: each GEMM starts with the rows its input's
             // producer wrote last (norms and attention write rows in ascending
             // order), so its first A panels come from the memory-side cache:
@@ -636,7 +637,7 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
             RIFT_TRY(mark(l, 1, 0));
             RIFT_TRY(launch_attention_bf16(static_cast<const uint16_t*>(qb), static_cast<const uint16_t*>(kb),
                                            static_cast<const uint16_t*>(vb), static_cast<uint16_t*>(h),
-                                           cu_seqlens, n_seq, max_seqlen, c.n_heads, n_prefix, st));
+                                           cu_seqlens, n_seq, max_seqlen, c.n_heads, c.head_dim, n_prefix, st));
             RIFT_TRY(mark(l, 1, 1));
             RIFT_TRY(mark(l, 2, 0));
             RIFT_TRY(launch_gemm_resid(static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w.wo),
@@ -801,11 +802,12 @@ rift_status rift_decode_step(const rift_model_cfg* cfg, const rift_layer_weights
             uint16_t* vn = static_cast<uint16_t*>(kv_new) + (size_t)(2 * l + 1) * nd;
             RIFT_TRY(launch_skinny_gemm(h, static_cast<const uint16_t*>(w.wq), static_cast<const uint16_t*>(w.wk),
                                         static_cast<const uint16_t*>(w.wv), d, n_seq, 3 * d, d, part, st));
-            RIFT_TRY(launch_skinny_qkv(part, s_qkv, n_seq, d, rope, pos, n_pos, qb, kn, vn, max_new, step, st));
+            RIFT_TRY(launch_skinny_qkv(part, s_qkv, n_seq, d, c.head_dim, rope, pos, n_pos, qb, kn, vn, max_new,
+                                       step, st));
             RIFT_TRY(launch_decode_attention(qb, static_cast<const uint16_t*>(kv_cache) + (size_t)(2 * l) * td,
                                              static_cast<const uint16_t*>(kv_cache) + (size_t)(2 * l + 1) * td, kn,
-                                             vn, cu_p, n_seq, total_tokens, n_prefix, c.n_heads, n_pos, max_new,
-                                             step, h, st));
+                                             vn, cu_p, n_seq, total_tokens, n_prefix, c.n_heads, c.head_dim,
+                                             n_pos, max_new, step, h, st));
             RIFT_TRY(launch_skinny_gemm(h, static_cast<const uint16_t*>(w.wo), nullptr, nullptr, d, n_seq, d, d,
                                         part, st));
             RIFT_TRY(launch_skinny_resid_norm(part, s_o, n_seq, d, hidden_out, static_cast<const uint16_t*>(w.g_ffn),
@@ -845,10 +847,11 @@ rift_status rift_decode_step(const rift_model_cfg* cfg, const rift_layer_weights
         qa.n_pos = n_pos;
         qa.M = n_seq;
         qa.d = d;
+        qa.hd = c.head_dim;
         RIFT_TRY(launch_gemm_qkv_rope(qa, st));
         RIFT_TRY(launch_kv_append(kb, vb, kn, vn, n_seq, d, max_new, step, st));
         RIFT_TRY(launch_decode_attention(qb, kp, vp, kn, vn, cu_p, n_seq, total_tokens, n_prefix, c.n_heads,
-                                         n_pos, max_new, step, h, st));
+                                         c.head_dim, n_pos, max_new, step, h, st));
         RIFT_TRY(launch_gemm_resid(h, static_cast<const uint16_t*>(w.wo), hidden_out, n_seq, d, d, st));
         RIFT_TRY(launch_rmsnorm(hidden_out, false, nullptr, w.g_ffn, true, h, true, n_seq, d, c.rms_eps, st));
         RIFT_TRY(launch_gemm_swiglu(h, static_cast<const uint16_t*>(w.w_gate), static_cast<const uint16_t*>(w.w_up),

@@ -9,22 +9,21 @@
 //
 //   decode_pos     position of each prompt's new token, L_i + step
 //   kv_append      this step's rotated key and value rows into slot `step`
-//   decode_attn    one workgroup (4 waves) per (prompt, head), the 16 lanes
-//                  of each row group reading one key or value row of 256
-//                  bytes whole: scores of every key in LDS (a dot product per
-//                  group, summed over its lanes); the max and the sum of
-//                  2^(s - max) over the workgroup; then the weighted sum of
-//                  the values, each lane 8 of the 128 dimensions over its
-//                  group's keys, the 16 group sums added in fixed order;
-//                  output rounded to bfloat16.
+//   decode_attn    one workgroup (4 waves) per (prompt, head), the HD / 8
+//                  lanes of each row group reading one key or value row of
+//                  2 HD bytes whole (HD = 128: 16 lanes, 16 groups; HD = 64: 8
+//                  lanes, 32 groups): scores of every key in LDS (a dot
+//                  product per group, summed over its lanes); the max and the
+//                  sum of 2^(s - max) over the workgroup; then the weighted sum
+//                  of the values, each lane 8 of the HD dimensions over its
+//                  group's keys, the group sums added in fixed order; output
+//                  rounded to bfloat16.
 #include "launch.h"
 #include "rift_common.h"
 
 namespace rift {
 
 namespace {
-
-constexpr int DHD = 128;
 
 // cu: the prompts' own row offsets (after the shared prefix sequence when
 // n_prefix > 0)
@@ -46,36 +45,42 @@ __global__ void kv_append_kernel(const u32x4_t* __restrict__ k, const u32x4_t* _
     vc[dst] = v[w];
 }
 
-// Sum over the 16 lanes of each row of the wave, every lane receiving the
-// same sum: pairs, quads (quad_perm), halves (row_half_mirror), rows
-// (row_mirror).  Each step adds two values that every lane of the group sees in
-// one of two orders, so the lanes agree bit for bit.
-__device__ __forceinline__ float row16_sum(float v) {
+// Sum over the G (16 or 8) lanes of each row group of the wave, every lane
+// receiving the same sum: pairs, quads (quad_perm), halves (row_half_mirror)
+// and, for G = 16, rows (row_mirror).  Each step adds two values that every
+// lane of the group sees in one of two orders, so the lanes agree bit for bit.
+template <int G>
+__device__ __forceinline__ float group_sum(float v) {
     v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xf, 0xf, false));
     v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x4E, 0xf, 0xf, false));
     v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x141, 0xf, 0xf, false));
-    v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x140, 0xf, 0xf, false));
+    if constexpr (G == 16)
+        v += __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0x140, 0xf, 0xf, false));
     return v;
 }
 
-// Keys are visited in groups of 64: slot s = 4 wave + (lane >> 4) of the 16
-// row groups takes keys j0 + 16 u + s, u < kDecU, and the 16 lanes of a group
-// read one 256-byte row, lane c its bytes 16 c .. 16 c + 15 (dims 8 c .. 8 c + 7).
+// Keys are visited in blocks of NS kDecU keys: slot s = (64 / G) wave +
+// lane / G of the NS = 256 / G row groups takes keys j0 + NS u + s, u < kDecU,
+// and the G lanes of a group read one row, lane c its bytes 16 c .. 16 c + 15
+// (dims 8 c .. 8 c + 7).
 constexpr int kDecU = 4;
 
+template <int HD>
 __global__ void __launch_bounds__(256)
 decode_attn_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ kp, const bf16_t* __restrict__ vp,
                    const bf16_t* __restrict__ kn, const bf16_t* __restrict__ vn, const int* __restrict__ cu,
                    int n_seq, int T, int n_prefix, int H, int max_keys, int max_new, int step, float scale_log2,
                    bf16_t* __restrict__ o) {
+    constexpr int G = HD / 8;        // lanes per row group
+    constexpr int NS = 256 / G;      // row groups (key slots) per workgroup
     extern __shared__ float sc[];   // one score per key
     __shared__ float red[4];
-    __shared__ float part[4][DHD];
+    __shared__ float part[4][HD];
     const int seq = blockIdx.x / H;
     const int head = blockIdx.x % H;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int c = lane & 15;
-    const int slot = 4 * wave + (lane >> 4);
+    const int c = lane % G;
+    const int slot = (64 / G) * wave + lane / G;
     int s0 = cu[seq];
     int L = cu[seq + 1] - s0;
     if (s0 < 0 || L < 0 || s0 + L > T) s0 = L = 0;   // offsets outside the prefill cache: no prompt keys
@@ -83,8 +88,8 @@ decode_attn_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ kp, 
     // prefix keys, the prompt's own keys, then the generated ones (at most
     // max_keys, the LDS size)
     const int nk = min(P + L + step + 1, max_keys);
-    const int ld = H * DHD;
-    const size_t hoff = (size_t)head * DHD + 8 * c;
+    const int ld = H * HD;
+    const size_t hoff = (size_t)head * HD + 8 * c;
     auto row = [&](int j, const bf16_t* prompt_base, const bf16_t* new_base) -> const u32x4_t* {
         return reinterpret_cast<const u32x4_t*>(
             j < P ? prompt_base + (size_t)j * ld + hoff
@@ -102,11 +107,11 @@ decode_attn_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ kp, 
     }
     // scores (base-2 logits), and the running max of this lane's keys
     float mx = -INFINITY;
-    for (int j0 = 0; j0 < nk; j0 += 16 * kDecU) {
+    for (int j0 = 0; j0 < nk; j0 += NS * kDecU) {
         u32x4_t kw[kDecU];
 #pragma unroll
         for (int u = 0; u < kDecU; ++u)
-            kw[u] = __builtin_nontemporal_load(row(min(j0 + 16 * u + slot, nk - 1), kp, kn));
+            kw[u] = __builtin_nontemporal_load(row(min(j0 + NS * u + slot, nk - 1), kp, kn));
 #pragma unroll
         for (int u = 0; u < kDecU; ++u) {
             float acc = 0.f;
@@ -115,8 +120,8 @@ decode_attn_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ kp, 
                 acc = fmaf(bf16_lo(kw[u][e]), qf[2 * e], acc);
                 acc = fmaf(bf16_hi(kw[u][e]), qf[2 * e + 1], acc);
             }
-            const float sl = row16_sum(acc) * scale_log2;
-            const int j = j0 + 16 * u + slot;
+            const float sl = group_sum<G>(acc) * scale_log2;
+            const int j = j0 + NS * u + slot;
             if (j < nk) {
                 mx = fmaxf(mx, sl);
                 if (c == 0) sc[j] = sl;
@@ -142,14 +147,14 @@ decode_attn_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ kp, 
     float acc[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[e] = 0.f;
-    for (int j0 = 0; j0 < nk; j0 += 16 * kDecU) {
+    for (int j0 = 0; j0 < nk; j0 += NS * kDecU) {
         u32x4_t vw[kDecU];
 #pragma unroll
         for (int u = 0; u < kDecU; ++u)
-            vw[u] = __builtin_nontemporal_load(row(min(j0 + 16 * u + slot, nk - 1), vp, vn));
+            vw[u] = __builtin_nontemporal_load(row(min(j0 + NS * u + slot, nk - 1), vp, vn));
 #pragma unroll
         for (int u = 0; u < kDecU; ++u) {
-            const int j = j0 + 16 * u + slot;
+            const int j = j0 + NS * u + slot;
             if (j < nk) {
                 const float p = sc[j];
 #pragma unroll
@@ -160,20 +165,19 @@ decode_attn_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ kp, 
             }
         }
     }
-    // the four row groups of a wave, then the four waves, in fixed order
+    // the row groups of a wave, then the four waves, in fixed order
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        acc[e] += __shfl_xor(acc[e], 16);
-        acc[e] += __shfl_xor(acc[e], 32);
-    }
-    if (lane < 16) {
+    for (int e = 0; e < 8; ++e)
+#pragma unroll
+        for (int sh = G; sh < 64; sh <<= 1) acc[e] += __shfl_xor(acc[e], sh);
+    if (lane < G) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) part[wave][8 * c + e] = acc[e];
     }
     __syncthreads();
-    if (tid < DHD) {
+    if (tid < HD) {
         const float r = ((part[0][tid] + part[1][tid]) + part[2][tid]) + part[3][tid];
-        o[(size_t)seq * ld + (size_t)head * DHD + tid] = f32_to_bf16(r * inv);
+        o[(size_t)seq * ld + (size_t)head * HD + tid] = f32_to_bf16(r * inv);
     }
 }
 
@@ -197,11 +201,17 @@ hipError_t launch_kv_append(const uint16_t* k, const uint16_t* v, uint16_t* kc, 
 
 hipError_t launch_decode_attention(const uint16_t* q, const uint16_t* kp, const uint16_t* vp, const uint16_t* kn,
                                    const uint16_t* vn, const int* cu, int n_seq, int T, int n_prefix, int n_heads,
-                                   int max_keys, int max_new, int step, uint16_t* o, hipStream_t st) {
-    const float scale_log2 = 1.4426950408889634f / sqrtf((float)DHD);
-    hipLaunchKernelGGL(decode_attn_kernel, dim3((unsigned)(n_seq * n_heads)), dim3(256),
-                       (size_t)max_keys * sizeof(float), st, q, kp, vp, kn, vn, cu, n_seq, T, n_prefix, n_heads,
-                       max_keys, max_new, step, scale_log2, o);
+                                   int hd, int max_keys, int max_new, int step, uint16_t* o, hipStream_t st) {
+    if (hd != 64 && hd != 128) return hipErrorInvalidValue;
+    const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
+    const dim3 grid((unsigned)(n_seq * n_heads));
+    const size_t lds = (size_t)max_keys * sizeof(float);
+    if (hd == 128)
+        hipLaunchKernelGGL(decode_attn_kernel<128>, grid, dim3(256), lds, st, q, kp, vp, kn, vn, cu, n_seq, T,
+                           n_prefix, n_heads, max_keys, max_new, step, scale_log2, o);
+    else
+        hipLaunchKernelGGL(decode_attn_kernel<64>, grid, dim3(256), lds, st, q, kp, vp, kn, vn, cu, n_seq, T,
+                           n_prefix, n_heads, max_keys, max_new, step, scale_log2, o);
     return hipGetLastError();
 }
 

@@ -52,6 +52,7 @@ struct GemmParams {
     const bf16_t* b2;
     int M, N, K;
     int d;            // QKV: width of each of q, k, v;  SWIGLU: ffn width
+    int hd;           // QKV: head dim, 128 or 64
     bf16_t* o0;
     bf16_t* o1;
     bf16_t* o2;
@@ -236,11 +237,42 @@ __device__ __forceinline__ void epilogue_staged(const GemmParams& p, f32x4_t (&a
         const int region = __builtin_amdgcn_readfirstlane((bn * BN) / p.d);
         const int j = 32 * (wn & 1) + col_in;            // block nb = 0 column within the head (+16 for nb = 1)
         const int sc = 128 * (wn >> 1) + j - cbase;      // staging column of j; j + 64 at sc + 64
+        // Head dim 64: the rotate-half partner of column c (c mod 64 < 32) is
+        // c + 32, held by the same lane and accumulator slot of wave wn ^ 1
+        // (wave index ^ 1, in whole and half tiles alike).  The two waves
+        // swap their float32 values through LDS one row block at a time; each
+        // keeps its own rotated half in acc, and the tile is then staged as v
+        // is.  Angle index of (nb, lane): 16 (nb & 1) + col_in.
+        const bool rope64 = p.hd == 64 && region < 2;
+        if (rope64) {
+            float* X = reinterpret_cast<float*>(stage);   // [wave][16 values][64 lanes] per row block
+            const int wave = threadIdx.x >> 6;
+            const bool first = (wn & 1) == 0;             // holds j < 32 of its head
+#pragma unroll
+            for (int mb = 0; mb < 8; ++mb) {
+#pragma unroll
+                for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) X[(wave * 16 + nb * 4 + v) * 64 + lane] = acc[mb][nb][v];
+                __syncthreads();
+                const int r0 = wm * 128 + mb * 16 + row_hi;
+#pragma unroll
+                for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const float other = X[((wave ^ 1) * 16 + nb * 4 + v) * 64 + lane];
+                        const float2 cs = p.rope[(size_t)pos_lds[r0 + v] * 32 + 16 * (nb & 1) + col_in];
+                        const float own = acc[mb][nb][v];
+                        acc[mb][nb][v] = first ? own * cs.x - other * cs.y : own * cs.x + other * cs.y;
+                    }
+                __syncthreads();
+            }
+        }
 #pragma unroll
         for (int mb = 0; mb < 8; ++mb) {
             __builtin_amdgcn_sched_barrier(0);
             const int r0 = wm * 128 + mb * 16 + row_hi;
-            if (region == 2) {
+            if (region == 2 || rope64) {
 #pragma unroll
                 for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
@@ -708,6 +740,7 @@ hipError_t launch_gemm_qkv_rope(const QkvArgs& a, hipStream_t st, bool reverse) 
     p.rope = a.rope;
     p.pos = a.pos;
     p.n_pos = a.n_pos;
+    p.hd = a.hd;
     p.reverse = reverse ? 1 : 0;
     return launch_gemm<EPI_QKV>(p, p.N / BN, st);
 }

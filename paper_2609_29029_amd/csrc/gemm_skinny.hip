@@ -239,37 +239,39 @@ skinny_resid_norm_kernel(const float* __restrict__ part, int S, int M, float* __
     }
 }
 
-// q | k | v of row m from the partials of [wq | wk | wv] (N = 3 d): thread
-// (m, region, head, j4 < 16) owns columns j = 4 j4 .. + 3 of its head and their
-// rotate-half partners j + 64; q goes to q[m], k and v to slot `step` of
-// prompt m in the decode cache.
+// q | k | v of row m from the partials of [wq | wk | wv] (N = 3 d): with
+// half = hd / 2, thread (m, region, head, j4 < half / 4) owns columns
+// j = 4 j4 .. + 3 of its head and their rotate-half partners j + half; q goes
+// to q[m], k and v to slot `step` of prompt m in the decode cache.
 __global__ void __launch_bounds__(256)
-skinny_qkv_kernel(const float* __restrict__ part, int S, int M, int d, const float2* __restrict__ rope,
+skinny_qkv_kernel(const float* __restrict__ part, int S, int M, int d, int hd, const float2* __restrict__ rope,
                   const int* __restrict__ pos, int n_pos, bf16_t* __restrict__ q, bf16_t* __restrict__ kc,
                   bf16_t* __restrict__ vc, int max_new, int step) {
     const int per_region = d >> 3;   // (head, j4) pairs
+    const int half = hd >> 1;
+    const int q4 = half >> 2;        // j4 per head
     const long long idx = (long long)blockIdx.x * blockDim.x + threadIdx.x;
     if (idx >= (long long)M * 3 * per_region) return;
     const int m = (int)(idx / (3 * per_region));
     const int rem = (int)(idx % (3 * per_region));
     const int region = rem / per_region;
     const int w = rem % per_region;
-    const int j = 4 * (w & 15);
-    const int hc = 128 * (w >> 4) + j;   // column of j within q, k or v
+    const int j = 4 * (w % q4);
+    const int hc = hd * (w / q4) + j;   // column of j within q, k or v
     const size_t N = 3 * (size_t)d;
     const float* p0 = part + (size_t)m * N + (size_t)region * d + hc;
     f32x4_t x1 = *reinterpret_cast<const f32x4_t*>(p0);
-    f32x4_t x2 = *reinterpret_cast<const f32x4_t*>(p0 + 64);
+    f32x4_t x2 = *reinterpret_cast<const f32x4_t*>(p0 + half);
     for (int s = 1; s < S; ++s) {
         const float* ps = p0 + (size_t)s * M * N;
         x1 += *reinterpret_cast<const f32x4_t*>(ps);
-        x2 += *reinterpret_cast<const f32x4_t*>(ps + 64);
+        x2 += *reinterpret_cast<const f32x4_t*>(ps + half);
     }
     f32x4_t y1 = x1, y2 = x2;
     if (region < 2) {
         int ps = pos[m];
         ps = ps < 0 ? 0 : (ps >= n_pos ? n_pos - 1 : ps);
-        const f32x4_t* cs = reinterpret_cast<const f32x4_t*>(rope + (size_t)ps * 64 + j);
+        const f32x4_t* cs = reinterpret_cast<const f32x4_t*>(rope + (size_t)ps * half + j);
         const f32x4_t c01 = cs[0], c23 = cs[1];   // (cos, sin) of j, j+1 and of j+2, j+3
         const float cv[4] = {c01[0], c01[2], c23[0], c23[2]};
         const float sv[4] = {c01[1], c01[3], c23[1], c23[3]};
@@ -287,7 +289,7 @@ skinny_qkv_kernel(const float* __restrict__ part, int S, int M, int d, const flo
     o2.x = (uint32_t)f32_to_bf16(y2[0]) | ((uint32_t)f32_to_bf16(y2[1]) << 16);
     o2.y = (uint32_t)f32_to_bf16(y2[2]) | ((uint32_t)f32_to_bf16(y2[3]) << 16);
     *reinterpret_cast<uint2*>(dst + hc) = o1;
-    *reinterpret_cast<uint2*>(dst + hc + 64) = o2;
+    *reinterpret_cast<uint2*>(dst + hc + half) = o2;
 }
 
 // a[m][f] = silu(gate) * up from the partials of [wg | wu] (N = 2 F), four
@@ -399,12 +401,14 @@ hipError_t launch_skinny_resid_norm(const float* part, int S, int M, int d, floa
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_skinny_qkv(const float* part, int S, int M, int d, const float2* rope, const int* pos, int n_pos,
-                             uint16_t* q, uint16_t* kc, uint16_t* vc, int max_new, int step, hipStream_t st) {
+hipError_t launch_skinny_qkv(const float* part, int S, int M, int d, int hd, const float2* rope, const int* pos,
+                             int n_pos, uint16_t* q, uint16_t* kc, uint16_t* vc, int max_new, int step,
+                             hipStream_t st) {
     if (M <= 0) return hipSuccess;
+    if (hd != 64 && hd != 128) return hipErrorInvalidValue;
     const long long n = (long long)M * 3 * (d / 8);
-    hipLaunchKernelGGL(skinny_qkv_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part, S, M, d, rope,
-                       pos, n_pos, q, kc, vc, max_new, step);
+    hipLaunchKernelGGL(skinny_qkv_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part, S, M, d, hd,
+                       rope, pos, n_pos, q, kc, vc, max_new, step);
     return hipGetLastError();
 }
 

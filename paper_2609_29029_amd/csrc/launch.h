@@ -64,6 +64,7 @@ struct QkvArgs {
     const int* pos;      // [M]
     int n_pos;
     int M, d;
+    int hd;              // head dim: 128, or 64
 };
 // The GEMMs walk their output tiles from the first row block to the last, or
 // with `reverse` from the last to the first.  The order changes no result; it
@@ -79,10 +80,10 @@ hipError_t launch_gemm_resid(const uint16_t* a, const uint16_t* b, float* resid,
 hipError_t launch_gemm_swiglu(const uint16_t* a, const uint16_t* wg, const uint16_t* wu,
                               uint16_t* out, int M, int F, int K, hipStream_t st, bool reverse = false);
 
-// Varlen causal attention, bf16, head_dim 128.  q, k, v, o: [T][H*128].
+// Varlen causal attention, bf16, head_dim hd (128 or 64).  q, k, v, o: [T][H*hd].
 hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                  uint16_t* o, const int* cu, int n_seq, int max_seqlen,
-                                 int n_heads, int n_prefix, hipStream_t st);
+                                 int n_heads, int hd, int n_prefix, hipStream_t st);
 
 // ---------------------------------------------------------------- decode (bf16)
 // pos[i] = (cu[i+1] - cu[i]) + step
@@ -93,7 +94,7 @@ hipError_t launch_kv_append(const uint16_t* k, const uint16_t* v, uint16_t* kc, 
 // one query per prompt over its prefill keys kp/vp [T][H*128] and slots 0..step of kn/vn
 hipError_t launch_decode_attention(const uint16_t* q, const uint16_t* kp, const uint16_t* vp, const uint16_t* kn,
                                    const uint16_t* vn, const int* cu, int n_seq, int T, int n_prefix, int n_heads,
-                                   int max_keys, int max_new, int step, uint16_t* o, hipStream_t st);
+                                   int hd, int max_keys, int max_new, int step, uint16_t* o, hipStream_t st);
 
 // Decode-shaped GEMMs (few rows): K split into S chunks (S from N and K only),
 // float32 partials part[S][M][N] of A [M][K] times the weight regions b0|b1|b2
@@ -107,9 +108,11 @@ hipError_t launch_skinny_gemm(const uint16_t* a, const uint16_t* b0, const uint1
 // x += sum of partials [S][M][d]; with h, h = bf16(RMSNorm(x) * g)
 hipError_t launch_skinny_resid_norm(const float* part, int S, int M, int d, float* x, const uint16_t* g,
                                     uint16_t* h, float eps, hipStream_t st);
-// q to q[M][d], k and v to slot `step` of kc, vc [M][max_new][d], RoPE at pos[m]
-hipError_t launch_skinny_qkv(const float* part, int S, int M, int d, const float2* rope, const int* pos, int n_pos,
-                             uint16_t* q, uint16_t* kc, uint16_t* vc, int max_new, int step, hipStream_t st);
+// q to q[M][d], k and v to slot `step` of kc, vc [M][max_new][d], RoPE at
+// pos[m] over heads of hd (128 or 64) dimensions
+hipError_t launch_skinny_qkv(const float* part, int S, int M, int d, int hd, const float2* rope, const int* pos,
+                             int n_pos, uint16_t* q, uint16_t* kc, uint16_t* vc, int max_new, int step,
+                             hipStream_t st);
 // a[M][F] = silu(gate) * up
 hipError_t launch_skinny_swiglu(const float* part, int S, int M, int F, uint16_t* a, hipStream_t st);
 

@@ -127,8 +127,8 @@ int main() {
     EXPECT(rift_prefill(&cfg, lw, FAKE, RIFT_BF16, I, I, 100, 18739, 643, 35, F, nullptr, ws, 64, nullptr, nullptr) ==
            RIFT_ERR_WORKSPACE);
     rift_model_cfg odd = cfg;
-    odd.head_dim = 64;
-    odd.n_heads = 64;
+    odd.head_dim = 32;
+    odd.n_heads = 128;
     EXPECT(rift_prefill(&odd, lw, FAKE, RIFT_BF16, I, I, 100, 18739, 643, 35, F, nullptr, ws, 1 << 20, nullptr,
                         nullptr) == RIFT_ERR_UNSUPPORTED);
     EXPECT(rift_decode_workspace_size(&cfg, 100, 643, 8) > 0);

@@ -181,13 +181,16 @@ def test_prefill_validation_and_workspace(R):
     # a shared prefix: within the batch and max_seqlen, with at least one sequence
     assert call(cfg, n_prefix=-1) == 2 and call(cfg, n_prefix=11) == 2
     assert call(cfg, T=20, max_len=10, n_prefix=11) == 2 and call(cfg, n_seq=0, n_prefix=3) == 2
-    for bad in (R.model_cfg(4096, 64, 64, 11008, 1, 1e-6, 1e4, R.RIFT_BF16),    # bf16 needs head_dim 128
+    for bad in (R.model_cfg(4096, 128, 32, 11008, 1, 1e-6, 1e4, R.RIFT_BF16),   # head_dim 64 or 128 only
                 R.model_cfg(4160, 32, 130, 11008, 1, 1e-6, 1e4, R.RIFT_BF16),
+                R.model_cfg(1088, 17, 64, 2816, 1, 1e-6, 1e4, R.RIFT_BF16),     # bf16: d % 256
                 R.model_cfg(256, 4, 64, 690, 1, 1e-6, 1e4, R.RIFT_F32)):        # ffn % 16
         assert call(bad) == 8   # RIFT_ERR_UNSUPPORTED
     assert call(R.model_cfg(4096, 31, 128, 11008, 1, 1e-6, 1e4, R.RIFT_BF16)) == 2
     assert call(R.model_cfg(4096, 32, 128, 11008, 1, 1e-6, 1e4, 9)) == 3
-    assert R.rift_prefill_workspace_size(R.model_cfg(4096, 64, 64, 11008, 1, 1e-6, 1e4, R.RIFT_BF16), 10, 10) == 0
+    assert R.rift_prefill_workspace_size(R.model_cfg(4096, 128, 32, 11008, 1, 1e-6, 1e4, R.RIFT_BF16), 10, 10) == 0
+    # bf16 with 64-dimensional heads is a supported shape
+    assert R.rift_prefill_workspace_size(R.model_cfg(4096, 64, 64, 11008, 1, 1e-6, 1e4, R.RIFT_BF16), 10, 10) > 0
 
 
 def test_utility_budgets_match_oracle(R):
