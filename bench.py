@@ -40,13 +40,13 @@ GEMM_SRC = os.path.join(ROOT, "paper_2609_29029_amd", "csrc", "gemm_bf16.hip")
 # system prefix (T = 18,739 packed rows), from two rocprofv3 --pmc runs of this
 # script with --traffic-calibration (FETCH_SIZE, then WRITE_SIZE), each scaled
 # by what the counter reads for the 1 GiB calibration copy (FETCH_SIZE reads
-# half the bytes, WRITE_SIZE all of them): 6.1857 GB fetched + 0.4126 GB written
+# half the bytes, WRITE_SIZE all of them): 5.9171 GB fetched + 0.4126 GB written
 # (profiles/scene20_l32_counters.md).  Valid only for the GEMM source it was
 # measured on, identified by its SHA-256; otherwise reported as null.
 TRAFFIC = {"stage": "gate_up_swiglu",
-           "gemm_src_sha256": "bf43d9a91066dd36ca510990d4128c5fef91cc0bf2c2942a217d099e5ecd5b6d",
+           "gemm_src_sha256": "931deef165838a0038bdde4f0cb0627c92b39c0c964563df294e0e4155407bb8",
            "packed_tokens": 18739,
-           "bytes": 6.5983e9}
+           "bytes": 6.3297e9}
 
 
 def log(*a):
