@@ -229,7 +229,10 @@ def mfma_ceiling(torch, seconds_per_form: float = 0.4) -> dict:
     nominal peak.  Also with all-zero operands (which draw far less power, so
     the clock stays near its maximum): two waves per SIMD, the instruction's
     own rate, and one wave per SIMD, the rate at which a lone wave can issue
-    (the ping-pong GEMM loop has one MFMA wave per SIMD at a time).  Three
+    (the ping-pong GEMM loop has one MFMA wave per SIMD at a time).  Last, the
+    random-operand MFMAs with the LDS reads (384 bytes per MFMA) and LDS DMA
+    (128 bytes per MFMA) of the gate/up loop but none of its waits: the
+    ceiling once the loop's data movement shares the power budget.  Three
     timed launches per case, median."""
     import ctypes
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_29029_amd", "libriftcalib.so"))
@@ -261,6 +264,28 @@ def mfma_ceiling(torch, seconds_per_form: float = 0.4) -> dict:
                 ts.append(e0.elapsed_time(e1))
         tf = per_iter * iters / (statistics.median(ts) * 1e-3) / 1e12
         res[name] = {"TFLOPs": round(tf, 1), "frac_nominal": round(tf / PEAK_BF16_TFLOPS, 4)}
+    # the same MFMAs with the gate/up loop's LDS reads and LDS DMA (no waits or
+    # barriers): the ceiling once the loop's own data movement draws power too
+    lib.rift_calib_mfma_bf16_moves.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_longlong,
+                                               ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    dsrc = torch.randn(1 << 21, device="cuda", generator=g).to(torch.bfloat16)   # 4 MiB
+    per_iter = blocks * 8 * 262144
+    iters = max(16, int(seconds_per_form * 1.5e15 / per_iter) // 16 * 16)
+    ts = []
+    for rep in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        rc = lib.rift_calib_mfma_bf16_moves(src.data_ptr(), dsrc.data_ptr(), dsrc.numel() * 2, out.data_ptr(),
+                                            blocks, iters, stream)
+        e1.record()
+        torch.cuda.synchronize()
+        if rc != 0:
+            raise RuntimeError(f"rift_calib_mfma_bf16_moves returned {rc}")
+        if rep:
+            ts.append(e0.elapsed_time(e1))
+    tf = per_iter * iters / (statistics.median(ts) * 1e-3) / 1e12
+    res["v_mfma_f32_16x16x32_bf16 with the gate/up loop's LDS reads and LDS DMA"] = {
+        "TFLOPs": round(tf, 1), "frac_nominal": round(tf / PEAK_BF16_TFLOPS, 4)}
     return res
 
 
@@ -880,6 +905,8 @@ def main() -> int:
     c16 = ceil["v_mfma_f32_16x16x32_bf16"]["TFLOPs"]
     out["roofline"]["measured_peak"] = c16
     out["roofline"]["frac_of_measured_peak"] = round(achieved / c16, 4)
+    cmv = ceil["v_mfma_f32_16x16x32_bf16 with the gate/up loop's LDS reads and LDS DMA"]["TFLOPs"]
+    out["roofline"]["frac_of_data_movement_ceiling"] = round(achieved / cmv, 4)
     if w.dtype == "bf16":
         out["gemm_operand_split"] = gemm_operand_split(R, torch, q)
         log(f"gemm operand split: {out['gemm_operand_split']['zero_over_query_time']}")

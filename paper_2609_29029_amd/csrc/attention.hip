@@ -8,7 +8,8 @@
 // (workgroups are numbered sequence by sequence, so prompts packed longest
 // first start first).  Keys and values stream 64 at a time through a ring of
 // S = 2 LDS stages that LDS DMA fills a block ahead, one barrier per block,
-// and two workgroups share a CU.  Tile rows are 256 bytes, unpadded; the
+// and two workgroups share a CU; the last key block of a query block loads
+// the first one of the next query block.  Tile rows are 256 bytes, unpadded; the
 // 16-byte chunks of row r sit at chunk ^ (r & 15) for keys and chunk ^
 // 4 (r & 3) for values, which keeps both the key-row reads and the
 // transposing value reads free of bank conflicts.  (The kernel also runs
@@ -61,6 +62,16 @@ __device__ __forceinline__ void dma16v(const void* gaddr, uint32_t lds_addr) {
                  :: "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(gaddr) : "memory", "m0");
 }
 
+// Same, saddr form: 64-bit wave-uniform base plus a 32-bit per-lane byte
+// offset.
+__device__ __forceinline__ void dma16s(const void* base, uint32_t voff, uint32_t lds_addr) {
+    const uint64_t b = (uint64_t)(uintptr_t)base;
+    const uint64_t ub = (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b) |
+                        ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32)) << 32);
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :: "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(ub) : "memory", "m0");
+}
+
 // wait until at most n of this wave's vector memory operations are outstanding
 __device__ __forceinline__ void wait_vm(int n) {
     switch (n) {
@@ -102,15 +113,41 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
     const size_t head_off = (size_t)head * HD;
     const uint32_t ring0 = (uint32_t)(uintptr_t)ring;
 
-    // DMA of logical key block `blk` into stage blk % 4: 32 instructions of
-    // four 256-byte rows each (0..15 keys, 16..31 values); wave w issues
-    // 4 w .. 4 w + 3 (waves 0-3 keys, 4-7 values).  Lane l moves chunk
-    // position l % 16 of row 4 jj + l / 16, i.e. global chunk position ^ swz.
+    // DMA of logical key block `blk` into ring stage slot % S: 32 instructions
+    // of four 256-byte rows each (0..15 keys, 16..31 values); wave w issues
+    // NDMA = 32 / W of them (the first W / 2 waves keys, the others values).
+    // Lane l moves chunk position l % 16 of row 4 jj + l / 16, i.e. global
+    // chunk position ^ swz.
     const bool dma_v = wave >= W / 2;
     const bf16_t* dma_src = dma_v ? v : k;
     const int dma_row_lo = lane >> 4;
-    auto dma_block = [&](int blk) {
-        const uint32_t sb = ring0 + (uint32_t)(blk % S) * kStageBytes + (dma_v ? kTileBytes : 0);
+    // Per-lane part of each instruction's source, for blocks that lie inside
+    // the sequence's own rows: byte offset of (row, chunk) from the block's
+    // first row; the wave-uniform rest goes into the scalar base.
+    uint32_t dma_off[NDMA];
+#pragma unroll
+    for (int i = 0; i < NDMA; ++i) {
+        const int jj = NDMA * (wave % (W / 2)) + i;
+        const int row = 4 * jj + dma_row_lo;
+        const int swz = dma_v ? 4 * (row & 3) : (row & 15);
+        const int c = (lane & 15) ^ swz;
+        dma_off[i] = ((uint32_t)row * (uint32_t)ld + (uint32_t)c * 8u) * 2u;
+    }
+    auto dma_block = [&](int blk, int slot) {
+        const uint32_t sb = ring0 + (uint32_t)(slot % S) * kStageBytes + (dma_v ? kTileBytes : 0);
+        const int k0 = blk * BKV;
+        if (k0 >= pre && k0 + BKV <= pre + L) {
+            const bf16_t* base = dma_src + (size_t)(s0 + k0 - pre) * ld + head_off;
+#pragma unroll
+            for (int i = 0; i < NDMA; ++i) {
+                const int jj = NDMA * (wave % (W / 2)) + i;
+                const int row = 4 * jj + dma_row_lo;
+                const int swz = dma_v ? 4 * (row & 3) : (row & 15);
+                const int c = (lane & 15) ^ swz;
+                if (HD == kLdsDims || c < HD / 8) dma16s(base, dma_off[i], sb + (uint32_t)jj * 1024u);
+            }
+            return;
+        }
 #pragma unroll
         for (int i = 0; i < NDMA; ++i) {
             const int jj = NDMA * (wave % (W / 2)) + i;
@@ -136,6 +173,11 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
     const int v_off = (4 * (tg >> 1) + tj) * kRowBytes + (2 * (tg & 1) + (tu >> 1)) * 16 + 8 * (tu & 1);
 
     const int nqb = (L + BQ - 1) / BQ;
+    // Ring position of each pass's first key block: positions run on across
+    // passes, so the last block of a pass can load the next pass's first block
+    // into the stage that is free by then.
+    int g0 = 0;
+    bool first_issued = false;
     for (int pr = 0; G * pr < nqb; ++pr) {
         const int qb_hi = nqb - 1 - G * pr;
         const int qb = qb_hi - grp;               // -1: the lower half has no block
@@ -169,7 +211,9 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
         const int kv_end = pre + ((qb_hi + 1) * BQ < L ? (qb_hi + 1) * BQ : L);
         const int nkv = (kv_end + BKV - 1) / BKV;
         const int pro = nkv < S - 1 ? nkv : S - 1;
-        for (int b = 0; b < pro; ++b) dma_block(b);
+        for (int b = first_issued ? 1 : 0; b < pro; ++b) dma_block(b, g0 + b);
+        const bool has_next = G * (pr + 1) < nqb;
+        bool issued_next = false;
         // The compiler waits for the Q loads here, once per pair (with them,
         // for the ring's first blocks, issued just after); in the loop it then
         // has no load of its own outstanding, and the explicit waits below
@@ -184,11 +228,16 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
             const int later = (nkv - 1 < b + S - 2 ? nkv - 1 : b + S - 2) - b;
             wait_vm(NDMA * later);
             asm volatile("s_barrier" ::: "memory");
-            if (b + S - 1 < nkv) dma_block(b + S - 1);    // into the stage block b-1 used
+            if (b + S - 1 < nkv) {
+                dma_block(b + S - 1, g0 + b + S - 1);    // into the stage block b-1 used
+            } else if (b == nkv - 1 && has_next) {
+                dma_block(0, g0 + nkv);                  // the next pass's first block
+                issued_next = true;
+            }
 
             const int kv0 = b * BKV;
             if (kv0 <= wave_last) {
-                const unsigned char* Kb = ring + (b % S) * kStageBytes;
+                const unsigned char* Kb = ring + ((g0 + b) % S) * kStageBytes;
                 const unsigned char* Vb = Kb + kTileBytes;
                 // scores for two 32-key sub-blocks; their MFMA chains interleaved
                 f32x16_t s[2];
@@ -281,17 +330,36 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
             }
         }
 
-        if (qb >= 0 && qidx < L) {
+        // Output row of this lane's query: slots 4 g .. 4 g + 3 of block t are
+        // dimensions 32 t + 8 g + 4 h + {0..3}.  Lanes h = 0 and 1 of a query
+        // swap the 8-byte halves of each 16-dimension group pair, so that
+        // each writes 16 contiguous bytes: h = 0 dimensions 32 t + 16 j + [0, 8),
+        // h = 1 dimensions 32 t + 16 j + [8, 16).
+        {
             const float inv = 1.0f / l_run;
-            bf16_t* orow = o + (size_t)(s0 + qidx) * ld + head_off;
+            const bool store = qb >= 0 && qidx < L;
+            bf16_t* orow = o + (size_t)(s0 + q_eff) * ld + head_off;
 #pragma unroll
             for (int t = 0; t < NT; ++t)
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    const int dcol = t * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-                    orow[dcol] = f32_to_bf16(oacc[t][i] * inv);
+                for (int j = 0; j < 2; ++j) {
+                    uint32_t a[2], b[2];
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) {
+                        a[e] = (uint32_t)f32_to_bf16(oacc[t][8 * j + 2 * e] * inv) |
+                               ((uint32_t)f32_to_bf16(oacc[t][8 * j + 2 * e + 1] * inv) << 16);
+                        b[e] = (uint32_t)f32_to_bf16(oacc[t][8 * j + 4 + 2 * e] * inv) |
+                               ((uint32_t)f32_to_bf16(oacc[t][8 * j + 4 + 2 * e + 1] * inv) << 16);
+                    }
+                    uint32_t r[2];
+#pragma unroll
+                    for (int e = 0; e < 2; ++e) r[e] = (uint32_t)__shfl_xor((int)(h ? a[e] : b[e]), 32);
+                    const u32x4_t v = h ? u32x4_t{r[0], r[1], b[0], b[1]} : u32x4_t{a[0], a[1], r[0], r[1]};
+                    if (store) *reinterpret_cast<u32x4_t*>(orow + t * 32 + 16 * j + 8 * h) = v;
                 }
         }
+        g0 += nkv;
+        first_issued = issued_next;
     }   // query block pairs
 }
 
