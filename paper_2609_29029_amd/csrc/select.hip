@@ -26,6 +26,12 @@
 //      counts).
 // Workgroup 0 writes the status word; the workgroup of the last tile writes
 // the total offset.
+//
+// Step 2 costs every workgroup a read of all budgets and ids, which grows with
+// the square of the tile count.  Calls of more than 8,192 kept tiles therefore
+// run two launches: one workgroup checks the call and writes the offsets and
+// the status word (select_scan_kernel), then the selection kernel reads its
+// tile's offset and the verdict instead of step 2.
 #include "launch.h"
 #include "rift_common.h"
 
@@ -76,9 +82,123 @@ __device__ __forceinline__ float wave_min(float v) {
 }
 __device__ __forceinline__ float wave_max(float v) { return -wave_min(-v); }
 
+// Large calls, first launch: one workgroup checks every budget (in [0, n_v])
+// and tile id (in [0, n_tiles)) of the call and the total (at most cap), and
+// writes the exclusive prefix sums of the budgets, their total and the status
+// word.  Chunks of kChunk entries: thread t loads entries t + 1024 j (whole
+// cache lines per instruction, the next chunk's loads in flight while this one
+// is scanned), the budgets go through LDS so that thread t sums the contiguous
+// run [kRun t, kRun (t + 1)), a wave scan and the 16 wave totals give each
+// run's base, and the offsets return through LDS to be stored as they were
+// loaded.  Offsets are written as they are found and, if the call turns out
+// invalid, all set to 0 afterwards.
+constexpr int kScanThreads = 1024;
+constexpr int kRun = 16;
+constexpr int kChunk = kRun * kScanThreads;
+// Kept tiles above which the two launches beat one: measured 28 against 25 us
+// at 6,400 tiles, 103 against 159 us at 51,200.
+constexpr int kScanFrom = 8192;
+// LDS word of chunk entry i: run t = i / 16 holds words [16 t, 16 t + 16), its
+// 4-entry quads rotated by (t / 4) mod 4 so that 16 consecutive runs' quad
+// reads (16 bytes a lane) meet 16 different bank groups.
+__device__ __forceinline__ unsigned scan_word(unsigned i) {
+    return 16u * (i >> 4) + 4u * ((((i >> 2) & 3u) + ((i >> 6) & 3u)) & 3u) + (i & 3u);
+}
+
+__global__ void __launch_bounds__(kScanThreads)
+select_scan_kernel(const int* __restrict__ kept, const int* __restrict__ budgets, int n_keep, int n_tiles,
+                   int n_v, int cap, int* __restrict__ offs, int* __restrict__ status) {
+    __shared__ __align__(16) unsigned lb[kChunk];
+    __shared__ unsigned wsum[kScanThreads / 64];
+    __shared__ int wbad[kScanThreads / 64];
+    const unsigned tid = threadIdx.x;
+    const unsigned lane = tid & 63u;
+    const unsigned wave = tid >> 6;
+    const unsigned n = (unsigned)n_keep;   // indices below n + kChunk < 2^32
+    unsigned carry = 0u;   // budgets of the earlier chunks (no wrap-around while they are valid)
+    bool bad = false;
+    unsigned nb[kRun], nt[kRun];
+    auto load = [&](unsigned c) {
+#pragma unroll
+        for (int j = 0; j < kRun; ++j) {
+            const unsigned i = c + (unsigned)j * kScanThreads + tid;
+            nb[j] = i < n ? (unsigned)budgets[i] : 0u;
+            nt[j] = i < n ? (unsigned)kept[i] : 0u;
+        }
+    };
+    load(0u);
+    for (unsigned c = 0; c < n; c += kChunk) {
+#pragma unroll
+        for (int j = 0; j < kRun; ++j) {
+            bad = bad || nb[j] > (unsigned)n_v || nt[j] >= (unsigned)n_tiles;   // negative values are huge
+            lb[scan_word((unsigned)j * kScanThreads + tid)] = nb[j];
+        }
+        if (c + kChunk < n) load(c + kChunk);
+        __syncthreads();
+        const unsigned rot = (tid >> 2) & 3u;
+        unsigned v[kRun];
+        unsigned sum = 0u;
+#pragma unroll
+        for (int q = 0; q < kRun / 4; ++q) {
+            const u32x4_t x = *reinterpret_cast<const u32x4_t*>(lb + 16u * tid + 4u * ((q + rot) & 3u));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                v[4 * q + e] = x[e];
+                sum += x[e];
+            }
+        }
+        const unsigned incl = wave_incl_scan(sum);
+        if (lane == 63) wsum[wave] = incl;
+        __syncthreads();
+        unsigned before = 0u, chunk = 0u;
+#pragma unroll
+        for (int w = 0; w < kScanThreads / 64; ++w) {
+            const unsigned x = wsum[w];
+            before += (unsigned)w < wave ? x : 0u;
+            chunk += x;
+        }
+        unsigned run = carry + before + incl - sum;
+#pragma unroll
+        for (int q = 0; q < kRun / 4; ++q) {
+            u32x4_t o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                o[e] = run;
+                run += v[4 * q + e];
+            }
+            *reinterpret_cast<u32x4_t*>(lb + 16u * tid + 4u * ((q + rot) & 3u)) = o;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kRun; ++j) {
+            const unsigned i = c + (unsigned)j * kScanThreads + tid;
+            if (i < n) offs[i] = (int)lb[scan_word((unsigned)j * kScanThreads + tid)];
+        }
+        carry += chunk;
+        __syncthreads();   // lb and wsum are refilled by the next chunk
+    }
+    const bool wave_bad = __ballot(bad) != 0ull;
+    if (lane == 0) wbad[wave] = wave_bad;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the offsets stored, before any is cleared
+    __syncthreads();
+    int any_bad = 0;
+#pragma unroll
+    for (int w = 0; w < kScanThreads / 64; ++w) any_bad |= wbad[w];
+    // valid budgets keep the total within n_tiles * n_v <= INT32_MAX
+    const bool valid = any_bad == 0 && carry <= (unsigned)cap;
+    if (!valid) {
+        for (unsigned i = tid; i < n; i += kScanThreads) offs[i] = 0;
+    }
+    if (tid == 0) {
+        offs[n_keep] = valid ? (int)carry : 0;
+        *status = valid ? 0 : (int)RIFT_ERR_BUDGET;
+    }
+}
+
 // NE: keys per lane the kernel is built for (n_v <= 64 NE); W: waves (kept
-// tiles) per workgroup.
-template <int NE, int W>
+// tiles) per workgroup; PRE: select_scan_kernel has checked the call and
+// written the offsets and the status word.
+template <int NE, int W, bool PRE>
 __global__ void __launch_bounds__(64 * W)
 select_kernel(const double* __restrict__ token_key, int n_tiles, int n_v, int n_keep,
               const int* __restrict__ kept, const int* __restrict__ budgets, int cap,
@@ -101,7 +221,7 @@ select_kernel(const double* __restrict__ token_key, int n_tiles, int n_v, int n_
     const bool vec = ((reinterpret_cast<uintptr_t>(budgets) | reinterpret_cast<uintptr_t>(kept)) & 15u) == 0;
     constexpr int kV = 4;                       // 16-byte vectors per thread per round
     constexpr int kRound = kV * 64 * W;         // vectors per round
-    const int n4 = vec ? n_keep >> 2 : 0;       // whole vectors; the rest one by one
+    const int n4 = (vec && !PRE) ? n_keep >> 2 : 0;   // whole vectors; the rest one by one
     i32x4_t bv[kV], tv[kV];
     if (n4 > 0) {
 #pragma unroll
@@ -120,82 +240,90 @@ select_kernel(const double* __restrict__ token_key, int n_tiles, int n_v, int n_
         raw[e] = *reinterpret_cast<const double*>(kb + i * 8u);
     }
     int off = 0, budget = 0;
+    if constexpr (PRE) {
+        // the first launch's verdict, this tile's offset and budget (checked)
+        if (!has_tile) return;
+        if (__builtin_amdgcn_readfirstlane(*status) != 0) return;
+        off = __builtin_amdgcn_readfirstlane(offs[rho]);
+        budget = __builtin_amdgcn_readfirstlane(budgets[rho]);
+    } else {
 #pragma unroll
-    for (int w = 0; w < W; ++w) {
-        const int bw = first + w < n_keep ? budgets[first + w] : 0;
-        off += w < wave ? bw : 0;
-        budget = w == wave ? bw : budget;
-    }
+        for (int w = 0; w < W; ++w) {
+            const int bw = first + w < n_keep ? budgets[first + w] : 0;
+            off += w < wave ? bw : 0;
+            budget = w == wave ? bw : budget;
+        }
 
-    // 2. validity, base offset and total of the call: the largest budget and
-    //    id as unsigned values (a negative one is huge), the sums
-    unsigned bmax = 0u, tmax = 0u, total = 0u, before = 0u;
-    auto acc4 = [&](int v, const i32x4_t& b4, const i32x4_t& t4) __attribute__((always_inline)) {
-        bmax = max(bmax, max(max((unsigned)b4[0], (unsigned)b4[1]), max((unsigned)b4[2], (unsigned)b4[3])));
-        tmax = max(tmax, max(max((unsigned)t4[0], (unsigned)t4[1]), max((unsigned)t4[2], (unsigned)t4[3])));
-        const unsigned s = (unsigned)b4[0] + (unsigned)b4[1] + (unsigned)b4[2] + (unsigned)b4[3];
-        total += s;
-        if (4 * v + 3 < first) {
-            before += s;
-        } else if (4 * v < first) {
+        // 2. validity, base offset and total of the call: the largest budget and
+        //    id as unsigned values (a negative one is huge), the sums
+        unsigned bmax = 0u, tmax = 0u, total = 0u, before = 0u;
+        auto acc4 = [&](int v, const i32x4_t& b4, const i32x4_t& t4) __attribute__((always_inline)) {
+            bmax = max(bmax, max(max((unsigned)b4[0], (unsigned)b4[1]), max((unsigned)b4[2], (unsigned)b4[3])));
+            tmax = max(tmax, max(max((unsigned)t4[0], (unsigned)t4[1]), max((unsigned)t4[2], (unsigned)t4[3])));
+            const unsigned s = (unsigned)b4[0] + (unsigned)b4[1] + (unsigned)b4[2] + (unsigned)b4[3];
+            total += s;
+            if (4 * v + 3 < first) {
+                before += s;
+            } else if (4 * v < first) {
 #pragma unroll
-            for (int c = 0; c < 4; ++c) before += 4 * v + c < first ? (unsigned)b4[c] : 0u;
-        }
-    };
-#pragma unroll
-    for (int j = 0; j < kV; ++j)
-        if (tid + j * 64 * W < n4) acc4(tid + j * 64 * W, bv[j], tv[j]);
-    for (int v0 = tid + kRound; v0 < n4; v0 += kRound) {   // calls of more than one round
-#pragma unroll
-        for (int j = 0; j < kV; ++j) {
-            const int v = min(v0 + j * 64 * W, n4 - 1);
-            bv[j] = reinterpret_cast<const i32x4_t*>(budgets)[v];
-            tv[j] = reinterpret_cast<const i32x4_t*>(kept)[v];
-        }
+                for (int c = 0; c < 4; ++c) before += 4 * v + c < first ? (unsigned)b4[c] : 0u;
+            }
+        };
 #pragma unroll
         for (int j = 0; j < kV; ++j)
-            if (v0 + j * 64 * W < n4) acc4(v0 + j * 64 * W, bv[j], tv[j]);
-    }
-    for (int i = 4 * n4 + tid; i < n_keep; i += 64 * W) {
-        const unsigned bi = (unsigned)budgets[i];
-        bmax = max(bmax, bi);
-        tmax = max(tmax, (unsigned)kept[i]);
-        total += bi;
-        before += i < first ? bi : 0u;
-    }
-    before = wave_sum((int)before);
-    total = wave_sum((int)total);
-    const bool any_bad = __ballot(bmax > (unsigned)n_v || tmax >= (unsigned)n_tiles) != 0ull;
-    if (lane == 0) {
-        red_before[wave] = (int)before;
-        red_total[wave] = (int)total;
-        red_bad[wave] = any_bad;
-    }
-    // only shared memory is waited for at the barrier, so the keys stay in flight
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    before = 0u;
-    total = 0u;
-    int badw = 0;
+            if (tid + j * 64 * W < n4) acc4(tid + j * 64 * W, bv[j], tv[j]);
+        for (int v0 = tid + kRound; v0 < n4; v0 += kRound) {   // calls of more than one round
 #pragma unroll
-    for (int w = 0; w < W; ++w) {
-        before += (unsigned)red_before[w];
-        total += (unsigned)red_total[w];
-        badw |= red_bad[w];
+            for (int j = 0; j < kV; ++j) {
+                const int v = min(v0 + j * 64 * W, n4 - 1);
+                bv[j] = reinterpret_cast<const i32x4_t*>(budgets)[v];
+                tv[j] = reinterpret_cast<const i32x4_t*>(kept)[v];
+            }
+#pragma unroll
+            for (int j = 0; j < kV; ++j)
+                if (v0 + j * 64 * W < n4) acc4(v0 + j * 64 * W, bv[j], tv[j]);
+        }
+        for (int i = 4 * n4 + tid; i < n_keep; i += 64 * W) {
+            const unsigned bi = (unsigned)budgets[i];
+            bmax = max(bmax, bi);
+            tmax = max(tmax, (unsigned)kept[i]);
+            total += bi;
+            before += i < first ? bi : 0u;
+        }
+        before = wave_sum((int)before);
+        total = wave_sum((int)total);
+        const bool any_bad = __ballot(bmax > (unsigned)n_v || tmax >= (unsigned)n_tiles) != 0ull;
+        if (lane == 0) {
+            red_before[wave] = (int)before;
+            red_total[wave] = (int)total;
+            red_bad[wave] = any_bad;
+        }
+        // only shared memory is waited for at the barrier, so the keys stay in flight
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        before = 0u;
+        total = 0u;
+        int badw = 0;
+#pragma unroll
+        for (int w = 0; w < W; ++w) {
+            before += (unsigned)red_before[w];
+            total += (unsigned)red_total[w];
+            badw |= red_bad[w];
+        }
+        // valid budgets and ids keep every sum within n_tiles * n_v <= INT32_MAX
+        if (badw == 0 && total > (unsigned)cap) badw = 1;
+        badw = __builtin_amdgcn_readfirstlane(badw);
+        if (blockIdx.x == 0 && tid == 0) {
+            *status = badw ? (int)RIFT_ERR_BUDGET : 0;
+            if (n_keep == 0) offs[0] = 0;
+        }
+        off = __builtin_amdgcn_readfirstlane((int)before + off);
+        if (has_tile && lane == 0) {
+            offs[rho] = badw ? 0 : off;
+            if (rho == n_keep - 1) offs[n_keep] = badw ? 0 : (int)total;
+        }
+        if (badw || !has_tile) return;
+        budget = __builtin_amdgcn_readfirstlane(budget);
     }
-    // valid budgets and ids keep every sum within n_tiles * n_v <= INT32_MAX
-    if (badw == 0 && total > (unsigned)cap) badw = 1;
-    badw = __builtin_amdgcn_readfirstlane(badw);
-    if (blockIdx.x == 0 && tid == 0) {
-        *status = badw ? (int)RIFT_ERR_BUDGET : 0;
-        if (n_keep == 0) offs[0] = 0;
-    }
-    off = __builtin_amdgcn_readfirstlane((int)before + off);
-    if (has_tile && lane == 0) {
-        offs[rho] = badw ? 0 : off;
-        if (rho == n_keep - 1) offs[n_keep] = badw ? 0 : (int)total;
-    }
-    if (badw || !has_tile) return;
-    budget = __builtin_amdgcn_readfirstlane(budget);
     if (budget <= 0) return;
     int* out = sel_idx + off;
     if (budget >= n_v) {
@@ -400,9 +528,10 @@ select_kernel(const double* __restrict__ token_key, int n_tiles, int n_v, int n_
 hipError_t launch_select(const double* token_key, int n_tiles, int n_v, const int* kept,
                          const int* budgets, int n_keep, int* sel_offsets, int* sel_idx,
                          long long cap, int* status, hipStream_t st) {
-    // Every workgroup reads all budgets: few tiles per workgroup spread a
-    // query's tiles over the CUs; more amortise those reads in large calls
-    // (eight waves: 16 left some CUs with twice the work of others).
+    // Up to kScanFrom kept tiles every workgroup reads all budgets (one
+    // launch), four tiles a workgroup up to 1,024 tiles to spread a query's
+    // tiles over the CUs, eight above (16 left some CUs with twice the work
+    // of others); larger calls scan the budgets once first.
     const int c = (int)(cap < 0x7fffffffLL ? cap : 0x7fffffffLL);
     auto go = [&](auto kernel, int W) {
         const unsigned wgs = (unsigned)((n_keep + W - 1) / W);
@@ -410,12 +539,21 @@ hipError_t launch_select(const double* token_key, int n_tiles, int n_v, const in
                            kept, budgets, c, sel_offsets, sel_idx, status);
     };
     const bool small = n_keep <= 4 * 256;
+    const bool scan = n_keep > kScanFrom;
+    if (scan) {
+        hipLaunchKernelGGL(select_scan_kernel, dim3(1), dim3(kScanThreads), 0, st, kept, budgets, n_keep, n_tiles,
+                           n_v, c, sel_offsets, status);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     if (n_v <= 64 * 9) {
-        if (small) go(select_kernel<9, 4>, 4);
-        else go(select_kernel<9, 8>, 8);
+        if (small) go(select_kernel<9, 4, false>, 4);
+        else if (!scan) go(select_kernel<9, 8, false>, 8);
+        else go(select_kernel<9, 8, true>, 8);
     } else {
-        if (small) go(select_kernel<16, 4>, 4);
-        else go(select_kernel<16, 8>, 8);
+        if (small) go(select_kernel<16, 4, false>, 4);
+        else if (!scan) go(select_kernel<16, 8, false>, 8);
+        else go(select_kernel<16, 8, true>, 8);
     }
     return hipGetLastError();
 }

@@ -268,6 +268,45 @@ def test_select_many_tiles(R):
     assert st == 0 and np.array_equal(offs, r_offs) and np.array_equal(sel, r_sel)
 
 
+@pytest.mark.parametrize("n_keep,n_v", [(1024, 48), (1025, 48), (8192, 24), (8193, 24), (8300, 700)])
+def test_select_large_call_paths(R, n_keep, n_v):
+    """Up to 8,192 kept tiles one launch reads every budget (four tiles a
+    workgroup up to 1,024, eight above); above, a first launch scans them
+    (offsets, status) and the selection reads its offset.  Both sides of each
+    switch, and keys per lane above 9 (n_v > 576) on the scanned path."""
+    rng = np.random.default_rng(n_keep + n_v)
+    n_tiles = n_keep + 7
+    keys = rng.integers(-30, 31, size=(n_tiles, n_v)).astype(np.float64) * 0.25
+    kept = list(rng.permutation(n_tiles)[:n_keep])
+    budgets = list(rng.integers(0, n_v + 1, size=n_keep))
+    offs, sel, st = run_select(R, keys, kept, budgets)
+    r_offs, r_sel = O.select_tokens(keys, kept, budgets)
+    assert st == 0 and np.array_equal(offs, r_offs) and np.array_equal(sel, r_sel)
+
+
+@pytest.mark.parametrize("flaw", ["budget", "negative", "tile", "capacity"])
+def test_select_large_call_rejects(R, flaw):
+    """The scanned path reports a bad call like the one-launch path: status
+    RIFT_ERR_BUDGET, every offset 0, nothing written to the selection."""
+    rng = np.random.default_rng(5)
+    n_tiles, n_v, n_keep = 17000, 20, 16500   # the scanned path, and more than one scan chunk
+    keys = rng.standard_normal((n_tiles, n_v))
+    kept = list(rng.permutation(n_tiles)[:n_keep])
+    budgets = [int(b) for b in rng.integers(0, n_v + 1, size=n_keep)]
+    cap = None
+    if flaw == "budget":
+        budgets[16390] = n_v + 1
+    elif flaw == "negative":
+        budgets[40] = -3
+    elif flaw == "tile":
+        kept[16499] = n_tiles
+    else:
+        cap = sum(budgets) - 1
+    offs, sel, st = run_select(R, keys, kept, budgets, cap=cap)
+    assert st == 4 and np.all(offs == 0)
+    assert np.all(sel == -7)
+
+
 def test_select_rejects_bad_budgets(R):
     keys = np.zeros((2, 10))
     for budgets, kept in (([11, 1], [0, 1]), ([-1, 1], [0, 1]), ([1, 1], [0, 2])):
