@@ -400,7 +400,9 @@ RIFT_API size_t rift_prefill_workspace_size(const rift_model_cfg* cfg, int32_t t
  *              events[10 l + 2 g + 1] are recorded on `stream` right before and
  *              after stage g of layer l -- g = 0 QKV projection (+RoPE),
  *              1 attention, 2 output projection, 3 gate/up projection (+SwiGLU),
- *              4 down projection.
+ *              4 down projection.  A NULL entry is skipped (each recorded
+ *              event adds a marker between kernels, so a benchmark records only
+ *              the pairs it needs).
  * Implemented: bf16 with head_dim in {64, 128}, d % 256 == 0, ffn % 128 == 0;
  *              f32 with head_dim in {64, 128}, d % 64 == 0, ffn % 16 == 0;
  *              anything else returns RIFT_ERR_UNSUPPORTED.

@@ -367,9 +367,10 @@ def layer_struct(w: dict) -> LayerWeights:
 def rift_prefill(cfg: ModelCfg, layers: Sequence[dict], x_in, cu_seqlens, position_ids,
                  n_seq: int, max_seqlen: int, hidden_out, workspace, kv_cache=None,
                  events=None, stream=None, n_prefix: int = 0) -> None:
-    """events: optional list of 10 * n_layers torch.cuda.Event(enable_timing=True),
-    recorded around each per-layer stage (see include/rift.h).  n_prefix > 0:
-    sequence 0 is a prefix shared by every other sequence."""
+    """events: optional list of 10 * n_layers torch.cuda.Event(enable_timing=True)
+    or None (that mark skipped), recorded around each per-layer stage (see
+    include/rift.h).  n_prefix > 0: sequence 0 is a prefix shared by every
+    other sequence."""
     torch = _torch()
     T = x_in.shape[0]
     if len(layers) != cfg.n_layers:
@@ -388,9 +389,9 @@ def rift_prefill(cfg: ModelCfg, layers: Sequence[dict], x_in, cu_seqlens, positi
         if len(events) != 10 * cfg.n_layers:
             raise ValueError("events needs 10 entries per layer")
         for e in events:          # torch creates the hipEvent on its first record()
-            if not e.cuda_event:
+            if e is not None and not e.cuda_event:
                 e.record()
-        ev = (ctypes.c_void_p * len(events))(*[int(e.cuda_event) for e in events])
+        ev = (ctypes.c_void_p * len(events))(*[None if e is None else int(e.cuda_event) for e in events])
     st = load().rift_prefill(ctypes.byref(cfg), arr, _ptr(x_in), _dt_code(x_in), _ptr(cu_seqlens),
                              _ptr(position_ids), int(n_seq), int(T), int(max_seqlen), int(n_prefix),
                              _ptr(hidden_out), _ptr(kv_cache), _ptr(workspace), workspace.numel(),

@@ -586,9 +586,9 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
         return RIFT_OK;
     }
     RIFT_TRY(launch_rope_table(rope, max_seqlen, c.head_dim, c.rope_base, st));
-    // benchmark hook: event pair around stage g of layer l
+    // benchmark hook: event pair around stage g of layer l (NULL entries skipped)
     auto mark = [&](int l, int g, int end) -> hipError_t {
-        if (events == nullptr) return hipSuccess;
+        if (events == nullptr || events[10 * l + 2 * g + end] == nullptr) return hipSuccess;
         return hipEventRecord(static_cast<hipEvent_t>(events[10 * l + 2 * g + end]), st);
     };
 
