@@ -1,13 +1,15 @@
 """GPU parity of the decoder prefill against the float64 oracle, plus the
 whole scene-query at full size.  Tolerance: rowwise max relative error
 <= 2e-2 for bf16 and <= 1e-4 for f32 (per-token hidden state)."""
+import dataclasses
+
 import numpy as np
 import pytest
 
 import synth
 from oracle import rift_oracle as O
 from tests.rift_testlib import (f64, oracle_layer_weights, oracle_stage1, plan_shape,
-                                rowwise_rel_err, torch_mod, upload, upload_layer,
+                                rowwise_rel_err, shared_layout, torch_mod, upload, upload_layer,
                                 download_stored)
 
 pytestmark = pytest.mark.gpu
@@ -308,3 +310,56 @@ def test_shared_prefix_prefill_matches_unshared(R, name):
         assert np.array_equal(ha[a0 + n_sys:a1], hb[b0:b1]), i
         assert np.array_equal(ka[:, :, a0:a0 + n_sys], kb[:, :, :n_sys]), i
         assert np.array_equal(ka[:, :, a0 + n_sys:a1], kb[:, :, b0:b1]), i
+
+
+@pytest.mark.parametrize("d,n_heads,hd,ffn", [(256, 2, 128, 688), (192, 3, 64, 528)])
+def test_f32_prefill_head_dims_and_widths(R, d, n_heads, hd, ffn):
+    """The float32 path's other shapes: 128-dimensional heads, and a width that
+    is a multiple of 64 but not of 128.  Two layers against the float64
+    oracle (rowwise 1e-4), and the shared-prefix packing equal to the
+    per-prompt one, bit for bit."""
+    torch = torch_mod()
+    m = synth.ModelShape(d=d, n_heads=n_heads, head_dim=hd, ffn=ffn, n_layers=2)
+    wl = dataclasses.replace(synth.get("tiny"), model=m, cid=50 + hd)
+    Ws = [synth.make_layer(wl, l) for l in range(m.n_layers)]
+    Wd = [upload_layer(W, "f32") for W in Ws]
+    cfg = R.model_cfg(m.d, m.n_heads, m.head_dim, m.ffn, m.n_layers, m.rms_eps, m.rope_base, R.RIFT_F32)
+    rng = np.random.default_rng(d + hd)
+
+    def run(xs, cus, poss, n_prefix=0):
+        T = xs.shape[0]
+        L = int(np.diff(cus).max()) + n_prefix
+        ws = torch.empty(R.rift_prefill_workspace_size(cfg, T, L), dtype=torch.uint8, device="cuda")
+        out = torch.empty(T, m.d, dtype=torch.float32, device="cuda")
+        R.rift_prefill(cfg, Wd, upload(xs, "f32"), torch.from_numpy(np.asarray(cus, dtype=np.int32)).cuda(),
+                       torch.from_numpy(np.asarray(poss, dtype=np.int32)).cuda(), len(cus) - 1, L, out, ws,
+                       n_prefix=n_prefix)
+        torch.cuda.synchronize()
+        return out.cpu().numpy().astype(np.float64)
+
+    lens = [5, 70, 33]
+    x = rng.standard_normal((sum(lens), m.d)).astype(np.float32)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    pos = np.concatenate([np.arange(l) for l in lens]).astype(np.int32)
+    hid = run(x, cu, pos)
+    ys = O.prefill(x.astype(np.float64), cu, pos, [oracle_layer_weights(W, "f32") for W in Ws], m.n_heads,
+                   m.head_dim, m.rms_eps, m.rope_base, list(range(len(lens))))
+    for i in range(len(lens)):
+        err = rowwise_rel_err(hid[cu[i]:cu[i + 1]], ys[i])
+        assert err <= TOL["f32"], (i, err)
+
+    n_sys, own = 6, [1, 20, 9]
+    sysr = rng.standard_normal((n_sys, m.d)).astype(np.float32)
+    rows = [np.concatenate([sysr, rng.standard_normal((k, m.d)).astype(np.float32)]) for k in own]
+    xa = np.concatenate(rows)
+    la = [n_sys + k for k in own]
+    cua = np.concatenate([[0], np.cumsum(la)]).astype(np.int32)
+    posa = np.concatenate([np.arange(l) for l in la]).astype(np.int32)
+    xb, cub, posb = shared_layout(xa, cua, posa, n_sys)
+    ha = run(xa, cua, posa)
+    hb = run(xb, cub, posb, n_prefix=n_sys)
+    for i in range(len(own)):
+        a0, a1 = int(cua[i]), int(cua[i + 1])
+        b0, b1 = int(cub[i + 1]), int(cub[i + 2])
+        assert np.array_equal(ha[a0:a0 + n_sys], hb[:n_sys]), i
+        assert np.array_equal(ha[a0 + n_sys:a1], hb[b0:b1]), i
