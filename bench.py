@@ -31,22 +31,22 @@ STAGES = ("qkv_rope", "attention", "out_proj", "gate_up_swiglu", "down_proj")
 # (each GEMM adds a half-tile tail launch when its last round over the CUs is at most half full)
 KERNEL_NAMES = {"qkv_rope": "QKV+RoPE GEMM (gemm_bf16_pp_kernel<0>)",
                 "attention": "varlen causal attention (attn_bf16_kernel)",
-                "out_proj": "output projection + residual (gemm_bf16_w8_kernel<1>)",
+                "out_proj": "output projection + residual (gemm_bf16_pp_kernel<1>)",
                 "gate_up_swiglu": "gate/up+SwiGLU GEMM (gemm_bf16_pp_kernel<2>)",
-                "down_proj": "down projection + residual (gemm_bf16_w8_kernel<1>)"}
+                "down_proj": "down projection + residual (gemm_bf16_pp_kernel<1>)"}
 GEMM_SRC = os.path.join(ROOT, "paper_2609_29029_amd", "csrc", "gemm_bf16.hip")
 
 # HBM traffic of one gate/up+SwiGLU launch at the 400-tile workload with the shared
 # system prefix (T = 18,739 packed rows), from two rocprofv3 --pmc runs of this
 # script with --traffic-calibration (FETCH_SIZE, then WRITE_SIZE), each scaled
 # by what the counter reads for the 1 GiB calibration copy (FETCH_SIZE reads
-# half the bytes, WRITE_SIZE all of them): 5.9171 GB fetched + 0.4126 GB written
+# half the bytes, WRITE_SIZE all of them): 6.0248 GB fetched + 0.4126 GB written
 # (profiles/scene20_l32_counters.md).  Valid only for the GEMM source it was
 # measured on, identified by its SHA-256; otherwise reported as null.
 TRAFFIC = {"stage": "gate_up_swiglu",
-           "gemm_src_sha256": "931deef165838a0038bdde4f0cb0627c92b39c0c964563df294e0e4155407bb8",
+           "gemm_src_sha256": "34055892b25f211f03b82410dff12b61d213cb804c0ffc919acb58c074931005",
            "packed_tokens": 18739,
-           "bytes": 6.3297e9}
+           "bytes": 6.4374e9}
 
 
 def log(*a):

@@ -10,12 +10,12 @@
 // each wave a 128x64 block of 8x4 v_mfma_f32_16x16x32_bf16 tiles (under the
 // board power limit this instruction sustains more throughput than the
 // 32x32x16 form on the same data).  K advances 64 per stage through two LDS
-// buffers of 64 KB that LDS DMA (global_load_lds) fills a stage ahead.  Two
-// main loops share that layout: the eight-wave loop (every wave reads its
-// operands for the next 32-deep sub-step while it runs the MFMAs of the
-// current one) and the ping-pong loop (the two waves on a SIMD alternate
-// between a whole stage of MFMAs and the LDS reads of the next stage).  The
-// last tiles of a GEMM can run as 256x128 halves on 4 waves.
+// buffers of 64 KB that LDS DMA (global_load_lds) fills a stage ahead.  The
+// whole tiles run the ping-pong loop (the two waves on a SIMD alternate
+// between a whole stage of MFMAs and the LDS reads of the next stage); the
+// last tiles of a GEMM can run as 256x128 halves on 4 waves, each of which
+// reads its operands for the next 32-deep sub-step while it runs the MFMAs of
+// the current one.
 //
 // Every output element is one fixed sequence of MFMA accumulations over K, no
 // matter which tile or batch row holds it, so a row's result does not depend on
@@ -342,47 +342,39 @@ __device__ __forceinline__ void epilogue_staged(const GemmParams& p, f32x4_t (&a
     }
 }
 
-// Eight-wave main loop (two waves per SIMD, so one wave's LDS or DMA issue
-// stalls are covered by the other's MFMAs).  Within a stage the two 32-deep
-// sub-steps each run 32 MFMAs while the next sub-step's operands are read from
-// LDS.  The barrier sits before sub-step 1: by then stage kt+1 has landed and
-// every wave has read the whole of stage kt, so sub-step 1 also issues the DMA
-// of stage kt+2 into the buffer stage kt used, a stage before it is needed.
-//
-// HALF: a workgroup of 4 waves computes one half (128 columns, h = 0 or 1) of
-// a 256x256 tile, as waves (wm, 2h + (wave & 1)) of the whole-tile layout would;
-// only those 128 B rows are loaded.  Used for the last tiles of a GEMM so that
-// the final round over the CUs is half as long.
-template <int EPI, bool HALF>
-__global__ void __launch_bounds__(HALF ? 256 : 512, 1) gemm_bf16_w8_kernel(GemmParams p) {
+// Half-tile kernel: a workgroup of 4 waves computes one half (128 columns,
+// h = 0 or 1) of a 256x256 tile, as waves (wm, 2h + (wave & 1)) of the
+// whole-tile layout would; only those 128 B rows are loaded.  Used for the last
+// tiles of a GEMM so that the final round over the CUs is half as long.  Each
+// wave reads its operands for the next 32-deep sub-step while it runs the 32
+// MFMAs of the current one.  The barrier sits before sub-step 1: by then stage
+// kt+1 has landed and every wave has read the whole of stage kt, so sub-step 1
+// also issues the DMA of stage kt+2 into the buffer stage kt used, a stage
+// before it is needed.
+template <int EPI>
+__global__ void __launch_bounds__(256, 1) gemm_bf16_half_kernel(GemmParams p) {
     __shared__ __align__(16) bf16_t lds[kStagingBytes / 2];   // two stages, then the epilogue tile
     __shared__ int pos_lds[BM];   // QKV: clamped position of each tile row
-    int bm, bn, h = 0;
-    if constexpr (HALF) {
+    int bm, bn, h;
+    {
         const int i = xcd_remap(blockIdx.x, 2 * (p.num_m * p.num_n - p.n_full));
         h = i & 1;
         group_coords(p.n_full + (i >> 1), p.num_m, p.num_n, bm, bn);
-    } else {
-        int t = round_remap(blockIdx.x, p.n_full);
-        if (p.reverse) t = p.n_full - 1 - t;
-        group_coords(t, p.num_m, p.num_n, bm, bn);
     }
     const int m0 = bm * BM;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = HALF ? (wave >> 1) : (wave >> 2);
-    const int wn = HALF ? (2 * h + (wave & 1)) : (wave & 3);
+    const int wm = wave >> 1;
+    const int wn = 2 * h + (wave & 1);
 
-    // DMA.  Whole tile: instruction j (0..3) of this wave moves A-tile rows
-    // 8 (4 wave + j) + (lane >> 3) and instruction 4 + j the same B-tile rows.
-    // Half tile: instructions 0..7 move A rows 8 (8 wave + j) + (lane >> 3),
-    // instructions 8..11 B rows 128 h + 8 (4 wave + j) + (lane >> 3).
-    // Per-lane byte offsets are fixed for the whole K loop; the stage's K
-    // offset goes into the wave-uniform base.  LDS rows sit at the same place
-    // in both modes.
-    constexpr int NA = HALF ? 8 : 4;
+    // DMA: instructions 0..7 of this wave move A rows 8 (8 wave + j) +
+    // (lane >> 3), instructions 8..11 B rows 128 h + 8 (4 wave + j) +
+    // (lane >> 3).  Per-lane byte offsets are fixed for the whole K loop; the
+    // stage's K offset goes into the wave-uniform base.  LDS rows sit where
+    // the whole-tile kernel puts them.
+    constexpr int NA = 8;
     constexpr int NB = 4;
     constexpr int NQ = NA + NB;
     uint32_t aoff[NA], boff[NB];
@@ -414,7 +406,7 @@ __global__ void __launch_bounds__(HALF ? 256 : 512, 1) gemm_bf16_w8_kernel(GemmP
     };
 
     if constexpr (EPI == EPI_QKV) {
-        for (int i = tid; i < BM; i += (HALF ? 256 : 512)) {
+        for (int i = tid; i < BM; i += 256) {
             int r = m0 + i;
             r = r < p.M ? r : p.M - 1;
             int ps = p.pos[r];
@@ -500,13 +492,13 @@ __global__ void __launch_bounds__(HALF ? 256 : 512, 1) gemm_bf16_w8_kernel(GemmP
     for (; kt + 2 < nk; ++kt) stage(kt, T_{}, T_{});
     if (kt + 1 < nk) stage(kt++, F_{}, T_{});
     stage(kt, F_{}, F_{});
-    epilogue_staged<EPI, HALF>(p, acc, m0, bn, h, wm, wn, lane, pos_lds, reinterpret_cast<unsigned char*>(lds));
+    epilogue_staged<EPI, true>(p, acc, m0, bn, h, wm, wn, lane, pos_lds, reinterpret_cast<unsigned char*>(lds));
 }
 
 // ---------------------------------------------------------------------------
-// Ping-pong variant.  Same tile, LDS stages, wave sub-tiles and order of
-// accumulation as the eight-wave kernel, but the two waves that share a SIMD
-// take turns: while one issues the 64 MFMAs of a whole 64-deep stage from
+// Ping-pong kernel (every whole tile).  The 2 x 4 wave layout above, with the
+// same LDS stages and order of accumulation as the half-tile kernel; the two
+// waves that share a SIMD take turns: while one issues the 64 MFMAs of a whole 64-deep stage from
 // registers, the other reads its operands for the next stage from LDS, and a
 // workgroup barrier separates the turns.  Waves 0-3 (rows 0-127 of the tile)
 // run one turn ahead of waves 4-7 (rows 128-255); the hardware places waves w
@@ -539,8 +531,8 @@ __global__ void __launch_bounds__(512, 1) gemm_bf16_pp_kernel(GemmParams p) {
     const int wm = wave >> 2;   // also the group
     const int wn = wave & 3;
 
-    // DMA: as the eight-wave kernel (instruction j moves A rows and B rows
-    // 8 (4 wave + j) + (lane >> 3) of the stage).
+    // DMA: instruction j (0..3) of a wave moves A-tile rows and B-tile rows
+    // 8 (4 wave + j) + (lane >> 3) of the stage.
     uint32_t aoff[4], boff[4];
     const bf16_t* bbase[4];
 #pragma unroll
@@ -695,11 +687,10 @@ int cu_count() {
     return cache[dev];
 }
 
-// Whole 256x256 tiles first (ping-pong kernel for the QKV and gate/up GEMMs,
-// eight-wave kernel for the residual ones), then, if the tiles of the last
+// Whole 256x256 tiles first (ping-pong kernel), then, if the tiles of the last
 // round over the CUs fill at most half of it, those tiles as two 256x128
-// halves each, so that round takes about half as long.  Every output element
-// is accumulated in the same order by all three kernels.
+// halves each (half-tile kernel), so that round takes about half as long.
+// Every output element is accumulated in the same order by both kernels.
 template <int EPI>
 hipError_t launch_gemm(GemmParams p, int num_n, hipStream_t st) {
     if (p.M <= 0) return hipSuccess;
@@ -710,15 +701,12 @@ hipError_t launch_gemm(GemmParams p, int num_n, hipStream_t st) {
     const int rem = nt % cus;
     p.n_full = (2 * rem <= cus) ? nt - rem : nt;
     if (p.n_full > 0) {
-        if constexpr (EPI == EPI_RESID)
-            hipLaunchKernelGGL((gemm_bf16_w8_kernel<EPI, false>), dim3(p.n_full), dim3(512), 0, st, p);
-        else
-            hipLaunchKernelGGL(gemm_bf16_pp_kernel<EPI>, dim3(p.n_full), dim3(512), 0, st, p);
+        hipLaunchKernelGGL(gemm_bf16_pp_kernel<EPI>, dim3(p.n_full), dim3(512), 0, st, p);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
     if (nt > p.n_full)
-        hipLaunchKernelGGL((gemm_bf16_w8_kernel<EPI, true>), dim3(2 * (nt - p.n_full)), dim3(256), 0, st, p);
+        hipLaunchKernelGGL(gemm_bf16_half_kernel<EPI>, dim3(2 * (nt - p.n_full)), dim3(256), 0, st, p);
     return hipGetLastError();
 }
 
