@@ -40,13 +40,13 @@ GEMM_SRC = os.path.join(ROOT, "paper_2609_29029_amd", "csrc", "gemm_bf16.hip")
 # system prefix (T = 18,739 packed rows), from two rocprofv3 --pmc runs of this
 # script with --traffic-calibration (FETCH_SIZE, then WRITE_SIZE), each scaled
 # by what the counter reads for the 1 GiB calibration copy (FETCH_SIZE reads
-# half the bytes, WRITE_SIZE all of them): 6.0248 GB fetched + 0.4126 GB written
+# half the bytes, WRITE_SIZE all of them): 5.8448 GB fetched + 0.4126 GB written
 # (profiles/scene20_l32_counters.md).  Valid only for the GEMM source it was
 # measured on, identified by its SHA-256; otherwise reported as null.
 TRAFFIC = {"stage": "gate_up_swiglu",
-           "gemm_src_sha256": "34055892b25f211f03b82410dff12b61d213cb804c0ffc919acb58c074931005",
+           "gemm_src_sha256": "cb39e4abfd0dc96cef4fed7d068d84fa7a9eb94d172530d4a6ec47f03dc73a45",
            "packed_tokens": 18739,
-           "bytes": 6.4374e9}
+           "bytes": 6.2574e9}
 
 
 def log(*a):

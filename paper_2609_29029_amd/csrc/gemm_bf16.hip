@@ -199,7 +199,12 @@ __device__ __forceinline__ void epilogue_staged(const GemmParams& p, f32x4_t (&a
     const int col_in = lane & 15;
     const int row_hi = 4 * (lane >> 4);
     const int cbase = HALF ? 128 * h : 0;
-    __syncthreads();   // every wave is done with the stage buffers
+    // No barrier here: in both kernels every wave's last operand read of the
+    // stage buffers completes before a workgroup barrier that every wave has
+    // passed before its last MFMAs (the ping-pong kernel: the end of group 1's
+    // last read turn; the half-tile kernel: the barrier before the last
+    // sub-step), so the buffers are free, and group 0 of the ping-pong kernel
+    // starts its epilogue while group 1 runs its last MFMA turn.
     if constexpr (EPI == EPI_SWIGLU) {
         constexpr int OC = HALF ? 64 : 128;   // outputs per row of this workgroup
         constexpr int LD = OC + 8;
