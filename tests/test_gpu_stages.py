@@ -172,20 +172,25 @@ def test_score_equal_tiles(R):
 
 
 # ----------------------------------------------------------------------------- select
-def run_select(R, keys, kept, budgets, cap=None):
+def run_select(R, keys, kept, budgets, cap=None, shift=0):
+    """`shift` > 0 places the ids, budgets and offsets `shift` int32 entries
+    past a 256-byte boundary (no 16-byte vector access)."""
     torch = torch_mod()
     n_tiles, n_v = keys.shape
     n_keep = len(kept)
     total = int(np.clip(budgets, 0, n_v).sum()) if n_keep else 0
     cap = total if cap is None else cap
     key_d = torch.from_numpy(np.ascontiguousarray(keys.reshape(-1))).cuda()
-    kept_d = torch.tensor(list(kept) or [0], dtype=torch.int32, device="cuda")
-    bud_d = torch.tensor(list(budgets) or [0], dtype=torch.int32, device="cuda")
-    offs = torch.full((n_keep + 1,), -7, dtype=torch.int32, device="cuda")
+    pad = [0] * shift
+    kept_d = torch.tensor(pad + (list(kept) or [0]), dtype=torch.int32, device="cuda")[shift:]
+    bud_d = torch.tensor(pad + (list(budgets) or [0]), dtype=torch.int32, device="cuda")[shift:]
+    offs_all = torch.full((shift + n_keep + 1,), -7, dtype=torch.int32, device="cuda")
+    offs = offs_all[shift:]
     sel = torch.full((max(1, cap),), -7, dtype=torch.int32, device="cuda")
     status = torch.full((1,), -7, dtype=torch.int32, device="cuda")
     R.rift_select_tokens(key_d, n_tiles, n_v, kept_d, bud_d, n_keep, offs, sel[:cap] if cap else sel[:0], status)
     torch.cuda.synchronize()
+    assert np.all(offs_all[:shift].cpu().numpy() == -7)   # nothing written before the offsets
     return offs.cpu().numpy(), sel.cpu().numpy()[:cap], int(status.item())
 
 
@@ -271,9 +276,10 @@ def test_select_many_tiles(R):
 @pytest.mark.parametrize("n_keep,n_v", [(1024, 48), (1025, 48), (8192, 24), (8193, 24), (8300, 700)])
 def test_select_large_call_paths(R, n_keep, n_v):
     """Up to 8,192 kept tiles one launch reads every budget (four tiles a
-    workgroup up to 1,024, eight above); above, a first launch scans them
-    (offsets, status) and the selection reads its offset.  Both sides of each
-    switch, and keys per lane above 9 (n_v > 576) on the scanned path."""
+    workgroup up to 1,024, eight above); above, two launches check the call
+    and find the offsets chunk by chunk and the selection reads its offset.
+    Both sides of each switch, and keys per lane above 9 (n_v > 576) on the
+    chunked path."""
     rng = np.random.default_rng(n_keep + n_v)
     n_tiles = n_keep + 7
     keys = rng.integers(-30, 31, size=(n_tiles, n_v)).astype(np.float64) * 0.25
@@ -284,12 +290,28 @@ def test_select_large_call_paths(R, n_keep, n_v):
     assert st == 0 and np.array_equal(offs, r_offs) and np.array_equal(sel, r_sel)
 
 
-@pytest.mark.parametrize("flaw", ["budget", "negative", "tile", "capacity"])
+@pytest.mark.parametrize("n_keep,n_v,shift", [(9216, 576, 0), (8200, 1024, 0), (10241, 576, 1), (8193, 333, 3)])
+def test_select_chunked_full_tiles(R, n_keep, n_v, shift):
+    """The chunked path on tiles of exactly 9 and 16 keys a lane (no key past
+    the tile's end) with normal keys, a whole number of 1,024-tile chunks and
+    a one-tile last chunk; ids, budgets and offsets off the 16-byte grid."""
+    rng = np.random.default_rng(n_keep * 7 + n_v)
+    n_tiles = n_keep + 3
+    keys = rng.standard_normal((n_tiles, n_v))
+    kept = list(rng.permutation(n_tiles)[:n_keep])
+    budgets = list(rng.integers(0, n_v + 1, size=n_keep))
+    offs, sel, st = run_select(R, keys, kept, budgets, shift=shift)
+    r_offs, r_sel = O.select_tokens(keys, kept, budgets)
+    assert st == 0 and np.array_equal(offs, r_offs) and np.array_equal(sel, r_sel)
+
+
+@pytest.mark.parametrize("flaw", ["budget", "negative", "tile", "capacity", "first", "chunk_start"])
 def test_select_large_call_rejects(R, flaw):
-    """The scanned path reports a bad call like the one-launch path: status
-    RIFT_ERR_BUDGET, every offset 0, nothing written to the selection."""
+    """The chunked path reports a bad call like the one-launch path: status
+    RIFT_ERR_BUDGET, every offset 0, nothing written to the selection; flaws
+    in a chunk's first entry (whose slot carries the chunk's total) too."""
     rng = np.random.default_rng(5)
-    n_tiles, n_v, n_keep = 17000, 20, 16500   # the scanned path, and more than one scan chunk
+    n_tiles, n_v, n_keep = 17000, 20, 16500   # the chunked path, 17 chunks
     keys = rng.standard_normal((n_tiles, n_v))
     kept = list(rng.permutation(n_tiles)[:n_keep])
     budgets = [int(b) for b in rng.integers(0, n_v + 1, size=n_keep)]
@@ -300,6 +322,10 @@ def test_select_large_call_rejects(R, flaw):
         budgets[40] = -3
     elif flaw == "tile":
         kept[16499] = n_tiles
+    elif flaw == "first":
+        budgets[0] = n_v + 1
+    elif flaw == "chunk_start":
+        kept[2048] = -1
     else:
         cap = sum(budgets) - 1
     offs, sel, st = run_select(R, keys, kept, budgets, cap=cap)
