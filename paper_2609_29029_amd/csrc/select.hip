@@ -638,7 +638,7 @@ hipError_t launch_select(const double* token_key, int n_tiles, int n_v, const in
                            kept, budgets, c, sel_offsets, sel_idx, status);
     };
     auto go_chunked = [&](auto kernel) {
-        constexpr int W = 8;
+        constexpr int W = 1;   // a wave's slot is free as soon as its tile is done
         hipLaunchKernelGGL(kernel, dim3((unsigned)((n_keep + W - 1) / W)), dim3(64 * W), 0, st, token_key, n_tiles,
                            n_v, n_keep, kept, budgets, sel_offsets, sel_idx, (const int*)status);
     };
@@ -657,11 +657,11 @@ hipError_t launch_select(const double* token_key, int n_tiles, int n_v, const in
     auto pick = [&](auto full) {
         constexpr bool F = decltype(full)::value;
         if (n_v <= 64 * 9) {
-            if (scan) go_chunked(select_chunked_kernel<9, 8, F>);
+            if (scan) go_chunked(select_chunked_kernel<9, 1, F>);
             else if (small) go(select_kernel<9, 4, F>, 4);
             else go(select_kernel<9, 8, F>, 8);
         } else {
-            if (scan) go_chunked(select_chunked_kernel<16, 8, F>);
+            if (scan) go_chunked(select_chunked_kernel<16, 1, F>);
             else if (small) go(select_kernel<16, 4, F>, 4);
             else go(select_kernel<16, 8, F>, 8);
         }
