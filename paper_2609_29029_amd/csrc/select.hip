@@ -333,10 +333,12 @@ __device__ __forceinline__ void select_tile(const double (&raw)[NE], int n_v, in
     if (ncand != k && ncand <= 64 && all_finite) {
         // Rank each candidate among the candidates by (key desc, index asc)
         // with plain float64 comparisons (-0 and +0 compare equal); take the
-        // first k.  The histogram's slice of shared memory holds them.
+        // first k.  The candidates move to lanes 0 .. ncand - 1 through the
+        // histogram's slice of shared memory, each lane counts the candidates
+        // ahead of its own from register reads of the others, and the chosen
+        // slots come back as a wave-wide mask.
         double* cx = reinterpret_cast<double*>(hist);
         int* ci = reinterpret_cast<int*>(hist + 128);
-        int* chosen = reinterpret_cast<int*>(hist + 192);
         int slot0[NE];
         int n0 = 0;
 #pragma unroll
@@ -352,23 +354,22 @@ __device__ __forceinline__ void select_tile(const double (&raw)[NE], int n_v, in
             }
         }
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        if (lane < ncand) {
-            const double mx = cx[lane];
-            const int mi = ci[lane];
-            int r = 0;
-            for (int j = 0; j < ncand; ++j) {
-                const double xj = cx[j];
-                const int ij = ci[j];
-                r += (xj > mx || (xj == mx && ij < mi)) ? 1 : 0;
-            }
-            chosen[lane] = r < k ? 1 : 0;
+        const bool has = lane < ncand;
+        const double mx = has ? cx[lane] : 0.0;
+        const int mi = has ? ci[lane] : 0;
+        const int mhi = __double2hiint(mx), mlo = __double2loint(mx);
+        int r = 0;
+        for (int j = 0; j < ncand; ++j) {
+            const double xj = __hiloint2double(__builtin_amdgcn_readlane(mhi, j), __builtin_amdgcn_readlane(mlo, j));
+            const int ij = __builtin_amdgcn_readlane(mi, j);
+            r += (xj > mx || (xj == mx && ij < mi)) ? 1 : 0;
         }
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        const uint64_t chosen = __ballot(has && r < k);
 #pragma unroll
         for (int e = 0; e < NE; ++e) {
             if (cand[e] != 0ull) {
                 bool ch = false;
-                if (lane_in(cand[e])) ch = chosen[rank_in(cand[e], slot0[e])] != 0;
+                if (lane_in(cand[e])) ch = ((chosen >> rank_in(cand[e], slot0[e])) & 1ull) != 0ull;
                 take[e] |= __ballot(ch);
                 cand[e] = 0ull;
             }
@@ -456,10 +457,8 @@ __device__ __forceinline__ void select_tile(const double (&raw)[NE], int n_v, in
 #pragma unroll
     for (int e = 0; e < NE; ++e) {
         const uint64_t t = take[e];
-        if (t != 0ull) {
-            if (lane_in(t)) out[rank_in(t, written)] = 64 * e + lane;
-            written += __popcll(t);
-        }
+        if (lane_in(t)) out[rank_in(t, written)] = 64 * e + lane;
+        written += __popcll(t);
     }
 }
 
