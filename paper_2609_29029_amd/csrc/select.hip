@@ -2,26 +2,22 @@
 // budget of dominant tokens, ranked by the per-token margin, ties to the lower
 // token index, emitted in ascending index order.
 //
-// One launch.  A workgroup of W waves handles W consecutive kept tiles, one
-// wave per tile:
+// One wave per kept tile, its keys in registers (lane l, element e = token
+// 64 e + l).  Up to 8,192 kept tiles, one launch; a workgroup of W waves
+// handles W consecutive kept tiles:
 //   1. the wave issues the loads of its tile's keys (tile id clamped so every
 //      read is in bounds whatever the ids hold);
 //   2. meanwhile the workgroup reads every budget and tile id of the call:
 //      the call is valid only if all of them are in range and the total fits
 //      (then every workgroup reaches the same verdict), and the sum of the
 //      budgets before its first tile is its base offset;
-//   3. each wave finds the budget-th key of its tile, (key desc, index asc),
-//      by deciding the order-preserving key bits one at a time from the
-//      highest bit in which its keys differ: per bit, a ballot per element
-//      counts the candidates with a 0 there; the side that holds the
-//      budget-th key stays candidate, and when that is the 1 side every
-//      0-side candidate is taken.  The search ends once the candidates left
-//      are exactly the ones still needed (on distinct keys after about
-//      log2(n_v) + 2 bits), else after bit 0 with equal keys, of which the
-//      lowest indices are taken.  Candidate and taken sets are wave-wide bit
-//      masks (lane l, element e = token 64 e + l), so the search is a few
-//      vector compares and scalar mask operations per bit, with no shared
-//      memory traffic;
+//   3. each wave finds the budget-th key of its tile, (key desc, index asc):
+//      one histogram pass over 256 value buckets of the keys' float32 range
+//      (a monotone bucket map, so whole buckets before the budget-th key's
+//      are taken), then that bucket's few candidates ranked by float64
+//      comparisons with index ties; wide ties, infinities or a crowded bucket
+//      fall back to deciding the order-preserving key bits one at a time with
+//      wave-wide candidate masks;
 //   4. the taken tokens are written in ascending index order (ballot prefix
 //      counts).
 // Workgroup 0 writes the status word; the workgroup of the last tile writes
@@ -30,8 +26,9 @@
 // Step 2 costs every workgroup a read of all budgets and ids, which grows with
 // the square of the tile count.  Calls of more than 8,192 kept tiles therefore
 // check the call and find the offsets in two small launches first
-// (select_chunk_kernel, select_base_kernel), and the selection kernel reads
-// its tile's offset and the verdict instead of step 2.
+// (select_chunk_kernel, select_base_kernel), and the selection kernel
+// (select_chunked_kernel, one wave a workgroup) reads its tile's offset and
+// the verdict instead of step 2.
 #include <climits>
 #include <type_traits>
 
@@ -292,14 +289,17 @@ __device__ __forceinline__ void select_tile(const double (&raw)[NE], int n_v, in
     const float his = hi * scale;
     if (all_finite && range > 0.0f && scale > 0.0f && __builtin_isfinite(scale) && __builtin_isfinite(his)) {
         int bkt[NE];
+        // A wave's shared-memory operations execute in the order issued, so
+        // the clearing, the increments and the read-back need no waits in
+        // between, only to stay in this order (compiler barriers).
         *reinterpret_cast<u32x4_t*>(hist + 4 * lane) = u32x4_t{0u, 0u, 0u, 0u};
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        asm volatile("" ::: "memory");
 #pragma unroll
         for (int e = 0; e < NE; ++e) {
             bkt[e] = (int)__builtin_amdgcn_fmed3f(__builtin_fmaf(f[e], -scale, his), 0.0f, 255.0f);
             if (FULL || 64 * e + lane < n_v) atomicAdd(&hist[bkt[e]], 1u);
         }
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        asm volatile("" ::: "memory");
         const u32x4_t c = *reinterpret_cast<const u32x4_t*>(hist + 4 * lane);
         const unsigned mine = c[0] + c[1] + c[2] + c[3];
         const unsigned incl = wave_incl_scan(mine);   // keys in buckets < 4 lane + 4
@@ -353,7 +353,7 @@ __device__ __forceinline__ void select_tile(const double (&raw)[NE], int n_v, in
                 n0 += __popcll(cand[e]);
             }
         }
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        asm volatile("" ::: "memory");   // in-order shared memory, as above
         const bool has = lane < ncand;
         const double mx = has ? cx[lane] : 0.0;
         const int mi = has ? ci[lane] : 0;
