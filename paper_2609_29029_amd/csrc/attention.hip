@@ -2,11 +2,18 @@
 // an independent sequence; Sec. 2.3 Stage 2).  Query i of a sequence attends
 // to keys 0..i of the same sequence, scale 1/sqrt(head_dim).
 //
-// bf16, head_dim 128 or 64, on MFMA.  One workgroup of W = 4 waves per (sequence,
-// head), looping over the sequence's 128-query blocks, the last
-// (longest-running) first; wave w owns queries [32 w, 32 w + 32) of the block
-// (workgroups are numbered sequence by sequence, so prompts packed longest
-// first start first).  Keys and values stream 64 at a time through a ring of
+// bf16, head_dim 128 or 64, on MFMA.  With a head count that is a multiple of
+// 8, one workgroup of W = 4 waves per (sequence, head, 128-query block), from
+// a work list built once per prefill: workgroup b runs entry b / 8 (sequence,
+// group of 8 heads, block) for head 8 g + b mod 8, so all blocks of one
+// (sequence, head) run on one XCD at about the same time and read its keys
+// and values from that XCD's L2 after the first fetch (HBM-side fetch per
+// layer 0.46 GB, the q, k and v bytes, against 0.79 GB when one workgroup
+// loops over a sequence's blocks and its later passes miss the L2).
+// Otherwise one workgroup per (sequence, head), looping over the sequence's
+// 128-query blocks, the last (longest-running) first.  Wave w owns queries
+// [32 w, 32 w + 32) of a block (sequences in packing order, so prompts packed
+// longest first start first).  Keys and values stream 64 at a time through a ring of
 // S = 2 LDS stages that LDS DMA fills a block ahead, one barrier per block,
 // and two workgroups share a CU; the last key block of a query block loads
 // the first one of the next query block.  Tile rows are 256 bytes, unpadded; the
@@ -87,17 +94,31 @@ __device__ __forceinline__ void wait_vm(int n) {
 // 64).  With HD = 64 the tiles keep their 256-byte rows: the DMA fills only
 // the head's 8 chunks of each row, and the score and output MFMAs stop at the
 // head's dimensions (the other chunks are never read).
-template <int W, int S, int HD>
+template <int W, int S, int HD, bool LIST>
 __global__ void __launch_bounds__(64 * W, W == 8 ? 1 : 2)
 attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
                  const bf16_t* __restrict__ v, bf16_t* __restrict__ o,
-                 const int* __restrict__ cu, int n_seq, int H, int n_prefix, float scale_log2) {
+                 const int* __restrict__ cu, int n_seq, int H, int n_prefix, float scale_log2,
+                 const int2* __restrict__ list) {
     constexpr int G = W / 4;                 // query blocks per pass
     constexpr int NDMA = 32 / W;             // DMA instructions per wave per key block
+    static_assert(!LIST || W == 4, "the query-block kernel runs one block per pass");
     __shared__ __align__(16) unsigned char ring[S * kStageBytes];
 
-    const int seq = blockIdx.x / H;
-    const int head = blockIdx.x % H;
+    int seq, head, qb_top = -1;
+    if constexpr (LIST) {
+        // entry blockIdx / 8: sequence, group of 8 heads, query block; the
+        // head within the group is blockIdx mod 8, the XCD the workgroup runs
+        // on, so one XCD runs every query block of a (sequence, head)
+        const int2 it = list[blockIdx.x >> 3];
+        if (it.x < 0) return;
+        seq = it.x;
+        head = (it.y >> 16) * 8 + (int)(blockIdx.x & 7);
+        qb_top = it.y & 0xffff;
+    } else {
+        seq = blockIdx.x / H;
+        head = blockIdx.x % H;
+    }
     const int s0 = cu[seq];
     const int L = cu[seq + 1] - s0;
     const int pre = seq > 0 ? n_prefix : 0;   // logical keys before the sequence's own rows
@@ -173,13 +194,15 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
     const int v_off = (4 * (tg >> 1) + tj) * kRowBytes + (2 * (tg & 1) + (tu >> 1)) * 16 + 8 * (tu & 1);
 
     const int nqb = (L + BQ - 1) / BQ;
+    const int top = LIST ? qb_top : nqb - 1;            // the first pass's upper block
+    const int n_pass = LIST ? 1 : (nqb + G - 1) / G;
     // Ring position of each pass's first key block: positions run on across
     // passes, so the last block of a pass can load the next pass's first block
     // into the stage that is free by then.
     int g0 = 0;
     bool first_issued = false;
-    for (int pr = 0; G * pr < nqb; ++pr) {
-        const int qb_hi = nqb - 1 - G * pr;
+    for (int pr = 0; pr < n_pass; ++pr) {
+        const int qb_hi = top - G * pr;
         const int qb = qb_hi - grp;               // -1: the lower half has no block
         const int q0 = qb >= 0 ? qb * BQ : 0;
         const int qw = q0 + wq * 32;              // first query of this wave
@@ -212,7 +235,7 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
         const int nkv = (kv_end + BKV - 1) / BKV;
         const int pro = nkv < S - 1 ? nkv : S - 1;
         for (int b = first_issued ? 1 : 0; b < pro; ++b) dma_block(b, g0 + b);
-        const bool has_next = G * (pr + 1) < nqb;
+        const bool has_next = pr + 1 < n_pass;
         bool issued_next = false;
         // The compiler waits for the Q loads here, once per pair (with them,
         // for the ring's first blocks, issued just after); in the loop it then
@@ -363,6 +386,48 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
     }   // query block pairs
 }
 
+// Work list of the query-block kernel: for each sequence s in order, for each
+// group g of 8 heads, its query blocks from the last (longest) to the first,
+// entry {s, (g << 16) | block}; entries past the list up to n_list: {-1, 0}.
+// One workgroup; sequences 1,024 at a time, their entry counts scanned.
+__global__ void __launch_bounds__(1024)
+attn_worklist_kernel(const int* __restrict__ cu, int n_seq, int hs, int2* __restrict__ list, int n_list) {
+    __shared__ int wsum[16];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    int carry = 0;
+    for (int base = 0; base < n_seq; base += 1024) {
+        const int s = base + tid;
+        int len = s < n_seq ? cu[s + 1] - cu[s] : 0;
+        len = len > 0 ? len : 0;
+        const int nqb = (len + BQ - 1) / BQ;
+        const int cnt = hs * nqb;
+        int incl = cnt;   // inclusive scan over the wave
+#pragma unroll
+        for (int sh = 1; sh < 64; sh <<= 1) {
+            const int x = __shfl_up(incl, sh);
+            incl += lane >= sh ? x : 0;
+        }
+        if (lane == 63) wsum[wave] = incl;
+        __syncthreads();
+        int before = 0, blk = 0;
+#pragma unroll
+        for (int w = 0; w < 16; ++w) {
+            before += w < wave ? wsum[w] : 0;
+            blk += wsum[w];
+        }
+        const int start = carry + before + incl - cnt;
+        for (int r = 0; r < cnt; ++r) {
+            const int i = start + r;
+            if (i < n_list) list[i] = int2{s, ((r / nqb) << 16) | (nqb - 1 - r % nqb)};
+        }
+        carry += blk;
+        __syncthreads();   // wsum is refilled by the next round
+    }
+    for (int i = carry + tid; i < n_list; i += 1024) list[i] = int2{-1, 0};
+}
+
 template <int D>
 __global__ void __launch_bounds__(128)
 attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
@@ -404,19 +469,44 @@ attn_f32_kernel(const float* __restrict__ q, const float* __restrict__ k,
 
 }  // namespace
 
+int attention_worklist_entries(int T, int n_seq, int n_heads) {
+    // sum over sequences of ceil(len / BQ) <= ceil(T / BQ) + (non-empty sequences)
+    const long long e = (long long)(n_heads / 8) * ((T + BQ - 1) / BQ + (n_seq < T ? n_seq : T));
+    return e < (1 << 28) ? (int)e : (1 << 28);
+}
+
+hipError_t launch_attention_worklist(const int* cu, int n_seq, int n_heads, int2* list, int n_list,
+                                     hipStream_t st) {
+    if (n_heads % 8 != 0 || n_heads / 8 > 0x7fff || n_list <= 0) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(attn_worklist_kernel, dim3(1), dim3(1024), 0, st, cu, n_seq, n_heads / 8, list, n_list);
+    return hipGetLastError();
+}
+
 hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                  uint16_t* o, const int* cu, int n_seq, int max_seqlen,
-                                 int n_heads, int hd, int n_prefix, hipStream_t st) {
+                                 int n_heads, int hd, int n_prefix, const int2* list, int n_list,
+                                 hipStream_t st) {
     if (n_seq <= 0 || max_seqlen <= 0) return hipSuccess;
     if (hd != 64 && hd != 128) return hipErrorInvalidValue;
     const float scale_log2 = 1.4426950408889634f / sqrtf((float)hd);
+    if (list != nullptr) {
+        if (n_heads % 8 != 0 || n_list <= 0) return hipErrorInvalidValue;
+        const dim3 grid((unsigned)n_list * 8u);
+        if (hd == 128)
+            hipLaunchKernelGGL((attn_bf16_kernel<4, 2, 128, true>), grid, dim3(256), 0, st, q, k, v, o, cu, n_seq,
+                               n_heads, n_prefix, scale_log2, list);
+        else
+            hipLaunchKernelGGL((attn_bf16_kernel<4, 2, 64, true>), grid, dim3(256), 0, st, q, k, v, o, cu, n_seq,
+                               n_heads, n_prefix, scale_log2, list);
+        return hipGetLastError();
+    }
     const long long blocks = (long long)n_seq * n_heads;
     if (hd == 128)
-        hipLaunchKernelGGL((attn_bf16_kernel<4, 2, 128>), dim3((unsigned)blocks), dim3(256), 0, st, q, k, v, o, cu,
-                           n_seq, n_heads, n_prefix, scale_log2);
+        hipLaunchKernelGGL((attn_bf16_kernel<4, 2, 128, false>), dim3((unsigned)blocks), dim3(256), 0, st, q, k, v,
+                           o, cu, n_seq, n_heads, n_prefix, scale_log2, nullptr);
     else
-        hipLaunchKernelGGL((attn_bf16_kernel<4, 2, 64>), dim3((unsigned)blocks), dim3(256), 0, st, q, k, v, o, cu,
-                           n_seq, n_heads, n_prefix, scale_log2);
+        hipLaunchKernelGGL((attn_bf16_kernel<4, 2, 64, false>), dim3((unsigned)blocks), dim3(256), 0, st, q, k, v,
+                           o, cu, n_seq, n_heads, n_prefix, scale_log2, nullptr);
     return hipGetLastError();
 }
 

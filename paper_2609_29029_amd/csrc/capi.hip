@@ -100,8 +100,15 @@ rift_status debug_scan(const DebugInput* in, int count, int* flag, hipStream_t s
 inline int dt_kind(rift_dtype dt) { return dt == RIFT_BF16 ? 0 : 1; }
 
 struct PrefillLayout {
-    size_t rope, h, q, k, v, a, gate2, dbg, total;
+    size_t rope, h, q, k, v, a, gate2, alist, dbg, total;
 };
+
+// Entries of the query-block attention's work list the workspace holds (any
+// number of sequences; 0 where that kernel does not run).
+int64_t attention_list_capacity(const rift_model_cfg& c, int64_t T) {
+    if (c.dt != RIFT_BF16 || c.n_heads % 8 != 0 || T <= 0) return 0;
+    return attention_worklist_entries((int)T, (int)T, c.n_heads);
+}
 
 PrefillLayout prefill_layout(const rift_model_cfg& c, int64_t T, int64_t P) {
     PrefillLayout L{};
@@ -121,6 +128,8 @@ PrefillLayout prefill_layout(const rift_model_cfg& c, int64_t T, int64_t P) {
     off += align_up((size_t)T * c.ffn * e);
     L.gate2 = off;
     if (c.dt == RIFT_F32) off += align_up((size_t)T * c.ffn * e);
+    L.alist = off;
+    off += align_up((size_t)attention_list_capacity(c, T) * sizeof(int2));
     L.dbg = off;   // debug mode: flag word of the input scan
     off += kAlign;
     L.total = off;
@@ -586,6 +595,15 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
         return RIFT_OK;
     }
     RIFT_TRY(launch_rope_table(rope, max_seqlen, c.head_dim, c.rope_base, st));
+    // attention work list (one entry per sequence, group of 8 heads and
+    // 128-query block), built once for every layer
+    int2* alist = nullptr;
+    int n_alist = 0;
+    if (attention_list_capacity(c, T) > 0) {
+        alist = reinterpret_cast<int2*>(ws + L.alist);
+        n_alist = attention_worklist_entries(T, n_seq, c.n_heads);
+        RIFT_TRY(launch_attention_worklist(cu_seqlens, n_seq, c.n_heads, alist, n_alist, st));
+    }
     // benchmark hook: event pair around stage g of layer l (NULL entries skipped)
     auto mark = [&](int l, int g, int end) -> hipError_t {
         if (events == nullptr || events[10 * l + 2 * g + end] == nullptr) return hipSuccess;
@@ -637,7 +655,8 @@ rift_status rift_prefill(const rift_model_cfg* cfg, const rift_layer_weights* la
             RIFT_TRY(mark(l, 1, 0));
             RIFT_TRY(launch_attention_bf16(static_cast<const uint16_t*>(qb), static_cast<const uint16_t*>(kb),
                                            static_cast<const uint16_t*>(vb), static_cast<uint16_t*>(h),
-                                           cu_seqlens, n_seq, max_seqlen, c.n_heads, c.head_dim, n_prefix, st));
+                                           cu_seqlens, n_seq, max_seqlen, c.n_heads, c.head_dim, n_prefix, alist,
+                                           n_alist, st));
             RIFT_TRY(mark(l, 1, 1));
             RIFT_TRY(mark(l, 2, 0));
             RIFT_TRY(launch_gemm_resid(static_cast<const uint16_t*>(h), static_cast<const uint16_t*>(w.wo),

@@ -81,9 +81,18 @@ hipError_t launch_gemm_swiglu(const uint16_t* a, const uint16_t* wg, const uint1
                               uint16_t* out, int M, int F, int K, hipStream_t st, bool reverse = false);
 
 // Varlen causal attention, bf16, head_dim hd (128 or 64).  q, k, v, o: [T][H*hd].
+// With `list` (from launch_attention_worklist, n_list entries) one workgroup
+// runs one 128-query block; without it one workgroup runs a whole sequence.
 hipError_t launch_attention_bf16(const uint16_t* q, const uint16_t* k, const uint16_t* v,
                                  uint16_t* o, const int* cu, int n_seq, int max_seqlen,
-                                 int n_heads, int hd, int n_prefix, hipStream_t st);
+                                 int n_heads, int hd, int n_prefix, const int2* list, int n_list,
+                                 hipStream_t st);
+// Work list of the query-block attention for n_heads a multiple of 8 (one
+// entry per sequence, group of 8 heads and query block; unused entries up to
+// n_list are marked empty); n_list >= attention_worklist_entries(T, n_seq, H).
+int attention_worklist_entries(int T, int n_seq, int n_heads);
+hipError_t launch_attention_worklist(const int* cu, int n_seq, int n_heads, int2* list, int n_list,
+                                     hipStream_t st);
 
 // ---------------------------------------------------------------- decode (bf16)
 // pos[i] = (cu[i+1] - cu[i]) + step
