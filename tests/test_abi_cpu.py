@@ -165,9 +165,17 @@ def test_prefill_validation_and_workspace(R):
     L = R.load()
     cfg = R.model_cfg(4096, 32, 128, 11008, 1, 1e-6, 10000.0, R.RIFT_BF16)
     ws = R.rift_prefill_workspace_size(cfg, 22204, 643)
-    # rope table + h, q, k, v [T][d] + a [T][ffn], bf16
-    expect = 643 * 64 * 8 + 4 * 22204 * 4096 * 2 + 22204 * 11008 * 2
+    # rope table + h, q, k, v [T][d] + a [T][ffn], bf16, + the attention work
+    # list: 8-byte entries, (heads / 8) per 128-row block and per sequence
+    # (at most T sequences)
+    expect = (643 * 64 * 8 + 4 * 22204 * 4096 * 2 + 22204 * 11008 * 2
+              + (32 // 8) * ((22204 + 127) // 128 + 22204) * 8)
     assert expect <= ws <= expect + 8 * 256
+    # no work list when the head count is not a multiple of 8
+    cfg12 = R.model_cfg(768, 12, 64, 2048, 1, 1e-6, 10000.0, R.RIFT_BF16)
+    ws12 = R.rift_prefill_workspace_size(cfg12, 1000, 200)
+    expect12 = 200 * 32 * 8 + 4 * 1000 * 768 * 2 + 1000 * 2048 * 2
+    assert expect12 <= ws12 <= expect12 + 8 * 256
     lw = (R.LayerWeights * 1)(R.LayerWeights(*([FAKE] * 9)))
 
     def call(c, T=10, n_seq=1, max_len=10, x=FAKE, x_dt=1, wsb=1 << 40, n_prefix=0):

@@ -61,9 +61,13 @@ def run_prefill(R, m, Wd, x, cu, pos, n_prefix=0):
     return hid.cpu().numpy().astype(np.float64), kv.float().cpu().numpy()
 
 
-@pytest.mark.parametrize("lens,n_check", [([7, 130, 300], 3), ([640] * 8, 2)])
-def test_hd64_prefill_parity_and_batch_invariance(R, lens, n_check):
-    m = model(1024, 2816)
+@pytest.mark.parametrize("d,ffn,lens,n_check", [(1024, 2816, [7, 130, 300], 3), (1024, 2816, [640] * 8, 2),
+                                                 (1280, 3456, [7, 130, 300], 3)])
+def test_hd64_prefill_parity_and_batch_invariance(R, d, ffn, lens, n_check):
+    """16 heads: attention from the query-block work list; 20 heads (not a
+    multiple of 8): one workgroup per (sequence, head) looping over its
+    blocks."""
+    m = model(d, ffn)
     rng = np.random.default_rng(sum(lens))
     Ws = layers_for(m, 40)
     Wd = [upload_layer(W, "bf16") for W in Ws]
