@@ -66,7 +66,7 @@ typedef enum {
     RIFT_ERR_WORKSPACE = 5,   /* workspace too small or not 256-byte aligned      */
     RIFT_ERR_HIP = 6,         /* a HIP runtime call or a kernel launch failed     */
     RIFT_ERR_NONFINITE = 7,   /* a floating-point input holds NaN or infinity     */
-    RIFT_ERR_UNSUPPORTED = 8  /* valid request outside what this build implements */
+    RIFT_ERR_UNSUPPORTED = 8  /* valid request outside what this library implements */
 } rift_status;
 
 typedef enum { RIFT_F32 = 0, RIFT_BF16 = 1 } rift_dtype;

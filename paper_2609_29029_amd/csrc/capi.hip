@@ -169,7 +169,7 @@ const char* rift_status_string(rift_status s) {
         case RIFT_ERR_BUDGET: return "budget, level or tier out of range";
         case RIFT_ERR_WORKSPACE: return "workspace too small or not 256-byte aligned";
         case RIFT_ERR_HIP: return "a HIP runtime call or kernel launch failed";
-        case RIFT_ERR_UNSUPPORTED: return "valid request outside what this build implements";
+        case RIFT_ERR_UNSUPPORTED: return "valid request outside what this library implements";
         case RIFT_ERR_NONFINITE: return "a floating-point input holds NaN or infinity";
     }
     return "unknown status";
