@@ -156,3 +156,30 @@ def test_hd64_decode_matches_oracle(R, d, ffn):
         err = rowwise_rel_err(got, ref)
         print(f"d={d} prompt {i} (L={L}): decode rel err {err:.3e}")
         assert err <= TOL, (i, err)
+
+
+def test_hd64_attention_worklist_many_sequences(R):
+    """Eight heads (one group of eight: the query-block work list) over 1,100
+    sequences, which the list kernel scans 1,024 at a time, empty ones among
+    them: sequences on both sides of the 1,024 boundary and the last against
+    the oracle, and one prefilled alone gives the same bits."""
+    m = model(512, 1408)
+    rng = np.random.default_rng(1100)
+    lens = [int(v) for v in rng.integers(1, 41, size=1100)]
+    lens[0], lens[5], lens[1023], lens[1024], lens[1030] = 130, 0, 0, 200, 0
+    Ws = layers_for(m, 41)
+    Wd = [upload_layer(W, "bf16") for W in Ws]
+    x = synth.store(rng.standard_normal((sum(lens), m.d)).astype(np.float32), "bf16")
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    pos = np.concatenate([np.arange(l) for l in lens]).astype(np.int32)
+    hid, _ = run_prefill(R, m, Wd, x, cu, pos)
+    seqs = [0, 1022, 1024, 1099]
+    ys = O.prefill(f64(x, "bf16"), cu, pos, [oracle_layer_weights(W, "bf16") for W in Ws], m.n_heads,
+                   m.head_dim, m.rms_eps, m.rope_base, seqs)
+    for i in seqs:
+        err = rowwise_rel_err(hid[cu[i]:cu[i + 1]], ys[i])
+        print(f"sequence {i} (L={lens[i]}): rowwise rel err {err:.3e}")
+        assert err <= TOL, (i, err)
+    i = 1024
+    alone, _ = run_prefill(R, m, Wd, x[cu[i]:cu[i + 1]], np.array([0, lens[i]]), np.arange(lens[i]))
+    assert np.array_equal(alone, hid[cu[i]:cu[i + 1]])
