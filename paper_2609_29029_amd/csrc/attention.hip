@@ -25,7 +25,7 @@
 // the SIMDs half idle on prompts of a single query block.)
 // The wave computes S^T = K Q^T (v_mfma_f32_32x32x16_bf16, M = keys,
 // N = queries), so each lane holds one query's scores in registers; the online
-// softmax runs in float32 (running max and sum per query); the unnormalised
+// softmax runs in float32 (a running reference and sum per query); the unnormalised
 // probabilities, rounded to bf16, are already in the B-operand layout of
 // O^T = V^T P^T, whose A operand (V^T) comes from transposing LDS reads.
 // Key blocks start at the sequence start, so a sequence's result does not
@@ -52,6 +52,7 @@ constexpr int BKV = 64;
 constexpr int kRowBytes = kLdsDims * 2;         // one key or value row
 constexpr int kTileBytes = BKV * kRowBytes;     // 16 KB
 constexpr int kStageBytes = 2 * kTileBytes;     // keys, then values
+constexpr float kLazy = 8.0f;                   // softmax reference slack (log2 units)
 
 typedef short v4s_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4s_t lds_v4s_t;
@@ -277,7 +278,7 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
                         s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], s[kb], 0, 0, 0);
                     }
                 // raw scores; keys past a query are masked only in blocks that
-                // cross the wave's diagonal.  The running max is kept on the raw
+                // cross the wave's diagonal.  The block max is taken on the raw
                 // scale (scale_log2 > 0 commutes with max), and p = 2^(s scale - m)
                 // takes one fma and the hardware exp2 (its flush of results below
                 // 2^-126 to zero drops terms far below the row sum's precision).
@@ -301,7 +302,14 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
 #pragma unroll
                     for (int i = 0; i < 16; ++i) bmax = fmaxf(bmax, sc[kb][i]);
                 bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
-                const float m_new = fmaxf(m_run, bmax * scale_log2);
+                // The reference m_run moves only when a query's block max
+                // passes it by more than kLazy (log2 units); until then the
+                // probabilities 2^(s scale - m_run) stay below 2^kLazy, and
+                // the sums and the output need no rescaling (on most blocks
+                // after the first).  The normalisation by the row sum at the
+                // end is the same whatever the reference.
+                const float m_blk = bmax * scale_log2;
+                const float m_new = m_blk > m_run + kLazy ? m_blk : m_run;
                 const float neg_m = -m_new;
                 float rsum = 0.f;
 #pragma unroll
@@ -313,7 +321,7 @@ attn_bf16_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ k,
                         rsum += pv;
                     }
                 rsum += __shfl_xor(rsum, 32);
-                // rescale the sums only when some query's max moved (exact skip)
+                // rescale the sums only when some query's reference moved
                 if (__any(m_new != m_run)) {
                     const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
                     l_run *= alpha;
